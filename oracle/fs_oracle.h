@@ -1,0 +1,82 @@
+/*
+ * CPU oracle for the FairServe policy hot path.  TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, obviously correct host code that states what the policy
+ * computes, written from the paper (Alg. 1, Eq. 1, Eq. 2 and the OIT/WSC
+ * prose of Sec. 4).  It shares no code with the HIP library: only the tests,
+ * the smoke check and the CPU-baseline leg of the benchmark may load it.
+ *
+ * All pointers are host pointers.  Functions return an fso_code; on failure
+ * the outputs are unspecified.  When several problems are present the largest
+ * code is returned (validation looks at every record).
+ */
+#ifndef FS_ORACLE_H
+#define FS_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum fso_code { FSO_OK = 0, FSO_E_ARG = 1, FSO_E_ORDER = 2, FSO_E_RANGE = 3, FSO_E_OVERFLOW = 4 };
+
+typedef struct fso_trace {
+  int32_t n_replicas, n_users, n_apps;
+  const int64_t *rep_off;            /* [R+1] record offsets */
+  const int64_t *ts_us;              /* arrival time, non-decreasing per replica */
+  const int32_t *user, *app;         /* [0,U), [0,A) */
+  const int32_t *call, *head, *prev; /* all NULL => every record is a first call */
+  const int32_t *len_in, *len_sys, *len_out; /* len_sys may be NULL (=0) */
+} fso_trace;
+
+/* Eq. 1 and the fixed-point coefficients: w_aj = a*E[in] + b*E[sys] + g*E[out]
+ * with (a,b,g) = (1,2,1); coef[a][j][x] = round_half_even(2^16 * K * x_weight / w_aj). */
+int fso_coef_from_expectations(int32_t n_apps, int32_t n_stages, const double *e_in,
+                               const double *e_sys, const double *e_out, int64_t K,
+                               int64_t *coef /* [A][J][3] */);
+
+/* Eq. 2, one LLM call: cost = floor(E_u * (c_in*L_I + c_sys*L_S + c_out*L_O) / 2^8). */
+int fso_cost(const fso_trace *t, int32_t n_stages, int64_t coef_rep_stride, const int64_t *coef,
+             int64_t prio_rep_stride, const int32_t *prio, int64_t *cost);
+
+/* OIT window counts and limit test (Alg. 1 monitoring stream).  reason[i]:
+ * raw mode: 0 within limits, 1 user limit exceeded, 2 app limit exceeded;
+ * gated mode: 0 not blocked, 1/2 head blocked by that limit, 3 inherited.
+ * bitmap bit i = (reason[i] != 0).  cnt_* may be NULL. */
+int fso_throttle(const fso_trace *t, int64_t window_us, int32_t t_user, const int32_t *t_app,
+                 const uint8_t *overloaded /* NULL => always */, int32_t raw, uint8_t *reason,
+                 uint32_t *bitmap, int32_t *cnt_user, int32_t *cnt_app);
+
+typedef struct fso_engine { int64_t step_us, cap_tokens, overload_tokens; } fso_engine;
+
+typedef struct fso_outputs {
+  int8_t *status;             /* [N] 0 admitted, 1/2/3 blocked, -1 not processed (bounded run) */
+  int32_t *admit_step;        /* [N] or NULL, -1 if not admitted */
+  int32_t *admit_seq;         /* [N] or NULL */
+  int64_t *counter_after;     /* [N] or NULL */
+  int64_t *counter_on_arrival;/* [N] or NULL, -1 if not processed */
+  int64_t *counter;           /* [R][U] or NULL */
+  int64_t *steps, *decisions, *max_gap; /* [R] or NULL */
+} fso_outputs;
+
+/* Per-replica step simulation (Alg. 1 execution + monitoring streams under the
+ * token-budget step model).  exceed_reason: raw throttle reasons (NULL = none).
+ * max_steps < 0: run until drained.  check != 0 verifies the paper's invariants
+ * on every decision and returns FSO_E_ARG (with a message on stderr) if one fails. */
+int fso_simulate(const fso_trace *t, const int64_t *cost, const uint8_t *exceed_reason,
+                 const fso_engine *e, int64_t max_steps, int32_t n_threads, int32_t check,
+                 fso_outputs *out);
+
+typedef struct fso_metrics {
+  double *jain, *max_gap_tokens, *svc_req_pct, *svc_int_pct, *served_users_pct, *delayed_users_pct;
+  int64_t *throttled, *aborted_midway, *wasted_tokens;
+} fso_metrics;
+
+int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *status,
+                         const int32_t *admit_step, const int64_t *max_gap, int64_t step_us,
+                         int32_t delay_steps, fso_metrics *m);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -200,10 +200,12 @@ fs_status fs_run_trace(const fs_trace *t, const fs_weights *w, const fs_limits *
                        hipStream_t stream);
 
 /* Per-replica metrics from a finished run (Sec. 5 definitions plus Jain's index).
+ * ws: device workspace of at least fs_metrics_workspace(t) bytes (256-byte aligned).
  * out->err receives data-dependent errors. */
+size_t fs_metrics_workspace(const fs_trace *t);
 fs_status fs_fairness_metrics(const fs_trace *t, const int64_t *cost, const fs_outputs *out,
-                              const fs_engine *eng, int32_t delay_steps, fs_metrics *m,
-                              hipStream_t stream);
+                              const fs_engine *eng, int32_t delay_steps, fs_metrics *m, void *ws,
+                              size_t ws_bytes, hipStream_t stream);
 
 /* Eq. 1 host helper: w_aj = 1*e_in + 2*e_sys + 1*e_out (expected tokens of app a at
  * stage j) and coef_h[a][j][x] = round-half-even(double(2^16 * K * class_weight_x) / w_aj)

@@ -43,15 +43,17 @@ Replica replica(const fso_trace *t, int32_t r) {
 
 int worse(int a, int b) { return a > b ? a : b; }
 
-// Structural checks shared by every entry point of the oracle.
-int validate_trace(const fso_trace *t, bool need_lengths) {
+// Structural checks.  Each entry point checks the fields it reads.
+enum Need : unsigned { kIds = 1, kOrder = 2, kChain = 4, kLengths = 8 };
+
+int validate_trace(const fso_trace *t, unsigned need) {
   if (!t || t->n_replicas < 1 || t->n_users < 1 || t->n_apps < 1 || !t->rep_off || !t->ts_us ||
       !t->user || !t->app)
     return FSO_E_ARG;
   bool any = t->call || t->head || t->prev;
   bool all = t->call && t->head && t->prev;
   if (any && !all) return FSO_E_ARG;
-  if (need_lengths && (!t->len_in || !t->len_out)) return FSO_E_ARG;
+  if ((need & kLengths) && (!t->len_in || !t->len_out)) return FSO_E_ARG;
   if (t->rep_off[0] != 0) return FSO_E_ARG;
   for (int32_t r = 0; r < t->n_replicas; ++r)
     if (t->rep_off[r + 1] < t->rep_off[r] || t->rep_off[r + 1] - t->rep_off[r] > INT32_MAX)
@@ -61,11 +63,16 @@ int validate_trace(const fso_trace *t, bool need_lengths) {
     Replica rp = replica(t, r);
     for (int64_t i = 0; i < rp.n; ++i) {
       int64_t g = rp.base + i;
-      if (t->ts_us[g] < 0) code = worse(code, FSO_E_RANGE);
-      if (i > 0 && t->ts_us[g] < t->ts_us[g - 1]) code = worse(code, FSO_E_ORDER);
-      if (t->user[g] < 0 || t->user[g] >= t->n_users) code = worse(code, FSO_E_RANGE);
-      if (t->app[g] < 0 || t->app[g] >= t->n_apps) code = worse(code, FSO_E_RANGE);
-      if (all) {
+      if (need & kOrder) {
+        if (t->ts_us[g] < 0) code = worse(code, FSO_E_RANGE);
+        if (i > 0 && t->ts_us[g] < t->ts_us[g - 1]) code = worse(code, FSO_E_ORDER);
+      }
+      if (need & kIds) {
+        if (t->user[g] < 0 || t->user[g] >= t->n_users) code = worse(code, FSO_E_RANGE);
+        if (t->app[g] < 0 || t->app[g] >= t->n_apps) code = worse(code, FSO_E_RANGE);
+        if (all && t->call[g] < 0) code = worse(code, FSO_E_RANGE);
+      }
+      if ((need & kChain) && all) {
         int32_t c = t->call[g], h = t->head[g], p = t->prev[g];
         bool ok;
         if (c == 0) {
@@ -79,7 +86,7 @@ int validate_trace(const fso_trace *t, bool need_lengths) {
         }
         if (!ok) code = worse(code, FSO_E_RANGE);
       }
-      if (need_lengths) {
+      if (need & kLengths) {
         int64_t li = t->len_in[g], lo = t->len_out[g], ls = t->len_sys ? t->len_sys[g] : 0;
         if (li < 0 || li >= kLenLimit || lo < 0 || lo >= kLenLimit || ls < 0 || ls >= kLenLimit)
           code = worse(code, FSO_E_RANGE);
@@ -330,7 +337,7 @@ int fso_coef_from_expectations(int32_t n_apps, int32_t n_stages, const double *e
 int fso_cost(const fso_trace *t, int32_t n_stages, int64_t coef_rep_stride, const int64_t *coef,
              int64_t prio_rep_stride, const int32_t *prio, int64_t *cost) {
   if (n_stages < 1 || !coef || !cost || coef_rep_stride < 0 || prio_rep_stride < 0) return FSO_E_ARG;
-  int code = validate_trace(t, true);
+  int code = validate_trace(t, kIds | kLengths);
   if (code == FSO_E_ARG) return code;
   for (int32_t r = 0; r < t->n_replicas; ++r) {
     Replica rp = replica(t, r);
@@ -369,7 +376,7 @@ int fso_throttle(const fso_trace *t, int64_t window_us, int32_t t_user, const in
                  const uint8_t *overloaded, int32_t raw, uint8_t *reason, uint32_t *bitmap,
                  int32_t *cnt_user, int32_t *cnt_app) {
   if (window_us <= 0 || t_user < 0 || !t_app || !reason) return FSO_E_ARG;
-  int code = validate_trace(t, false);
+  int code = validate_trace(t, kIds | kOrder | (raw ? 0u : unsigned(kChain)));
   if (code == FSO_E_ARG) return code;
   for (int32_t a = 0; a < t->n_apps; ++a)
     if (t_app[a] < 0) return FSO_E_ARG;
@@ -417,7 +424,7 @@ int fso_simulate(const fso_trace *t, const int64_t *cost, const uint8_t *exceed_
                  fso_outputs *out) {
   if (!e || !out || !out->status || !cost) return FSO_E_ARG;
   if (e->step_us <= 0 || e->cap_tokens <= 0 || e->cap_tokens > kCapLimit) return FSO_E_ARG;
-  int code = validate_trace(t, true);
+  int code = validate_trace(t, kIds | kOrder | kChain | kLengths);
   if (code != FSO_OK) return code;
   int64_t N = t->rep_off[t->n_replicas];
   for (int64_t g = 0; g < N; ++g) {
@@ -438,7 +445,7 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
                          const int32_t *admit_step, const int64_t *max_gap, int64_t step_us,
                          int32_t delay_steps, fso_metrics *m) {
   if (!cost || !status || !admit_step || !m || step_us <= 0 || delay_steps < 0) return FSO_E_ARG;
-  int code = validate_trace(t, false);
+  int code = validate_trace(t, kIds | kChain);
   if (code != FSO_OK) return code;
   const int32_t U = t->n_users;
   for (int32_t r = 0; r < t->n_replicas; ++r) {

@@ -1,0 +1,258 @@
+// Per-replica fairness and served-experience metrics (Sec. 5 definitions: service
+// provided for requests and interactions, served users, delayed users, aborted
+// interactions and wasted tokens) plus Jain's index of the charged service.
+// Integer accumulation only (atomics on integers are order-independent, so the
+// result is deterministic); Jain's sums are exact 128-bit before the fp64 division.
+#include "fs_device.h"
+#include "fs_launch.h"
+
+namespace fs {
+namespace {
+
+enum : int { C_ADMITTED, C_THROTTLED, C_INTERACTIONS, C_FULL, C_ABORTED, C_WASTED, C_NUM = 8 };
+enum : uint32_t { U_HAS = 1, U_FULL = 2, U_DELAYED = 4 };
+enum : uint32_t { I_SERVED = 1, I_UNSERVED = 2 };
+
+size_t up(size_t x) { return (x + 255) / 256 * 256; }
+
+struct MLayout {
+  size_t charged, uflags, iflags, counters, total;
+};
+
+MLayout mlayout(const fs_trace *t) {
+  MLayout L;
+  size_t ru = size_t(t->n_replicas) * size_t(t->n_users);
+  size_t n = size_t(t->rep_off_h[t->n_replicas]);
+  size_t o = 0;
+  L.charged = o; o += up(ru * 8);
+  L.uflags = o; o += up(ru * 4);
+  L.iflags = o; o += up((n > 0 ? n : 1) * 4);
+  L.counters = o; o += up(size_t(t->n_replicas) * C_NUM * 8);
+  L.total = o;
+  return L;
+}
+
+struct MArgs {
+  DevTrace t;
+  const int64_t *cost;
+  const int8_t *status;
+  const int32_t *admit_step;
+  const int64_t *max_gap;
+  int64_t tau;
+  int32_t D;
+  unsigned long long *charged;
+  uint32_t *uflags, *iflags;
+  unsigned long long *counters;
+  fs_metrics m;
+  int32_t *err;
+};
+
+__global__ void k_m_zero(MArgs a, int64_t RU, int64_t N) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < RU; i += stride) {
+    a.charged[i] = 0;
+    a.uflags[i] = 0;
+  }
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < N; i += stride)
+    a.iflags[i] = 0;
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < int64_t(a.t.R) * C_NUM;
+       i += stride)
+    a.counters[i] = 0;
+}
+
+__device__ inline bool first_call(const DevTrace &t, int64_t g) { return !t.call || t.call[g] == 0; }
+
+// wave-aggregated add to a per-replica counter (all lanes of the wave may differ in r)
+__device__ inline void count_add(unsigned long long *p, unsigned long long v) {
+  if (v) atomicAdd(p, v);
+}
+
+// Pass 1: per record -- validity, user flags, charged service, interaction flags.
+__global__ void __launch_bounds__(256) k_m_records(MArgs a) {
+  const DevTrace &t = a.t;
+  int32_t code = 0;
+  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
+       g += int64_t(gridDim.x) * blockDim.x) {
+    int32_t r = replica_of(t.rep_off, t.R, g);
+    int64_t base = t.rep_off[r], i = g - base, n = t.rep_off[r + 1] - base;
+    int32_t k = t.user[g];
+    if (k < 0 || k >= t.U || t.app[g] < 0 || t.app[g] >= t.A) {
+      code = max(code, int32_t(FS_E_RANGE));
+      continue;
+    }
+    int64_t h = i;
+    if (!first_call(t, g)) {
+      h = t.head[g];
+      if (h < 0 || h >= i) {
+        code = max(code, int32_t(FS_E_RANGE));
+        continue;
+      }
+    }
+    int64_t uk = int64_t(r) * t.U + k;
+    int8_t st = a.status[g];
+    uint32_t uf = U_HAS;
+    if (st == 0) {
+      atomicAdd(a.charged + uk, (unsigned long long)a.cost[g]);
+      atomicOr(a.iflags + base + h, I_SERVED);
+      if (int64_t(a.admit_step[g]) - t.ts[g] / a.tau > a.D) uf |= U_DELAYED;
+      count_add(a.counters + r * C_NUM + C_ADMITTED, 1);
+    } else {
+      atomicOr(a.iflags + base + h, I_UNSERVED);
+      if (st > 0) count_add(a.counters + r * C_NUM + C_THROTTLED, 1);
+    }
+    if (first_call(t, g)) count_add(a.counters + r * C_NUM + C_INTERACTIONS, 1);
+    atomicOr(a.uflags + uk, uf);
+    (void)n;
+  }
+  if (code) raise_err(a.err, code);
+}
+
+// Pass 2: per interaction (first call) -- fully served, aborted midway.
+__global__ void __launch_bounds__(256) k_m_interactions(MArgs a) {
+  const DevTrace &t = a.t;
+  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
+       g += int64_t(gridDim.x) * blockDim.x) {
+    if (!first_call(t, g)) continue;
+    int32_t k = t.user[g];
+    if (k < 0 || k >= t.U) continue;
+    int32_t r = replica_of(t.rep_off, t.R, g);
+    uint32_t f = a.iflags[g];
+    if (!(f & I_UNSERVED)) {
+      count_add(a.counters + r * C_NUM + C_FULL, 1);
+      atomicOr(a.uflags + int64_t(r) * t.U + k, U_FULL);
+    }
+    if ((f & I_SERVED) && (f & I_UNSERVED)) count_add(a.counters + r * C_NUM + C_ABORTED, 1);
+  }
+}
+
+// Pass 3: per admitted record of an aborted interaction -- wasted tokens.
+__global__ void __launch_bounds__(256) k_m_wasted(MArgs a) {
+  const DevTrace &t = a.t;
+  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
+       g += int64_t(gridDim.x) * blockDim.x) {
+    if (a.status[g] != 0) continue;
+    int32_t r = replica_of(t.rep_off, t.R, g);
+    int64_t base = t.rep_off[r], i = g - base;
+    int64_t h = first_call(t, g) ? i : t.head[g];
+    if (h < 0 || h > i) continue;
+    uint32_t f = a.iflags[base + h];
+    if ((f & I_SERVED) && (f & I_UNSERVED))
+      count_add(a.counters + r * C_NUM + C_WASTED, (unsigned long long)tokens_of(t, g));
+  }
+}
+
+struct U128 {
+  unsigned long long lo, hi;
+};
+__device__ inline U128 add128(U128 a, U128 b) {
+  U128 c;
+  c.lo = a.lo + b.lo;
+  c.hi = a.hi + b.hi + (c.lo < a.lo ? 1ull : 0ull);
+  return c;
+}
+__device__ inline double to_double(U128 v) {
+  return double(v.hi) * 18446744073709551616.0 + double(v.lo);
+}
+
+// Pass 4: one block per replica -- Jain's index and the percentages.
+__global__ void __launch_bounds__(256) k_m_finish(MArgs a) {
+  const int32_t r = blockIdx.x;
+  const int32_t U = a.t.U;
+  __shared__ U128 s1s[256], s2s[256];
+  __shared__ unsigned long long cnt[256][3];
+  U128 s1 = {0, 0}, s2 = {0, 0};
+  unsigned long long users = 0, full = 0, delayed = 0;
+  for (int32_t k = threadIdx.x; k < U; k += blockDim.x) {
+    int64_t uk = int64_t(r) * U + k;
+    uint32_t f = a.uflags[uk];
+    if (!(f & U_HAS)) continue;
+    unsigned long long x = a.charged[uk];
+    users += 1;
+    full += (f & U_FULL) ? 1 : 0;
+    delayed += (f & U_DELAYED) ? 1 : 0;
+    s1 = add128(s1, U128{x, 0});
+    U128 sq{x * x, __umul64hi(x, x)};
+    s2 = add128(s2, sq);
+  }
+  s1s[threadIdx.x] = s1;
+  s2s[threadIdx.x] = s2;
+  cnt[threadIdx.x][0] = users;
+  cnt[threadIdx.x][1] = full;
+  cnt[threadIdx.x][2] = delayed;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      s1s[threadIdx.x] = add128(s1s[threadIdx.x], s1s[threadIdx.x + w]);
+      s2s[threadIdx.x] = add128(s2s[threadIdx.x], s2s[threadIdx.x + w]);
+      for (int c = 0; c < 3; ++c) cnt[threadIdx.x][c] += cnt[threadIdx.x + w][c];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const unsigned long long *C = a.counters + r * C_NUM;
+    const int64_t n = a.t.rep_off[r + 1] - a.t.rep_off[r];
+    U128 S1 = s1s[0], S2 = s2s[0];
+    const unsigned long long nu = cnt[0][0];
+    double jain = 1.0;
+    if (S2.lo != 0 || S2.hi != 0) {
+      double d1 = to_double(S1);
+      jain = (d1 * d1) / (double(nu) * to_double(S2));
+    }
+    auto pct = [](unsigned long long x, unsigned long long y) {
+      return y == 0 ? 0.0 : 100.0 * double(x) / double(y);
+    };
+    a.m.jain[r] = jain;
+    a.m.max_gap_tokens[r] = double(a.max_gap[r]) / 65536.0;
+    a.m.svc_req_pct[r] = pct(C[C_ADMITTED], (unsigned long long)n);
+    a.m.svc_int_pct[r] = pct(C[C_FULL], C[C_INTERACTIONS]);
+    a.m.served_users_pct[r] = pct(cnt[0][1], nu);
+    a.m.delayed_users_pct[r] = pct(cnt[0][2], nu);
+    a.m.throttled[r] = int64_t(C[C_THROTTLED]);
+    a.m.aborted_midway[r] = int64_t(C[C_ABORTED]);
+    a.m.wasted_tokens[r] = int64_t(C[C_WASTED]);
+  }
+}
+
+int grid_for(int64_t n, int threads) {
+  int64_t b = (n + threads - 1) / threads;
+  if (b < 1) b = 1;
+  if (b > 65536) b = 65536;
+  return int(b);
+}
+
+}  // namespace
+
+size_t metrics_workspace_bytes(const fs_trace *t) { return mlayout(t).total; }
+
+hipError_t launch_metrics(const fs_trace *t, const int64_t *cost, const fs_outputs *out,
+                          const fs_engine *eng, int32_t delay_steps, fs_metrics *m, void *ws,
+                          hipStream_t s) {
+  MLayout L = mlayout(t);
+  char *w = static_cast<char *>(ws);
+  MArgs a;
+  a.t = dev_trace(t);
+  a.cost = cost;
+  a.status = out->status;
+  a.admit_step = out->admit_step;
+  a.max_gap = out->max_gap;
+  a.tau = eng->step_us;
+  a.D = delay_steps;
+  a.charged = reinterpret_cast<unsigned long long *>(w + L.charged);
+  a.uflags = reinterpret_cast<uint32_t *>(w + L.uflags);
+  a.iflags = reinterpret_cast<uint32_t *>(w + L.iflags);
+  a.counters = reinterpret_cast<unsigned long long *>(w + L.counters);
+  a.m = *m;
+  a.err = out->err;
+  const int64_t RU = int64_t(t->n_replicas) * t->n_users;
+  const int64_t N = a.t.N;
+  hipLaunchKernelGGL(k_m_zero, dim3(grid_for(RU > N ? RU : N, 256)), dim3(256), 0, s, a, RU, N);
+  if (N > 0) {
+    hipLaunchKernelGGL(k_m_records, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_m_interactions, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_m_wasted, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
+  }
+  hipLaunchKernelGGL(k_m_finish, dim3(t->n_replicas), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace fs

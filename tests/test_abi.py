@@ -1,0 +1,82 @@
+"""The C-ABI library loads and exports every entry point include/fairserve.h declares;
+host-only behaviour (argument checks, the Eq. 1 helper) needs no GPU."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2411_15997_amd as fs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", fn)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(fs_[a-z_0-9]+)\s*\(", src))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"fs_cost", "fs_throttle", "fs_schedule_step", "fs_run_trace",
+            "fs_fairness_metrics"} <= names
+    lib = C.CDLL(fs.LIB_PATH)
+    for n in sorted(names):
+        assert hasattr(lib, n), n
+    assert set(fs.EXPORTED) == names
+
+
+def test_status_strings():
+    lib = fs._lib()
+    for code in range(8):
+        assert lib.fs_status_string(code)
+
+
+def test_coef_helper_matches_oracle_and_worked_example():
+    rng = np.random.default_rng(0)
+    for A, J in ((2, 1), (8, 1), (32, 20)):
+        e_in = rng.uniform(1, 5000, (A, J))
+        e_sys = rng.uniform(0, 500, (A, J))
+        e_out = rng.uniform(1, 2000, (A, J))
+        got = fs.fs_coef_from_expectations(e_in, e_sys, e_out, 1024)
+        want = oracle.coef_from_expectations(e_in, e_sys, e_out, 1024)
+        assert (got == want).all()
+    c = fs.fs_coef_from_expectations(np.array([[10.0], [50.0]]), np.zeros((2, 1)), np.zeros((2, 1)))
+    assert c[0, 0, 0] == round(2 ** 26 / 10) and c[1, 0, 0] == round(2 ** 26 / 50)
+    with pytest.raises(fs.FairServeError) as e:
+        fs.fs_coef_from_expectations(np.zeros((1, 1)), np.zeros((1, 1)), np.zeros((1, 1)))
+    assert e.value.code == fs.FS_E_ARG
+
+
+def test_synchronous_argument_errors_need_no_gpu():
+    lib = fs._lib()
+    assert lib.fs_cost(None, None, None, None, None) == fs.FS_E_ARG
+    t = fs.fs_trace(0, 1, 1, None, None, None, None, None, None, None, None, None, None, None)
+    assert lib.fs_throttle_workspace(C.byref(t)) == 0
+    assert lib.fs_state_bytes(C.byref(t)) == 0
+    rep = np.array([0, 4], np.int64)
+    t2 = fs.fs_trace(1, 2, 2, rep.ctypes.data, 16, 16, 16, 16, None, None, None, 16, None, 16)
+    w = fs.fs_weights(0, 0, 16, 0, None)          # zero stages
+    assert lib.fs_cost(C.byref(t2), C.byref(w), 16, 16, None) == fs.FS_E_ARG
+    t3 = fs.fs_trace(1, 2, 2, rep.ctypes.data, 16, 16, 16, 16, 16, None, None, 16, None, 16)
+    w2 = fs.fs_weights(1, 0, 16, 0, None)         # call without head/prev
+    assert lib.fs_cost(C.byref(t3), C.byref(w2), 16, 16, None) == fs.FS_E_ARG
+    eng = fs.fs_engine(0, 10, 10, 0)               # zero step length
+    out = fs.fs_outputs(*([16] * 10))
+    assert lib.fs_schedule_step(256, C.byref(t2), 16, None, C.byref(eng), C.byref(out), -1,
+                                None) == fs.FS_E_ARG
+    t_app = np.array([-1, 3], np.int32)            # negative limit
+    lim = fs.fs_limits(1000, 5, t_app.ctypes.data)
+    assert lib.fs_throttle(C.byref(t2), C.byref(lim), None, 1, 16, None, None, None, 256, 1 << 20,
+                           16, None) == fs.FS_E_ARG
+    t_app2 = np.array([1, 3], np.int32)
+    lim2 = fs.fs_limits(1000, 5, t_app2.ctypes.data)
+    assert lib.fs_throttle(C.byref(t2), C.byref(lim2), None, 1, 16, None, None, None, 256, 0,
+                           16, None) == fs.FS_E_WORKSPACE

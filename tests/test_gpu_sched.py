@@ -1,0 +1,158 @@
+"""Parity of the WSC scheduler (fs_schedule_step / fs_run_trace) with the oracle, bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2411_15997_amd as fs
+from gpu_common import compare_sim, gpu_schedule, say, workload_trace
+from tiny import load_golden, random_trace, trace_from_case
+from paper_2411_15997_amd import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("case", load_golden("hand_traces.json")["cases"], ids=lambda c: c["name"])
+def test_hand_traces(case):
+    tr = trace_from_case(case)
+    g = gpu_schedule(tr, case["cost"], case["reason"], case["tau"], case["C"], case["theta"])
+    for k in ("status", "admit_step", "admit_seq", "counter_after", "counter_on_arrival", "counter"):
+        assert g[k].tolist() == case[k], k
+    assert int(g["steps"][0]) == case["steps"] and int(g["max_gap"][0]) == case["max_gap"]
+
+
+def _batch_of_random(rng, count, n_max, U_max, multi=True):
+    reps = []
+    for _ in range(count):
+        n = int(rng.integers(1, n_max))
+        reps.append(random_trace(rng, n, int(rng.integers(1, U_max)), 2, int(rng.integers(1, 400)),
+                                 multi=multi, max_tok=6))
+    # all replicas share U = max; user ids stay valid
+    return tg.concat(reps)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_many_tiny_replicas_one_launch(seed):
+    """Hundreds of random tiny traces, each a replica of one launch."""
+    rng = np.random.default_rng(50 + seed)
+    tr = _batch_of_random(rng, 400, 40, 5)
+    cost = rng.integers(0, 50, tr.n).astype(np.int64)
+    reason = rng.integers(0, 3, tr.n).astype(np.uint8)
+    step, cap, theta = int(rng.integers(1, 40)), int(rng.integers(1, 12)), int(rng.integers(-1, 8))
+    say("sched tiny", seed, tr.n)
+    o = oracle.simulate(tr, cost, reason, step, cap, theta)
+    g = gpu_schedule(tr, cost, reason, step, cap, theta)
+    compare_sim(g, o)
+
+
+def _run_workload(wl, tr, global_only=False):
+    coef, per_rep = fs.workload_weights(wl, tr)
+    c = oracle.cost(tr, coef, coef_per_replica=per_rep)
+    th = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
+    o = oracle.simulate(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens,
+                        n_threads=8)
+    g = gpu_schedule(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens,
+                     global_only=global_only)
+    return g, o, c, th
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c1_small", {}),
+    ("c2_replicas", dict(replicas=4)),
+    ("c4_sweep", dict(replicas=64)),
+    ("c5_tenant", dict(records=400_003, users=40_000)),
+])
+def test_workloads_schedule(name, kw):
+    wl, tr = workload_trace(name, **kw)
+    say("sched", name, tr.n)
+    g, o, _, _ = _run_workload(wl, tr)
+    compare_sim(g, o)
+
+
+def test_global_memory_path_matches():
+    wl, tr = workload_trace("c2_replicas", replicas=2, records=20000)
+    g, o, _, _ = _run_workload(wl, tr, global_only=True)
+    compare_sim(g, o)
+
+
+def test_onchip_overflow_resumes_in_global_memory():
+    """More backlogged users and queued requests than fit on chip: with no
+    throttling and a tiny capacity the queue grows to thousands of requests."""
+    rng = np.random.default_rng(60)
+    n, U = 6000, 700
+    ts = np.sort(rng.integers(0, 2000, n)).astype(np.int64)
+    user = rng.integers(0, U, n).astype(np.int32)
+    tr = tg.Trace(1, U, 1, np.array([0, n], np.int64), ts, user, np.zeros(n, np.int32), None, None,
+                  None, rng.integers(1, 9, n).astype(np.int32), None, np.zeros(n, np.int32))
+    cost = rng.integers(1, 1000, n).astype(np.int64)
+    o = oracle.simulate(tr, cost, None, 100, 40, 10 ** 9)
+    g = gpu_schedule(tr, cost, None, 100, 40, 10 ** 9)
+    compare_sim(g, o)
+    # and with chained calls (later calls pile up as pending entries)
+    tr2 = random_trace(rng, 5000, 300, 2, 3000, multi=True, max_tok=8)
+    c2 = rng.integers(1, 1000, tr2.n).astype(np.int64)
+    o2 = oracle.simulate(tr2, c2, None, 100, 30, 10 ** 9)
+    g2 = gpu_schedule(tr2, c2, None, 100, 30, 10 ** 9)
+    compare_sim(g2, o2)
+
+
+@pytest.mark.parametrize("chunk", [1, 7, 250])
+def test_stepwise_equals_one_call(chunk):
+    """k calls of fs_schedule_step give the outputs of a single call (checkpoint/resume)."""
+    wl, tr = workload_trace("c2_replicas", replicas=2, records=8000)
+    coef, per_rep = fs.workload_weights(wl, tr)
+    c = oracle.cost(tr, coef, coef_per_replica=per_rep)
+    th = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
+    o = oracle.simulate(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens)
+    g = gpu_schedule(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens, chunks=chunk)
+    compare_sim(g, o)
+
+
+def test_bounded_run_matches_oracle_prefix():
+    wl, tr = workload_trace("c1_small")
+    coef, _ = fs.workload_weights(wl, tr)
+    c = oracle.cost(tr, coef)
+    th = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
+    for s in (1, 13, 100):
+        o = oracle.simulate(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens,
+                            max_steps=s)
+        g = gpu_schedule(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens, n_steps=s)
+        compare_sim(g, o, decided_only=True)
+
+
+def test_counter_overflow_reported():
+    n = 3
+    tr = tg.Trace(1, 1, 1, np.array([0, n], np.int64), np.zeros(n, np.int64), np.zeros(n, np.int32),
+                  np.zeros(n, np.int32), None, None, None, np.ones(n, np.int32), None,
+                  np.zeros(n, np.int32))
+    cost = np.array([(1 << 61), (1 << 61) - 1, 1], np.int64)
+    with pytest.raises(oracle.OracleError) as oe:
+        oracle.simulate(tr, cost, None, 10, 100, 100)
+    with pytest.raises(fs.FairServeError) as ge:
+        gpu_schedule(tr, cost, None, 10, 100, 100)
+    assert ge.value.code == oe.value.code == fs.FS_E_OVERFLOW
+
+
+def test_run_trace_and_metrics_full_path():
+    """fs_run_trace (cost + raw throttle + steps) and fs_fairness_metrics end to end."""
+    wl, tr = workload_trace("c2_replicas", replicas=3, records=30000)
+    dt = fs.DeviceTrace(tr)
+    coef, per_rep = fs.workload_weights(wl, tr)
+    w, keep = fs.make_weights(dt, coef, None, per_rep)
+    lim = fs.make_limits(wl.window_us, wl.t_user, wl.t_app)
+    eng = fs.make_engine(wl.step_us, wl.cap_tokens, wl.overload_tokens)
+    out = fs.Outputs(dt)
+    ws, cost_view, reason_view = fs.run_trace_buffers(dt)
+    fs.fs_run_trace(dt, w, lim, eng, out, ws)
+    m = fs.fs_fairness_metrics(dt, cost_view, out, eng, delay_steps=0).host()
+    c, th, sim, met = oracle.run_workload(wl, tr, n_threads=8)
+    assert (cost_view.cpu().numpy() == c).all()
+    assert (reason_view.cpu().numpy() == th.reason).all()
+    h = out.host()
+    compare_sim({k: (v[:tr.n] if v is not None and v.shape[0] >= tr.n and k not in ("counter",) else v)
+                 for k, v in h.items()}, sim)
+    for k in ("jain", "max_gap_tokens", "svc_req_pct", "svc_int_pct", "served_users_pct",
+              "delayed_users_pct"):
+        np.testing.assert_allclose(m[k], getattr(met, k), rtol=1e-9, atol=0, err_msg=k)
+    for k in ("throttled", "aborted_midway", "wasted_tokens"):
+        assert (m[k] == getattr(met, k)).all(), k

@@ -1,0 +1,101 @@
+"""Parity of fs_throttle (OIT window counts and limit checks) with the oracle, bit-exact."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_common import bits_of, gpu_throttle, say, workload_trace
+from tiny import load_golden, random_trace
+from paper_2411_15997_amd import tracegen as tg
+import paper_2411_15997_amd as fs
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(tr, W, tu, ta, overloaded=None, raw=True, counts=True):
+    g = gpu_throttle(tr, W, tu, ta, overloaded, raw, counts)
+    o = oracle.throttle(tr, W, tu, ta, overloaded=overloaded, raw=raw, counts=counts)
+    bad = np.nonzero(g["reason"] != o.reason)[0]
+    assert bad.size == 0, f"reason mismatch at {bad[:10]}: gpu {g['reason'][bad[:10]]} oracle {o.reason[bad[:10]]}"
+    assert (bits_of(g["bitmap"], tr.n) == bits_of(o.bitmap, tr.n)).all()
+    if counts:
+        assert (g["cnt_user"] == o.cnt_user).all() and (g["cnt_app"] == o.cnt_app).all()
+    return g, o
+
+
+def test_golden_window():
+    gd = load_golden("window_counts.json")
+    n = len(gd["ts"])
+    tr = tg.Trace(1, gd["U"], gd["A"], np.array([0, n], np.int64), np.asarray(gd["ts"], np.int64),
+                  np.asarray(gd["user"], np.int32), np.asarray(gd["app"], np.int32), None, None,
+                  None, None, None, None)
+    g = gpu_throttle(tr, gd["W"], gd["t_user"], gd["t_app"])
+    assert g["reason"].tolist() == gd["raw"]
+    assert g["cnt_user"].tolist() == gd["cnt_user"] and g["cnt_app"].tolist() == gd["cnt_app"]
+    g2 = gpu_throttle(tr, gd["W"], gd["t_user"], gd["t_app"], overloaded=gd["overloaded"], raw=False)
+    assert g2["reason"].tolist() == gd["gated"]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_multi_replica(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 9000))
+    tr = random_trace(rng, n, int(rng.integers(1, 40)), int(rng.integers(1, 6)),
+                      int(rng.integers(1, 20000)), multi=True, n_replicas=int(rng.integers(1, 5)))
+    A = tr.n_apps
+    W = int(rng.integers(1, 5000))
+    tu = int(rng.integers(0, 30)) if seed % 2 else 2 ** 31 - 1
+    ta = rng.integers(0, 20, size=A).tolist()
+    say("throttle random", seed, tr.n)
+    _check(tr, W, tu, ta)
+    ov = rng.integers(0, 2, size=tr.n).astype(np.uint8)
+    _check(tr, W, tu, ta, overloaded=ov, raw=False)
+    _check(tr, W, tu, ta, overloaded=None, raw=False, counts=False)
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c1_small", {}),
+    ("c2_replicas", dict(replicas=4, records=30001)),
+    ("c3_throttle", dict(records=1_000_003)),
+    ("c4_sweep", dict(replicas=64)),
+    ("c5_tenant", dict(records=300_007, users=30_000)),
+])
+def test_workloads(name, kw):
+    wl, tr = workload_trace(name, **kw)
+    say("throttle", name, tr.n)
+    _check(tr, wl.window_us, wl.t_user, wl.t_app)
+
+
+def test_tiny_and_ragged_sizes():
+    rng = np.random.default_rng(11)
+    for n in (1, 2, 31, 32, 33, 63, 64, 65, 4095, 4096, 4097):
+        tr = random_trace(rng, n, 3, 2, 50, multi=True)
+        _check(tr, 10, 2, [1, 3])
+        _check(tr, 10, 2, [1, 3], raw=False)
+
+
+def test_errors_match_oracle():
+    rng = np.random.default_rng(12)
+    tr = random_trace(rng, 500, 5, 2, 1000, multi=False)
+    bad = tg.Trace(**{**tr.__dict__, "ts_us": tr.ts_us.copy()})
+    bad.ts_us[100], bad.ts_us[101] = bad.ts_us[101] + 5, bad.ts_us[100]
+    with pytest.raises(oracle.OracleError) as oe:
+        oracle.throttle(bad, 10, 1, [1, 1])
+    with pytest.raises(fs.FairServeError) as ge:
+        gpu_throttle(bad, 10, 1, [1, 1])
+    assert ge.value.code == oe.value.code == fs.FS_E_ORDER
+    bad2 = tg.Trace(**{**tr.__dict__, "app": tr.app.copy()})
+    bad2.app[7] = 2
+    with pytest.raises(fs.FairServeError) as ge:
+        gpu_throttle(bad2, 10, 1, [1, 1])
+    assert ge.value.code == fs.FS_E_RANGE
+
+
+def test_full_throttle_stream():
+    """The 50M-request throttle-only stream at full size: bitmap bit-exact."""
+    wl, tr = workload_trace("c3_throttle")
+    say("throttle full", tr.n)
+    g = gpu_throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
+    o = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
+    assert (g["reason"] == o.reason).all()
+    nw = (tr.n + 31) // 32
+    assert (g["bitmap"][:nw] == o.bitmap[:nw]).all()

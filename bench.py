@@ -1,0 +1,213 @@
+"""Benchmark of the FairServe policy hot path on one MI355X.
+
+One step = the whole path over one synthetic workload resident in HBM:
+fs_cost -> fs_throttle (raw) -> fs_state_init -> fs_schedule_step (until drained)
+-> fs_fairness_metrics, i.e. the sequence fs_run_trace runs plus the metrics.
+Prints one JSON line (metric, value = scheduler decisions per second of the whole
+step, per-stage times from HIP events, the roofline of the dominant kernel, and the
+CPU oracle timed on this host on the same workload).
+"""
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "scheduler decisions/sec + throttle evals/sec on 1 MI355X; % of HBM roofline"
+HBM_PEAK_GBS = 8000.0
+# Algorithmic bytes per record of each stage (the minimum the method must move):
+#   cost      app 4 + lengths 8 (+ sys 4) + cost write 8                       = 20 (24)
+#   throttle  ts 8 + user 4 + app 4 + interaction link 4 + 1/8 bitmap bit       = 20.125
+#   scheduler ts 8 + user 4 + link 4 + tokens 4 + cost 8 + reason 1/8 + status 1
+#             + admit_step 4 + admit_seq 4                                      = 37.125
+#   metrics   status 1 + admit_step 4 + ts 8 + user 4 + cost 8                  = 25
+ALGO_BYTES = {"cost": 20.0, "throttle": 20.125, "schedule": 37.125, "metrics": 25.0}
+SCHED_SRC = os.path.join(ROOT, "paper_2411_15997_amd", "csrc", "fs_sched.hip")
+
+# HBM traffic of the dominant kernel measured with rocprofv3 --pmc (FETCH_SIZE and
+# WRITE_SIZE), scaled by the copy-kernel calibration; keyed by workload and the
+# sha256 of the kernel source it was measured on (stale entries are ignored).
+MEASURED_TRAFFIC = {}
+
+
+def src_hash(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c2_replicas")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--stage-only", default="", help="time only this stage (profiling runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the policy's replicas are independent and this "
+              f"build measures one GPU's share (asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2411_15997_amd as fs
+    from paper_2411_15997_amd import tracegen as tg
+
+    wl = tg.WORKLOADS[args.workload]
+    t0 = time.time()
+    tr = tg.generate(wl)
+    gen_s = time.time() - t0
+    print(f"[bench] generated {wl.name}: {tr.n} requests in {gen_s:.1f}s", file=sys.stderr, flush=True)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dt = fs.DeviceTrace(tr, device=dev)
+    coef, per_rep = fs.workload_weights(wl, tr)
+    w, keep = fs.make_weights(dt, coef, None, per_rep)
+    lim = fs.make_limits(wl.window_us, wl.t_user, wl.t_app)
+    theta = wl.overload_tokens if wl.overload_tokens is not None else -1
+    eng = fs.make_engine(wl.step_us, wl.cap_tokens, theta)
+    out = fs.Outputs(dt, parity=False)
+    N = tr.n
+    cost = torch.empty(max(N, 1), dtype=torch.int64, device=dev)
+    err = fs.err_word(dev)
+    tws = torch.empty(max(fs.fs_throttle_workspace(dt), 1), dtype=torch.uint8, device=dev)
+    state = torch.empty(fs.fs_state_bytes(dt), dtype=torch.uint8, device=dev)
+    mws = torch.empty(max(fs.fs_metrics_workspace(dt), 1), dtype=torch.uint8, device=dev)
+    metrics = fs.Metrics(dt)
+    throttle_only = wl.throttle_only
+
+    stages = ["throttle"] if throttle_only else ["cost", "throttle", "schedule", "metrics"]
+    if args.stage_only:
+        stages = [args.stage_only]
+
+    def step(evs):
+        i = 0
+        if "cost" in stages:
+            evs[i].record(); i += 1
+            fs.fs_cost(dt, w, cost, err, check=False)
+        if "throttle" in stages:
+            evs[i].record(); i += 1
+            fs.fs_throttle(dt, lim, raw=not throttle_only, ws=tws, err=err, check=False,
+                           bitmap=bitmap, reason=reason_buf)
+        if "schedule" in stages:
+            evs[i].record(); i += 1
+            fs.fs_state_init(dt, state)
+            fs.fs_schedule_step(dt, state, cost, reason_buf, eng, out, -1, check=False)
+        if "metrics" in stages:
+            evs[i].record(); i += 1
+            fs.fs_fairness_metrics(dt, cost, out, eng, 0, metrics, mws, check=False)
+        evs[i].record()
+
+    # the throttle's raw reasons feed the scheduler (same buffers every step)
+    bitmap = torch.empty((N + 31) // 32 + 1, dtype=torch.int32, device=dev)
+    reason_buf = None if throttle_only else torch.empty(max(N, 1), dtype=torch.uint8, device=dev)
+    if args.stage_only in ("schedule", "metrics"):
+        fs.fs_cost(dt, w, cost, err)
+        fs.fs_throttle(dt, lim, raw=True, ws=tws, err=err, bitmap=bitmap, reason=reason_buf)
+        if args.stage_only == "metrics":
+            fs.fs_state_init(dt, state)
+            fs.fs_schedule_step(dt, state, cost, reason_buf, eng, out, -1)
+
+    ne = len(stages) + 1
+    for _ in range(args.warmup):
+        step([torch.cuda.Event(enable_timing=True) for _ in range(ne)])
+    torch.cuda.synchronize()
+    if "schedule" in stages or "metrics" in stages:
+        fs.sync_check(out.err, "warmup")
+    runs = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(ne)]
+        step(evs)
+        runs.append(evs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    if "schedule" in stages or "metrics" in stages:
+        fs.sync_check(out.err, "timed steps")
+    stage_ms = {s: float(np.mean([r[i].elapsed_time(r[i + 1]) for r in runs]))
+                for i, s in enumerate(stages)}
+    ms_per_step = wall * 1000.0 / args.steps
+
+    R = tr.n_replicas
+    decisions = int(out.decisions.cpu().numpy().sum()) if "schedule" in stages else 0
+    result = {
+        "metric": METRIC,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int64", "data": "synthetic",
+        "config": {"workload": wl.name, "replicas": R, "users": tr.n_users, "apps": tr.n_apps,
+                   "requests": N, "trace_sha256": tr.sha256()[:16],
+                   "step_us": wl.step_us, "cap_tokens": wl.cap_tokens, "window_us": wl.window_us},
+        "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+    }
+    if "schedule" in stages:
+        result["value"] = decisions / (ms_per_step / 1000.0)
+        result["unit"] = "decisions/s"
+        result["decisions"] = decisions
+    else:
+        result["value"] = N / (stage_ms["throttle"] / 1000.0)
+        result["unit"] = "throttle evals/s"
+    if "throttle" in stage_ms:
+        result["throttle_evals_per_s"] = N / (stage_ms["throttle"] / 1000.0)
+    result["requests_per_s"] = N / (ms_per_step / 1000.0)
+
+    # dominant stage and its roofline (algorithmic bytes / measured duration)
+    dom = max(stage_ms, key=stage_ms.get)
+    algo = ALGO_BYTES[dom] * N
+    achieved = algo / (stage_ms[dom] / 1000.0) / 1e9
+    tkey = (wl.name, dom, src_hash(SCHED_SRC) if dom == "schedule" else None)
+    traffic = MEASURED_TRAFFIC.get(tkey)
+    result["roofline"] = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2),
+                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(achieved / HBM_PEAK_GBS, 6),
+                          "algorithmic_bytes": int(algo), "traffic": traffic}
+    all_stage_gbs = {s: round(ALGO_BYTES[s] * N / (stage_ms[s] / 1000.0) / 1e9, 2) for s in stage_ms}
+    result["stage_gbs"] = all_stage_gbs
+
+    if not args.no_cpu_baseline and not args.stage_only:
+        result["cpu_baseline"] = cpu_baseline(wl, tr, args.cpu_threads, throttle_only)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(wl, tr, threads, throttle_only):
+    """The CPU oracle (as it stands) on this host, same workload, whole path."""
+    import numpy as np
+
+    import oracle
+
+    ncpu = os.cpu_count() or 1
+    th = threads or min(16, ncpu, tr.n_replicas) if not throttle_only else 1
+    t0 = time.perf_counter()
+    if throttle_only:
+        # bounded sample: the first 5M requests of the stream
+        from paper_2411_15997_amd.tracegen import Trace
+        n = min(tr.n, 5_000_000)
+        sub = Trace(1, tr.n_users, tr.n_apps, np.array([0, n], np.int64), tr.ts_us[:n],
+                    tr.user[:n], tr.app[:n], tr.call[:n], tr.head[:n], tr.prev[:n],
+                    None, None, None)
+        oracle.throttle(sub, wl.window_us, wl.t_user, wl.t_app, raw=False, counts=False)
+        dt = time.perf_counter() - t0
+        return {"value": n / dt, "unit": "throttle evals/s", "cores": 1, "kind": "oracle",
+                "sample": f"first {n} requests of {wl.name}", "seconds": round(dt, 3),
+                "host": platform.processor() or platform.machine()}
+    c, thr, sim, met = oracle.run_workload(wl, tr, n_threads=th)
+    dt = time.perf_counter() - t0
+    dec = int(sim.decisions.sum())
+    return {"value": dec / dt, "unit": "decisions/s", "cores": th, "kind": "oracle",
+            "sample": f"whole {wl.name} workload ({tr.n} requests, {tr.n_replicas} replicas), "
+                      f"cost+throttle+schedule+metrics",
+            "seconds": round(dt, 3), "host_cpus": ncpu}
+
+
+if __name__ == "__main__":
+    main()

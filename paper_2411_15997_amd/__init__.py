@@ -225,12 +225,14 @@ class ThrottleOut:
 
 
 def fs_throttle(dt: DeviceTrace, limits, overloaded=None, raw=True, want_reason=True,
-                want_counts=False, ws=None, err=None, check=True):
+                want_counts=False, ws=None, err=None, check=True, bitmap=None, reason=None):
     torch = _torch()
     lim, keep = limits
     n = dt.n
-    bitmap = _empty(((n + 31) // 32 + 1,), torch.int32, dt.device)
-    reason = _empty((max(n, 1),), torch.uint8, dt.device) if want_reason else None
+    if bitmap is None:
+        bitmap = _empty(((n + 31) // 32 + 1,), torch.int32, dt.device)
+    if reason is None and want_reason:
+        reason = _empty((max(n, 1),), torch.uint8, dt.device)
     cu = _empty((max(n, 1),), torch.int32, dt.device) if want_counts else None
     ca = _empty((max(n, 1),), torch.int32, dt.device) if want_counts else None
     nb = fs_throttle_workspace(dt)

@@ -27,4 +27,9 @@ size_t metrics_workspace_bytes(const fs_trace *t);
 
 hipError_t launch_zero_i32(int32_t *p, hipStream_t stream);
 
+// Device-wide exclusive prefix sum of n uint32 values in place; `part` needs
+// scan_partials_bytes(n) bytes of scratch.
+size_t scan_partials_bytes(int64_t n);
+hipError_t exclusive_scan(uint32_t *data, int64_t n, uint32_t *part, hipStream_t stream);
+
 }  // namespace fs

@@ -62,47 +62,87 @@ __global__ void k_m_zero(MArgs a, int64_t RU, int64_t N) {
 
 __device__ inline bool first_call(const DevTrace &t, int64_t g) { return !t.call || t.call[g] == 0; }
 
-// wave-aggregated add to a per-replica counter (all lanes of the wave may differ in r)
-__device__ inline void count_add(unsigned long long *p, unsigned long long v) {
-  if (v) atomicAdd(p, v);
+__device__ inline unsigned long long wave_sum(unsigned long long v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    unsigned long long o = (unsigned long long)__shfl_xor((long long)v, m, 64);
+    v += o;
+  }
+  return v;
+}
+__device__ inline uint32_t wave_or(uint32_t v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v |= uint32_t(__shfl_xor(int(v), m, 64));
+  return v;
+}
+
+// Per-key aggregation within a wave before touching global memory: heavy users
+// repeat many times in a wave, and all lanes usually share one replica.
+// For each distinct key among the active lanes: one atomic add (and one atomic or).
+__device__ inline void wave_add_by_key(bool active, int64_t key, unsigned long long v,
+                                       unsigned long long *sum_base, uint32_t f,
+                                       uint32_t *or_base) {
+  const int lane = threadIdx.x & 63;
+  uint64_t pending = __ballot(active);
+  while (pending) {
+    const int leader = __ffsll((long long)pending) - 1;
+    const int64_t kl = __shfl(key, leader, 64);
+    const bool mine = active && key == kl;
+    const unsigned long long total = wave_sum(mine ? v : 0ull);
+    const uint32_t flags = or_base ? wave_or(mine ? f : 0u) : 0u;
+    if (lane == leader) {
+      if (total) atomicAdd(sum_base + kl, total);
+      if (or_base && flags) atomicOr(or_base + kl, flags);
+    }
+    pending &= ~__ballot(mine);
+  }
 }
 
 // Pass 1: per record -- validity, user flags, charged service, interaction flags.
 __global__ void __launch_bounds__(256) k_m_records(MArgs a) {
   const DevTrace &t = a.t;
   int32_t code = 0;
-  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
-       g += int64_t(gridDim.x) * blockDim.x) {
-    int32_t r = replica_of(t.rep_off, t.R, g);
-    int64_t base = t.rep_off[r], i = g - base, n = t.rep_off[r + 1] - base;
-    int32_t k = t.user[g];
-    if (k < 0 || k >= t.U || t.app[g] < 0 || t.app[g] >= t.A) {
-      code = max(code, int32_t(FS_E_RANGE));
-      continue;
-    }
-    int64_t h = i;
-    if (!first_call(t, g)) {
-      h = t.head[g];
-      if (h < 0 || h >= i) {
+  // grid-stride over whole waves so that every lane takes part in the wave reductions
+  for (int64_t base0 = blockIdx.x * int64_t(blockDim.x); base0 < t.N;
+       base0 += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t g = base0 + threadIdx.x;
+    bool ok = g < t.N;
+    int32_t r = 0, k = 0;
+    int64_t base = 0, i = 0, h = 0;
+    if (ok) {
+      r = replica_of(t.rep_off, t.R, g);
+      base = t.rep_off[r];
+      i = g - base;
+      k = t.user[g];
+      if (k < 0 || k >= t.U || t.app[g] < 0 || t.app[g] >= t.A) {
         code = max(code, int32_t(FS_E_RANGE));
-        continue;
+        ok = false;
       }
     }
-    int64_t uk = int64_t(r) * t.U + k;
-    int8_t st = a.status[g];
-    uint32_t uf = U_HAS;
-    if (st == 0) {
-      atomicAdd(a.charged + uk, (unsigned long long)a.cost[g]);
-      atomicOr(a.iflags + base + h, I_SERVED);
-      if (int64_t(a.admit_step[g]) - t.ts[g] / a.tau > a.D) uf |= U_DELAYED;
-      count_add(a.counters + r * C_NUM + C_ADMITTED, 1);
-    } else {
-      atomicOr(a.iflags + base + h, I_UNSERVED);
-      if (st > 0) count_add(a.counters + r * C_NUM + C_THROTTLED, 1);
+    if (ok) {
+      h = i;
+      if (!first_call(t, g)) {
+        h = t.head[g];
+        if (h < 0 || h >= i) {
+          code = max(code, int32_t(FS_E_RANGE));
+          ok = false;
+        }
+      }
     }
-    if (first_call(t, g)) count_add(a.counters + r * C_NUM + C_INTERACTIONS, 1);
-    atomicOr(a.uflags + uk, uf);
-    (void)n;
+    const int8_t st = ok ? a.status[g] : int8_t(-1);
+    const bool served = ok && st == 0;
+    uint32_t uf = U_HAS;
+    if (served && int64_t(a.admit_step[g]) - t.ts[g] / a.tau > a.D) uf |= U_DELAYED;
+    if (ok) atomicOr(a.iflags + base + h, served ? I_SERVED : I_UNSERVED);
+    const int64_t uk = int64_t(r) * t.U + k;
+    wave_add_by_key(ok, uk, served ? (unsigned long long)a.cost[g] : 0ull, a.charged, uf,
+                    a.uflags);
+    wave_add_by_key(ok, int64_t(r) * C_NUM + C_ADMITTED, served ? 1ull : 0ull, a.counters, 0,
+                    nullptr);
+    wave_add_by_key(ok, int64_t(r) * C_NUM + C_THROTTLED, (ok && st > 0) ? 1ull : 0ull,
+                    a.counters, 0, nullptr);
+    wave_add_by_key(ok, int64_t(r) * C_NUM + C_INTERACTIONS,
+                    (ok && first_call(t, g)) ? 1ull : 0ull, a.counters, 0, nullptr);
   }
   if (code) raise_err(a.err, code);
 }
@@ -110,34 +150,43 @@ __global__ void __launch_bounds__(256) k_m_records(MArgs a) {
 // Pass 2: per interaction (first call) -- fully served, aborted midway.
 __global__ void __launch_bounds__(256) k_m_interactions(MArgs a) {
   const DevTrace &t = a.t;
-  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
-       g += int64_t(gridDim.x) * blockDim.x) {
-    if (!first_call(t, g)) continue;
-    int32_t k = t.user[g];
-    if (k < 0 || k >= t.U) continue;
-    int32_t r = replica_of(t.rep_off, t.R, g);
-    uint32_t f = a.iflags[g];
-    if (!(f & I_UNSERVED)) {
-      count_add(a.counters + r * C_NUM + C_FULL, 1);
-      atomicOr(a.uflags + int64_t(r) * t.U + k, U_FULL);
-    }
-    if ((f & I_SERVED) && (f & I_UNSERVED)) count_add(a.counters + r * C_NUM + C_ABORTED, 1);
+  for (int64_t base0 = blockIdx.x * int64_t(blockDim.x); base0 < t.N;
+       base0 += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t g = base0 + threadIdx.x;
+    bool ok = g < t.N && first_call(t, g);
+    int32_t k = ok ? t.user[g] : 0;
+    ok = ok && k >= 0 && k < t.U;
+    const int32_t r = ok ? replica_of(t.rep_off, t.R, g) : 0;
+    const uint32_t f = ok ? a.iflags[g] : 0u;
+    const bool full = ok && !(f & I_UNSERVED);
+    const bool aborted = ok && (f & I_SERVED) && (f & I_UNSERVED);
+    if (full) atomicOr(a.uflags + int64_t(r) * t.U + k, U_FULL);
+    wave_add_by_key(ok, int64_t(r) * C_NUM + C_FULL, full ? 1ull : 0ull, a.counters, 0, nullptr);
+    wave_add_by_key(ok, int64_t(r) * C_NUM + C_ABORTED, aborted ? 1ull : 0ull, a.counters, 0,
+                    nullptr);
   }
 }
 
 // Pass 3: per admitted record of an aborted interaction -- wasted tokens.
 __global__ void __launch_bounds__(256) k_m_wasted(MArgs a) {
   const DevTrace &t = a.t;
-  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
-       g += int64_t(gridDim.x) * blockDim.x) {
-    if (a.status[g] != 0) continue;
-    int32_t r = replica_of(t.rep_off, t.R, g);
-    int64_t base = t.rep_off[r], i = g - base;
-    int64_t h = first_call(t, g) ? i : t.head[g];
-    if (h < 0 || h > i) continue;
-    uint32_t f = a.iflags[base + h];
-    if ((f & I_SERVED) && (f & I_UNSERVED))
-      count_add(a.counters + r * C_NUM + C_WASTED, (unsigned long long)tokens_of(t, g));
+  for (int64_t base0 = blockIdx.x * int64_t(blockDim.x); base0 < t.N;
+       base0 += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t g = base0 + threadIdx.x;
+    bool ok = g < t.N && a.status[g] == 0;
+    int32_t r = 0;
+    unsigned long long w = 0;
+    if (ok) {
+      r = replica_of(t.rep_off, t.R, g);
+      const int64_t base = t.rep_off[r], i = g - base;
+      const int64_t h = first_call(t, g) ? i : t.head[g];
+      ok = h >= 0 && h <= i;
+      if (ok) {
+        const uint32_t f = a.iflags[base + h];
+        if ((f & I_SERVED) && (f & I_UNSERVED)) w = (unsigned long long)tokens_of(t, g);
+      }
+    }
+    wave_add_by_key(ok, int64_t(r) * C_NUM + C_WASTED, w, a.counters, 0, nullptr);
   }
 }
 

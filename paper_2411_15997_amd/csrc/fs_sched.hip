@@ -3,38 +3,44 @@
 //
 // Per replica the state is the paper's: service counters u_i, the waiting queue Q
 // (a dictionary from user to queued requests), the last user to leave Q, and the
-// overload measure (tokens queued).  The wave keeps the hot part on chip:
-//   X table   compact slots [0, nX) of users with something queued: user id, a key
+// overload measure (tokens queued).  The wave keeps what each decision touches on
+// chip and never waits on HBM inside a decision in the common case:
+//   X table   slots [0, nX) of users with something queued: user id, key
 //             (tier << 62 | u) whose tier is 0 while the user has a ready later call of
-//             an incomplete interaction, its first-call FIFO (pool entries) and counts.
-//             The argmin over (key, user id) is a lane-parallel scan plus a wave
-//             reduction: tier 0 first, then least counter, then lowest user id.
-//   pool      queued requests (record, cost, tokens, next call, FIFO link).
-//   CL        queued later calls: ready (previous call admitted) or pending.
-//   window    the next 64 records in registers (one per lane) with the user's slot,
-//             idle counter, "previous call admitted" and "first call throttled" flags
-//             prefetched; every state change patches the lanes it affects, so the
-//             arrival loop never waits on memory.
-// Counters of idle users live in LDS when they fit, else in the state buffer.  If
-// an on-chip capacity overflows, the wave saves its state and the same code resumes
-// with every structure in global memory (second launch, same stream).
+//             an incomplete interaction, a FIFO of queued first calls and a list of
+//             ready later calls.  The argmin over (key, user id) is one LDS read per
+//             lane plus a DPP wave reduction.
+//   pool      LDS entries of queued requests: record, cost, tokens, next call, link,
+//             and the next call's data when that call has already arrived, so serving
+//             a request releases its successor without touching HBM.
+//   HBM FIFO  first calls beyond the pool go to a per-user segment in the state buffer
+//             (sized by the user's number of first calls) and are refilled into the
+//             pool 64 at a time with one coalesced load.
+//   pending   later calls waiting for their previous call are not stored: their data
+//             is read from the inputs when the previous call enters the pool.
+//   window    the next 64 records, one per lane, with their step, the user's slot and
+//             idle counter, "previous call admitted" and "first call throttled"
+//             prefetched; every state change patches the lanes it affects.
+// Counters of idle users live in LDS when they fit, else in the state buffer.  If an
+// on-chip capacity overflows the wave saves its state and the same code resumes with
+// every structure in global memory (a second launch on the same stream).
 #include "fs_device.h"
 #include "fs_launch.h"
 
 namespace fs {
 namespace {
 
-constexpr uint64_t kMagic = 0x31535652'49414646ull;  // "FFAIRVS1"
-constexpr int32_t kVersion = 1;
+constexpr uint64_t kMagic = 0x32535652'49414646ull;
+constexpr int32_t kVersion = 2;
 constexpr uint64_t kTierShift = 62;
 constexpr uint64_t kValMask = (uint64_t(1) << 62) - 1;
 constexpr uint64_t kEmptyKey = ~uint64_t(0);
-constexpr int kUsersLdsMax = 1024;   // per-user arrays on chip up to this many users
-constexpr int kXCap = 128;            // on-chip backlogged-user slots
-constexpr int kCLCap = 256;           // on-chip queued later calls
+constexpr int kUsersLdsMax = 1024;  // per-user arrays on chip up to this many users
+constexpr int kXCap = 128;           // on-chip backlogged-user slots (two per lane)
+constexpr int kReserve = 32;         // pool entries first calls leave for later calls
 
 struct RepState {
-  int64_t s, nxt, debt, backlog, seq, gap, last_exit_u, nq, s_end;
+  int64_t s, nxt, debt, backlog, seq, gap, last_exit_u, low, s_end;
   int32_t last_exit, done, overflow, pad;
   int64_t pad2[5];
 };
@@ -50,42 +56,56 @@ struct Header {
 size_t up(size_t x) { return (x + 255) / 256 * 256; }
 
 struct StateLayout {
-  size_t hdr, reps, u_all, xslot_all, fate, succ, qsave;
-  // global-mode scratch (capacity n_r per replica, offset rep_off[r])
-  size_t xkey, xuser, xq, xfh, xft, xrdy, p_cost, p_rec, p_tok, p_succ, p_next, p_free, cl_rec,
-      cl_prev, cl_user, cl_e, cl_rdy;
+  size_t hdr, reps, u_all, xslot_all, fate, succ, seg_start, seg_part, seg_rec, seg_tok, seg_cost,
+      seg_succ;
+  // global-memory scheduler structures (n_r + 1 entries per replica, at rep_off[r] + r)
+  size_t xkey, xuser, xq, xfh, xft, xhh, xht, xsb, xrh, xrdy;
+  size_t e_rec, e_tok, e_cost, e_succ, e_next, e_sv, e_scost, e_stok, e_ssucc, e_free;
   size_t total;
 };
 
 StateLayout state_layout(int32_t R, int32_t U, int64_t N) {
   StateLayout L;
   size_t n = size_t(N > 0 ? N : 1), ru = size_t(R) * size_t(U);
-  size_t nr = size_t(N) + size_t(R) + 1;  // global-mode scratch: n_r + 1 entries per replica
+  size_t nr = size_t(N) + size_t(R) + 1;
   size_t o = 0;
-  L.hdr = o; o += up(sizeof(Header));
-  L.reps = o; o += up(sizeof(RepState) * size_t(R));
-  L.u_all = o; o += up(ru * 8);
-  L.xslot_all = o; o += up(ru * 4);
-  L.fate = o; o += up(n);
-  L.succ = o; o += up(n * 4);
-  L.qsave = o; o += up(n * 4);
-  L.xkey = o; o += up(nr * 8);
-  L.xuser = o; o += up(nr * 4);
-  L.xq = o; o += up(nr * 4);
-  L.xfh = o; o += up(nr * 4);
-  L.xft = o; o += up(nr * 4);
-  L.xrdy = o; o += up(nr * 4);
-  L.p_cost = o; o += up(nr * 8);
-  L.p_rec = o; o += up(nr * 4);
-  L.p_tok = o; o += up(nr * 4);
-  L.p_succ = o; o += up(nr * 4);
-  L.p_next = o; o += up(nr * 4);
-  L.p_free = o; o += up(nr * 4);
-  L.cl_rec = o; o += up(nr * 4);
-  L.cl_prev = o; o += up(nr * 4);
-  L.cl_user = o; o += up(nr * 4);
-  L.cl_e = o; o += up(nr * 4);
-  L.cl_rdy = o; o += up(nr * 4);
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o += up(bytes);
+    return at;
+  };
+  L.hdr = take(sizeof(Header));
+  L.reps = take(sizeof(RepState) * size_t(R));
+  L.u_all = take(ru * 8);
+  L.xslot_all = take(ru * 4);
+  L.fate = take(n);
+  L.succ = take(n * 4);
+  L.seg_start = take((ru + 1) * 4);
+  L.seg_part = take(scan_partials_bytes(int64_t(ru + 1)));
+  L.seg_rec = take(n * 4);
+  L.seg_tok = take(n * 4);
+  L.seg_cost = take(n * 8);
+  L.seg_succ = take(n * 4);
+  L.xkey = take(nr * 8);
+  L.xuser = take(nr * 4);
+  L.xq = take(nr * 4);
+  L.xfh = take(nr * 4);
+  L.xft = take(nr * 4);
+  L.xhh = take(nr * 4);
+  L.xht = take(nr * 4);
+  L.xsb = take(nr * 4);
+  L.xrh = take(nr * 4);
+  L.xrdy = take(nr * 4);
+  L.e_rec = take(nr * 4);
+  L.e_tok = take(nr * 4);
+  L.e_cost = take(nr * 8);
+  L.e_succ = take(nr * 4);
+  L.e_next = take(nr * 4);
+  L.e_sv = take(nr * 4);
+  L.e_scost = take(nr * 8);
+  L.e_stok = take(nr * 4);
+  L.e_ssucc = take(nr * 4);
+  L.e_free = take(nr * 4);
   L.total = o;
   return L;
 }
@@ -97,18 +117,16 @@ struct SchedArgs {
   int64_t tau, cap, theta;
   int64_t n_steps;
   bool global_only;
-  // outputs
   int8_t *status;
   int32_t *admit_step, *admit_seq;
   int64_t *counter_after, *counter_on_arrival, *counter, *steps, *decisions, *max_gap;
   int32_t *err;
-  // state
   char *state;
   StateLayout L;
-  int32_t pcap;   // on-chip pool entries
+  int32_t pcap;  // on-chip pool entries
 };
 
-// -------------------------------------------------------------- small wave helpers
+// -------------------------------------------------------------- wave helpers
 
 __device__ inline int32_t rdl(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
 __device__ inline int64_t rdl64(int64_t v, int l) {
@@ -119,18 +137,14 @@ __device__ inline int64_t rdl64(int64_t v, int l) {
 __device__ inline int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ inline int64_t uni64(int64_t v) { return rdl64(v, 0); }
 
-__device__ inline uint64_t shfl_xor64(uint64_t v, int m) {
-  uint32_t lo = __shfl_xor(uint32_t(v), m, 64);
-  uint32_t hi = __shfl_xor(uint32_t(v >> 32), m, 64);
-  return (uint64_t(hi) << 32) | lo;
-}
-
+// Every structure of a replica is read and written by that replica's single wave,
+// so work-group scope is enough for a load to see the wave's own earlier stores.
 template <class T>
-__device__ inline T ld_fresh(const T *p) {  // global load that sees this wave's own stores
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ inline T ld_fresh(const T *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
+__device__ inline void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup"); }
 
-// Reads of the scheduler structures: plain for LDS, coherent for global memory.
 template <bool G, class T>
 __device__ inline T RD(const T *p) {
   if constexpr (G)
@@ -139,26 +153,67 @@ __device__ inline T RD(const T *p) {
     return *p;
 }
 
+// DPP moves for a full-wave reduction (result in lane 63): swap within pairs, swap
+// pairs, mirror within 8, mirror within 16, then broadcast row ends to later rows.
+template <int CTRL, int ROWS>
+__device__ inline uint32_t dpp(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(int(v), int(v), CTRL, ROWS, 0xF, false));
+}
+
+template <int CTRL, int ROWS>
+__device__ inline void argmin_step(uint64_t &k, uint32_t &us, uint32_t &x) {
+  const uint32_t lo = dpp<CTRL, ROWS>(uint32_t(k)), hi = dpp<CTRL, ROWS>(uint32_t(k >> 32));
+  const uint32_t ous = dpp<CTRL, ROWS>(us), ox = dpp<CTRL, ROWS>(x);
+  const uint64_t ok = (uint64_t(hi) << 32) | lo;
+  const bool take = ok < k || (ok == k && ous < us);
+  k = take ? ok : k;
+  us = take ? ous : us;
+  x = take ? ox : x;
+}
+
+__device__ inline void wave_argmin(uint64_t &k, uint32_t &us, uint32_t &x) {
+  argmin_step<0xB1, 0xF>(k, us, x);
+  argmin_step<0x4E, 0xF>(k, us, x);
+  argmin_step<0x141, 0xF>(k, us, x);
+  argmin_step<0x140, 0xF>(k, us, x);
+  argmin_step<0x142, 0xA>(k, us, x);
+  argmin_step<0x143, 0xC>(k, us, x);
+}
+
+template <int CTRL, int ROWS>
+__device__ inline void minmax_step(uint64_t &lo, uint64_t &hi) {
+  const uint64_t a = (uint64_t(dpp<CTRL, ROWS>(uint32_t(lo >> 32))) << 32) |
+                     dpp<CTRL, ROWS>(uint32_t(lo));
+  const uint64_t b = (uint64_t(dpp<CTRL, ROWS>(uint32_t(hi >> 32))) << 32) |
+                     dpp<CTRL, ROWS>(uint32_t(hi));
+  lo = a < lo ? a : lo;
+  hi = b > hi ? b : hi;
+}
+
+__device__ inline void wave_minmax(uint64_t &lo, uint64_t &hi) {
+  minmax_step<0xB1, 0xF>(lo, hi);
+  minmax_step<0x4E, 0xF>(lo, hi);
+  minmax_step<0x141, 0xF>(lo, hi);
+  minmax_step<0x140, 0xF>(lo, hi);
+  minmax_step<0x142, 0xA>(lo, hi);
+  minmax_step<0x143, 0xC>(lo, hi);
+}
+
 // Storage of the scheduler structures: LDS (on chip) or the state buffer (global).
 struct Store {
-  // per-user (for the replica)
-  int64_t *u;
+  int64_t *u;         // per user of the replica
   int32_t *xslot;
-  // X table
-  uint64_t *xkey;
-  int32_t *xuser, *xq, *xfh, *xft, *xrdy;
-  // pool of queued requests
-  int64_t *p_cost;
-  int32_t *p_rec, *p_tok, *p_succ, *p_next, *p_free;
-  // queued later calls
-  int32_t *cl_rec, *cl_prev, *cl_user, *cl_e, *cl_rdy;
-  int32_t xcap, pcap, clcap;
-  bool users_global;  // u / xslot in global memory (coherent loads needed)
+  uint64_t *xkey;     // X table
+  int32_t *xuser, *xq, *xfh, *xft, *xhh, *xht, *xsb, *xrh, *xrdy;
+  int32_t *e_rec, *e_tok, *e_succ, *e_next, *e_sv, *e_stok, *e_ssucc, *e_free;  // pool
+  int64_t *e_cost, *e_scost;
+  int32_t xcap, pcap;
+  bool users_global;
 };
 
 // ---------------------------------------------------------------------------
-// The scheduler body.  All control flow is wave-uniform; per-record work of the
-// arrival window is held one record per lane.
+// The scheduler body.  All control flow is wave-uniform; the arrival window holds
+// one record per lane.
 // ---------------------------------------------------------------------------
 template <bool G>
 __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip) {
@@ -170,270 +225,359 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
   RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
   int8_t *fate = reinterpret_cast<int8_t *>(a.state + a.L.fate) + base;
   const int32_t *succ = reinterpret_cast<const int32_t *>(a.state + a.L.succ) + base;
-  int32_t *qsave = reinterpret_cast<int32_t *>(a.state + a.L.qsave) + base;
+  const uint32_t *seg_start = reinterpret_cast<const uint32_t *>(a.state + a.L.seg_start);
+  int32_t *seg_rec = reinterpret_cast<int32_t *>(a.state + a.L.seg_rec);
+  int32_t *seg_tok = reinterpret_cast<int32_t *>(a.state + a.L.seg_tok);
+  int64_t *seg_cost = reinterpret_cast<int64_t *>(a.state + a.L.seg_cost);
+  int32_t *seg_succ = reinterpret_cast<int32_t *>(a.state + a.L.seg_succ);
   int64_t *u_all = reinterpret_cast<int64_t *>(a.state + a.L.u_all) + int64_t(r) * U;
 
   // ---- scalar state
   int64_t s = uni64(rs->s), nxt = uni64(rs->nxt), debt = uni64(rs->debt);
   int64_t backlog = uni64(rs->backlog), seq = uni64(rs->seq), gap = uni64(rs->gap);
-  int64_t last_exit_u = uni64(rs->last_exit_u), nq = uni64(rs->nq);
+  int64_t last_exit_u = uni64(rs->last_exit_u), low = uni64(rs->low);
   int32_t last_exit = uni(rs->last_exit);
   int64_t s_end;
-  if (onchip || !rs->overflow) {
+  if (onchip || !rs->overflow)
     s_end = a.n_steps < 0 ? INT64_MAX : s + a.n_steps;
-  } else {
+  else
     s_end = uni64(rs->s_end);  // resuming a launch that overflowed on chip
-  }
   const int64_t tau = a.tau, C = a.cap, theta = a.theta;
 
-  // ---- per-user arrays
   if (!S.users_global) {
     for (int32_t k = lane; k < U; k += 64) {
       S.u[k] = u_all[k];
       S.xslot[k] = -1;
     }
   }
-  // pool free stack
-  for (int32_t e = lane; e < S.pcap; e += 64) S.p_free[e] = S.pcap - 1 - e;
-  int32_t nfree = S.pcap, nX = 0, ncl = 0;
+  for (int32_t e = lane; e < S.pcap; e += 64) {
+    S.e_free[e] = S.pcap - 1 - e;
+    S.e_rec[e] = -1;
+  }
+  int32_t nfree = S.pcap, nX = 0;
   int32_t code = 0;
   bool overflow = false;
   __syncthreads();
 
-  auto get_u = [&](int32_t k) -> int64_t {
-    return S.users_global ? ld_fresh(S.u + k) : S.u[k];
-  };
+  auto get_u = [&](int32_t k) -> int64_t { return S.users_global ? ld_fresh(S.u + k) : S.u[k]; };
   auto get_xslot = [&](int32_t k) -> int32_t {
     return S.users_global ? ld_fresh(S.xslot + k) : S.xslot[k];
   };
-  auto key_of = [&](int32_t x, int64_t uval) -> uint64_t {
-    return (uint64_t(RD<G>(&S.xrdy[x]) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval);
+  auto slot_u = [&](int32_t x) -> int64_t {
+    return int64_t(uint64_t(uni64(int64_t(RD<G>(&S.xkey[x])))) & kValMask);
+  };
+  auto set_key = [&](int32_t x, int64_t uval) {
+    if (lane == 0)
+      S.xkey[x] = (uint64_t(RD<G>(&S.xrdy[x]) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval);
+  };
+  auto tokens_at = [&](int64_t i) -> int32_t {
+    const int64_t g = base + i;
+    return t.len_in[g] + t.len_out[g] + (t.len_sys ? t.len_sys[g] : 0);
   };
 
-  // ---- window of upcoming records (one per lane)
+  // ---- window of upcoming records (one per lane), branch-free so it stays in registers
   int64_t wbase = nxt;
-  int64_t w_ts = 0, w_cost = 0, c_u = 0;
-  int32_t w_user = 0, w_call = 0, w_head = 0, w_prev = -1, w_succ = -1, w_tok = 0, w_reason = 0;
-  int32_t c_xslot = -1, c_prev_adm = 0, c_head_blk = 0;
+  int64_t w_cost = 0, c_u = 0;
+  int32_t w_step = 0, w_user = -1, w_call = 0, w_head = -1, w_prev = -1, w_succ = -1, w_tok = 0,
+          w_reason = 0, w_seg = 0, c_xslot = -1, c_prev_adm = 0, c_head_blk = 0;
   auto load_window = [&]() {
-    __threadfence();
-    int64_t i = wbase + lane;
-    if (i < n) {
-      int64_t g = base + i;
-      w_ts = t.ts[g];
-      w_user = t.user[g];
-      w_call = t.call ? t.call[g] : 0;
-      w_head = t.call ? t.head[g] : int32_t(i);
-      w_prev = t.call ? t.prev[g] : -1;
-      w_succ = succ[i];
-      w_tok = t.len_in[g] + t.len_out[g] + (t.len_sys ? t.len_sys[g] : 0);
-      w_cost = a.cost[g];
-      w_reason = a.reason ? a.reason[g] : 0;
-      c_xslot = get_xslot(w_user);
-      c_u = get_u(w_user);
-      c_prev_adm = (w_call > 0) ? (ld_fresh(fate + w_prev) == 0) : 0;
-      int8_t hf = (w_call > 0) ? ld_fresh(fate + w_head) : int8_t(-1);
-      c_head_blk = (hf == 1 || hf == 2) ? 1 : 0;
-    } else {
-      w_user = -1;
-      w_call = 0;
-      w_head = -1;
-      w_prev = -1;
-    }
+    wave_fence();
+    const int64_t i = wbase + lane;
+    const bool valid = i < n;
+    const int64_t li = valid ? i : 0;
+    const int64_t g = base + li;
+    const int32_t call = (valid && t.call) ? t.call[g] : 0;
+    const int32_t usr = valid ? t.user[g] : 0;
+    const int32_t hd = (valid && t.call) ? t.head[g] : int32_t(li);
+    const int32_t pv = (valid && t.call) ? t.prev[g] : -1;
+    const int64_t ts = valid ? t.ts[g] : 0;
+    w_step = int32_t(ts / tau);
+    w_user = valid ? usr : -1;
+    w_call = call;
+    w_head = valid ? hd : -1;
+    w_prev = pv;
+    w_succ = valid ? succ[li] : -1;
+    w_tok = valid ? tokens_at(li) : 0;
+    w_cost = valid ? a.cost[g] : 0;
+    w_reason = (valid && a.reason) ? a.reason[g] : 0;
+    w_seg = int32_t(seg_start[int64_t(r) * U + usr]);
+    const int32_t xs = get_xslot(usr);
+    const int64_t uu = get_u(usr);
+    c_xslot = valid ? xs : -1;
+    c_u = valid ? uu : 0;
+    const int8_t pf = call > 0 ? ld_fresh(fate + pv) : int8_t(-1);
+    const int8_t hf = call > 0 ? ld_fresh(fate + hd) : int8_t(-1);
+    c_prev_adm = (call > 0 && pf == 0) ? 1 : 0;
+    c_head_blk = (call > 0 && (hf == 1 || hf == 2)) ? 1 : 0;
   };
 
-  // ---- structure operations (wave-uniform arguments)
-  auto fifo_push = [&](int32_t x, int32_t e) {
-    if (lane == 0) {
-      S.p_next[e] = -1;
-      int32_t tl = RD<G>(&S.xft[x]);
-      if (tl < 0) S.xfh[x] = e; else S.p_next[tl] = e;
-      S.xft[x] = e;
-    }
-  };
-  auto join_x = [&](int32_t k, int64_t uval) -> int32_t {
-    int32_t x = nX++;
+  // ---- X table
+  auto join_x = [&](int32_t k, int64_t uval, int32_t segb) -> int32_t {
+    const int32_t x = nX++;
     if (lane == 0) {
       S.xuser[x] = k;
       S.xq[x] = 0;
       S.xfh[x] = -1;
       S.xft[x] = -1;
+      S.xhh[x] = 0;
+      S.xht[x] = 0;
+      S.xsb[x] = segb;
+      S.xrh[x] = -1;
       S.xrdy[x] = 0;
       S.xkey[x] = (uint64_t(1) << kTierShift) | uint64_t(uval);
       S.xslot[k] = x;
     }
-    if (w_user == k) c_xslot = x;
+    c_xslot = (w_user == k) ? x : c_xslot;
     return x;
   };
-  // Remove slot x (its user leaves Q with counter uval): swap the last slot into x.
   auto leave_x = [&](int32_t x, int32_t k, int64_t uval) {
-    int32_t last = nX - 1;
+    const int32_t last = nX - 1;
     if (lane == 0) {
       S.u[k] = uval;
       S.xslot[k] = -1;
     }
-    if (w_user == k) {
-      c_xslot = -1;
-      c_u = uval;
-    }
+    c_xslot = (w_user == k) ? -1 : c_xslot;
+    c_u = (w_user == k) ? uval : c_u;
     if (x != last) {
-      int32_t k2 = uni(RD<G>(&S.xuser[last]));
+      const int32_t k2 = uni(RD<G>(&S.xuser[last]));
       if (lane == 0) {
         S.xuser[x] = k2;
         S.xq[x] = RD<G>(&S.xq[last]);
         S.xfh[x] = RD<G>(&S.xfh[last]);
         S.xft[x] = RD<G>(&S.xft[last]);
+        S.xhh[x] = RD<G>(&S.xhh[last]);
+        S.xht[x] = RD<G>(&S.xht[last]);
+        S.xsb[x] = RD<G>(&S.xsb[last]);
+        S.xrh[x] = RD<G>(&S.xrh[last]);
         S.xrdy[x] = RD<G>(&S.xrdy[last]);
         S.xkey[x] = RD<G>(&S.xkey[last]);
         S.xslot[k2] = x;
       }
-      if (w_user == k2) c_xslot = x;
+      c_xslot = (w_user == k2) ? x : c_xslot;
     }
     nX = last;
   };
-  // argmin over X of (key, user id); returns slot
   auto argmin_x = [&](uint64_t &bk, int32_t &bu) -> int32_t {
     uint64_t k = kEmptyKey;
-    int32_t us = INT32_MAX, bx = -1;
+    uint32_t us = 0xffffffffu, bx = 0xffffffffu;
     for (int32_t x = lane; x < nX; x += 64) {
-      uint64_t kk = RD<G>(&S.xkey[x]);
-      int32_t uu = RD<G>(&S.xuser[x]);
-      if (kk < k || (kk == k && uu < us)) {
-        k = kk;
-        us = uu;
-        bx = x;
-      }
+      const uint64_t kk = RD<G>(&S.xkey[x]);
+      const uint32_t uu = uint32_t(RD<G>(&S.xuser[x]));
+      const bool take = kk < k || (kk == k && uu < us);
+      k = take ? kk : k;
+      us = take ? uu : us;
+      bx = take ? uint32_t(x) : bx;
     }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      uint64_t k2 = shfl_xor64(k, m);
-      int32_t u2 = __shfl_xor(us, m, 64);
-      int32_t x2 = __shfl_xor(bx, m, 64);
-      if (k2 < k || (k2 == k && u2 < us)) {
-        k = k2;
-        us = u2;
-        bx = x2;
-      }
-    }
-    bk = uni64(int64_t(k));
-    bu = uni(us);
-    return uni(bx);
+    wave_argmin(k, us, bx);
+    bk = uint64_t(rdl64(int64_t(k), 63));
+    bu = rdl(int32_t(us), 63);
+    return rdl(int32_t(bx), 63);
   };
   auto minmax_x = [&](int64_t &mn, int64_t &mx) {
     uint64_t lo = kEmptyKey, hi = 0;
     for (int32_t x = lane; x < nX; x += 64) {
-      uint64_t v = RD<G>(&S.xkey[x]) & kValMask;
+      const uint64_t v = RD<G>(&S.xkey[x]) & kValMask;
       lo = v < lo ? v : lo;
       hi = v > hi ? v : hi;
     }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      uint64_t l2 = shfl_xor64(lo, m), h2 = shfl_xor64(hi, m);
-      lo = l2 < lo ? l2 : lo;
-      hi = h2 > hi ? h2 : hi;
-    }
-    mn = uni64(int64_t(lo));
-    mx = uni64(int64_t(hi));
+    wave_minmax(lo, hi);
+    mn = rdl64(int64_t(lo), 63);
+    mx = rdl64(int64_t(hi), 63);
   };
-  // the user's lowest-index ready later call: CL position
-  auto cl_ready_min = [&](int32_t k) -> int32_t {
-    int32_t best = INT32_MAX, bc = -1;
-    for (int32_t c = lane; c < ncl; c += 64) {
-      const int32_t rec_c = RD<G>(&S.cl_rec[c]);
-      if (RD<G>(&S.cl_rdy[c]) && RD<G>(&S.cl_user[c]) == k && rec_c < best) {
-        best = rec_c;
-        bc = c;
-      }
+
+  // ---- pool
+  auto alloc_e = [&]() -> int32_t { return uni(RD<G>(&S.e_free[--nfree])); };
+  auto free_e = [&](int32_t e) {
+    if (lane == 0) {
+      S.e_free[nfree] = e;
+      S.e_rec[e] = -1;
     }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      int32_t b2 = __shfl_xor(best, m, 64), c2 = __shfl_xor(bc, m, 64);
-      if (b2 < best) {
-        best = b2;
-        bc = c2;
-      }
-    }
-    return uni(bc);
+    ++nfree;
   };
-  auto cl_find_pending = [&](int32_t prev_rec) -> int32_t {
+  auto fill_e = [&](int32_t e, int32_t rec, int32_t tok, int64_t cst, int32_t sc, int32_t sv,
+                    int64_t scost, int32_t stok, int32_t ssucc) {
+    if (lane == 0) {
+      S.e_rec[e] = rec;
+      S.e_tok[e] = tok;
+      S.e_cost[e] = cst;
+      S.e_succ[e] = sc;
+      S.e_next[e] = -1;
+      S.e_sv[e] = sv;
+      S.e_scost[e] = scost;
+      S.e_stok[e] = stok;
+      S.e_ssucc[e] = ssucc;
+    }
+  };
+  // Data of record i (an arrived later call) read from the inputs.
+  auto load_record = [&](int32_t i, int64_t &cst, int32_t &tok, int32_t &sc) {
+    cst = uni64(a.cost[base + i]);
+    tok = uni(tokens_at(i));
+    sc = uni(succ[i]);
+  };
+  auto fifo_append = [&](int32_t x, int32_t e) {
+    if (lane == 0) {
+      const int32_t tl = RD<G>(&S.xft[x]);
+      if (tl < 0)
+        S.xfh[x] = e;
+      else
+        S.e_next[tl] = e;
+      S.xft[x] = e;
+    }
+  };
+  auto ready_push = [&](int32_t x, int32_t e) {
+    if (lane == 0) {
+      S.e_next[e] = RD<G>(&S.xrh[x]);
+      S.xrh[x] = e;
+      S.xrdy[x] = RD<G>(&S.xrdy[x]) + 1;
+    }
+  };
+  // A first call joins its user's FIFO: in the pool while the user has nothing in its
+  // HBM segment and the pool has room, else at the segment's tail.
+  auto enqueue_first = [&](int32_t x, int32_t rec, int32_t tok, int64_t cst, int32_t sc) -> bool {
+    const int32_t hh = uni(RD<G>(&S.xhh[x])), ht = uni(RD<G>(&S.xht[x]));
+    if (ht == hh && nfree > kReserve) {
+      const int32_t e = alloc_e();
+      fill_e(e, rec, tok, cst, sc, 0, 0, 0, -1);
+      fifo_append(x, e);
+      return true;
+    }
+    const int32_t k = uni(RD<G>(&S.xuser[x]));
+    const int64_t at = int64_t(uni(RD<G>(&S.xsb[x]))) + ht;
+    const int64_t cap_end = int64_t(seg_start[int64_t(r) * U + k + 1]);
+    if (at >= cap_end) return false;  // cannot happen: a segment holds all the user's first calls
+    if (lane == 0) {
+      seg_rec[at] = rec;
+      seg_tok[at] = tok;
+      seg_cost[at] = cst;
+      seg_succ[at] = sc;
+      S.xht[x] = ht + 1;
+    }
+    return true;
+  };
+  // Refill the user's pool FIFO from its HBM segment (up to 64 entries, one load).
+  auto refill = [&](int32_t x) -> bool {
+    const int32_t hh = uni(RD<G>(&S.xhh[x])), ht = uni(RD<G>(&S.xht[x]));
+    int32_t m = ht - hh;
+    if (m > 64) m = 64;
+    if (m > nfree) m = nfree;
+    if (m <= 0) return false;
+    wave_fence();
+    const int64_t at = int64_t(uni(RD<G>(&S.xsb[x]))) + hh + lane;
+    const bool mine = lane < m;
+    int32_t e = -1, en = -1;
+    if (mine) {
+      const int32_t rec = ld_fresh(seg_rec + at);
+      const int32_t tok = ld_fresh(seg_tok + at);
+      const int64_t cst = ld_fresh(seg_cost + at);
+      const int32_t sc = ld_fresh(seg_succ + at);
+      int32_t sv = 0, stok = 0, ssucc = -1;
+      int64_t scost = 0;
+      if (sc >= 0 && sc < nxt) {  // its next call has already arrived: stage its data
+        sv = 1;
+        scost = a.cost[base + sc];
+        stok = tokens_at(sc);
+        ssucc = succ[sc];
+      }
+      e = RD<G>(&S.e_free[nfree - 1 - lane]);
+      en = lane + 1 < m ? RD<G>(&S.e_free[nfree - 2 - lane]) : -1;
+      S.e_rec[e] = rec;
+      S.e_tok[e] = tok;
+      S.e_cost[e] = cst;
+      S.e_succ[e] = sc;
+      S.e_next[e] = en;
+      S.e_sv[e] = sv;
+      S.e_scost[e] = scost;
+      S.e_stok[e] = stok;
+      S.e_ssucc[e] = ssucc;
+    }
+    const int32_t first = rdl(e, 0), last = rdl(e, m - 1);
+    if (lane == 0) {
+      S.xfh[x] = first;
+      S.xft[x] = last;
+      S.xhh[x] = hh + m;
+    }
+    nfree -= m;
+    return true;
+  };
+  // Stage an arrived later call's data in its previous call's pool entry, if there.
+  auto stage_in_prev = [&](int32_t prev_rec, int64_t cst, int32_t tok, int32_t sc) {
     int32_t found = -1;
-    for (int32_t c = lane; c < ncl; c += 64)
-      if (!RD<G>(&S.cl_rdy[c]) && RD<G>(&S.cl_prev[c]) == prev_rec) found = c;
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      int32_t f2 = __shfl_xor(found, m, 64);
-      found = f2 > found ? f2 : found;
-    }
-    return uni(found);
-  };
-  auto cl_remove = [&](int32_t c) {
-    int32_t last = ncl - 1;
-    if (lane == 0 && c != last) {
-      S.cl_rec[c] = RD<G>(&S.cl_rec[last]);
-      S.cl_prev[c] = RD<G>(&S.cl_prev[last]);
-      S.cl_user[c] = RD<G>(&S.cl_user[last]);
-      S.cl_e[c] = RD<G>(&S.cl_e[last]);
-      S.cl_rdy[c] = RD<G>(&S.cl_rdy[last]);
-    }
-    ncl = last;
-  };
-  auto cl_add = [&](int32_t rec, int32_t prev_rec, int32_t k, int32_t e, int32_t rdy) {
-    int32_t c = ncl++;
-    if (lane == 0) {
-      S.cl_rec[c] = rec;
-      S.cl_prev[c] = prev_rec;
-      S.cl_user[c] = k;
-      S.cl_e[c] = e;
-      S.cl_rdy[c] = rdy;
-    }
-  };
-  auto set_key = [&](int32_t x, int64_t uval) {
-    if (lane == 0) S.xkey[x] = key_of(x, uval);
-  };
-  // Put one queued record (already counted in backlog) into the structures.
-  // Returns false if an on-chip capacity would overflow (nothing changed then).
-  auto enqueue = [&](int32_t rec, int32_t k, int32_t call, int32_t prev_rec, int32_t sc,
-                     int32_t tok, int64_t cst, int32_t xs, int64_t uval, bool prev_adm) -> bool {
-    if ((xs < 0 && nX >= S.xcap) || nfree == 0 || (call > 0 && ncl >= S.clcap)) return false;
-    int32_t x = xs >= 0 ? xs : join_x(k, uval);
-    int32_t e = uni(RD<G>(&S.p_free[--nfree]));
-    if (lane == 0) {
-      S.p_rec[e] = rec;
-      S.p_cost[e] = cst;
-      S.p_tok[e] = tok;
-      S.p_succ[e] = sc;
-      S.xq[x] = RD<G>(&S.xq[x]) + 1;
-    }
-    if (call == 0) {
-      fifo_push(x, e);
-    } else {
-      cl_add(rec, prev_rec, k, e, prev_adm ? 1 : 0);
-      if (prev_adm) {
-        if (lane == 0) S.xrdy[x] = RD<G>(&S.xrdy[x]) + 1;
-        set_key(x, uval);
+    for (int32_t e = lane; e < S.pcap; e += 64)
+      if (RD<G>(&S.e_rec[e]) == prev_rec) found = e;
+    const uint64_t m = __ballot(found >= 0);
+    if (m) {
+      const int32_t e = rdl(found, __ffsll((long long)m) - 1);
+      if (lane == 0) {
+        S.e_sv[e] = 1;
+        S.e_scost[e] = cst;
+        S.e_stok[e] = tok;
+        S.e_ssucc[e] = sc;
       }
+    }
+  };
+
+  // Queue one arrived, unthrottled record (counted in backlog by the caller).
+  // Returns false when an on-chip capacity would overflow (nothing changed then).
+  auto enqueue = [&](int32_t rec, int32_t k, int32_t call, int32_t prev_rec, int32_t sc,
+                     int32_t tok, int64_t cst, int32_t xs, int64_t uval, bool prev_adm,
+                     int32_t segb) -> bool {
+    if (xs < 0 && nX >= S.xcap) return false;
+    if (call > 0 && prev_adm && nfree == 0) return false;
+    const int32_t x = xs >= 0 ? xs : join_x(k, uval, segb);
+    if (lane == 0) S.xq[x] = RD<G>(&S.xq[x]) + 1;
+    if (call == 0) {
+      if (!enqueue_first(x, rec, tok, cst, sc)) code = FS_E_STATE;
+    } else if (prev_adm) {
+      const int32_t e = alloc_e();
+      fill_e(e, rec, tok, cst, sc, 0, 0, 0, -1);
+      ready_push(x, e);
+      set_key(x, uval);
+    } else {
+      stage_in_prev(prev_rec, cst, tok, sc);
     }
     return true;
   };
 
-  // ---- rebuild the queue saved by a previous call
-  for (int64_t q = 0; q < nq && !overflow; ++q) {
-    int32_t rec = uni(qsave[q]);
-    int64_t g = base + rec;
-    int32_t k = uni(t.user[g]);
-    int32_t call = t.call ? uni(t.call[g]) : 0;
-    int32_t prev_rec = t.call ? uni(t.prev[g]) : -1;
-    int32_t tok = uni(t.len_in[g] + t.len_out[g] + (t.len_sys ? t.len_sys[g] : 0));
-    int64_t cst = uni64(a.cost[g]);
-    int32_t xs = uni(get_xslot(k));
-    int64_t uval = xs >= 0 ? int64_t(uni64(int64_t(RD<G>(&S.xkey[xs]))) & int64_t(kValMask)) : uni64(get_u(k));
-    bool prev_adm = call > 0 && ld_fresh(fate + prev_rec) == 0;
-    if (!enqueue(rec, k, call, prev_rec, succ[rec], tok, cst, xs, uval, prev_adm)) overflow = true;
+  // ---- rebuild the queue of a previous call: every arrived record still undecided
+  for (int64_t b0 = low; b0 < nxt && !overflow && code == 0; b0 += 64) {
+    const int64_t i = b0 + lane;
+    const bool q = i < nxt && ld_fresh(fate + i) == -1;
+    uint64_t m = __ballot(q);
+    while (m && !overflow && code == 0) {
+      const int l = __ffsll((long long)m) - 1;
+      m &= m - 1;
+      const int32_t rec = int32_t(b0 + l);
+      const int64_t g = base + rec;
+      const int32_t k = uni(t.user[g]);
+      const int32_t call = t.call ? uni(t.call[g]) : 0;
+      const int32_t prev_rec = t.call ? uni(t.prev[g]) : -1;
+      int64_t cst;
+      int32_t tok, sc;
+      load_record(rec, cst, tok, sc);
+      const int32_t xs = uni(get_xslot(k));
+      const int64_t uval = xs >= 0 ? slot_u(xs) : uni64(get_u(k));
+      const bool prev_adm = call > 0 && ld_fresh(fate + prev_rec) == 0;
+      const int32_t segb = int32_t(seg_start[int64_t(r) * U + k]);
+      if (!enqueue(rec, k, call, prev_rec, sc, tok, cst, xs, uval, prev_adm, segb)) overflow = true;
+      // a ready later call whose own next call already arrived: stage that call's data
+      if (!overflow && code == 0 && call > 0 && prev_adm && sc >= 0 && sc < nxt) {
+        const int32_t xx = uni(get_xslot(k));
+        const int32_t e = uni(RD<G>(&S.xrh[xx]));
+        int64_t c2;
+        int32_t t2, s2;
+        load_record(sc, c2, t2, s2);
+        if (lane == 0) {
+          S.e_sv[e] = 1;
+          S.e_scost[e] = c2;
+          S.e_stok[e] = t2;
+          S.e_ssucc[e] = s2;
+        }
+      }
+    }
   }
   if (overflow) {
-    // leave the saved state untouched for the global-memory pass
     for (int32_t x = 0; x < nX; ++x) {
-      int32_t k = uni(RD<G>(&S.xuser[x]));
+      const int32_t k = uni(RD<G>(&S.xuser[x]));
       if (lane == 0) S.xslot[k] = -1;
     }
     if (lane == 0) {
@@ -459,10 +603,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     }
     if (nX == 0 && nxt < n) {
       // nothing queued: the steps before the next arrival only pay back debt
-      int64_t target = rdl64(w_ts, int(nxt - wbase)) / tau;
+      int64_t target = rdl(w_step, int(nxt - wbase));
       if (target > s_end) target = s_end;
       if (target > s) {
-        int64_t k = target - s;
+        const int64_t k = target - s;
         debt = (k >= (-debt + C - 1) / C) ? 0 : debt + k * C;
         s = target;
         if (s >= s_end) break;
@@ -480,13 +624,13 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
         load_window();
       }
       const int j = int(nxt - wbase);
-      if (rdl64(w_ts, j) / tau > s) break;
+      if (rdl(w_step, j) > s) break;
       const int32_t rec = int32_t(nxt);
       const int32_t k = rdl(w_user, j);
       const int32_t call = rdl(w_call, j);
       const int32_t xs = rdl(c_xslot, j);
       const bool in_x = xs >= 0;
-      int64_t uk = in_x ? int64_t(uni64(int64_t(RD<G>(&S.xkey[xs]))) & int64_t(kValMask)) : rdl64(c_u, j);
+      int64_t uk = in_x ? slot_u(xs) : rdl64(c_u, j);
       const int64_t u_before = uk;
       if (!in_x) {  // counter lift for a user with nothing queued
         if (nX == 0) {
@@ -508,21 +652,22 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       if (!blocked) {
         const bool prev_adm = rdl(c_prev_adm, j) != 0;
         if (!enqueue(rec, k, call, rdl(w_prev, j), rdl(w_succ, j), tok, rdl64(w_cost, j), xs, uk,
-                     prev_adm)) {
+                     prev_adm, rdl(w_seg, j))) {
           overflow = true;  // state is as before this arrival
           break;
         }
+        if (code) break;
         if (!in_x && nX == 1) minX = uk;
         backlog += tok;
       } else {
         if (lane == 0) fate[rec] = why;
         if (!in_x && uk != u_before) {
           if (lane == 0) S.u[k] = uk;
-          if (w_user == k) c_u = uk;
+          c_u = (w_user == k) ? uk : c_u;
         }
-        if (call == 0 && w_head == rec && w_call > 0) c_head_blk = 1;
+        c_head_blk = (call == 0 && w_head == rec && w_call > 0) ? 1 : c_head_blk;
         if (lane == 0) {
-          int64_t g = base + rec;
+          const int64_t g = base + rec;
           a.status[g] = why;
           a.admit_step[g] = -1;
           if (a.admit_seq) a.admit_seq[g] = -1;
@@ -532,7 +677,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       if (lane == 0 && a.counter_on_arrival) a.counter_on_arrival[base + rec] = uk;
       ++nxt;
     }
-    if (overflow) break;
+    if (overflow || code) break;
 
     // execution stream: admit while the step has budget
     int64_t budget = C + debt;
@@ -540,43 +685,72 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       uint64_t bk;
       int32_t k;
       const int32_t x = argmin_x(bk, k);
-      const int64_t uk = int64_t(bk & kValMask);
-      int32_t e;
       if (x < 0 || x >= nX) {
-        code = FS_E_STATE;  // internal bookkeeping error: stop instead of reading out of bounds
+        code = FS_E_STATE;  // internal bookkeeping error: stop rather than read out of bounds
         break;
       }
+      const int64_t uk = int64_t(bk & kValMask);
+      int32_t e;
       if ((bk >> kTierShift) == 0) {
-        const int32_t c = cl_ready_min(k);
-        if (c < 0) {
+        // the user's ready later call with the lowest record index
+        int32_t best = INT32_MAX, be = -1, bprev = -1, prevp = -1;
+        int32_t walked = 0;
+        for (int32_t c = uni(RD<G>(&S.xrh[x])); c >= 0 && walked < S.pcap;
+             c = uni(RD<G>(&S.e_next[c])), ++walked) {
+          const int32_t rc = uni(RD<G>(&S.e_rec[c]));
+          if (rc < best) {
+            best = rc;
+            be = c;
+            bprev = prevp;
+          }
+          prevp = c;
+        }
+        if (be < 0) {
           code = FS_E_STATE;
           break;
         }
-        e = uni(RD<G>(&S.cl_e[c]));
-        cl_remove(c);
-        if (lane == 0) S.xrdy[x] = RD<G>(&S.xrdy[x]) - 1;
+        e = be;
+        const int32_t nx = uni(RD<G>(&S.e_next[e]));
+        if (lane == 0) {
+          if (bprev < 0)
+            S.xrh[x] = nx;
+          else
+            S.e_next[bprev] = nx;
+          S.xrdy[x] = RD<G>(&S.xrdy[x]) - 1;
+        }
       } else {
+        if (uni(RD<G>(&S.xfh[x])) < 0) {
+          if (nfree == 0) {
+            overflow = true;  // nothing modified for this decision yet
+            break;
+          }
+          if (!refill(x)) {
+            code = FS_E_STATE;
+            break;
+          }
+        }
         e = uni(RD<G>(&S.xfh[x]));
         if (e < 0 || e >= S.pcap) {
           code = FS_E_STATE;
           break;
         }
-        const int32_t nx = uni(RD<G>(&S.p_next[e]));
+        const int32_t nx = uni(RD<G>(&S.e_next[e]));
         if (lane == 0) {
           S.xfh[x] = nx;
           if (nx < 0) S.xft[x] = -1;
         }
       }
-      const int32_t rec = uni(RD<G>(&S.p_rec[e]));
-      const int64_t cst = uni64(RD<G>(&S.p_cost[e]));
-      const int32_t tok = uni(RD<G>(&S.p_tok[e]));
-      const int32_t sc = uni(RD<G>(&S.p_succ[e]));
+      const int32_t rec = uni(RD<G>(&S.e_rec[e]));
+      const int64_t cst = uni64(RD<G>(&S.e_cost[e]));
+      const int32_t tok = uni(RD<G>(&S.e_tok[e]));
+      const int32_t sc = uni(RD<G>(&S.e_succ[e]));
+      const int32_t sv = uni(RD<G>(&S.e_sv[e]));
+      const int64_t scost = uni64(RD<G>(&S.e_scost[e]));
+      const int32_t stok = uni(RD<G>(&S.e_stok[e]));
+      const int32_t ssucc = uni(RD<G>(&S.e_ssucc[e]));
       const int32_t left = uni(RD<G>(&S.xq[x])) - 1;
-      if (lane == 0) {
-        S.p_free[nfree] = e;
-        S.xq[x] = left;
-      }
-      ++nfree;
+      free_e(e);
+      if (lane == 0) S.xq[x] = left;
       budget -= tok;
       backlog -= tok;
       const int64_t unew = uk + cst;
@@ -585,7 +759,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
         break;
       }
       if (lane == 0) {
-        int64_t g = base + rec;
+        const int64_t g = base + rec;
         fate[rec] = 0;
         a.status[g] = 0;
         a.admit_step[g] = int32_t(s);
@@ -593,16 +767,21 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
         if (a.counter_after) a.counter_after[g] = unew;
       }
       ++seq;
-      if (w_prev == rec) c_prev_adm = 1;
+      c_prev_adm = (w_prev == rec) ? 1 : c_prev_adm;
       if (sc >= 0 && sc < nxt) {
         // the next call arrived while this one was queued: it becomes ready now
-        const int32_t c = cl_find_pending(rec);
-        if (c >= 0) {
-          if (lane == 0) {
-            S.cl_rdy[c] = 1;
-            S.xrdy[x] = RD<G>(&S.xrdy[x]) + 1;
-          }
+        int64_t c1 = scost;
+        int32_t t1 = stok, s1 = ssucc;
+        if (!sv) load_record(sc, c1, t1, s1);
+        int32_t sv2 = 0, t2 = 0, s2 = -1;
+        int64_t c2 = 0;
+        if (s1 >= 0 && s1 < nxt) {  // and the call after it too
+          sv2 = 1;
+          load_record(s1, c2, t2, s2);
         }
+        const int32_t e2 = alloc_e();  // the entry just freed guarantees room
+        fill_e(e2, sc, t1, c1, s1, sv2, c2, t2, s2);
+        ready_push(x, e2);
       }
       if (left == 0) {
         last_exit = k;
@@ -612,7 +791,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
         set_key(x, unew);
       }
     }
-    if (code) break;
+    if (code || overflow) break;
     debt = budget < 0 ? budget : 0;
     if (nX > 0) {
       int64_t mn, mx;
@@ -625,30 +804,32 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
 
   if (code) raise_err(a.err, code);
 
-  // ---- save: counters of queued users back to u, queue contents to qsave
-  int64_t q = 0;
+  // ---- save: counters of queued users back to u; the queue itself is recovered next
+  // time from the records that have arrived and are still undecided
   for (int32_t x = 0; x < nX; ++x) {
     const int32_t k = uni(RD<G>(&S.xuser[x]));
-    const int64_t uval = int64_t(uni64(int64_t(RD<G>(&S.xkey[x]))) & int64_t(kValMask));
+    const int64_t uval = slot_u(x);
     if (lane == 0) {
       S.u[k] = uval;
       S.xslot[k] = -1;
     }
-    int32_t walked = 0;
-    for (int32_t e = uni(RD<G>(&S.xfh[x])); e >= 0 && e < S.pcap && walked < S.pcap;
-         e = uni(RD<G>(&S.p_next[e])), ++walked) {
-      if (lane == 0) qsave[q] = RD<G>(&S.p_rec[e]);
-      ++q;
-    }
   }
-  for (int32_t c = 0; c < ncl; ++c) {
-    if (lane == 0) qsave[q] = RD<G>(&S.cl_rec[c]);
-    ++q;
-  }
+  wave_fence();
   __syncthreads();
-  if (!S.users_global) {
+  if (!S.users_global)
     for (int32_t k = lane; k < U; k += 64) u_all[k] = S.u[k];
+  // lowest record index that may still be queued
+  while (low < nxt) {
+    const int64_t i = low + lane;
+    const bool q = i < nxt && ld_fresh(fate + i) == -1;
+    const uint64_t m = __ballot(q);
+    if (m) {
+      low += __ffsll((long long)m) - 1;
+      break;
+    }
+    low += 64;
   }
+  if (low > nxt) low = nxt;
   const bool drained = nxt == n && nX == 0;
   if (lane == 0) {
     rs->s = s;
@@ -658,7 +839,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     rs->seq = seq;
     rs->gap = gap;
     rs->last_exit_u = last_exit_u;
-    rs->nq = q;
+    rs->low = low;
     rs->last_exit = last_exit;
     rs->done = drained ? 1 : 0;
     rs->overflow = overflow ? 1 : 0;
@@ -669,11 +850,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       a.max_gap[r] = gap;
     }
   }
-  __threadfence();
-  if (!overflow) {
+  wave_fence();
+  if (!overflow)
     for (int32_t k = lane; k < U; k += 64)
       a.counter[int64_t(r) * U + k] = S.users_global ? ld_fresh(u_all + k) : u_all[k];
-  }
 }
 
 __device__ inline bool state_header_ok(const SchedArgs &a) {
@@ -682,24 +862,28 @@ __device__ inline bool state_header_ok(const SchedArgs &a) {
          h->N == a.t.N;
 }
 
-// On-chip pass: LDS holds the X table, pool, CL (and the counters when U is small).
+__device__ inline bool finish_if_done(const SchedArgs &a, int32_t r) {
+  RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
+  if (!rs->done) return false;
+  if (threadIdx.x == 0) {
+    a.steps[r] = rs->s;
+    a.decisions[r] = rs->seq;
+    a.max_gap[r] = rs->gap;
+  }
+  const int64_t *u_all =
+      reinterpret_cast<const int64_t *>(a.state + a.L.u_all) + int64_t(r) * a.t.U;
+  for (int32_t k = threadIdx.x; k < a.t.U; k += 64) a.counter[int64_t(r) * a.t.U + k] = u_all[k];
+  return true;
+}
+
+// On-chip pass: LDS holds the X table and the pool (and the counters when U is small).
 template <bool USERS_LDS>
 __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int32_t r = blockIdx.x;
   if (*a.err) return;
   if (!state_header_ok(a)) return;
-  RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
-  if (rs->done) {
-    if (threadIdx.x == 0) {
-      a.steps[r] = rs->s;
-      a.decisions[r] = rs->seq;
-      a.max_gap[r] = rs->gap;
-    }
-    const int64_t *u_all = reinterpret_cast<const int64_t *>(a.state + a.L.u_all) + int64_t(r) * a.t.U;
-    for (int32_t k = threadIdx.x; k < a.t.U; k += 64) a.counter[int64_t(r) * a.t.U + k] = u_all[k];
-    return;
-  }
+  if (finish_if_done(a, r)) return;
   Store S;
   char *p = smem;
   auto take = [&](size_t bytes) {
@@ -707,26 +891,29 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     p += (bytes + 15) & ~size_t(15);
     return q;
   };
+  const size_t pc = size_t(a.pcap);
   S.xcap = kXCap;
   S.pcap = a.pcap;
-  S.clcap = kCLCap;
   S.xkey = reinterpret_cast<uint64_t *>(take(8 * kXCap));
-  S.p_cost = reinterpret_cast<int64_t *>(take(8 * size_t(a.pcap)));
+  S.e_cost = reinterpret_cast<int64_t *>(take(8 * pc));
+  S.e_scost = reinterpret_cast<int64_t *>(take(8 * pc));
   S.xuser = reinterpret_cast<int32_t *>(take(4 * kXCap));
   S.xq = reinterpret_cast<int32_t *>(take(4 * kXCap));
   S.xfh = reinterpret_cast<int32_t *>(take(4 * kXCap));
   S.xft = reinterpret_cast<int32_t *>(take(4 * kXCap));
+  S.xhh = reinterpret_cast<int32_t *>(take(4 * kXCap));
+  S.xht = reinterpret_cast<int32_t *>(take(4 * kXCap));
+  S.xsb = reinterpret_cast<int32_t *>(take(4 * kXCap));
+  S.xrh = reinterpret_cast<int32_t *>(take(4 * kXCap));
   S.xrdy = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.p_rec = reinterpret_cast<int32_t *>(take(4 * size_t(a.pcap)));
-  S.p_tok = reinterpret_cast<int32_t *>(take(4 * size_t(a.pcap)));
-  S.p_succ = reinterpret_cast<int32_t *>(take(4 * size_t(a.pcap)));
-  S.p_next = reinterpret_cast<int32_t *>(take(4 * size_t(a.pcap)));
-  S.p_free = reinterpret_cast<int32_t *>(take(4 * size_t(a.pcap)));
-  S.cl_rec = reinterpret_cast<int32_t *>(take(4 * kCLCap));
-  S.cl_prev = reinterpret_cast<int32_t *>(take(4 * kCLCap));
-  S.cl_user = reinterpret_cast<int32_t *>(take(4 * kCLCap));
-  S.cl_e = reinterpret_cast<int32_t *>(take(4 * kCLCap));
-  S.cl_rdy = reinterpret_cast<int32_t *>(take(4 * kCLCap));
+  S.e_rec = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e_tok = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e_succ = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e_next = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e_sv = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e_stok = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e_ssucc = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e_free = reinterpret_cast<int32_t *>(take(4 * pc));
   if (USERS_LDS) {
     S.u = reinterpret_cast<int64_t *>(take(8 * size_t(a.t.U)));
     S.xslot = reinterpret_cast<int32_t *>(take(4 * size_t(a.t.U)));
@@ -739,50 +926,44 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   run_replica<false>(a, S, r, true);
 }
 
-// Global-memory pass: resumes replicas that overflowed on chip (or all replicas
-// when the engine asks for global memory only).
+// Global-memory pass: resumes replicas that overflowed on chip (or runs all
+// replicas when the engine asks for global memory only).
 __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   const int32_t r = blockIdx.x;
   if (*a.err) return;
   if (!state_header_ok(a)) return;
   RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
   if (!a.global_only && !rs->overflow) return;
-  if (rs->done) {
-    if (threadIdx.x == 0) {
-      a.steps[r] = rs->s;
-      a.decisions[r] = rs->seq;
-      a.max_gap[r] = rs->gap;
-    }
-    const int64_t *u_all = reinterpret_cast<const int64_t *>(a.state + a.L.u_all) + int64_t(r) * a.t.U;
-    for (int32_t k = threadIdx.x; k < a.t.U; k += 64) a.counter[int64_t(r) * a.t.U + k] = u_all[k];
-    return;
-  }
-  const int64_t base = a.t.rep_off[r];
-  const int32_t cap = int32_t(a.t.rep_off[r + 1] - base) + 1;
-  Store S;
+  if (finish_if_done(a, r)) return;
+  const int64_t off = a.t.rep_off[r] + r;
+  const int32_t cap = int32_t(a.t.rep_off[r + 1] - a.t.rep_off[r]) + 1;
   char *st = a.state;
+  const StateLayout &L = a.L;
+  Store S;
   S.xcap = cap;
   S.pcap = cap;
-  S.clcap = cap;
-  S.xkey = reinterpret_cast<uint64_t *>(st + a.L.xkey) + base + r;
-  S.xuser = reinterpret_cast<int32_t *>(st + a.L.xuser) + base + r;
-  S.xq = reinterpret_cast<int32_t *>(st + a.L.xq) + base + r;
-  S.xfh = reinterpret_cast<int32_t *>(st + a.L.xfh) + base + r;
-  S.xft = reinterpret_cast<int32_t *>(st + a.L.xft) + base + r;
-  S.xrdy = reinterpret_cast<int32_t *>(st + a.L.xrdy) + base + r;
-  S.p_cost = reinterpret_cast<int64_t *>(st + a.L.p_cost) + base + r;
-  S.p_rec = reinterpret_cast<int32_t *>(st + a.L.p_rec) + base + r;
-  S.p_tok = reinterpret_cast<int32_t *>(st + a.L.p_tok) + base + r;
-  S.p_succ = reinterpret_cast<int32_t *>(st + a.L.p_succ) + base + r;
-  S.p_next = reinterpret_cast<int32_t *>(st + a.L.p_next) + base + r;
-  S.p_free = reinterpret_cast<int32_t *>(st + a.L.p_free) + base + r;
-  S.cl_rec = reinterpret_cast<int32_t *>(st + a.L.cl_rec) + base + r;
-  S.cl_prev = reinterpret_cast<int32_t *>(st + a.L.cl_prev) + base + r;
-  S.cl_user = reinterpret_cast<int32_t *>(st + a.L.cl_user) + base + r;
-  S.cl_e = reinterpret_cast<int32_t *>(st + a.L.cl_e) + base + r;
-  S.cl_rdy = reinterpret_cast<int32_t *>(st + a.L.cl_rdy) + base + r;
-  S.u = reinterpret_cast<int64_t *>(st + a.L.u_all) + int64_t(r) * a.t.U;
-  S.xslot = reinterpret_cast<int32_t *>(st + a.L.xslot_all) + int64_t(r) * a.t.U;
+  S.xkey = reinterpret_cast<uint64_t *>(st + L.xkey) + off;
+  S.xuser = reinterpret_cast<int32_t *>(st + L.xuser) + off;
+  S.xq = reinterpret_cast<int32_t *>(st + L.xq) + off;
+  S.xfh = reinterpret_cast<int32_t *>(st + L.xfh) + off;
+  S.xft = reinterpret_cast<int32_t *>(st + L.xft) + off;
+  S.xhh = reinterpret_cast<int32_t *>(st + L.xhh) + off;
+  S.xht = reinterpret_cast<int32_t *>(st + L.xht) + off;
+  S.xsb = reinterpret_cast<int32_t *>(st + L.xsb) + off;
+  S.xrh = reinterpret_cast<int32_t *>(st + L.xrh) + off;
+  S.xrdy = reinterpret_cast<int32_t *>(st + L.xrdy) + off;
+  S.e_rec = reinterpret_cast<int32_t *>(st + L.e_rec) + off;
+  S.e_tok = reinterpret_cast<int32_t *>(st + L.e_tok) + off;
+  S.e_cost = reinterpret_cast<int64_t *>(st + L.e_cost) + off;
+  S.e_succ = reinterpret_cast<int32_t *>(st + L.e_succ) + off;
+  S.e_next = reinterpret_cast<int32_t *>(st + L.e_next) + off;
+  S.e_sv = reinterpret_cast<int32_t *>(st + L.e_sv) + off;
+  S.e_scost = reinterpret_cast<int64_t *>(st + L.e_scost) + off;
+  S.e_stok = reinterpret_cast<int32_t *>(st + L.e_stok) + off;
+  S.e_ssucc = reinterpret_cast<int32_t *>(st + L.e_ssucc) + off;
+  S.e_free = reinterpret_cast<int32_t *>(st + L.e_free) + off;
+  S.u = reinterpret_cast<int64_t *>(st + L.u_all) + int64_t(r) * a.t.U;
+  S.xslot = reinterpret_cast<int32_t *>(st + L.xslot_all) + int64_t(r) * a.t.U;
   S.users_global = true;
   run_replica<true>(a, S, r, false);
   if (threadIdx.x == 0) rs->overflow = 0;
@@ -802,20 +983,22 @@ __global__ void k_state_header(char *state, StateLayout L, int32_t R, int32_t U,
 }
 
 __global__ void k_state_reps(char *state, StateLayout L, int32_t R) {
-  int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r < R) {
-    RepState *rs = reinterpret_cast<RepState *>(state + L.reps) + r;
     RepState z = {};
     z.last_exit = -1;
-    *rs = z;
+    reinterpret_cast<RepState *>(state + L.reps)[r] = z;
   }
 }
 
 __global__ void k_state_users(char *state, StateLayout L, int64_t RU) {
-  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < RU;
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i <= RU;
        i += int64_t(gridDim.x) * blockDim.x) {
-    reinterpret_cast<int64_t *>(state + L.u_all)[i] = 0;
-    reinterpret_cast<int32_t *>(state + L.xslot_all)[i] = -1;
+    if (i < RU) {
+      reinterpret_cast<int64_t *>(state + L.u_all)[i] = 0;
+      reinterpret_cast<int32_t *>(state + L.xslot_all)[i] = -1;
+    }
+    reinterpret_cast<uint32_t *>(state + L.seg_start)[i] = 0;
   }
 }
 
@@ -827,18 +1010,22 @@ __global__ void k_state_records(char *state, StateLayout L, int64_t N) {
   }
 }
 
-// next-call links: succ[prev] = i within each replica (prev is validated by the
-// scheduler's checks before use; invalid links are skipped here)
-__global__ void k_state_succ(char *state, StateLayout L, DevTrace t) {
-  if (!t.call) return;
+// next-call links (succ[prev] = i) and the number of first calls per (replica, user);
+// links and ids are checked again before the scheduler runs
+__global__ void k_state_links(char *state, StateLayout L, DevTrace t) {
+  uint32_t *cnt = reinterpret_cast<uint32_t *>(state + L.seg_start);
   for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
        g += int64_t(gridDim.x) * blockDim.x) {
-    int32_t c = t.call[g];
-    if (c <= 0) continue;
-    int32_t r = replica_of(t.rep_off, t.R, g);
-    int64_t base = t.rep_off[r], i = g - base;
-    int32_t p = t.prev[g];
-    if (p >= 0 && p < i) reinterpret_cast<int32_t *>(state + L.succ)[base + p] = int32_t(i);
+    const int32_t c = t.call ? t.call[g] : 0;
+    const int32_t r = replica_of(t.rep_off, t.R, g);
+    const int64_t b = t.rep_off[r], i = g - b;
+    const int32_t u = t.user[g];
+    if (c == 0) {
+      if (u >= 0 && u < t.U) atomicAdd(cnt + int64_t(r) * t.U + u, 1u);
+    } else if (c > 0) {
+      const int32_t p = t.prev[g];
+      if (p >= 0 && p < i) reinterpret_cast<int32_t *>(state + L.succ)[b + p] = int32_t(i);
+    }
   }
 }
 
@@ -862,30 +1049,30 @@ __global__ void __launch_bounds__(256) k_sched_check(CheckArgs a) {
   }
   for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
        g += int64_t(gridDim.x) * blockDim.x) {
-    int32_t r = replica_of(t.rep_off, t.R, g);
-    int64_t base = t.rep_off[r], i = g - base;
-    int32_t u = t.user[g], ap = t.app[g];
-    int64_t ts = t.ts[g];
+    const int32_t r = replica_of(t.rep_off, t.R, g);
+    const int64_t base = t.rep_off[r], i = g - base;
+    const int32_t u = t.user[g], ap = t.app[g];
+    const int64_t ts = t.ts[g];
     if (u < 0 || u >= t.U || ap < 0 || ap >= t.A) code = max(code, int32_t(FS_E_RANGE));
     if (ts < 0) code = max(code, int32_t(FS_E_RANGE));
     if (g > base && t.ts[g - 1] > ts) code = max(code, int32_t(FS_E_ORDER));
     if (!len_ok(t.len_in[g]) || !len_ok(t.len_out[g]) || (t.len_sys && !len_ok(t.len_sys[g])))
       code = max(code, int32_t(FS_E_RANGE));
     if (t.call) {
-      int32_t c = t.call[g], h = t.head[g], p = t.prev[g];
+      const int32_t c = t.call[g], h = t.head[g], p = t.prev[g];
       bool ok;
       if (c == 0) {
         ok = h == i && p == -1;
       } else {
         ok = c > 0 && p >= 0 && p < i;
         if (ok) {
-          int64_t gp = base + p;
+          const int64_t gp = base + p;
           ok = t.call[gp] == c - 1 && t.user[gp] == u && t.head[gp] == h;
         }
       }
       if (!ok) code = max(code, int32_t(FS_E_RANGE));
     }
-    int64_t cst = a.cost[g];
+    const int64_t cst = a.cost[g];
     if (cst < 0 || cst >= kValueLimit) code = max(code, int32_t(FS_E_RANGE));
     if (a.reason && a.reason[g] > 2) code = max(code, int32_t(FS_E_RANGE));
   }
@@ -904,9 +1091,9 @@ size_t onchip_lds_bytes(int32_t pcap, int32_t U, bool users_lds) {
   auto add = [&](size_t x) { b += (x + 15) & ~size_t(15); };
   add(8 * kXCap);
   add(8 * size_t(pcap));
-  for (int i = 0; i < 5; ++i) add(4 * kXCap);
-  for (int i = 0; i < 5; ++i) add(4 * size_t(pcap));
-  for (int i = 0; i < 5; ++i) add(4 * kCLCap);
+  add(8 * size_t(pcap));
+  for (int i = 0; i < 9; ++i) add(4 * kXCap);
+  for (int i = 0; i < 8; ++i) add(4 * size_t(pcap));
   if (users_lds) {
     add(8 * size_t(U));
     add(4 * size_t(U));
@@ -922,17 +1109,22 @@ size_t state_bytes(const fs_trace *t) {
 
 hipError_t launch_state_init(void *state, const fs_trace *t, hipStream_t s) {
   const int64_t N = t->rep_off_h[t->n_replicas];
-  StateLayout L = state_layout(t->n_replicas, t->n_users, N);
+  const StateLayout L = state_layout(t->n_replicas, t->n_users, N);
   char *st = static_cast<char *>(state);
   hipLaunchKernelGGL(k_state_header, dim3(1), dim3(64), 0, s, st, L, t->n_replicas, t->n_users, N);
   hipLaunchKernelGGL(k_state_reps, dim3((t->n_replicas + 255) / 256), dim3(256), 0, s, st, L,
                      t->n_replicas);
   const int64_t RU = int64_t(t->n_replicas) * t->n_users;
-  hipLaunchKernelGGL(k_state_users, dim3(grid_for(RU, 256)), dim3(256), 0, s, st, L, RU);
+  hipLaunchKernelGGL(k_state_users, dim3(grid_for(RU + 1, 256)), dim3(256), 0, s, st, L, RU);
   if (N > 0) {
     hipLaunchKernelGGL(k_state_records, dim3(grid_for(N, 256)), dim3(256), 0, s, st, L, N);
-    hipLaunchKernelGGL(k_state_succ, dim3(grid_for(N, 256)), dim3(256), 0, s, st, L, dev_trace(t));
+    hipLaunchKernelGGL(k_state_links, dim3(grid_for(N, 256)), dim3(256), 0, s, st, L,
+                       dev_trace(t));
   }
+  // per-user first-call segments: exclusive prefix of the counts
+  hipError_t e = exclusive_scan(reinterpret_cast<uint32_t *>(st + L.seg_start), RU + 1,
+                                reinterpret_cast<uint32_t *>(st + L.seg_part), s);
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 
@@ -962,13 +1154,13 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.state = static_cast<char *>(state);
   a.L = state_layout(t->n_replicas, t->n_users, N);
   const bool users_lds = t->n_users <= kUsersLdsMax;
-  a.pcap = t->n_users > 512 ? 512 : 1024;
+  a.pcap = t->n_users > 512 ? 384 : 768;
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
   hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);
   const dim3 grid(t->n_replicas), block(64);
   if (!a.global_only) {
-    size_t lds = onchip_lds_bytes(a.pcap, t->n_users, users_lds);
+    const size_t lds = onchip_lds_bytes(a.pcap, t->n_users, users_lds);
     if (users_lds)
       hipLaunchKernelGGL(k_schedule_onchip<true>, grid, block, lds, s, a);
     else

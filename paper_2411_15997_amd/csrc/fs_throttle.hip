@@ -313,13 +313,6 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const uint32_t *in,
   }
 }
 
-hipError_t exclusive_scan(uint32_t *data, int64_t n, uint32_t *part, hipStream_t s) {
-  int64_t blocks = (n + kScanChunk - 1) / kScanChunk;
-  hipLaunchKernelGGL(k_scan_partials, dim3(blocks), dim3(kScanThreads), 0, s, data, n, part);
-  hipLaunchKernelGGL(k_scan_spine, dim3(1), dim3(kScanThreads), 0, s, part, blocks);
-  hipLaunchKernelGGL(k_scan_apply, dim3(blocks), dim3(kScanThreads), 0, s, data, n, part, data);
-  return hipGetLastError();
-}
 
 // ---------------------------------------------------------------- window tests
 
@@ -438,6 +431,17 @@ int grid_for(int64_t n, int threads) {
 }
 
 }  // namespace
+
+size_t scan_partials_bytes(int64_t n) { return size_t((n + kScanChunk - 1) / kScanChunk + 1) * 4; }
+
+hipError_t exclusive_scan(uint32_t *data, int64_t n, uint32_t *part, hipStream_t s) {
+  int64_t blocks = (n + kScanChunk - 1) / kScanChunk;
+  if (blocks < 1) return hipSuccess;
+  hipLaunchKernelGGL(k_scan_partials, dim3(blocks), dim3(kScanThreads), 0, s, data, n, part);
+  hipLaunchKernelGGL(k_scan_spine, dim3(1), dim3(kScanThreads), 0, s, part, blocks);
+  hipLaunchKernelGGL(k_scan_apply, dim3(blocks), dim3(kScanThreads), 0, s, data, n, part, data);
+  return hipGetLastError();
+}
 
 size_t throttle_workspace_bytes(const fs_trace *t) { return layout(t).total; }
 

@@ -156,3 +156,44 @@ def test_run_trace_and_metrics_full_path():
         np.testing.assert_allclose(m[k], getattr(met, k), rtol=1e-9, atol=0, err_msg=k)
     for k in ("throttled", "aborted_midway", "wasted_tokens"):
         assert (m[k] == getattr(met, k)).all(), k
+
+
+def test_long_fifos_spill_to_hbm_segments_and_refill():
+    """A few users with thousands of queued first calls: the pool fills, later first
+    calls go to the users' HBM segments and come back in refills."""
+    rng = np.random.default_rng(61)
+    n, U = 12000, 5
+    ts = np.sort(rng.integers(0, 3000, n)).astype(np.int64)
+    user = rng.integers(0, U, n).astype(np.int32)
+    tr = tg.Trace(1, U, 1, np.array([0, n], np.int64), ts, user, np.zeros(n, np.int32), None,
+                  None, None, rng.integers(1, 9, n).astype(np.int32), None, np.zeros(n, np.int32))
+    cost = rng.integers(1, 1000, n).astype(np.int64)
+    o = oracle.simulate(tr, cost, None, 100, 30, 10 ** 9)
+    g = gpu_schedule(tr, cost, None, 100, 30, 10 ** 9)
+    compare_sim(g, o)
+
+
+def test_long_queues_with_pending_chains():
+    """Chained calls of users with long queues: later calls arrive while their previous
+    call waits (pending), some staged in the pool, some read at refill."""
+    rng = np.random.default_rng(62)
+    reps = []
+    for _ in range(4):
+        reps.append(random_trace(rng, 6000, 6, 2, 20000, multi=True, max_tok=9))
+    tr = tg.concat(reps)
+    cost = rng.integers(1, 5000, tr.n).astype(np.int64)
+    reason = rng.integers(0, 3, tr.n).astype(np.uint8)
+    for theta in (10 ** 9, 40):
+        o = oracle.simulate(tr, cost, reason, 50, 20, theta)
+        g = gpu_schedule(tr, cost, reason, 50, 20, theta)
+        compare_sim(g, o)
+        g2 = gpu_schedule(tr, cost, reason, 50, 20, theta, chunks=37)
+        compare_sim(g2, o)
+
+
+def test_full_replica_workload_c2():
+    """All 64 replicas of the 64 x 256 x 8 workload (6.4M requests), bit-exact."""
+    wl, tr = workload_trace("c2_replicas")
+    say("sched full c2", tr.n)
+    g, o, _, _ = _run_workload(wl, tr)
+    compare_sim(g, o)

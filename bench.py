@@ -69,20 +69,20 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dt = fs.DeviceTrace(tr, device=dev)
-    coef, per_rep = fs.workload_weights(wl, tr)
-    w, keep = fs.make_weights(dt, coef, None, per_rep)
+    throttle_only = wl.throttle_only
     lim = fs.make_limits(wl.window_us, wl.t_user, wl.t_app)
-    theta = wl.overload_tokens if wl.overload_tokens is not None else -1
-    eng = fs.make_engine(wl.step_us, wl.cap_tokens, theta)
-    out = fs.Outputs(dt, parity=False)
     N = tr.n
-    cost = torch.empty(max(N, 1), dtype=torch.int64, device=dev)
     err = fs.err_word(dev)
     tws = torch.empty(max(fs.fs_throttle_workspace(dt), 1), dtype=torch.uint8, device=dev)
-    state = torch.empty(fs.fs_state_bytes(dt), dtype=torch.uint8, device=dev)
-    mws = torch.empty(max(fs.fs_metrics_workspace(dt), 1), dtype=torch.uint8, device=dev)
-    metrics = fs.Metrics(dt)
-    throttle_only = wl.throttle_only
+    if not throttle_only:
+        coef, per_rep = fs.workload_weights(wl, tr)
+        w, keep = fs.make_weights(dt, coef, None, per_rep)
+        eng = fs.make_engine(wl.step_us, wl.cap_tokens, wl.overload_tokens)
+        out = fs.Outputs(dt, parity=False)
+        cost = torch.empty(max(N, 1), dtype=torch.int64, device=dev)
+        state = torch.empty(fs.fs_state_bytes(dt), dtype=torch.uint8, device=dev)
+        mws = torch.empty(max(fs.fs_metrics_workspace(dt), 1), dtype=torch.uint8, device=dev)
+        metrics = fs.Metrics(dt)
 
     stages = ["throttle"] if throttle_only else ["cost", "throttle", "schedule", "metrics"]
     if args.stage_only:

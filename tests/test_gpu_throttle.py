@@ -88,14 +88,3 @@ def test_errors_match_oracle():
     with pytest.raises(fs.FairServeError) as ge:
         gpu_throttle(bad2, 10, 1, [1, 1])
     assert ge.value.code == fs.FS_E_RANGE
-
-
-def test_full_throttle_stream():
-    """The 50M-request throttle-only stream at full size: bitmap bit-exact."""
-    wl, tr = workload_trace("c3_throttle")
-    say("throttle full", tr.n)
-    g = gpu_throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
-    o = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
-    assert (g["reason"] == o.reason).all()
-    nw = (tr.n + 31) // 32
-    assert (g["bitmap"][:nw] == o.bitmap[:nw]).all()

@@ -5,11 +5,11 @@
 // (a dictionary from user to queued requests), the last user to leave Q, and the
 // overload measure (tokens queued).  The wave keeps what each decision touches on
 // chip and never waits on HBM inside a decision in the common case:
-//   X table   slots [0, nX) of users with something queued: user id, key
-//             (tier << 62 | u) whose tier is 0 while the user has a ready later call of
-//             an incomplete interaction, a FIFO of queued first calls and a list of
-//             ready later calls.  The argmin over (key, user id) is one LDS read per
-//             lane plus a DPP wave reduction.
+//   X table   slots [0, nX) of users with something queued, one slot per lane with
+//             every field in that lane's registers: user id, key (tier << 62 | u) whose
+//             tier is 0 while the user has a ready later call of an incomplete
+//             interaction, a FIFO of queued first calls and a list of ready later calls.
+//             The argmin over (key, user id) is a DPP wave reduction over registers.
 //   pool      LDS entries of queued requests: record, cost, tokens, next call, link,
 //             and the next call's data when that call has already arrived, so serving
 //             a request releases its successor without touching HBM.
@@ -36,7 +36,6 @@ constexpr uint64_t kTierShift = 62;
 constexpr uint64_t kValMask = (uint64_t(1) << 62) - 1;
 constexpr uint64_t kEmptyKey = ~uint64_t(0);
 constexpr int kUsersLdsMax = 1024;  // per-user arrays on chip up to this many users
-constexpr int kXCap = 128;           // on-chip backlogged-user slots (two per lane)
 constexpr int kReserve = 32;         // pool entries first calls leave for later calls
 
 struct RepState {
@@ -199,24 +198,155 @@ __device__ inline void wave_minmax(uint64_t &lo, uint64_t &hi) {
   minmax_step<0x143, 0xC>(lo, hi);
 }
 
-// Storage of the scheduler structures: LDS (on chip) or the state buffer (global).
+// Storage of the pool and per-user arrays: LDS (on chip) or the state buffer (global).
 struct Store {
   int64_t *u;         // per user of the replica
   int32_t *xslot;
-  uint64_t *xkey;     // X table
-  int32_t *xuser, *xq, *xfh, *xft, *xhh, *xht, *xsb, *xrh, *xrdy;
   int32_t *e_rec, *e_tok, *e_succ, *e_next, *e_sv, *e_stok, *e_ssucc, *e_free;  // pool
   int64_t *e_cost, *e_scost;
-  int32_t xcap, pcap;
+  int32_t pcap;
   bool users_global;
+};
+
+// The backlogged-user table.  On chip: one slot per lane, every field in a register
+// of that lane (read with v_readlane, written with v_writelane); the argmin is a DPP
+// reduction over the lanes' keys with no memory access.
+struct XReg {
+  uint32_t klo, khi;  // key = tier << 62 | counter
+  int32_t user, q, fh, ft, hh, ht, sb, rh, rdy;
+  static constexpr int32_t cap = 64;
+  __device__ void init() {
+    klo = khi = 0xffffffffu;
+    user = q = 0;
+    fh = ft = rh = -1;
+    hh = ht = sb = rdy = 0;
+  }
+  static __device__ int32_t wl(int32_t old, int32_t x, int32_t v) {
+    return int32_t(threadIdx.x) == x ? v : old;
+  }
+  __device__ uint64_t key(int32_t x) const {
+    return (uint64_t(uint32_t(rdl(int32_t(khi), x))) << 32) | uint32_t(rdl(int32_t(klo), x));
+  }
+  __device__ void set_key(int32_t x, uint64_t v) {
+    klo = uint32_t(wl(int32_t(klo), x, int32_t(uint32_t(v))));
+    khi = uint32_t(wl(int32_t(khi), x, int32_t(uint32_t(v >> 32))));
+  }
+#define FS_XREG_FIELD(f)                                              \
+  __device__ int32_t get_##f(int32_t x) const { return rdl(f, x); } \
+  __device__ void set_##f(int32_t x, int32_t v) { f = wl(f, x, v); }
+  FS_XREG_FIELD(user)
+  FS_XREG_FIELD(q)
+  FS_XREG_FIELD(fh)
+  FS_XREG_FIELD(ft)
+  FS_XREG_FIELD(hh)
+  FS_XREG_FIELD(ht)
+  FS_XREG_FIELD(sb)
+  FS_XREG_FIELD(rh)
+  FS_XREG_FIELD(rdy)
+#undef FS_XREG_FIELD
+  __device__ void copy(int32_t from, int32_t to) {
+    set_key(to, key(from));
+    set_user(to, get_user(from));
+    set_q(to, get_q(from));
+    set_fh(to, get_fh(from));
+    set_ft(to, get_ft(from));
+    set_hh(to, get_hh(from));
+    set_ht(to, get_ht(from));
+    set_sb(to, get_sb(from));
+    set_rh(to, get_rh(from));
+    set_rdy(to, get_rdy(from));
+  }
+  __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
+    const int lane = threadIdx.x;
+    uint64_t k = lane < nX ? ((uint64_t(khi) << 32) | klo) : kEmptyKey;
+    uint32_t us = lane < nX ? uint32_t(user) : 0xffffffffu, bx = uint32_t(lane);
+    wave_argmin(k, us, bx);
+    bk = uint64_t(rdl64(int64_t(k), 63));
+    bu = rdl(int32_t(us), 63);
+    return rdl(int32_t(bx), 63);
+  }
+  __device__ void minmax(int32_t nX, int64_t &mn, int64_t &mx) const {
+    const int lane = threadIdx.x;
+    const uint64_t v = ((uint64_t(khi) << 32) | klo) & kValMask;
+    uint64_t lo = lane < nX ? v : kEmptyKey, hi = lane < nX ? v : 0;
+    wave_minmax(lo, hi);
+    mn = rdl64(int64_t(lo), 63);
+    mx = rdl64(int64_t(hi), 63);
+  }
+};
+
+// The same table in global memory (after an on-chip overflow): capacity n_r + 1.
+struct XMem {
+  uint64_t *k;
+  int32_t *user, *q, *fh, *ft, *hh, *ht, *sb, *rh, *rdy;
+  int32_t cap;
+  __device__ void init() {}
+  __device__ uint64_t key(int32_t x) const { return uint64_t(uni64(int64_t(ld_fresh(k + x)))); }
+  __device__ void set_key(int32_t x, uint64_t v) {
+    if (threadIdx.x == 0) k[x] = v;
+  }
+#define FS_XMEM_FIELD(f)                                                          \
+  __device__ int32_t get_##f(int32_t x) const { return uni(ld_fresh(f + x)); } \
+  __device__ void set_##f(int32_t x, int32_t v) {                                 \
+    if (threadIdx.x == 0) f[x] = v;                                               \
+  }
+  FS_XMEM_FIELD(user)
+  FS_XMEM_FIELD(q)
+  FS_XMEM_FIELD(fh)
+  FS_XMEM_FIELD(ft)
+  FS_XMEM_FIELD(hh)
+  FS_XMEM_FIELD(ht)
+  FS_XMEM_FIELD(sb)
+  FS_XMEM_FIELD(rh)
+  FS_XMEM_FIELD(rdy)
+#undef FS_XMEM_FIELD
+  __device__ void copy(int32_t from, int32_t to) {
+    set_key(to, key(from));
+    set_user(to, get_user(from));
+    set_q(to, get_q(from));
+    set_fh(to, get_fh(from));
+    set_ft(to, get_ft(from));
+    set_hh(to, get_hh(from));
+    set_ht(to, get_ht(from));
+    set_sb(to, get_sb(from));
+    set_rh(to, get_rh(from));
+    set_rdy(to, get_rdy(from));
+  }
+  __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
+    uint64_t kk = kEmptyKey;
+    uint32_t us = 0xffffffffu, bx = 0xffffffffu;
+    for (int32_t x = threadIdx.x; x < nX; x += 64) {
+      const uint64_t a = ld_fresh(k + x);
+      const uint32_t b = uint32_t(ld_fresh(user + x));
+      const bool take = a < kk || (a == kk && b < us);
+      kk = take ? a : kk;
+      us = take ? b : us;
+      bx = take ? uint32_t(x) : bx;
+    }
+    wave_argmin(kk, us, bx);
+    bk = uint64_t(rdl64(int64_t(kk), 63));
+    bu = rdl(int32_t(us), 63);
+    return rdl(int32_t(bx), 63);
+  }
+  __device__ void minmax(int32_t nX, int64_t &mn, int64_t &mx) const {
+    uint64_t lo = kEmptyKey, hi = 0;
+    for (int32_t x = threadIdx.x; x < nX; x += 64) {
+      const uint64_t v = ld_fresh(k + x) & kValMask;
+      lo = v < lo ? v : lo;
+      hi = v > hi ? v : hi;
+    }
+    wave_minmax(lo, hi);
+    mn = rdl64(int64_t(lo), 63);
+    mx = rdl64(int64_t(hi), 63);
+  }
 };
 
 // ---------------------------------------------------------------------------
 // The scheduler body.  All control flow is wave-uniform; the arrival window holds
 // one record per lane.
 // ---------------------------------------------------------------------------
-template <bool G>
-__device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip) {
+template <bool G, class XT>
+__device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool onchip) {
   const int lane = threadIdx.x;
   const DevTrace &t = a.t;
   const int64_t base = t.rep_off[r];
@@ -254,6 +384,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     S.e_free[e] = S.pcap - 1 - e;
     S.e_rec[e] = -1;
   }
+  X.init();
   int32_t nfree = S.pcap, nX = 0;
   int32_t code = 0;
   bool overflow = false;
@@ -263,12 +394,9 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
   auto get_xslot = [&](int32_t k) -> int32_t {
     return S.users_global ? ld_fresh(S.xslot + k) : S.xslot[k];
   };
-  auto slot_u = [&](int32_t x) -> int64_t {
-    return int64_t(uint64_t(uni64(int64_t(RD<G>(&S.xkey[x])))) & kValMask);
-  };
+  auto slot_u = [&](int32_t x) -> int64_t { return int64_t(X.key(x) & kValMask); };
   auto set_key = [&](int32_t x, int64_t uval) {
-    if (lane == 0)
-      S.xkey[x] = (uint64_t(RD<G>(&S.xrdy[x]) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval);
+    X.set_key(x, (uint64_t(X.get_rdy(x) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval));
   };
   auto tokens_at = [&](int64_t i) -> int32_t {
     const int64_t g = base + i;
@@ -311,22 +439,20 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     c_head_blk = (call > 0 && (hf == 1 || hf == 2)) ? 1 : 0;
   };
 
-  // ---- X table
+  // ---- backlogged users
   auto join_x = [&](int32_t k, int64_t uval, int32_t segb) -> int32_t {
     const int32_t x = nX++;
-    if (lane == 0) {
-      S.xuser[x] = k;
-      S.xq[x] = 0;
-      S.xfh[x] = -1;
-      S.xft[x] = -1;
-      S.xhh[x] = 0;
-      S.xht[x] = 0;
-      S.xsb[x] = segb;
-      S.xrh[x] = -1;
-      S.xrdy[x] = 0;
-      S.xkey[x] = (uint64_t(1) << kTierShift) | uint64_t(uval);
-      S.xslot[k] = x;
-    }
+    X.set_user(x, k);
+    X.set_q(x, 0);
+    X.set_fh(x, -1);
+    X.set_ft(x, -1);
+    X.set_hh(x, 0);
+    X.set_ht(x, 0);
+    X.set_sb(x, segb);
+    X.set_rh(x, -1);
+    X.set_rdy(x, 0);
+    X.set_key(x, (uint64_t(1) << kTierShift) | uint64_t(uval));
+    if (lane == 0) S.xslot[k] = x;
     c_xslot = (w_user == k) ? x : c_xslot;
     return x;
   };
@@ -339,50 +465,13 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     c_xslot = (w_user == k) ? -1 : c_xslot;
     c_u = (w_user == k) ? uval : c_u;
     if (x != last) {
-      const int32_t k2 = uni(RD<G>(&S.xuser[last]));
-      if (lane == 0) {
-        S.xuser[x] = k2;
-        S.xq[x] = RD<G>(&S.xq[last]);
-        S.xfh[x] = RD<G>(&S.xfh[last]);
-        S.xft[x] = RD<G>(&S.xft[last]);
-        S.xhh[x] = RD<G>(&S.xhh[last]);
-        S.xht[x] = RD<G>(&S.xht[last]);
-        S.xsb[x] = RD<G>(&S.xsb[last]);
-        S.xrh[x] = RD<G>(&S.xrh[last]);
-        S.xrdy[x] = RD<G>(&S.xrdy[last]);
-        S.xkey[x] = RD<G>(&S.xkey[last]);
-        S.xslot[k2] = x;
-      }
+      const int32_t k2 = X.get_user(last);
+      X.copy(last, x);
+      if (lane == 0) S.xslot[k2] = x;
       c_xslot = (w_user == k2) ? x : c_xslot;
     }
+    X.set_key(last, kEmptyKey);
     nX = last;
-  };
-  auto argmin_x = [&](uint64_t &bk, int32_t &bu) -> int32_t {
-    uint64_t k = kEmptyKey;
-    uint32_t us = 0xffffffffu, bx = 0xffffffffu;
-    for (int32_t x = lane; x < nX; x += 64) {
-      const uint64_t kk = RD<G>(&S.xkey[x]);
-      const uint32_t uu = uint32_t(RD<G>(&S.xuser[x]));
-      const bool take = kk < k || (kk == k && uu < us);
-      k = take ? kk : k;
-      us = take ? uu : us;
-      bx = take ? uint32_t(x) : bx;
-    }
-    wave_argmin(k, us, bx);
-    bk = uint64_t(rdl64(int64_t(k), 63));
-    bu = rdl(int32_t(us), 63);
-    return rdl(int32_t(bx), 63);
-  };
-  auto minmax_x = [&](int64_t &mn, int64_t &mx) {
-    uint64_t lo = kEmptyKey, hi = 0;
-    for (int32_t x = lane; x < nX; x += 64) {
-      const uint64_t v = RD<G>(&S.xkey[x]) & kValMask;
-      lo = v < lo ? v : lo;
-      hi = v > hi ? v : hi;
-    }
-    wave_minmax(lo, hi);
-    mn = rdl64(int64_t(lo), 63);
-    mx = rdl64(int64_t(hi), 63);
   };
 
   // ---- pool
@@ -415,34 +504,30 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     sc = uni(succ[i]);
   };
   auto fifo_append = [&](int32_t x, int32_t e) {
-    if (lane == 0) {
-      const int32_t tl = RD<G>(&S.xft[x]);
-      if (tl < 0)
-        S.xfh[x] = e;
-      else
-        S.e_next[tl] = e;
-      S.xft[x] = e;
-    }
+    const int32_t tl = X.get_ft(x);
+    if (tl < 0)
+      X.set_fh(x, e);
+    else if (lane == 0)
+      S.e_next[tl] = e;
+    X.set_ft(x, e);
   };
   auto ready_push = [&](int32_t x, int32_t e) {
-    if (lane == 0) {
-      S.e_next[e] = RD<G>(&S.xrh[x]);
-      S.xrh[x] = e;
-      S.xrdy[x] = RD<G>(&S.xrdy[x]) + 1;
-    }
+    if (lane == 0) S.e_next[e] = X.get_rh(x);
+    X.set_rh(x, e);
+    X.set_rdy(x, X.get_rdy(x) + 1);
   };
   // A first call joins its user's FIFO: in the pool while the user has nothing in its
   // HBM segment and the pool has room, else at the segment's tail.
   auto enqueue_first = [&](int32_t x, int32_t rec, int32_t tok, int64_t cst, int32_t sc) -> bool {
-    const int32_t hh = uni(RD<G>(&S.xhh[x])), ht = uni(RD<G>(&S.xht[x]));
+    const int32_t hh = X.get_hh(x), ht = X.get_ht(x);
     if (ht == hh && nfree > kReserve) {
       const int32_t e = alloc_e();
       fill_e(e, rec, tok, cst, sc, 0, 0, 0, -1);
       fifo_append(x, e);
       return true;
     }
-    const int32_t k = uni(RD<G>(&S.xuser[x]));
-    const int64_t at = int64_t(uni(RD<G>(&S.xsb[x]))) + ht;
+    const int32_t k = X.get_user(x);
+    const int64_t at = int64_t(X.get_sb(x)) + ht;
     const int64_t cap_end = int64_t(seg_start[int64_t(r) * U + k + 1]);
     if (at >= cap_end) return false;  // cannot happen: a segment holds all the user's first calls
     if (lane == 0) {
@@ -450,19 +535,19 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       seg_tok[at] = tok;
       seg_cost[at] = cst;
       seg_succ[at] = sc;
-      S.xht[x] = ht + 1;
     }
+    X.set_ht(x, ht + 1);
     return true;
   };
   // Refill the user's pool FIFO from its HBM segment (up to 64 entries, one load).
   auto refill = [&](int32_t x) -> bool {
-    const int32_t hh = uni(RD<G>(&S.xhh[x])), ht = uni(RD<G>(&S.xht[x]));
+    const int32_t hh = X.get_hh(x), ht = X.get_ht(x);
     int32_t m = ht - hh;
     if (m > 64) m = 64;
     if (m > nfree) m = nfree;
     if (m <= 0) return false;
     wave_fence();
-    const int64_t at = int64_t(uni(RD<G>(&S.xsb[x]))) + hh + lane;
+    const int64_t at = int64_t(X.get_sb(x)) + hh + lane;
     const bool mine = lane < m;
     int32_t e = -1, en = -1;
     if (mine) {
@@ -490,12 +575,9 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       S.e_stok[e] = stok;
       S.e_ssucc[e] = ssucc;
     }
-    const int32_t first = rdl(e, 0), last = rdl(e, m - 1);
-    if (lane == 0) {
-      S.xfh[x] = first;
-      S.xft[x] = last;
-      S.xhh[x] = hh + m;
-    }
+    X.set_fh(x, rdl(e, 0));
+    X.set_ft(x, rdl(e, m - 1));
+    X.set_hh(x, hh + m);
     nfree -= m;
     return true;
   };
@@ -521,10 +603,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
   auto enqueue = [&](int32_t rec, int32_t k, int32_t call, int32_t prev_rec, int32_t sc,
                      int32_t tok, int64_t cst, int32_t xs, int64_t uval, bool prev_adm,
                      int32_t segb) -> bool {
-    if (xs < 0 && nX >= S.xcap) return false;
+    if (xs < 0 && nX >= X.cap) return false;
     if (call > 0 && prev_adm && nfree == 0) return false;
     const int32_t x = xs >= 0 ? xs : join_x(k, uval, segb);
-    if (lane == 0) S.xq[x] = RD<G>(&S.xq[x]) + 1;
+    X.set_q(x, X.get_q(x) + 1);
     if (call == 0) {
       if (!enqueue_first(x, rec, tok, cst, sc)) code = FS_E_STATE;
     } else if (prev_adm) {
@@ -562,7 +644,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       // a ready later call whose own next call already arrived: stage that call's data
       if (!overflow && code == 0 && call > 0 && prev_adm && sc >= 0 && sc < nxt) {
         const int32_t xx = uni(get_xslot(k));
-        const int32_t e = uni(RD<G>(&S.xrh[xx]));
+        const int32_t e = X.get_rh(xx);
         int64_t c2;
         int32_t t2, s2;
         load_record(sc, c2, t2, s2);
@@ -577,7 +659,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
   }
   if (overflow) {
     for (int32_t x = 0; x < nX; ++x) {
-      const int32_t k = uni(RD<G>(&S.xuser[x]));
+      const int32_t k = X.get_user(x);
       if (lane == 0) S.xslot[k] = -1;
     }
     if (lane == 0) {
@@ -589,7 +671,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
   int64_t minX = 0;
   if (nX > 0) {
     int64_t mx;
-    minmax_x(minX, mx);
+    X.minmax(nX, minX, mx);
   }
   load_window();
 
@@ -684,7 +766,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     while (budget > 0 && nX > 0) {
       uint64_t bk;
       int32_t k;
-      const int32_t x = argmin_x(bk, k);
+      const int32_t x = X.argmin(nX, bk, k);
       if (x < 0 || x >= nX) {
         code = FS_E_STATE;  // internal bookkeeping error: stop rather than read out of bounds
         break;
@@ -695,7 +777,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
         // the user's ready later call with the lowest record index
         int32_t best = INT32_MAX, be = -1, bprev = -1, prevp = -1;
         int32_t walked = 0;
-        for (int32_t c = uni(RD<G>(&S.xrh[x])); c >= 0 && walked < S.pcap;
+        for (int32_t c = X.get_rh(x); c >= 0 && walked < S.pcap;
              c = uni(RD<G>(&S.e_next[c])), ++walked) {
           const int32_t rc = uni(RD<G>(&S.e_rec[c]));
           if (rc < best) {
@@ -711,15 +793,13 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
         }
         e = be;
         const int32_t nx = uni(RD<G>(&S.e_next[e]));
-        if (lane == 0) {
-          if (bprev < 0)
-            S.xrh[x] = nx;
-          else
-            S.e_next[bprev] = nx;
-          S.xrdy[x] = RD<G>(&S.xrdy[x]) - 1;
-        }
+        if (bprev < 0)
+          X.set_rh(x, nx);
+        else if (lane == 0)
+          S.e_next[bprev] = nx;
+        X.set_rdy(x, X.get_rdy(x) - 1);
       } else {
-        if (uni(RD<G>(&S.xfh[x])) < 0) {
+        if (X.get_fh(x) < 0) {
           if (nfree == 0) {
             overflow = true;  // nothing modified for this decision yet
             break;
@@ -729,16 +809,14 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
             break;
           }
         }
-        e = uni(RD<G>(&S.xfh[x]));
+        e = X.get_fh(x);
         if (e < 0 || e >= S.pcap) {
           code = FS_E_STATE;
           break;
         }
         const int32_t nx = uni(RD<G>(&S.e_next[e]));
-        if (lane == 0) {
-          S.xfh[x] = nx;
-          if (nx < 0) S.xft[x] = -1;
-        }
+        X.set_fh(x, nx);
+        if (nx < 0) X.set_ft(x, -1);
       }
       const int32_t rec = uni(RD<G>(&S.e_rec[e]));
       const int64_t cst = uni64(RD<G>(&S.e_cost[e]));
@@ -748,9 +826,9 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
       const int64_t scost = uni64(RD<G>(&S.e_scost[e]));
       const int32_t stok = uni(RD<G>(&S.e_stok[e]));
       const int32_t ssucc = uni(RD<G>(&S.e_ssucc[e]));
-      const int32_t left = uni(RD<G>(&S.xq[x])) - 1;
+      const int32_t left = X.get_q(x) - 1;
       free_e(e);
-      if (lane == 0) S.xq[x] = left;
+      X.set_q(x, left);
       budget -= tok;
       backlog -= tok;
       const int64_t unew = uk + cst;
@@ -795,7 +873,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
     debt = budget < 0 ? budget : 0;
     if (nX > 0) {
       int64_t mn, mx;
-      minmax_x(mn, mx);
+      X.minmax(nX, mn, mx);
       gap = mx - mn > gap ? mx - mn : gap;
       minX = mn;
     }
@@ -807,7 +885,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, int32_t r, bool onchip
   // ---- save: counters of queued users back to u; the queue itself is recovered next
   // time from the records that have arrived and are still undecided
   for (int32_t x = 0; x < nX; ++x) {
-    const int32_t k = uni(RD<G>(&S.xuser[x]));
+    const int32_t k = X.get_user(x);
     const int64_t uval = slot_u(x);
     if (lane == 0) {
       S.u[k] = uval;
@@ -892,20 +970,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     return q;
   };
   const size_t pc = size_t(a.pcap);
-  S.xcap = kXCap;
   S.pcap = a.pcap;
-  S.xkey = reinterpret_cast<uint64_t *>(take(8 * kXCap));
   S.e_cost = reinterpret_cast<int64_t *>(take(8 * pc));
   S.e_scost = reinterpret_cast<int64_t *>(take(8 * pc));
-  S.xuser = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xq = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xfh = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xft = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xhh = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xht = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xsb = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xrh = reinterpret_cast<int32_t *>(take(4 * kXCap));
-  S.xrdy = reinterpret_cast<int32_t *>(take(4 * kXCap));
   S.e_rec = reinterpret_cast<int32_t *>(take(4 * pc));
   S.e_tok = reinterpret_cast<int32_t *>(take(4 * pc));
   S.e_succ = reinterpret_cast<int32_t *>(take(4 * pc));
@@ -923,7 +990,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     S.xslot = reinterpret_cast<int32_t *>(a.state + a.L.xslot_all) + int64_t(r) * a.t.U;
     S.users_global = true;
   }
-  run_replica<false>(a, S, r, true);
+  XReg X;
+  run_replica<false>(a, S, X, r, true);
 }
 
 // Global-memory pass: resumes replicas that overflowed on chip (or runs all
@@ -940,18 +1008,19 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   char *st = a.state;
   const StateLayout &L = a.L;
   Store S;
-  S.xcap = cap;
   S.pcap = cap;
-  S.xkey = reinterpret_cast<uint64_t *>(st + L.xkey) + off;
-  S.xuser = reinterpret_cast<int32_t *>(st + L.xuser) + off;
-  S.xq = reinterpret_cast<int32_t *>(st + L.xq) + off;
-  S.xfh = reinterpret_cast<int32_t *>(st + L.xfh) + off;
-  S.xft = reinterpret_cast<int32_t *>(st + L.xft) + off;
-  S.xhh = reinterpret_cast<int32_t *>(st + L.xhh) + off;
-  S.xht = reinterpret_cast<int32_t *>(st + L.xht) + off;
-  S.xsb = reinterpret_cast<int32_t *>(st + L.xsb) + off;
-  S.xrh = reinterpret_cast<int32_t *>(st + L.xrh) + off;
-  S.xrdy = reinterpret_cast<int32_t *>(st + L.xrdy) + off;
+  XMem X;
+  X.cap = cap;
+  X.k = reinterpret_cast<uint64_t *>(st + L.xkey) + off;
+  X.user = reinterpret_cast<int32_t *>(st + L.xuser) + off;
+  X.q = reinterpret_cast<int32_t *>(st + L.xq) + off;
+  X.fh = reinterpret_cast<int32_t *>(st + L.xfh) + off;
+  X.ft = reinterpret_cast<int32_t *>(st + L.xft) + off;
+  X.hh = reinterpret_cast<int32_t *>(st + L.xhh) + off;
+  X.ht = reinterpret_cast<int32_t *>(st + L.xht) + off;
+  X.sb = reinterpret_cast<int32_t *>(st + L.xsb) + off;
+  X.rh = reinterpret_cast<int32_t *>(st + L.xrh) + off;
+  X.rdy = reinterpret_cast<int32_t *>(st + L.xrdy) + off;
   S.e_rec = reinterpret_cast<int32_t *>(st + L.e_rec) + off;
   S.e_tok = reinterpret_cast<int32_t *>(st + L.e_tok) + off;
   S.e_cost = reinterpret_cast<int64_t *>(st + L.e_cost) + off;
@@ -965,7 +1034,7 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   S.u = reinterpret_cast<int64_t *>(st + L.u_all) + int64_t(r) * a.t.U;
   S.xslot = reinterpret_cast<int32_t *>(st + L.xslot_all) + int64_t(r) * a.t.U;
   S.users_global = true;
-  run_replica<true>(a, S, r, false);
+  run_replica<true>(a, S, X, r, false);
   if (threadIdx.x == 0) rs->overflow = 0;
 }
 
@@ -1089,10 +1158,8 @@ int grid_for(int64_t n, int threads) {
 size_t onchip_lds_bytes(int32_t pcap, int32_t U, bool users_lds) {
   size_t b = 0;
   auto add = [&](size_t x) { b += (x + 15) & ~size_t(15); };
-  add(8 * kXCap);
   add(8 * size_t(pcap));
   add(8 * size_t(pcap));
-  for (int i = 0; i < 9; ++i) add(4 * kXCap);
   for (int i = 0; i < 8; ++i) add(4 * size_t(pcap));
   if (users_lds) {
     add(8 * size_t(U));
@@ -1154,7 +1221,7 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.state = static_cast<char *>(state);
   a.L = state_layout(t->n_replicas, t->n_users, N);
   const bool users_lds = t->n_users <= kUsersLdsMax;
-  a.pcap = t->n_users > 512 ? 384 : 768;
+  a.pcap = t->n_users > 512 ? 512 : 1024;
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
   hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);

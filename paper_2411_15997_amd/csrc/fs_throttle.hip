@@ -7,18 +7,25 @@
 // taken in stream order.  The window count of record i exceeds T iff the record T
 // positions earlier in the same key sequence exists and arrived after ts_i - W
 // (the T+1 most recent arrivals of the key, i included, all lie in the window).
-// So the test is O(1) once each key's records are contiguous in stream order:
-//   1. key = replica*U + user (low B_u bits) with the app above it (B_a bits);
-//   2. stable LSD radix sort of (key, index) over the user bits -> user order;
-//      test the user limit at distance T_user;
-//   3. one more stable radix pass over the app bits -> (app, user) order, where
-//      every (user, app) pair is contiguous and still in stream order;
-//      test the app limit at distance T_app[app];
-//   4. back in stream order: combine the two flags, apply overload gating and the
-//      interaction rule, pack the bitmap with wave ballots.
-// Radix passes: per-tile digit histograms, a device-wide exclusive scan, then a
-// stable scatter (wave-match ranking, tile reordered in LDS so the global writes
-// of each digit run are contiguous).
+// So the test is O(1) once each key's records are contiguous in stream order.
+//
+// Every record becomes one 64-bit element, most significant field first:
+//   key   B_k bits   (app << B_u) | (replica * U + user)
+//   index B_i bits   global record index
+//   time  B_q bits   (ts - ts of the replica's first record) >> sh, sh the smallest
+//                    shift that fits every replica's span
+//   flag  1 bit      user limit exceeded (set by the pass that tests it)
+// A stable LSD radix sort over the user bits of the key gives each user's records
+// in stream order; the first radix pass over the app bits tests the user limit as it
+// reads that order and sets the flag; after the app passes every (user, app) pair
+// is contiguous and the app limit is tested.  The result goes back to stream order
+// with one scatter through the index field.  The window test on the quantised
+// time is exact whenever it is decisive (the interval of possible gaps lies wholly
+// below or above W) and falls back to the two exact arrival times otherwise.
+// Radix pass: per-tile digit histograms (the first one fused into element
+// construction), a device-wide exclusive scan, then a stable scatter (wave-match
+// ranking, the tile reordered in LDS so the global writes of each digit run are
+// contiguous).
 #include "fs_device.h"
 #include "fs_launch.h"
 
@@ -28,7 +35,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kItems = 16;
 constexpr int kTile = kThreads * kItems;  // 4096 records per radix tile
-constexpr int kRadixBits = 8;
+constexpr int kRadixBits = 8;              // widest digit
 constexpr int kRadix = 1 << kRadixBits;
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 4;
@@ -42,11 +49,34 @@ int bits_for(int64_t n_values) {  // bits to represent 0 .. n_values-1 (at least
 
 size_t up(size_t x) { return (x + 255) / 256 * 256; }
 
+// Field positions of the packed element.
+struct Pack {
+  int Bu, Ba, Bk, Bi, Bq;
+  int SK;  // key shift (64 - Bk)
+  int SI;  // index shift (1 + Bq)
+  uint64_t imask, qmask;
+};
+
+Pack make_pack(const fs_trace *t, int64_t N) {
+  Pack p;
+  p.Bu = bits_for(int64_t(t->n_replicas) * t->n_users);
+  p.Ba = bits_for(t->n_apps);
+  p.Bk = p.Bu + p.Ba;
+  p.Bi = bits_for(N > 0 ? N : 1);
+  p.Bq = 64 - p.Bk - p.Bi - 1;
+  if (p.Bq < 0) p.Bq = 0;
+  p.SK = 64 - p.Bk;
+  p.SI = 1 + p.Bq;
+  p.imask = (uint64_t(1) << p.Bi) - 1;
+  p.qmask = p.Bq > 0 ? (uint64_t(1) << p.Bq) - 1 : 0;
+  return p;
+}
+
 struct Layout {
   int64_t N;
   int64_t tiles;
-  int Bu, Ba;
-  size_t off_keyA, off_idxA, off_keyB, off_idxB, off_eu, off_ea, off_hist, off_part, off_tapp;
+  Pack pk;
+  size_t off_a, off_b, off_rr, off_hist, off_part, off_tapp, off_sh;
   size_t total;
 };
 
@@ -54,20 +84,17 @@ Layout layout(const fs_trace *t) {
   Layout L;
   L.N = t->rep_off_h[t->n_replicas];
   L.tiles = (L.N + kTile - 1) / kTile;
-  L.Bu = bits_for(int64_t(t->n_replicas) * t->n_users);
-  L.Ba = bits_for(t->n_apps);
+  L.pk = make_pack(t, L.N);
   size_t n = size_t(L.N > 0 ? L.N : 1);
   size_t hist_len = size_t(kRadix) * size_t(L.tiles > 0 ? L.tiles : 1);
   size_t o = 0;
-  L.off_keyA = o; o += up(n * 4);
-  L.off_idxA = o; o += up(n * 4);
-  L.off_keyB = o; o += up(n * 4);
-  L.off_idxB = o; o += up(n * 4);
-  L.off_eu = o; o += up(n);
-  L.off_ea = o; o += up(n);
+  L.off_a = o; o += up(n * 8);
+  L.off_b = o; o += up(n * 8);
+  L.off_rr = o; o += up(n);
   L.off_hist = o; o += up(hist_len * 4);
   L.off_part = o; o += up(((hist_len + kScanChunk - 1) / kScanChunk + 1) * 4);
   L.off_tapp = o; o += up(kMaxApps * 4);
+  L.off_sh = o; o += up(4);
   L.total = o;
   return L;
 }
@@ -101,60 +128,173 @@ __device__ uint32_t block_inclusive_scan(uint32_t v, uint32_t *s_waves, uint32_t
   return x + before;
 }
 
-// ---------------------------------------------------------------- init + checks
+// Lanes of the wave holding the same digit as this lane (ballot per digit bit).
+__device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
+  uint64_t peers = __ballot(valid);
+#pragma unroll
+  for (int b = 0; b < kRadixBits; ++b) {
+    const uint64_t m = __ballot((d >> b) & 1u);
+    peers &= ((d >> b) & 1u) ? m : ~m;
+  }
+  return peers;
+}
+
+// Adds one item row to the tile histogram in LDS (equal digits aggregated per wave).
+__device__ inline void hist_add(uint32_t *h, uint32_t d, bool valid) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t peers = digit_peers(d, valid);
+  if (valid && (peers & ((uint64_t(1) << lane) - 1)) == 0) atomicAdd(&h[d], uint32_t(__popcll(peers)));
+}
+
+// ---------------------------------------------------------------- window test
+
+struct Win {
+  int64_t W;
+  const int32_t *sh_dev;  // written on the device by k_thr_span
+  int sh;                 // loaded from sh_dev at the start of each kernel
+  bool has_q;
+  Pack pk;
+  const int64_t *ts;
+};
+
+__device__ inline Win load_win(const Win &w) {
+  Win v = w;
+  v.sh = *w.sh_dev;
+  return v;
+}
+
+// Is ts(p) - ts(q) < W for two records of the same key, q earlier in the stream?
+__device__ inline bool in_window(uint64_t ep, uint64_t eq, const Win &w) {
+  if (w.has_q) {
+    const uint64_t tp = (ep >> 1) & w.pk.qmask, tq = (eq >> 1) & w.pk.qmask;
+    const uint64_t d = tp - tq;
+    const uint64_t span = (uint64_t(1) << w.sh) - 1;  // the quantisation error bound
+    const uint64_t mid = d << w.sh;
+    // the true gap lies in [mid - span, mid + span]
+    if (mid + span < uint64_t(w.W)) return true;
+    if (mid >= span && mid - span >= uint64_t(w.W)) return false;
+  }
+  const int64_t gp = int64_t((ep >> w.pk.SI) & w.pk.imask);
+  const int64_t gq = int64_t((eq >> w.pk.SI) & w.pk.imask);
+  return w.ts[gp] - w.ts[gq] < w.W;
+}
+
+// ---------------------------------------------------------------- shift of the time field
+
+__global__ void __launch_bounds__(kThreads) k_thr_span(const int64_t *rep_off, const int64_t *ts,
+                                                        int32_t R, int Bq, int32_t *sh_out) {
+  __shared__ int64_t s_max[kThreads];
+  int64_t m = 0;
+  for (int32_t r = threadIdx.x; r < R; r += kThreads) {
+    const int64_t a = rep_off[r], b = rep_off[r + 1];
+    if (b > a) {
+      const int64_t span = ts[b - 1] - ts[a];
+      m = span > m ? span : m;
+    }
+  }
+  s_max[threadIdx.x] = m;
+  __syncthreads();
+  for (int s = kThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s && s_max[threadIdx.x + s] > s_max[threadIdx.x])
+      s_max[threadIdx.x] = s_max[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    int sh = 0;
+    if (Bq > 0)
+      while (sh < 63 && (uint64_t(s_max[0]) >> sh) >= (uint64_t(1) << Bq)) ++sh;
+    *sh_out = sh;
+  }
+}
+
+// ---------------------------------------------------------------- element construction
 
 struct InitArgs {
   DevTrace t;
-  int Bu;
+  Pack pk;
   bool check_chain;
-  uint32_t *key;
-  uint32_t *idx;
+  const int32_t *sh;
+  uint64_t *el;
+  int shift;      // first radix digit
+  uint32_t mask;
+  uint32_t *hist;
+  int64_t tiles;
   int32_t *err;
 };
 
+// Builds the elements of one tile in stream order, checks the fields the throttle
+// reads, and counts the tile's first radix digit.
 __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
+  __shared__ uint32_t h[kRadix];
+  __shared__ int32_t s_r0;
+  const int t = threadIdx.x;
+  const DevTrace &tr = a.t;
+  const int64_t base = blockIdx.x * int64_t(kTile);
+  h[t] = 0;
+  if (t == 0) s_r0 = replica_of(tr.rep_off, tr.R, base);
+  __syncthreads();
+  const int sh = *a.sh;
+  int32_t r = s_r0;
+  int64_t r_end = tr.rep_off[r + 1], r_base = tr.rep_off[r];
+  int64_t ts_base = tr.ts[r_base];
   int32_t code = 0;
-  const DevTrace &t = a.t;
-  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
-       g += int64_t(gridDim.x) * blockDim.x) {
-    int32_t r = replica_of(t.rep_off, t.R, g);
-    int64_t base = t.rep_off[r];
-    int32_t u = t.user[g], ap = t.app[g];
-    int64_t ts = t.ts[g];
-    bool ok_ids = u >= 0 && u < t.U && ap >= 0 && ap < t.A;
-    if (!ok_ids) code = max(code, int32_t(FS_E_RANGE));
-    if (ts < 0) code = max(code, int32_t(FS_E_RANGE));
-    if (g > base && t.ts[g - 1] > ts) code = max(code, int32_t(FS_E_ORDER));
-    if (t.call) {
-      int32_t c = t.call[g];
-      if (c < 0) code = max(code, int32_t(FS_E_RANGE));
-      if (a.check_chain) {
-        int64_t i = g - base;
-        int32_t h = t.head[g], p = t.prev[g];
-        bool ok;
-        if (c == 0) {
-          ok = h == i && p == -1;
-        } else {
-          ok = c > 0 && p >= 0 && p < i;
-          if (ok) {
-            int64_t gp = base + p;
-            ok = t.call[gp] == c - 1 && t.user[gp] == u && t.head[gp] == h;
-          }
-        }
-        if (!ok) code = max(code, int32_t(FS_E_RANGE));
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t g = base + int64_t(i) * kThreads + t;
+    const bool valid = g < tr.N;
+    uint32_t d = 0;
+    if (valid) {
+      if (g >= r_end) {
+        while (g >= tr.rep_off[r + 1]) ++r;
+        r_base = tr.rep_off[r];
+        r_end = tr.rep_off[r + 1];
+        ts_base = tr.ts[r_base];
       }
+      const int32_t u = tr.user[g], ap = tr.app[g];
+      const int64_t ts = tr.ts[g];
+      const bool ok_ids = u >= 0 && u < tr.U && ap >= 0 && ap < tr.A;
+      if (!ok_ids) code = max(code, int32_t(FS_E_RANGE));
+      if (ts < 0) code = max(code, int32_t(FS_E_RANGE));
+      if (g > r_base && tr.ts[g - 1] > ts) code = max(code, int32_t(FS_E_ORDER));
+      if (tr.call) {
+        const int32_t c = tr.call[g];
+        if (c < 0) code = max(code, int32_t(FS_E_RANGE));
+        if (a.check_chain) {
+          const int64_t li = g - r_base;
+          const int32_t hd = tr.head[g], pv = tr.prev[g];
+          bool ok;
+          if (c == 0) {
+            ok = hd == li && pv == -1;
+          } else {
+            ok = c > 0 && pv >= 0 && pv < li;
+            if (ok) {
+              const int64_t gp = r_base + pv;
+              ok = tr.call[gp] == c - 1 && tr.user[gp] == u && tr.head[gp] == hd;
+            }
+          }
+          if (!ok) code = max(code, int32_t(FS_E_RANGE));
+        }
+      }
+      const uint64_t key = ok_ids ? ((uint64_t(ap) << a.pk.Bu) | uint64_t(int64_t(r) * tr.U + u)) : 0;
+      uint64_t q = 0;
+      if (a.pk.Bq > 0) {
+        const int64_t rel = ts - ts_base;
+        q = rel > 0 ? uint64_t(rel) >> sh : 0;
+        if (q > a.pk.qmask) q = a.pk.qmask;  // only for unsorted input, which is an error
+      }
+      const uint64_t e = (key << a.pk.SK) | (uint64_t(g) << a.pk.SI) | (q << 1);
+      a.el[g] = e;
+      d = uint32_t(e >> (a.pk.SK + a.shift)) & a.mask;
     }
-    uint32_t ku = ok_ids ? uint32_t(int64_t(r) * t.U + u) : 0u;
-    uint32_t ka = ok_ids ? uint32_t(ap) : 0u;
-    a.key[g] = (ka << a.Bu) | ku;
-    a.idx[g] = uint32_t(g);
+    hist_add(h, d, valid);
   }
   if (code) raise_err(a.err, code);
+  __syncthreads();
+  if (t <= int(a.mask)) a.hist[int64_t(t) * a.tiles + blockIdx.x] = h[t];
 }
 
 // ---------------------------------------------------------------- radix sort pass
 
-__global__ void __launch_bounds__(kThreads) k_radix_hist(const uint32_t *key, int64_t N, int shift,
+__global__ void __launch_bounds__(kThreads) k_radix_hist(const uint64_t *el, int64_t N, int shift,
                                                           uint32_t mask, uint32_t *hist,
                                                           int64_t tiles) {
   __shared__ uint32_t h[kRadix];
@@ -162,32 +302,34 @@ __global__ void __launch_bounds__(kThreads) k_radix_hist(const uint32_t *key, in
   h[t] = 0;
   __syncthreads();
   const int64_t base = blockIdx.x * int64_t(kTile);
-  const int lane = t & 63;
 #pragma unroll 4
   for (int i = 0; i < kItems; ++i) {
-    int64_t e = base + i * kThreads + t;
-    bool valid = e < N;
-    uint32_t d = valid ? (key[e] >> shift) & mask : 0u;
-    // aggregate equal digits within the wave before touching LDS
-    uint64_t peers = __ballot(valid);
-    for (int b = 0; b < kRadixBits; ++b) {
-      uint64_t m = __ballot((d >> b) & 1u);
-      peers &= ((d >> b) & 1u) ? m : ~m;
-    }
-    if (valid && (peers & ((uint64_t(1) << lane) - 1)) == 0)
-      atomicAdd(&h[d], uint32_t(__popcll(peers)));
+    const int64_t e = base + i * kThreads + t;
+    const bool valid = e < N;
+    const uint32_t d = valid ? uint32_t(el[e] >> shift) & mask : 0u;
+    hist_add(h, d, valid);
   }
   __syncthreads();
-  hist[int64_t(t) * tiles + blockIdx.x] = h[t];
+  if (t <= int(mask)) hist[int64_t(t) * tiles + blockIdx.x] = h[t];
 }
 
-__global__ void __launch_bounds__(kThreads) k_radix_scatter(const uint32_t *kin,
-                                                             const uint32_t *iin, uint32_t *kout,
-                                                             uint32_t *iout, int64_t N, int shift,
-                                                             uint32_t mask, const uint32_t *offs,
-                                                             int64_t tiles) {
-  __shared__ uint32_t s_key[kTile];
-  __shared__ uint32_t s_idx[kTile];
+struct ScatterArgs {
+  const uint64_t *in;
+  uint64_t *out;
+  int64_t N;
+  int shift;  // absolute bit position of the digit in the element
+  uint32_t mask;
+  const uint32_t *offs;
+  int64_t tiles;
+  // user-limit test on the way through (the input is in user order)
+  int32_t t_user;
+  uint64_t user_mask;  // element bits of the user part of the key
+  Win win;
+};
+
+template <bool TEST_USER>
+__global__ void __launch_bounds__(kThreads) k_radix_scatter(ScatterArgs a) {
+  __shared__ uint64_t s_el[kTile];
   __shared__ uint32_t run[kRadix];
   __shared__ uint32_t wcnt[kThreads / 64][kRadix];
   __shared__ uint32_t loc[kRadix];
@@ -195,27 +337,29 @@ __global__ void __launch_bounds__(kThreads) k_radix_scatter(const uint32_t *kin,
   __shared__ uint32_t s_waves[kThreads / 64];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int64_t base = blockIdx.x * int64_t(kTile);
-  goff[t] = offs[int64_t(t) * tiles + blockIdx.x];
+  const Win win = TEST_USER ? load_win(a.win) : a.win;
+  goff[t] = t <= int(a.mask) ? a.offs[int64_t(t) * a.tiles + blockIdx.x] : 0u;
   run[t] = 0;
 #pragma unroll
   for (int w = 0; w < kThreads / 64; ++w) wcnt[w][t] = 0;
   __syncthreads();
 
-  uint32_t k_r[kItems], i_r[kItems], rank[kItems];
+  uint64_t k_r[kItems];
+  uint32_t rank[kItems];
   const uint64_t lt = (uint64_t(1) << lane) - 1;
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
-    int64_t e = base + i * kThreads + t;
-    bool valid = e < N;
-    k_r[i] = valid ? kin[e] : 0u;
-    i_r[i] = valid ? iin[e] : 0u;
-    uint32_t d = (k_r[i] >> shift) & mask;
-    uint64_t peers = __ballot(valid);
-    for (int b = 0; b < kRadixBits; ++b) {
-      uint64_t m = __ballot((d >> b) & 1u);
-      peers &= ((d >> b) & 1u) ? m : ~m;
+    const int64_t e = base + i * kThreads + t;
+    const bool valid = e < a.N;
+    uint64_t el = valid ? a.in[e] : 0u;
+    if (TEST_USER && valid && int64_t(a.t_user) <= e) {
+      const uint64_t eq = a.in[e - a.t_user];
+      if (((el ^ eq) & a.user_mask) == 0 && in_window(el, eq, win)) el |= 1u;
     }
-    uint32_t rw = uint32_t(__popcll(peers & lt));
+    k_r[i] = el;
+    const uint32_t d = uint32_t(el >> a.shift) & a.mask;
+    const uint64_t peers = digit_peers(d, valid);
+    const uint32_t rw = uint32_t(__popcll(peers & lt));
     if (valid && (peers & lt) == 0) wcnt[wave][d] = uint32_t(__popcll(peers));
     __syncthreads();
     if (valid) {
@@ -237,28 +381,23 @@ __global__ void __launch_bounds__(kThreads) k_radix_scatter(const uint32_t *kin,
   }
   // tile-local exclusive offsets of each digit
   uint32_t total;
-  uint32_t incl = block_inclusive_scan(run[t], s_waves, total);
+  const uint32_t incl = block_inclusive_scan(run[t], s_waves, total);
   loc[t] = incl - run[t];
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
     if (rank[i] != 0xffffffffu) {
-      uint32_t d = (k_r[i] >> shift) & mask;
-      uint32_t pos = loc[d] + rank[i];
-      s_key[pos] = k_r[i];
-      s_idx[pos] = i_r[i];
+      const uint32_t d = uint32_t(k_r[i] >> a.shift) & a.mask;
+      s_el[loc[d] + rank[i]] = k_r[i];
     }
   }
   __syncthreads();
-  const int64_t n_here = N - base < kTile ? N - base : kTile;
+  const int64_t n_here = a.N - base < kTile ? a.N - base : kTile;
   for (int j = t; j < n_here; j += kThreads) {
-    uint32_t k = s_key[j];
-    uint32_t d = (k >> shift) & mask;
-    uint32_t dst = goff[d] + (uint32_t(j) - loc[d]);
-    if (dst < N) {
-      kout[dst] = k;
-      iout[dst] = s_idx[j];
-    }
+    const uint64_t el = s_el[j];
+    const uint32_t d = uint32_t(el >> a.shift) & a.mask;
+    const uint32_t dst = goff[d] + (uint32_t(j) - loc[d]);
+    if (dst < a.N) a.out[dst] = el;
   }
 }
 
@@ -313,63 +452,67 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const uint32_t *in,
   }
 }
 
+// ---------------------------------------------------------------- app-limit test
 
-// ---------------------------------------------------------------- window tests
-
-struct TestArgs {
-  const uint32_t *key;
-  const uint32_t *idx;
+struct AppTestArgs {
+  const uint64_t *el;  // (user, app) order, user flag set
   int64_t N;
-  uint32_t cmp_mask;  // key bits that identify the key (user, or user and app)
-  int Bu;
-  bool per_app;       // limit from t_app[key >> Bu], else t_user
-  int32_t t_user;
   const int32_t *t_app;
   int32_t A;
-  const int64_t *ts;
-  int64_t window;
-  uint8_t *flag;      // [N] stream order
-  int32_t *cnt;       // [N] stream order, optional
+  Win win;
+  uint8_t *rr;  // [N] stream order: raw reason
 };
 
-__global__ void __launch_bounds__(kThreads) k_thr_test(TestArgs a) {
+__global__ void __launch_bounds__(kThreads) k_thr_apptest(AppTestArgs a) {
+  const Win win = load_win(a.win);
+  const Pack &pk = win.pk;
   for (int64_t p = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; p < a.N;
        p += int64_t(gridDim.x) * blockDim.x) {
-    uint32_t kp = a.key[p];
-    uint32_t k = kp & a.cmp_mask;
-    uint32_t g = a.idx[p];
-    if (g >= a.N) continue;
-    int64_t T;
-    if (a.per_app) {
-      uint32_t ap = kp >> a.Bu;
-      T = ap < uint32_t(a.A) ? a.t_app[ap] : 0;
-    } else {
-      T = a.t_user;
-    }
-    int64_t lo = a.ts[g] - a.window;  // window is (ts - W, ts]
-    uint8_t f = 0;
+    const uint64_t ep = a.el[p];
+    const uint32_t ap = uint32_t((ep >> pk.SK) >> pk.Bu);
+    const int64_t T = ap < uint32_t(a.A) ? a.t_app[ap] : 0;
+    bool fa = false;
     if (T <= p) {
-      int64_t q = p - T;
-      uint32_t gq = a.idx[q];
-      if ((a.key[q] & a.cmp_mask) == k && gq < a.N && a.ts[gq] > lo) f = 1;
+      const uint64_t eq = a.el[p - T];
+      fa = (ep >> pk.SK) == (eq >> pk.SK) && in_window(ep, eq, win);
     }
-    a.flag[g] = f;
-    if (a.cnt) {
-      // first position of this key: keys are sorted by the compared bits
-      int64_t l = 0, h = p;
-      while (l < h) {
-        int64_t m = (l + h) >> 1;
-        if ((a.key[m] & a.cmp_mask) < k) l = m + 1; else h = m;
-      }
-      // first position in [l, p] whose arrival lies in the window
-      int64_t h2 = p;
-      while (l < h2) {
-        int64_t m = (l + h2) >> 1;
-        uint32_t gm = a.idx[m];
-        if (gm < a.N && a.ts[gm] > lo) h2 = m; else l = m + 1;
-      }
-      a.cnt[g] = int32_t(p - l + 1);
+    const uint8_t code = (ep & 1u) ? 1 : (fa ? 2 : 0);
+    a.rr[(ep >> pk.SI) & pk.imask] = code;
+  }
+}
+
+// ---------------------------------------------------------------- window counts (optional)
+
+struct CountArgs {
+  const uint64_t *el;  // key order in which every compared key is contiguous
+  int64_t N;
+  uint64_t key_mask;   // element bits compared
+  Win win;
+  int32_t *cnt;        // [N] stream order
+};
+
+// cnt = p - (first position of the key whose arrival is still in the window) + 1,
+// by binary search over the exact arrival times.
+__global__ void __launch_bounds__(kThreads) k_thr_count(CountArgs a) {
+  const Pack &pk = a.win.pk;
+  for (int64_t p = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; p < a.N;
+       p += int64_t(gridDim.x) * blockDim.x) {
+    const uint64_t ep = a.el[p];
+    const uint64_t k = ep & a.key_mask;
+    const int64_t gp = int64_t((ep >> pk.SI) & pk.imask);
+    const int64_t lo_ts = a.win.ts[gp] - a.win.W;  // window is (ts - W, ts]
+    int64_t l = 0, h = p;
+    while (l < h) {
+      const int64_t m = (l + h) >> 1;
+      if ((a.el[m] & a.key_mask) < k) l = m + 1; else h = m;
     }
+    int64_t h2 = p;
+    while (l < h2) {
+      const int64_t m = (l + h2) >> 1;
+      const int64_t gm = int64_t((a.el[m] >> pk.SI) & pk.imask);
+      if (a.win.ts[gm] > lo_ts) h2 = m; else l = m + 1;
+    }
+    a.cnt[gp] = int32_t(p - l + 1);
   }
 }
 
@@ -377,7 +520,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_test(TestArgs a) {
 
 struct CombineArgs {
   DevTrace t;
-  const uint8_t *eu, *ea;
+  const uint8_t *rr;
   const uint8_t *overloaded;
   bool raw;
   uint32_t *bitmap;
@@ -385,38 +528,34 @@ struct CombineArgs {
   int64_t n_words;
 };
 
-__device__ inline uint8_t raw_reason(const CombineArgs &a, int64_t g) {
-  return a.eu[g] ? 1 : (a.ea[g] ? 2 : 0);
-}
-
 __global__ void __launch_bounds__(kThreads) k_thr_combine(CombineArgs a) {
   const int64_t N = a.t.N;
   const int lane = threadIdx.x & 63;
   for (int64_t base = blockIdx.x * int64_t(blockDim.x); base < N;
        base += int64_t(gridDim.x) * blockDim.x) {
-    int64_t g = base + threadIdx.x;
+    const int64_t g = base + threadIdx.x;
     uint8_t code = 0;
     if (g < N) {
-      uint8_t rr = raw_reason(a, g);
+      const uint8_t rr = a.rr[g];
       if (a.raw) {
         code = rr;
       } else if (!a.t.call || a.t.call[g] == 0) {
-        bool over = a.overloaded ? a.overloaded[g] != 0 : true;
+        const bool over = a.overloaded ? a.overloaded[g] != 0 : true;
         code = over ? rr : 0;
       } else {
-        int32_t r = replica_of(a.t.rep_off, a.t.R, g);
-        int64_t lo = a.t.rep_off[r], hi = a.t.rep_off[r + 1];
-        int64_t h = lo + a.t.head[g];
+        const int32_t r = replica_of(a.t.rep_off, a.t.R, g);
+        const int64_t lo = a.t.rep_off[r], hi = a.t.rep_off[r + 1];
+        const int64_t h = lo + a.t.head[g];
         if (h >= lo && h < hi) {
-          bool hover = a.overloaded ? a.overloaded[h] != 0 : true;
-          code = (hover && raw_reason(a, h) != 0) ? 3 : 0;
+          const bool hover = a.overloaded ? a.overloaded[h] != 0 : true;
+          code = (hover && a.rr[h] != 0) ? 3 : 0;
         }
       }
       if (a.reason) a.reason[g] = code;
     }
-    uint64_t bits = __ballot(g < N && code != 0);
+    const uint64_t bits = __ballot(g < N && code != 0);
     if (lane == 0) {
-      int64_t w = (base + (threadIdx.x & ~63)) >> 5;
+      const int64_t w = (base + (threadIdx.x & ~63)) >> 5;
       if (w < a.n_words) a.bitmap[w] = uint32_t(bits);
       if (w + 1 < a.n_words) a.bitmap[w + 1] = uint32_t(bits >> 32);
     }
@@ -449,53 +588,80 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
                            uint32_t flags, uint32_t *bitmap, uint8_t *reason, int32_t *cnt_user,
                            int32_t *cnt_app, void *ws, int32_t *err, hipStream_t s) {
   Layout L = layout(t);
-  if (L.Bu + L.Ba > 32) return hipErrorInvalidValue;
+  const Pack &pk = L.pk;
+  if (pk.Bk > 32 || pk.Bk + pk.Bi + 1 > 64) return hipErrorInvalidValue;
   if (L.N == 0) return hipSuccess;
   char *w = static_cast<char *>(ws);
-  uint32_t *keyA = reinterpret_cast<uint32_t *>(w + L.off_keyA);
-  uint32_t *idxA = reinterpret_cast<uint32_t *>(w + L.off_idxA);
-  uint32_t *keyB = reinterpret_cast<uint32_t *>(w + L.off_keyB);
-  uint32_t *idxB = reinterpret_cast<uint32_t *>(w + L.off_idxB);
-  uint8_t *eu = reinterpret_cast<uint8_t *>(w + L.off_eu);
-  uint8_t *ea = reinterpret_cast<uint8_t *>(w + L.off_ea);
+  uint64_t *A = reinterpret_cast<uint64_t *>(w + L.off_a);
+  uint64_t *B = reinterpret_cast<uint64_t *>(w + L.off_b);
+  uint8_t *rr = reinterpret_cast<uint8_t *>(w + L.off_rr);
   uint32_t *hist = reinterpret_cast<uint32_t *>(w + L.off_hist);
   uint32_t *part = reinterpret_cast<uint32_t *>(w + L.off_part);
   int32_t *tapp = reinterpret_cast<int32_t *>(w + L.off_tapp);
+  int32_t *sh = reinterpret_cast<int32_t *>(w + L.off_sh);
   const bool raw = (flags & FS_THROTTLE_RAW) != 0;
   hipError_t e = hipMemcpyAsync(tapp, lim->t_app_h, sizeof(int32_t) * t->n_apps,
                                 hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return e;
+  const DevTrace dt = dev_trace(t);
+  hipLaunchKernelGGL(k_thr_span, dim3(1), dim3(kThreads), 0, s, dt.rep_off, dt.ts, dt.R, pk.Bq, sh);
 
-  InitArgs ia{dev_trace(t), L.Bu, !raw, keyA, idxA, err};
-  hipLaunchKernelGGL(k_thr_init, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ia);
-
-  uint32_t *kin = keyA, *iin = idxA, *kout = keyB, *iout = idxB;
-  auto pass = [&](int shift, int width) {
-    uint32_t mask = (1u << width) - 1u;
-    hipLaunchKernelGGL(k_radix_hist, dim3(L.tiles), dim3(kThreads), 0, s, kin, L.N, shift, mask,
-                       hist, L.tiles);
-    (void)exclusive_scan(hist, int64_t(kRadix) * L.tiles, part, s);
-    hipLaunchKernelGGL(k_radix_scatter, dim3(L.tiles), dim3(kThreads), 0, s, kin, iin, kout,
-                       iout, L.N, shift, mask, hist, L.tiles);
-    uint32_t *tk = kin, *ti = iin;
-    kin = kout; iin = iout; kout = tk; iout = ti;
-  };
-  for (int sh = 0; sh < L.Bu; sh += kRadixBits) pass(sh, L.Bu - sh < kRadixBits ? L.Bu - sh : kRadixBits);
-
-  const uint32_t umask = L.Bu >= 32 ? 0xffffffffu : ((1u << L.Bu) - 1u);
-  TestArgs ta{kin, iin, L.N, umask, L.Bu, false, lim->t_user, tapp, t->n_apps, t->ts_us,
-              lim->window_us, eu, cnt_user};
-  hipLaunchKernelGGL(k_thr_test, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ta);
-
-  for (int sh = L.Bu; sh < L.Bu + L.Ba; sh += kRadixBits) {
-    int end = L.Bu + L.Ba;
-    pass(sh, end - sh < kRadixBits ? end - sh : kRadixBits);
+  // digits: the user bits in passes of at most kRadixBits, then the app bits
+  struct Digit { int shift, width; };
+  Digit dig[8];
+  int nd = 0, n_user = 0;
+  for (int b0 = 0, left = pk.Bu; left > 0;) {
+    const int passes = (left + kRadixBits - 1) / kRadixBits;
+    const int wd = (left + passes - 1) / passes;
+    dig[nd++] = {b0, wd};
+    b0 += wd;
+    left -= wd;
   }
-  TestArgs tb{kin, iin, L.N, 0xffffffffu, L.Bu, true, lim->t_user, tapp, t->n_apps, t->ts_us,
-              lim->window_us, ea, cnt_app};
-  hipLaunchKernelGGL(k_thr_test, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, tb);
+  n_user = nd;
+  for (int b0 = pk.Bu, left = pk.Ba; left > 0;) {
+    const int passes = (left + kRadixBits - 1) / kRadixBits;
+    const int wd = (left + passes - 1) / passes;
+    dig[nd++] = {b0, wd};
+    b0 += wd;
+    left -= wd;
+  }
 
-  CombineArgs ca{dev_trace(t), eu, ea, overloaded, raw, bitmap, reason, (L.N + 31) / 32};
+  InitArgs ia{dt, pk, !raw, sh, A, dig[0].shift, (1u << dig[0].width) - 1u, hist, L.tiles, err};
+  hipLaunchKernelGGL(k_thr_init, dim3(L.tiles), dim3(kThreads), 0, s, ia);
+
+  const Win win{lim->window_us, sh, 0, pk.Bq > 0, pk, dt.ts};
+
+  const uint64_t user_mask = ((uint64_t(1) << pk.Bu) - 1) << pk.SK;
+  uint64_t *in = A, *out = B;
+  for (int k = 0; k < nd; ++k) {
+    const uint32_t mask = (1u << dig[k].width) - 1u;
+    const int shift = pk.SK + dig[k].shift;
+    if (k > 0)
+      hipLaunchKernelGGL(k_radix_hist, dim3(L.tiles), dim3(kThreads), 0, s, in, L.N, shift, mask,
+                         hist, L.tiles);
+    (void)exclusive_scan(hist, int64_t(mask + 1) * L.tiles, part, s);
+    if (k == n_user && cnt_user) {
+      CountArgs ca{in, L.N, user_mask, win, cnt_user};
+      hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
+    }
+    ScatterArgs sa{in, out, L.N, shift, mask, hist, L.tiles, lim->t_user, user_mask, win};
+    if (k == n_user)
+      hipLaunchKernelGGL(k_radix_scatter<true>, dim3(L.tiles), dim3(kThreads), 0, s, sa);
+    else
+      hipLaunchKernelGGL(k_radix_scatter<false>, dim3(L.tiles), dim3(kThreads), 0, s, sa);
+    uint64_t *tmp = in;
+    in = out;
+    out = tmp;
+  }
+  AppTestArgs aa{in, L.N, tapp, t->n_apps, win, rr};
+  hipLaunchKernelGGL(k_thr_apptest, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, aa);
+  if (cnt_app) {
+    const uint64_t key_mask = ((uint64_t(1) << pk.Bk) - 1) << pk.SK;
+    CountArgs ca{in, L.N, key_mask, win, cnt_app};
+    hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
+  }
+
+  CombineArgs ca{dt, rr, overloaded, raw, bitmap, reason, (L.N + 31) / 32};
   hipLaunchKernelGGL(k_thr_combine, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
   return hipGetLastError();
 }

@@ -88,3 +88,25 @@ def test_errors_match_oracle():
     with pytest.raises(fs.FairServeError) as ge:
         gpu_throttle(bad2, 10, 1, [1, 1])
     assert ge.value.code == fs.FS_E_RANGE
+
+
+@pytest.mark.parametrize("jump_bits", [40, 52])
+def test_coarse_time_field(jump_bits):
+    # Arrival times spanning far more than the element's time field force a coarse
+    # (shifted) time; gaps at W - 1, W and W + 1 make the quantised test undecided,
+    # so the exact-time fallback decides them.
+    rng = np.random.default_rng(jump_bits)
+    n, U, A, W = 6000, 7, 3, 1000
+    gaps = rng.choice(np.array([0, 1, W - 1, W, W + 1, 7, 333], np.int64), size=n)
+    jumps = rng.random(n) < 0.01
+    gaps[jumps] = np.int64(1) << jump_bits
+    gaps[0] = 5
+    ts = np.cumsum(gaps).astype(np.int64)
+    assert int(ts[-1]) < 2 ** 62
+    user = rng.integers(0, U, size=n).astype(np.int32)
+    app = rng.integers(0, A, size=n).astype(np.int32)
+    tr = tg.Trace(1, U, A, np.array([0, n], np.int64), ts, user, app, None, None, None,
+                  None, None, None)
+    say("throttle coarse time", jump_bits, int(ts[-1]).bit_length())
+    _check(tr, W, 2, [1, 2, 3])
+    _check(tr, W, 2**31 - 1, [0, 4, 1], raw=False)

@@ -327,68 +327,76 @@ struct ScatterArgs {
   Win win;
 };
 
+// Stable scatter of one tile.  Wave w owns the contiguous sub-tile
+// [w * kWaveSpan, (w + 1) * kWaveSpan) and ranks its rows in order against a
+// wave-private digit counter, so the tile needs only a handful of barriers; the
+// waves' counts then give each digit's offset per wave and per tile.
+constexpr int kWaves = kThreads / 64;
+constexpr int kWaveSpan = kTile / kWaves;  // 1024 records, kItems rows of 64
+
 template <bool TEST_USER>
 __global__ void __launch_bounds__(kThreads) k_radix_scatter(ScatterArgs a) {
   __shared__ uint64_t s_el[kTile];
-  __shared__ uint32_t run[kRadix];
-  __shared__ uint32_t wcnt[kThreads / 64][kRadix];
+  __shared__ uint32_t cnt[kWaves][kRadix];
   __shared__ uint32_t loc[kRadix];
   __shared__ uint32_t goff[kRadix];
-  __shared__ uint32_t s_waves[kThreads / 64];
+  __shared__ uint32_t s_waves[kWaves];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int64_t base = blockIdx.x * int64_t(kTile);
+  const int64_t wbase = base + int64_t(wave) * kWaveSpan;
   const Win win = TEST_USER ? load_win(a.win) : a.win;
   goff[t] = t <= int(a.mask) ? a.offs[int64_t(t) * a.tiles + blockIdx.x] : 0u;
-  run[t] = 0;
 #pragma unroll
-  for (int w = 0; w < kThreads / 64; ++w) wcnt[w][t] = 0;
+  for (int w = 0; w < kWaves; ++w) cnt[w][t] = 0;
   __syncthreads();
 
   uint64_t k_r[kItems];
-  uint32_t rank[kItems];
-  const uint64_t lt = (uint64_t(1) << lane) - 1;
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
-    const int64_t e = base + i * kThreads + t;
-    const bool valid = e < a.N;
-    uint64_t el = valid ? a.in[e] : 0u;
-    if (TEST_USER && valid && int64_t(a.t_user) <= e) {
-      const uint64_t eq = a.in[e - a.t_user];
-      if (((el ^ eq) & a.user_mask) == 0 && in_window(el, eq, win)) el |= 1u;
-    }
-    k_r[i] = el;
-    const uint32_t d = uint32_t(el >> a.shift) & a.mask;
-    const uint64_t peers = digit_peers(d, valid);
-    const uint32_t rw = uint32_t(__popcll(peers & lt));
-    if (valid && (peers & lt) == 0) wcnt[wave][d] = uint32_t(__popcll(peers));
-    __syncthreads();
-    if (valid) {
-      uint32_t r = run[d] + rw;
-      for (int w = 0; w < wave; ++w) r += wcnt[w][d];
-      rank[i] = r;
-    } else {
-      rank[i] = 0xffffffffu;
-    }
-    __syncthreads();
-    uint32_t add = 0;
-#pragma unroll
-    for (int w = 0; w < kThreads / 64; ++w) {
-      add += wcnt[w][t];
-      wcnt[w][t] = 0;
-    }
-    run[t] += add;
-    __syncthreads();
+    const int64_t e = wbase + i * 64 + lane;
+    k_r[i] = e < a.N ? a.in[e] : 0u;
   }
-  // tile-local exclusive offsets of each digit
+  if (TEST_USER) {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int64_t e = wbase + i * 64 + lane;
+      if (e < a.N && int64_t(a.t_user) <= e) {
+        const uint64_t eq = a.in[e - a.t_user];
+        if (((k_r[i] ^ eq) & a.user_mask) == 0 && in_window(k_r[i], eq, win)) k_r[i] |= 1u;
+      }
+    }
+  }
+  uint32_t rank[kItems];
+  const uint64_t lt = (uint64_t(1) << lane) - 1;
+  uint32_t *my = cnt[wave];
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t e = wbase + i * 64 + lane;
+    const bool valid = e < a.N;
+    const uint32_t d = uint32_t(k_r[i] >> a.shift) & a.mask;
+    const uint64_t peers = digit_peers(d, valid);
+    const uint32_t before = valid ? my[d] : 0u;  // this wave's earlier rows with digit d
+    rank[i] = valid ? before + uint32_t(__popcll(peers & lt)) : 0xffffffffu;
+    if (valid && (peers & lt) == 0) my[d] = before + uint32_t(__popcll(peers));
+  }
+  __syncthreads();
+  // per digit: offsets of the waves within the digit, then tile-local digit offsets
+  uint32_t tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t c = cnt[w][t];
+    cnt[w][t] = tot;
+    tot += c;
+  }
   uint32_t total;
-  const uint32_t incl = block_inclusive_scan(run[t], s_waves, total);
-  loc[t] = incl - run[t];
+  const uint32_t incl = block_inclusive_scan(tot, s_waves, total);
+  loc[t] = incl - tot;
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
     if (rank[i] != 0xffffffffu) {
       const uint32_t d = uint32_t(k_r[i] >> a.shift) & a.mask;
-      s_el[loc[d] + rank[i]] = k_r[i];
+      s_el[loc[d] + my[d] + rank[i]] = k_r[i];
     }
   }
   __syncthreads();

@@ -90,7 +90,7 @@ Layout layout(const fs_trace *t) {
   size_t o = 0;
   L.off_a = o; o += up(n * 8);
   L.off_b = o; o += up(n * 8);
-  L.off_rr = o; o += up(n);
+  L.off_rr = o; o += up((n + 15) / 16 * 4);
   L.off_hist = o; o += up(hist_len * 4);
   L.off_part = o; o += up(((hist_len + kScanChunk - 1) / kScanChunk + 1) * 4);
   L.off_tapp = o; o += up(kMaxApps * 4);
@@ -128,22 +128,37 @@ __device__ uint32_t block_inclusive_scan(uint32_t v, uint32_t *s_waves, uint32_t
   return x + before;
 }
 
-// Lanes of the wave holding the same digit as this lane (ballot per digit bit).
-__device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
+// Lanes of the wave holding the same digit as this lane (one ballot per digit bit;
+// `width` is the digit's bit count, at most kRadixBits).
+__device__ inline uint64_t digit_peers(uint32_t d, bool valid, int width) {
   uint64_t peers = __ballot(valid);
-#pragma unroll
-  for (int b = 0; b < kRadixBits; ++b) {
+  for (int b = 0; b < width; ++b) {
     const uint64_t m = __ballot((d >> b) & 1u);
     peers &= ((d >> b) & 1u) ? m : ~m;
   }
   return peers;
 }
 
+__host__ __device__ inline int mask_width(uint32_t mask) {
+  int w = 0;
+  while (w < 32 && (mask >> w) != 0) ++w;
+  return w;
+}
+
 // Adds one item row to the tile histogram in LDS (equal digits aggregated per wave).
-__device__ inline void hist_add(uint32_t *h, uint32_t d, bool valid) {
+__device__ inline void hist_add(uint32_t *h, uint32_t d, bool valid, int width) {
   const int lane = threadIdx.x & 63;
-  const uint64_t peers = digit_peers(d, valid);
+  const uint64_t peers = digit_peers(d, valid, width);
   if (valid && (peers & ((uint64_t(1) << lane) - 1)) == 0) atomicAdd(&h[d], uint32_t(__popcll(peers)));
+}
+
+// Work-groups are dealt to the 8 XCDs round robin (block b runs on XCD b % 8).  This
+// maps blocks to tiles so that each XCD sweeps one contiguous range of tiles in
+// order; a record's interaction links then point mostly into data that XCD's own
+// L2 has just cached.
+__device__ inline int64_t xcd_tile(int64_t b, int64_t n) {
+  const int64_t x = b & 7, i = b >> 3, per = n >> 3, extra = n & 7;
+  return x * per + (x < extra ? x : extra) + i;
 }
 
 // ---------------------------------------------------------------- window test
@@ -229,11 +244,13 @@ __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
   __shared__ int32_t s_r0;
   const int t = threadIdx.x;
   const DevTrace &tr = a.t;
-  const int64_t base = blockIdx.x * int64_t(kTile);
+  const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int64_t base = tile * kTile;
   h[t] = 0;
   if (t == 0) s_r0 = replica_of(tr.rep_off, tr.R, base);
   __syncthreads();
   const int sh = *a.sh;
+  const int width = mask_width(a.mask);
   int32_t r = s_r0;
   int64_t r_end = tr.rep_off[r + 1], r_base = tr.rep_off[r];
   int64_t ts_base = tr.ts[r_base];
@@ -285,11 +302,11 @@ __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
       a.el[g] = e;
       d = uint32_t(e >> (a.pk.SK + a.shift)) & a.mask;
     }
-    hist_add(h, d, valid);
+    hist_add(h, d, valid, width);
   }
   if (code) raise_err(a.err, code);
   __syncthreads();
-  if (t <= int(a.mask)) a.hist[int64_t(t) * a.tiles + blockIdx.x] = h[t];
+  if (t <= int(a.mask)) a.hist[int64_t(t) * a.tiles + tile] = h[t];
 }
 
 // ---------------------------------------------------------------- radix sort pass
@@ -302,12 +319,13 @@ __global__ void __launch_bounds__(kThreads) k_radix_hist(const uint64_t *el, int
   h[t] = 0;
   __syncthreads();
   const int64_t base = blockIdx.x * int64_t(kTile);
+  const int width = mask_width(mask);
 #pragma unroll 4
   for (int i = 0; i < kItems; ++i) {
     const int64_t e = base + i * kThreads + t;
     const bool valid = e < N;
     const uint32_t d = valid ? uint32_t(el[e] >> shift) & mask : 0u;
-    hist_add(h, d, valid);
+    hist_add(h, d, valid, width);
   }
   __syncthreads();
   if (t <= int(mask)) hist[int64_t(t) * tiles + blockIdx.x] = h[t];
@@ -369,12 +387,13 @@ __global__ void __launch_bounds__(kThreads) k_radix_scatter(ScatterArgs a) {
   uint32_t rank[kItems];
   const uint64_t lt = (uint64_t(1) << lane) - 1;
   uint32_t *my = cnt[wave];
+  const int width = mask_width(a.mask);
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
     const int64_t e = wbase + i * 64 + lane;
     const bool valid = e < a.N;
     const uint32_t d = uint32_t(k_r[i] >> a.shift) & a.mask;
-    const uint64_t peers = digit_peers(d, valid);
+    const uint64_t peers = digit_peers(d, valid, width);
     const uint32_t before = valid ? my[d] : 0u;  // this wave's earlier rows with digit d
     rank[i] = valid ? before + uint32_t(__popcll(peers & lt)) : 0xffffffffu;
     if (valid && (peers & lt) == 0) my[d] = before + uint32_t(__popcll(peers));
@@ -462,31 +481,136 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const uint32_t *in,
 
 // ---------------------------------------------------------------- app-limit test
 
+// The app limit is tested in (user, app) order and the raw reason goes back to
+// stream order in two coalesced steps instead of one random byte store per record:
+// each tile scatters compact words (index low bits << 2 | reason) into buckets by
+// the high bits of the index (a stable radix pass), then one work-group per bucket
+// assembles its contiguous stream range in LDS and writes it out.
+constexpr int kUnsortBits = 18;  // stream records per unsort chunk: 2^18, 2 bits each in LDS
+
 struct AppTestArgs {
   const uint64_t *el;  // (user, app) order, user flag set
   int64_t N;
   const int32_t *t_app;
   int32_t A;
   Win win;
-  uint8_t *rr;  // [N] stream order: raw reason
+  int bs;              // bucket = index >> bs
+  uint32_t mask;       // bucket digit mask
+  const uint32_t *offs;
+  int64_t tiles;
+  uint32_t *out;       // [N] words grouped by bucket
 };
 
 __global__ void __launch_bounds__(kThreads) k_thr_apptest(AppTestArgs a) {
+  __shared__ uint32_t s_w[kTile];
+  __shared__ uint8_t s_d[kTile];
+  __shared__ uint32_t cnt[kWaves][kRadix];
+  __shared__ uint32_t loc[kRadix];
+  __shared__ uint32_t goff[kRadix];
+  __shared__ uint32_t s_waves[kWaves];
   const Win win = load_win(a.win);
   const Pack &pk = win.pk;
-  for (int64_t p = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; p < a.N;
-       p += int64_t(gridDim.x) * blockDim.x) {
-    const uint64_t ep = a.el[p];
-    const uint32_t ap = uint32_t((ep >> pk.SK) >> pk.Bu);
-    const int64_t T = ap < uint32_t(a.A) ? a.t_app[ap] : 0;
-    bool fa = false;
-    if (T <= p) {
-      const uint64_t eq = a.el[p - T];
-      fa = (ep >> pk.SK) == (eq >> pk.SK) && in_window(ep, eq, win);
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int64_t base = blockIdx.x * int64_t(kTile);
+  const int64_t wbase = base + int64_t(wave) * kWaveSpan;
+  goff[t] = t <= int(a.mask) ? a.offs[int64_t(t) * a.tiles + blockIdx.x] : 0u;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) cnt[w][t] = 0;
+  __syncthreads();
+
+  uint32_t wd[kItems], dg[kItems];
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t p = wbase + i * 64 + lane;
+    wd[i] = 0;
+    dg[i] = 0;
+    if (p < a.N) {
+      const uint64_t ep = a.el[p];
+      const uint32_t ap = uint32_t((ep >> pk.SK) >> pk.Bu);
+      const int64_t T = ap < uint32_t(a.A) ? a.t_app[ap] : 0;
+      bool fa = false;
+      if (T <= p) {
+        const uint64_t eq = a.el[p - T];
+        fa = (ep >> pk.SK) == (eq >> pk.SK) && in_window(ep, eq, win);
+      }
+      const uint32_t code = (ep & 1u) ? 1u : (fa ? 2u : 0u);
+      const uint64_t g = (ep >> pk.SI) & pk.imask;
+      wd[i] = (uint32_t(g & ((uint64_t(1) << a.bs) - 1)) << 2) | code;
+      dg[i] = uint32_t(g >> a.bs) & a.mask;
     }
-    const uint8_t code = (ep & 1u) ? 1 : (fa ? 2 : 0);
-    a.rr[(ep >> pk.SI) & pk.imask] = code;
   }
+  uint32_t rank[kItems];
+  const uint64_t lt = (uint64_t(1) << lane) - 1;
+  uint32_t *my = cnt[wave];
+  const int width = mask_width(a.mask);
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const bool valid = wbase + i * 64 + lane < a.N;
+    const uint64_t peers = digit_peers(dg[i], valid, width);
+    const uint32_t before = valid ? my[dg[i]] : 0u;
+    rank[i] = valid ? before + uint32_t(__popcll(peers & lt)) : 0xffffffffu;
+    if (valid && (peers & lt) == 0) my[dg[i]] = before + uint32_t(__popcll(peers));
+  }
+  __syncthreads();
+  uint32_t tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t c = cnt[w][t];
+    cnt[w][t] = tot;
+    tot += c;
+  }
+  uint32_t total;
+  const uint32_t incl = block_inclusive_scan(tot, s_waves, total);
+  loc[t] = incl - tot;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kItems; ++i)
+    if (rank[i] != 0xffffffffu) {
+      const uint32_t pos = loc[dg[i]] + my[dg[i]] + rank[i];
+      s_w[pos] = wd[i];
+      s_d[pos] = uint8_t(dg[i]);
+    }
+  __syncthreads();
+  const int64_t n_here = a.N - base < kTile ? a.N - base : kTile;
+  for (int j = t; j < n_here; j += kThreads) {
+    const uint32_t d = s_d[j];
+    const uint32_t dst = goff[d] + (uint32_t(j) - loc[d]);
+    if (dst < a.N) a.out[dst] = s_w[j];
+  }
+}
+
+struct UnsortArgs {
+  const uint32_t *words;   // grouped by bucket
+  const uint32_t *offs;    // bucket starts at offs[bucket * tiles]
+  int64_t tiles;
+  int32_t n_buckets;
+  int64_t N;
+  int bs;                  // records per bucket: 2^bs, bs >= 4
+  int chunks;              // chunks of 2^kUnsortBits records per bucket
+  uint32_t *rr;            // [ceil(N/16)] raw reasons in stream order, 2 bits each
+};
+
+__global__ void __launch_bounds__(1024) k_thr_unsort(UnsortArgs a) {
+  __shared__ uint32_t codes[(1 << kUnsortBits) / 16];
+  const int32_t b = blockIdx.x / a.chunks, c = blockIdx.x % a.chunks;
+  const int csh = a.bs > kUnsortBits ? kUnsortBits : a.bs;  // records per chunk: 2^csh
+  for (int j = threadIdx.x; j < (1 << csh) / 16 + 1 && j < (1 << kUnsortBits) / 16; j += 1024)
+    codes[j] = 0;
+  __syncthreads();
+  const int64_t start = a.offs[int64_t(b) * a.tiles];
+  const int64_t stop = b + 1 < a.n_buckets ? int64_t(a.offs[int64_t(b + 1) * a.tiles]) : a.N;
+  for (int64_t k = start + threadIdx.x; k < stop; k += 1024) {
+    const uint32_t w = a.words[k];
+    const uint32_t lo = w >> 2;
+    if (int(lo >> csh) != c) continue;
+    const uint32_t o = lo & ((1u << csh) - 1);
+    atomicOr(&codes[o >> 4], (w & 3u) << ((o & 15) * 2));
+  }
+  __syncthreads();
+  // chunk starts are multiples of 16 records, so whole words belong to one chunk
+  const int64_t g0 = (int64_t(b) << a.bs) + (int64_t(c) << csh);
+  const int64_t n = a.N - g0 < (int64_t(1) << csh) ? a.N - g0 : (int64_t(1) << csh);
+  for (int64_t j = threadIdx.x; j < (n + 15) >> 4; j += 1024) a.rr[(g0 >> 4) + j] = codes[j];
 }
 
 // ---------------------------------------------------------------- window counts (optional)
@@ -528,7 +652,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_count(CountArgs a) {
 
 struct CombineArgs {
   DevTrace t;
-  const uint8_t *rr;
+  const uint32_t *rr;  // 2-bit raw reasons, 16 per word
   const uint8_t *overloaded;
   bool raw;
   uint32_t *bitmap;
@@ -536,15 +660,18 @@ struct CombineArgs {
   int64_t n_words;
 };
 
+constexpr int kCombineSpan = kThreads * 16;  // records per combine block
+
 __global__ void __launch_bounds__(kThreads) k_thr_combine(CombineArgs a) {
   const int64_t N = a.t.N;
   const int lane = threadIdx.x & 63;
-  for (int64_t base = blockIdx.x * int64_t(blockDim.x); base < N;
-       base += int64_t(gridDim.x) * blockDim.x) {
+  const int64_t start = xcd_tile(blockIdx.x, gridDim.x) * kCombineSpan;
+  const int64_t stop = start + kCombineSpan < N ? start + kCombineSpan : N;
+  for (int64_t base = start; base < stop; base += blockDim.x) {
     const int64_t g = base + threadIdx.x;
     uint8_t code = 0;
     if (g < N) {
-      const uint8_t rr = a.rr[g];
+      const uint8_t rr = uint8_t((a.rr[g >> 4] >> ((g & 15) * 2)) & 3u);
       if (a.raw) {
         code = rr;
       } else if (!a.t.call || a.t.call[g] == 0) {
@@ -556,7 +683,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_combine(CombineArgs a) {
         const int64_t h = lo + a.t.head[g];
         if (h >= lo && h < hi) {
           const bool hover = a.overloaded ? a.overloaded[h] != 0 : true;
-          code = (hover && a.rr[h] != 0) ? 3 : 0;
+          code = (hover && ((a.rr[h >> 4] >> ((h & 15) * 2)) & 3u) != 0) ? 3 : 0;
         }
       }
       if (a.reason) a.reason[g] = code;
@@ -602,7 +729,7 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   char *w = static_cast<char *>(ws);
   uint64_t *A = reinterpret_cast<uint64_t *>(w + L.off_a);
   uint64_t *B = reinterpret_cast<uint64_t *>(w + L.off_b);
-  uint8_t *rr = reinterpret_cast<uint8_t *>(w + L.off_rr);
+  uint32_t *rrw = reinterpret_cast<uint32_t *>(w + L.off_rr);
   uint32_t *hist = reinterpret_cast<uint32_t *>(w + L.off_hist);
   uint32_t *part = reinterpret_cast<uint32_t *>(w + L.off_part);
   int32_t *tapp = reinterpret_cast<int32_t *>(w + L.off_tapp);
@@ -661,16 +788,30 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
     in = out;
     out = tmp;
   }
-  AppTestArgs aa{in, L.N, tapp, t->n_apps, win, rr};
-  hipLaunchKernelGGL(k_thr_apptest, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, aa);
+  {
+    // app test in (user, app) order, results bucketed by the index's high bits
+    const int bs = pk.Bi - kRadixBits > 4 ? pk.Bi - kRadixBits : 4;
+    const uint32_t bmask = pk.Bi > bs ? (1u << (pk.Bi - bs)) - 1u : 0u;
+    const int32_t n_buckets = int32_t((L.N + (int64_t(1) << bs) - 1) >> bs);
+    hipLaunchKernelGGL(k_radix_hist, dim3(L.tiles), dim3(kThreads), 0, s, in, L.N, pk.SI + bs,
+                       bmask, hist, L.tiles);
+    (void)exclusive_scan(hist, int64_t(bmask + 1) * L.tiles, part, s);
+    uint32_t *words = reinterpret_cast<uint32_t *>(out);  // the free sort buffer
+    AppTestArgs aa{in, L.N, tapp, t->n_apps, win, bs, bmask, hist, L.tiles, words};
+    hipLaunchKernelGGL(k_thr_apptest, dim3(L.tiles), dim3(kThreads), 0, s, aa);
+    const int chunks = bs > kUnsortBits ? 1 << (bs - kUnsortBits) : 1;
+    UnsortArgs ua{words, hist, L.tiles, n_buckets, L.N, bs, chunks, rrw};
+    hipLaunchKernelGGL(k_thr_unsort, dim3(n_buckets * chunks), dim3(1024), 0, s, ua);
+  }
   if (cnt_app) {
     const uint64_t key_mask = ((uint64_t(1) << pk.Bk) - 1) << pk.SK;
     CountArgs ca{in, L.N, key_mask, win, cnt_app};
     hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
   }
 
-  CombineArgs ca{dt, rr, overloaded, raw, bitmap, reason, (L.N + 31) / 32};
-  hipLaunchKernelGGL(k_thr_combine, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
+  CombineArgs ca{dt, rrw, overloaded, raw, bitmap, reason, (L.N + 31) / 32};
+  hipLaunchKernelGGL(k_thr_combine, dim3((L.N + kCombineSpan - 1) / kCombineSpan), dim3(kThreads),
+                     0, s, ca);
   return hipGetLastError();
 }
 

@@ -31,7 +31,7 @@ namespace fs {
 namespace {
 
 constexpr uint64_t kMagic = 0x32535652'49414646ull;
-constexpr int32_t kVersion = 2;
+constexpr int32_t kVersion = 3;
 constexpr uint64_t kTierShift = 62;
 constexpr uint64_t kValMask = (uint64_t(1) << 62) - 1;
 constexpr uint64_t kEmptyKey = ~uint64_t(0);
@@ -59,7 +59,8 @@ struct StateLayout {
       seg_succ;
   // global-memory scheduler structures (n_r + 1 entries per replica, at rep_off[r] + r)
   size_t xkey, xuser, xq, xfh, xft, xhh, xht, xsb, xrh, xrdy;
-  size_t e_rec, e_tok, e_cost, e_succ, e_next, e_sv, e_scost, e_stok, e_ssucc, e_free;
+  size_t e_all, e_free;
+  size_t emap;  // per record: the pool entry it last occupied (checked before use)
   size_t total;
 };
 
@@ -95,16 +96,9 @@ StateLayout state_layout(int32_t R, int32_t U, int64_t N) {
   L.xsb = take(nr * 4);
   L.xrh = take(nr * 4);
   L.xrdy = take(nr * 4);
-  L.e_rec = take(nr * 4);
-  L.e_tok = take(nr * 4);
-  L.e_cost = take(nr * 8);
-  L.e_succ = take(nr * 4);
-  L.e_next = take(nr * 4);
-  L.e_sv = take(nr * 4);
-  L.e_scost = take(nr * 8);
-  L.e_stok = take(nr * 4);
-  L.e_ssucc = take(nr * 4);
+  L.e_all = take(nr * 48);
   L.e_free = take(nr * 4);
+  L.emap = take(n * 4);
   L.total = o;
   return L;
 }
@@ -198,28 +192,99 @@ __device__ inline void wave_minmax(uint64_t &lo, uint64_t &hi) {
   minmax_step<0x143, 0xC>(lo, hi);
 }
 
+template <int CTRL, int ROWS>
+__device__ inline void min64_step(uint64_t &k) {
+  const uint64_t o = (uint64_t(dpp<CTRL, ROWS>(uint32_t(k >> 32))) << 32) | dpp<CTRL, ROWS>(uint32_t(k));
+  k = o < k ? o : k;
+}
+
+// Wave minimum of a 64-bit value (result in lane 63).
+__device__ inline void wave_min64(uint64_t &k) {
+  min64_step<0xB1, 0xF>(k);
+  min64_step<0x4E, 0xF>(k);
+  min64_step<0x141, 0xF>(k);
+  min64_step<0x140, 0xF>(k);
+  min64_step<0x142, 0xA>(k);
+  min64_step<0x143, 0xC>(k);
+}
+
+template <int CTRL, int ROWS>
+__device__ inline void min32_step(uint32_t &v) {
+  const uint32_t o = dpp<CTRL, ROWS>(v);
+  v = o < v ? o : v;
+}
+
+__device__ inline void wave_min32(uint32_t &v) {
+  min32_step<0xB1, 0xF>(v);
+  min32_step<0x4E, 0xF>(v);
+  min32_step<0x141, 0xF>(v);
+  min32_step<0x140, 0xF>(v);
+  min32_step<0x142, 0xA>(v);
+  min32_step<0x143, 0xC>(v);
+}
+
+// A queued request in the pool: three 16-byte words.
+struct Entry {
+  int32_t rec, tok, succ, next;  // record, tokens, its next call (-1: none), list link
+  int64_t cost, scost;           // its cost; the staged cost of its next call
+  int32_t sv, stok, ssucc, pad;  // staged next call: present, its tokens, its own next call
+};
+static_assert(sizeof(Entry) == 48, "Entry layout");
+
 // Storage of the pool and per-user arrays: LDS (on chip) or the state buffer (global).
 struct Store {
-  int64_t *u;         // per user of the replica
-  int32_t *xslot;
-  int32_t *e_rec, *e_tok, *e_succ, *e_next, *e_sv, *e_stok, *e_ssucc, *e_free;  // pool
-  int64_t *e_cost, *e_scost;
+  Entry *e;         // pool entries
+  int32_t *e_free;  // stack of free entries
+  int64_t *u;       // counters of the replica's users (current for users not in X)
+  int32_t *xslot;   // user -> X slot (global-memory table only)
   int32_t pcap;
   bool users_global;
 };
 
-// The backlogged-user table.  On chip: one slot per lane, every field in a register
-// of that lane (read with v_readlane, written with v_writelane); the argmin is a DPP
-// reduction over the lanes' keys with no memory access.
+template <bool G>
+__device__ inline Entry ld_entry(const Entry *p) {
+  Entry v;
+  if constexpr (G) {
+    v.rec = ld_fresh(&p->rec);
+    v.tok = ld_fresh(&p->tok);
+    v.succ = ld_fresh(&p->succ);
+    v.next = ld_fresh(&p->next);
+    v.cost = ld_fresh(&p->cost);
+    v.scost = ld_fresh(&p->scost);
+    v.sv = ld_fresh(&p->sv);
+    v.stok = ld_fresh(&p->stok);
+    v.ssucc = ld_fresh(&p->ssucc);
+  } else {
+    v = *p;
+  }
+  v.rec = uni(v.rec);
+  v.tok = uni(v.tok);
+  v.succ = uni(v.succ);
+  v.next = uni(v.next);
+  v.cost = uni64(v.cost);
+  v.scost = uni64(v.scost);
+  v.sv = uni(v.sv);
+  v.stok = uni(v.stok);
+  v.ssucc = uni(v.ssucc);
+  v.pad = 0;
+  return v;
+}
+
+// The backlogged-user table on chip: one slot per lane, every field in a register of
+// that lane (read with v_readlane, written with a lane select).  Free lanes hold user
+// -1 and the empty key, so a user's slot is one ballot and the argmin needs no mask.
 struct XReg {
   uint32_t klo, khi;  // key = tier << 62 | counter
   int32_t user, q, fh, ft, hh, ht, sb, rh, rdy;
+  uint64_t occ;       // lanes in use
   static constexpr int32_t cap = 64;
   __device__ void init() {
     klo = khi = 0xffffffffu;
-    user = q = 0;
+    user = -1;
+    q = 0;
     fh = ft = rh = -1;
     hh = ht = sb = rdy = 0;
+    occ = 0;
   }
   static __device__ int32_t wl(int32_t old, int32_t x, int32_t v) {
     return int32_t(threadIdx.x) == x ? v : old;
@@ -244,38 +309,58 @@ struct XReg {
   FS_XREG_FIELD(rh)
   FS_XREG_FIELD(rdy)
 #undef FS_XREG_FIELD
-  __device__ void copy(int32_t from, int32_t to) {
-    set_key(to, key(from));
-    set_user(to, get_user(from));
-    set_q(to, get_q(from));
-    set_fh(to, get_fh(from));
-    set_ft(to, get_ft(from));
-    set_hh(to, get_hh(from));
-    set_ht(to, get_ht(from));
-    set_sb(to, get_sb(from));
-    set_rh(to, get_rh(from));
-    set_rdy(to, get_rdy(from));
+  __device__ int32_t find(int32_t k, const Store &) const {
+    const uint64_t m = __ballot(user == k);
+    return m ? __ffsll((long long)m) - 1 : -1;
   }
-  __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
-    const int lane = threadIdx.x;
-    uint64_t k = lane < nX ? ((uint64_t(khi) << 32) | klo) : kEmptyKey;
-    uint32_t us = lane < nX ? uint32_t(user) : 0xffffffffu, bx = uint32_t(lane);
-    wave_argmin(k, us, bx);
-    bk = uint64_t(rdl64(int64_t(k), 63));
-    bu = rdl(int32_t(us), 63);
-    return rdl(int32_t(bx), 63);
+  __device__ int32_t alloc(int32_t, int32_t, const Store &) {
+    const int32_t x = __ffsll((long long)~occ) - 1;
+    occ |= uint64_t(1) << x;
+    return x;
   }
-  __device__ void minmax(int32_t nX, int64_t &mn, int64_t &mx) const {
-    const int lane = threadIdx.x;
+  __device__ void release(int32_t x, int32_t, int32_t, const Store &) {
+    occ &= ~(uint64_t(1) << x);
+    set_key(x, kEmptyKey);
+    set_user(x, -1);
+  }
+  __device__ int32_t slot(int32_t i, int32_t) const {  // i-th slot in use
+    uint64_t m = occ;
+    for (int32_t j = 0; j < i; ++j) m &= m - 1;
+    return __ffsll((long long)m) - 1;
+  }
+  // Slot of the least (key, user id): a 64-bit DPP minimum, then a ballot of the lanes
+  // holding it; only a tie on the key needs the minimum over user ids.
+  __device__ int32_t argmin(int32_t, uint64_t &bk, int32_t &bu) const {
+    const uint64_t k = (uint64_t(khi) << 32) | klo;
+    uint64_t m = k;
+    wave_min64(m);
+    const uint64_t mn = uint64_t(rdl64(int64_t(m), 63));
+    const uint64_t eq = __ballot(k == mn);
+    int32_t x;
+    if ((eq & (eq - 1)) == 0) {
+      x = __ffsll((long long)eq) - 1;
+    } else {
+      uint32_t us = k == mn ? uint32_t(user) : 0xffffffffu;
+      wave_min32(us);
+      const uint32_t umin = uint32_t(rdl(int32_t(us), 63));
+      x = __ffsll((long long)__ballot(k == mn && uint32_t(user) == umin)) - 1;
+    }
+    bk = mn;
+    bu = rdl(user, x);
+    return x;
+  }
+  __device__ void minmax(int32_t, int64_t &mn, int64_t &mx) const {
+    const bool in = (occ >> threadIdx.x) & 1u;
     const uint64_t v = ((uint64_t(khi) << 32) | klo) & kValMask;
-    uint64_t lo = lane < nX ? v : kEmptyKey, hi = lane < nX ? v : 0;
+    uint64_t lo = in ? v : kEmptyKey, hi = in ? v : 0;
     wave_minmax(lo, hi);
     mn = rdl64(int64_t(lo), 63);
     mx = rdl64(int64_t(hi), 63);
   }
 };
 
-// The same table in global memory (after an on-chip overflow): capacity n_r + 1.
+// The same table in global memory (after an on-chip overflow): slots [0, nX) packed,
+// capacity n_r + 1, with the user -> slot table S.xslot.
 struct XMem {
   uint64_t *k;
   int32_t *user, *q, *fh, *ft, *hh, *ht, *sb, *rh, *rdy;
@@ -312,6 +397,23 @@ struct XMem {
     set_rh(to, get_rh(from));
     set_rdy(to, get_rdy(from));
   }
+  __device__ int32_t find(int32_t kk, const Store &S) const { return uni(ld_fresh(S.xslot + kk)); }
+  __device__ int32_t alloc(int32_t kk, int32_t nX, const Store &S) {
+    if (threadIdx.x == 0) S.xslot[kk] = nX;
+    return nX;
+  }
+  // Moves the last slot into the freed one.
+  __device__ void release(int32_t x, int32_t kk, int32_t nX, const Store &S) {
+    const int32_t last = nX - 1;
+    if (threadIdx.x == 0) S.xslot[kk] = -1;
+    if (x != last) {
+      const int32_t k2 = get_user(last);
+      copy(last, x);
+      if (threadIdx.x == 0) S.xslot[k2] = x;
+    }
+    set_key(last, kEmptyKey);
+  }
+  __device__ int32_t slot(int32_t i, int32_t) const { return i; }
   __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
     uint64_t kk = kEmptyKey;
     uint32_t us = 0xffffffffu, bx = 0xffffffffu;
@@ -343,7 +445,9 @@ struct XMem {
 
 // ---------------------------------------------------------------------------
 // The scheduler body.  All control flow is wave-uniform; the arrival window holds
-// one record per lane.
+// one record per lane.  Per-record outputs are collected in registers and written
+// with one store per field for up to 64 records: arrival outcomes by window lane,
+// admissions by admission order.
 // ---------------------------------------------------------------------------
 template <bool G, class XT>
 __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool onchip) {
@@ -355,6 +459,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
   int8_t *fate = reinterpret_cast<int8_t *>(a.state + a.L.fate) + base;
   const int32_t *succ = reinterpret_cast<const int32_t *>(a.state + a.L.succ) + base;
+  int32_t *emap = reinterpret_cast<int32_t *>(a.state + a.L.emap) + base;
   const uint32_t *seg_start = reinterpret_cast<const uint32_t *>(a.state + a.L.seg_start);
   int32_t *seg_rec = reinterpret_cast<int32_t *>(a.state + a.L.seg_rec);
   int32_t *seg_tok = reinterpret_cast<int32_t *>(a.state + a.L.seg_tok);
@@ -374,16 +479,9 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     s_end = uni64(rs->s_end);  // resuming a launch that overflowed on chip
   const int64_t tau = a.tau, C = a.cap, theta = a.theta;
 
-  if (!S.users_global) {
-    for (int32_t k = lane; k < U; k += 64) {
-      S.u[k] = u_all[k];
-      S.xslot[k] = -1;
-    }
-  }
-  for (int32_t e = lane; e < S.pcap; e += 64) {
-    S.e_free[e] = S.pcap - 1 - e;
-    S.e_rec[e] = -1;
-  }
+  if (!S.users_global)
+    for (int32_t k = lane; k < U; k += 64) S.u[k] = u_all[k];
+  for (int32_t e = lane; e < S.pcap; e += 64) S.e_free[e] = S.pcap - 1 - e;
   X.init();
   int32_t nfree = S.pcap, nX = 0;
   int32_t code = 0;
@@ -391,9 +489,6 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   __syncthreads();
 
   auto get_u = [&](int32_t k) -> int64_t { return S.users_global ? ld_fresh(S.u + k) : S.u[k]; };
-  auto get_xslot = [&](int32_t k) -> int32_t {
-    return S.users_global ? ld_fresh(S.xslot + k) : S.xslot[k];
-  };
   auto slot_u = [&](int32_t x) -> int64_t { return int64_t(X.key(x) & kValMask); };
   auto set_key = [&](int32_t x, int64_t uval) {
     X.set_key(x, (uint64_t(X.get_rdy(x) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval));
@@ -403,11 +498,44 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     return t.len_in[g] + t.len_out[g] + (t.len_sys ? t.len_sys[g] : 0);
   };
 
+  // ---- admissions waiting to be written: lane i holds the i-th of nd
+  int32_t d_rec = 0, d_step = 0, nd = 0;
+  int64_t d_cnt = 0;
+  auto flush_decisions = [&]() {
+    if (nd == 0) return;
+    if (lane < nd) {
+      const int64_t g = base + d_rec;
+      fate[d_rec] = 0;
+      a.status[g] = 0;
+      a.admit_step[g] = d_step;
+      if (a.admit_seq) a.admit_seq[g] = int32_t(seq - nd + lane);
+      if (a.counter_after) a.counter_after[g] = d_cnt;
+    }
+    nd = 0;
+  };
+
   // ---- window of upcoming records (one per lane), branch-free so it stays in registers
   int64_t wbase = nxt;
-  int64_t w_cost = 0, c_u = 0;
+  int64_t w_cost = 0, c_u = 0, o_coa = 0;
   int32_t w_step = 0, w_user = -1, w_call = 0, w_head = -1, w_prev = -1, w_succ = -1, w_tok = 0,
-          w_reason = 0, w_seg = 0, c_xslot = -1, c_prev_adm = 0, c_head_blk = 0;
+          w_reason = 0, w_seg = 0, c_prev_adm = 0, c_head_blk = 0, c_pe = -1, o_st = 0;
+  // Arrival outcomes of the window's processed lanes: throttled ones get their status
+  // and fate, every one its counter on arrival.
+  auto flush_window = [&]() {
+    const int64_t done = nxt - wbase;
+    if (lane < done) {
+      const int64_t i = wbase + lane, g = base + i;
+      if (o_st > 0) {
+        fate[i] = int8_t(o_st);
+        a.status[g] = int8_t(o_st);
+        a.admit_step[g] = -1;
+        if (a.admit_seq) a.admit_seq[g] = -1;
+        if (a.counter_after) a.counter_after[g] = -1;
+      }
+      if (a.counter_on_arrival) a.counter_on_arrival[g] = o_coa;
+    }
+    o_st = 0;
+  };
   auto load_window = [&]() {
     wave_fence();
     const int64_t i = wbase + lane;
@@ -429,19 +557,27 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     w_cost = valid ? a.cost[g] : 0;
     w_reason = (valid && a.reason) ? a.reason[g] : 0;
     w_seg = int32_t(seg_start[int64_t(r) * U + usr]);
-    const int32_t xs = get_xslot(usr);
     const int64_t uu = get_u(usr);
-    c_xslot = valid ? xs : -1;
     c_u = valid ? uu : 0;
     const int8_t pf = call > 0 ? ld_fresh(fate + pv) : int8_t(-1);
     const int8_t hf = call > 0 ? ld_fresh(fate + hd) : int8_t(-1);
+    const int32_t pe = call > 0 ? ld_fresh(emap + pv) : -1;
     c_prev_adm = (call > 0 && pf == 0) ? 1 : 0;
     c_head_blk = (call > 0 && (hf == 1 || hf == 2)) ? 1 : 0;
+    c_pe = pe;
+    o_st = 0;
+  };
+  auto advance_window = [&]() {
+    flush_window();
+    flush_decisions();
+    wbase = nxt;
+    load_window();
   };
 
   // ---- backlogged users
   auto join_x = [&](int32_t k, int64_t uval, int32_t segb) -> int32_t {
-    const int32_t x = nX++;
+    const int32_t x = X.alloc(k, nX, S);
+    ++nX;
     X.set_user(x, k);
     X.set_q(x, 0);
     X.set_fh(x, -1);
@@ -452,50 +588,43 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     X.set_rh(x, -1);
     X.set_rdy(x, 0);
     X.set_key(x, (uint64_t(1) << kTierShift) | uint64_t(uval));
-    if (lane == 0) S.xslot[k] = x;
-    c_xslot = (w_user == k) ? x : c_xslot;
     return x;
   };
   auto leave_x = [&](int32_t x, int32_t k, int64_t uval) {
-    const int32_t last = nX - 1;
-    if (lane == 0) {
-      S.u[k] = uval;
-      S.xslot[k] = -1;
-    }
-    c_xslot = (w_user == k) ? -1 : c_xslot;
+    if (lane == 0) S.u[k] = uval;
     c_u = (w_user == k) ? uval : c_u;
-    if (x != last) {
-      const int32_t k2 = X.get_user(last);
-      X.copy(last, x);
-      if (lane == 0) S.xslot[k2] = x;
-      c_xslot = (w_user == k2) ? x : c_xslot;
-    }
-    X.set_key(last, kEmptyKey);
-    nX = last;
+    X.release(x, k, nX, S);
+    --nX;
   };
 
   // ---- pool
   auto alloc_e = [&]() -> int32_t { return uni(RD<G>(&S.e_free[--nfree])); };
   auto free_e = [&](int32_t e) {
-    if (lane == 0) {
-      S.e_free[nfree] = e;
-      S.e_rec[e] = -1;
-    }
+    if (lane == 0) S.e_free[nfree] = e;
     ++nfree;
   };
-  auto fill_e = [&](int32_t e, int32_t rec, int32_t tok, int64_t cst, int32_t sc, int32_t sv,
-                    int64_t scost, int32_t stok, int32_t ssucc) {
+  // A record entered the pool at entry e: remember it for its next call's arrival.
+  auto note_pool = [&](int32_t rec, int32_t e) {
+    if (lane == 0) emap[rec] = e;
+    c_pe = (w_prev == rec) ? e : c_pe;
+  };
+  auto put_entry = [&](int32_t e, int32_t rec, int32_t tok, int64_t cst, int32_t sc, int32_t sv,
+                       int64_t scost, int32_t stok, int32_t ssucc) {
     if (lane == 0) {
-      S.e_rec[e] = rec;
-      S.e_tok[e] = tok;
-      S.e_cost[e] = cst;
-      S.e_succ[e] = sc;
-      S.e_next[e] = -1;
-      S.e_sv[e] = sv;
-      S.e_scost[e] = scost;
-      S.e_stok[e] = stok;
-      S.e_ssucc[e] = ssucc;
+      Entry v;
+      v.rec = rec;
+      v.tok = tok;
+      v.succ = sc;
+      v.next = -1;
+      v.cost = cst;
+      v.scost = scost;
+      v.sv = sv;
+      v.stok = stok;
+      v.ssucc = ssucc;
+      v.pad = 0;
+      S.e[e] = v;
     }
+    note_pool(rec, e);
   };
   // Data of record i (an arrived later call) read from the inputs.
   auto load_record = [&](int32_t i, int64_t &cst, int32_t &tok, int32_t &sc) {
@@ -508,11 +637,11 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     if (tl < 0)
       X.set_fh(x, e);
     else if (lane == 0)
-      S.e_next[tl] = e;
+      S.e[tl].next = e;
     X.set_ft(x, e);
   };
   auto ready_push = [&](int32_t x, int32_t e) {
-    if (lane == 0) S.e_next[e] = X.get_rh(x);
+    if (lane == 0) S.e[e].next = X.get_rh(x);
     X.set_rh(x, e);
     X.set_rdy(x, X.get_rdy(x) + 1);
   };
@@ -522,7 +651,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     const int32_t hh = X.get_hh(x), ht = X.get_ht(x);
     if (ht == hh && nfree > kReserve) {
       const int32_t e = alloc_e();
-      fill_e(e, rec, tok, cst, sc, 0, 0, 0, -1);
+      put_entry(e, rec, tok, cst, sc, 0, 0, 0, -1);
       fifo_append(x, e);
       return true;
     }
@@ -549,12 +678,12 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     wave_fence();
     const int64_t at = int64_t(X.get_sb(x)) + hh + lane;
     const bool mine = lane < m;
-    int32_t e = -1, en = -1;
+    int32_t e = -1, rec = -1, sc = -1;
     if (mine) {
-      const int32_t rec = ld_fresh(seg_rec + at);
+      rec = ld_fresh(seg_rec + at);
       const int32_t tok = ld_fresh(seg_tok + at);
       const int64_t cst = ld_fresh(seg_cost + at);
-      const int32_t sc = ld_fresh(seg_succ + at);
+      sc = ld_fresh(seg_succ + at);
       int32_t sv = 0, stok = 0, ssucc = -1;
       int64_t scost = 0;
       if (sc >= 0 && sc < nxt) {  // its next call has already arrived: stage its data
@@ -564,16 +693,28 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
         ssucc = succ[sc];
       }
       e = RD<G>(&S.e_free[nfree - 1 - lane]);
-      en = lane + 1 < m ? RD<G>(&S.e_free[nfree - 2 - lane]) : -1;
-      S.e_rec[e] = rec;
-      S.e_tok[e] = tok;
-      S.e_cost[e] = cst;
-      S.e_succ[e] = sc;
-      S.e_next[e] = en;
-      S.e_sv[e] = sv;
-      S.e_scost[e] = scost;
-      S.e_stok[e] = stok;
-      S.e_ssucc[e] = ssucc;
+      const int32_t en = lane + 1 < m ? RD<G>(&S.e_free[nfree - 2 - lane]) : -1;
+      Entry v;
+      v.rec = rec;
+      v.tok = tok;
+      v.succ = sc;
+      v.next = en;
+      v.cost = cst;
+      v.scost = scost;
+      v.sv = sv;
+      v.stok = stok;
+      v.ssucc = ssucc;
+      v.pad = 0;
+      S.e[e] = v;
+      emap[rec] = e;
+    }
+    // next calls in the current window that have not arrived yet: point them at the entry
+    uint64_t hit = __ballot(mine && sc >= nxt && sc < wbase + 64);
+    while (hit) {
+      const int l = __ffsll((long long)hit) - 1;
+      hit &= hit - 1;
+      const int32_t j = rdl(sc, l) - int32_t(wbase);
+      c_pe = lane == j ? rdl(e, l) : c_pe;
     }
     X.set_fh(x, rdl(e, 0));
     X.set_ft(x, rdl(e, m - 1));
@@ -582,19 +723,14 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     return true;
   };
   // Stage an arrived later call's data in its previous call's pool entry, if there.
-  auto stage_in_prev = [&](int32_t prev_rec, int64_t cst, int32_t tok, int32_t sc) {
-    int32_t found = -1;
-    for (int32_t e = lane; e < S.pcap; e += 64)
-      if (RD<G>(&S.e_rec[e]) == prev_rec) found = e;
-    const uint64_t m = __ballot(found >= 0);
-    if (m) {
-      const int32_t e = rdl(found, __ffsll((long long)m) - 1);
-      if (lane == 0) {
-        S.e_sv[e] = 1;
-        S.e_scost[e] = cst;
-        S.e_stok[e] = tok;
-        S.e_ssucc[e] = sc;
-      }
+  auto stage_in_prev = [&](int32_t prev_rec, int32_t pe, int64_t cst, int32_t tok, int32_t sc) {
+    if (pe < 0 || pe >= S.pcap) return;
+    if (uni(RD<G>(&S.e[pe].rec)) != prev_rec) return;
+    if (lane == 0) {
+      S.e[pe].sv = 1;
+      S.e[pe].scost = cst;
+      S.e[pe].stok = tok;
+      S.e[pe].ssucc = sc;
     }
   };
 
@@ -602,7 +738,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   // Returns false when an on-chip capacity would overflow (nothing changed then).
   auto enqueue = [&](int32_t rec, int32_t k, int32_t call, int32_t prev_rec, int32_t sc,
                      int32_t tok, int64_t cst, int32_t xs, int64_t uval, bool prev_adm,
-                     int32_t segb) -> bool {
+                     int32_t segb, int32_t pe) -> bool {
     if (xs < 0 && nX >= X.cap) return false;
     if (call > 0 && prev_adm && nfree == 0) return false;
     const int32_t x = xs >= 0 ? xs : join_x(k, uval, segb);
@@ -611,11 +747,11 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       if (!enqueue_first(x, rec, tok, cst, sc)) code = FS_E_STATE;
     } else if (prev_adm) {
       const int32_t e = alloc_e();
-      fill_e(e, rec, tok, cst, sc, 0, 0, 0, -1);
+      put_entry(e, rec, tok, cst, sc, 0, 0, 0, -1);
       ready_push(x, e);
       set_key(x, uval);
     } else {
-      stage_in_prev(prev_rec, cst, tok, sc);
+      stage_in_prev(prev_rec, pe, cst, tok, sc);
     }
     return true;
   };
@@ -636,32 +772,30 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       int64_t cst;
       int32_t tok, sc;
       load_record(rec, cst, tok, sc);
-      const int32_t xs = uni(get_xslot(k));
+      const int32_t xs = X.find(k, S);
       const int64_t uval = xs >= 0 ? slot_u(xs) : uni64(get_u(k));
       const bool prev_adm = call > 0 && ld_fresh(fate + prev_rec) == 0;
       const int32_t segb = int32_t(seg_start[int64_t(r) * U + k]);
-      if (!enqueue(rec, k, call, prev_rec, sc, tok, cst, xs, uval, prev_adm, segb)) overflow = true;
+      const int32_t pe = call > 0 ? uni(ld_fresh(emap + prev_rec)) : -1;
+      if (!enqueue(rec, k, call, prev_rec, sc, tok, cst, xs, uval, prev_adm, segb, pe))
+        overflow = true;
       // a ready later call whose own next call already arrived: stage that call's data
       if (!overflow && code == 0 && call > 0 && prev_adm && sc >= 0 && sc < nxt) {
-        const int32_t xx = uni(get_xslot(k));
+        const int32_t xx = X.find(k, S);
         const int32_t e = X.get_rh(xx);
         int64_t c2;
         int32_t t2, s2;
         load_record(sc, c2, t2, s2);
         if (lane == 0) {
-          S.e_sv[e] = 1;
-          S.e_scost[e] = c2;
-          S.e_stok[e] = t2;
-          S.e_ssucc[e] = s2;
+          S.e[e].sv = 1;
+          S.e[e].scost = c2;
+          S.e[e].stok = t2;
+          S.e[e].ssucc = s2;
         }
       }
     }
   }
   if (overflow) {
-    for (int32_t x = 0; x < nX; ++x) {
-      const int32_t k = X.get_user(x);
-      if (lane == 0) S.xslot[k] = -1;
-    }
     if (lane == 0) {
       rs->overflow = 1;
       rs->s_end = s_end;
@@ -679,10 +813,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   while (!overflow && code == 0) {
     if (s >= s_end) break;
     if (nxt == n && nX == 0) break;
-    if (nxt < n && nxt - wbase >= 64) {
-      wbase = nxt;
-      load_window();
-    }
+    if (nxt < n && nxt - wbase >= 64) advance_window();
     if (nX == 0 && nxt < n) {
       // nothing queued: the steps before the next arrival only pay back debt
       int64_t target = rdl(w_step, int(nxt - wbase));
@@ -701,16 +832,13 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
 
     // monitoring stream: arrivals of step s in stream order
     while (nxt < n) {
-      if (nxt - wbase == 64) {
-        wbase = nxt;
-        load_window();
-      }
+      if (nxt - wbase == 64) advance_window();
       const int j = int(nxt - wbase);
       if (rdl(w_step, j) > s) break;
       const int32_t rec = int32_t(nxt);
       const int32_t k = rdl(w_user, j);
       const int32_t call = rdl(w_call, j);
-      const int32_t xs = rdl(c_xslot, j);
+      const int32_t xs = X.find(k, S);
       const bool in_x = xs >= 0;
       int64_t uk = in_x ? slot_u(xs) : rdl64(c_u, j);
       const int64_t u_before = uk;
@@ -722,19 +850,18 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
         }
       }
       bool blocked;
-      int8_t why;
+      int32_t why;
       if (call > 0) {
         blocked = rdl(c_head_blk, j) != 0;
         why = 3;
       } else {
-        why = int8_t(rdl(w_reason, j));
+        why = rdl(w_reason, j);
         blocked = backlog > theta && why != 0;
       }
       const int32_t tok = rdl(w_tok, j);
       if (!blocked) {
-        const bool prev_adm = rdl(c_prev_adm, j) != 0;
         if (!enqueue(rec, k, call, rdl(w_prev, j), rdl(w_succ, j), tok, rdl64(w_cost, j), xs, uk,
-                     prev_adm, rdl(w_seg, j))) {
+                     rdl(c_prev_adm, j) != 0, rdl(w_seg, j), rdl(c_pe, j))) {
           overflow = true;  // state is as before this arrival
           break;
         }
@@ -742,21 +869,14 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
         if (!in_x && nX == 1) minX = uk;
         backlog += tok;
       } else {
-        if (lane == 0) fate[rec] = why;
+        o_st = lane == j ? why : o_st;
         if (!in_x && uk != u_before) {
           if (lane == 0) S.u[k] = uk;
           c_u = (w_user == k) ? uk : c_u;
         }
         c_head_blk = (call == 0 && w_head == rec && w_call > 0) ? 1 : c_head_blk;
-        if (lane == 0) {
-          const int64_t g = base + rec;
-          a.status[g] = why;
-          a.admit_step[g] = -1;
-          if (a.admit_seq) a.admit_seq[g] = -1;
-          if (a.counter_after) a.counter_after[g] = -1;
-        }
       }
-      if (lane == 0 && a.counter_on_arrival) a.counter_on_arrival[base + rec] = uk;
+      o_coa = lane == j ? uk : o_coa;
       ++nxt;
     }
     if (overflow || code) break;
@@ -767,7 +887,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       uint64_t bk;
       int32_t k;
       const int32_t x = X.argmin(nX, bk, k);
-      if (x < 0 || x >= nX) {
+      if (x < 0 || x >= X.cap) {
         code = FS_E_STATE;  // internal bookkeeping error: stop rather than read out of bounds
         break;
       }
@@ -778,8 +898,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
         int32_t best = INT32_MAX, be = -1, bprev = -1, prevp = -1;
         int32_t walked = 0;
         for (int32_t c = X.get_rh(x); c >= 0 && walked < S.pcap;
-             c = uni(RD<G>(&S.e_next[c])), ++walked) {
-          const int32_t rc = uni(RD<G>(&S.e_rec[c]));
+             c = uni(RD<G>(&S.e[c].next)), ++walked) {
+          const int32_t rc = uni(RD<G>(&S.e[c].rec));
           if (rc < best) {
             best = rc;
             be = c;
@@ -792,11 +912,11 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           break;
         }
         e = be;
-        const int32_t nx = uni(RD<G>(&S.e_next[e]));
+        const int32_t nx = uni(RD<G>(&S.e[e].next));
         if (bprev < 0)
           X.set_rh(x, nx);
         else if (lane == 0)
-          S.e_next[bprev] = nx;
+          S.e[bprev].next = nx;
         X.set_rdy(x, X.get_rdy(x) - 1);
       } else {
         if (X.get_fh(x) < 0) {
@@ -814,43 +934,33 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           code = FS_E_STATE;
           break;
         }
-        const int32_t nx = uni(RD<G>(&S.e_next[e]));
+        const int32_t nx = uni(RD<G>(&S.e[e].next));
         X.set_fh(x, nx);
         if (nx < 0) X.set_ft(x, -1);
       }
-      const int32_t rec = uni(RD<G>(&S.e_rec[e]));
-      const int64_t cst = uni64(RD<G>(&S.e_cost[e]));
-      const int32_t tok = uni(RD<G>(&S.e_tok[e]));
-      const int32_t sc = uni(RD<G>(&S.e_succ[e]));
-      const int32_t sv = uni(RD<G>(&S.e_sv[e]));
-      const int64_t scost = uni64(RD<G>(&S.e_scost[e]));
-      const int32_t stok = uni(RD<G>(&S.e_stok[e]));
-      const int32_t ssucc = uni(RD<G>(&S.e_ssucc[e]));
+      const Entry v = ld_entry<G>(&S.e[e]);
       const int32_t left = X.get_q(x) - 1;
       free_e(e);
       X.set_q(x, left);
-      budget -= tok;
-      backlog -= tok;
-      const int64_t unew = uk + cst;
+      budget -= v.tok;
+      backlog -= v.tok;
+      const int64_t unew = uk + v.cost;
       if (unew >= kValueLimit) {
         code = FS_E_OVERFLOW;
         break;
       }
-      if (lane == 0) {
-        const int64_t g = base + rec;
-        fate[rec] = 0;
-        a.status[g] = 0;
-        a.admit_step[g] = int32_t(s);
-        if (a.admit_seq) a.admit_seq[g] = int32_t(seq);
-        if (a.counter_after) a.counter_after[g] = unew;
-      }
       ++seq;
-      c_prev_adm = (w_prev == rec) ? 1 : c_prev_adm;
+      d_rec = lane == nd ? v.rec : d_rec;
+      d_step = lane == nd ? int32_t(s) : d_step;
+      d_cnt = lane == nd ? unew : d_cnt;
+      if (++nd == 64) flush_decisions();
+      c_prev_adm = (w_prev == v.rec) ? 1 : c_prev_adm;
+      const int32_t sc = v.succ;
       if (sc >= 0 && sc < nxt) {
         // the next call arrived while this one was queued: it becomes ready now
-        int64_t c1 = scost;
-        int32_t t1 = stok, s1 = ssucc;
-        if (!sv) load_record(sc, c1, t1, s1);
+        int64_t c1 = v.scost;
+        int32_t t1 = v.stok, s1 = v.ssucc;
+        if (!v.sv) load_record(sc, c1, t1, s1);
         int32_t sv2 = 0, t2 = 0, s2 = -1;
         int64_t c2 = 0;
         if (s1 >= 0 && s1 < nxt) {  // and the call after it too
@@ -858,7 +968,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           load_record(s1, c2, t2, s2);
         }
         const int32_t e2 = alloc_e();  // the entry just freed guarantees room
-        fill_e(e2, sc, t1, c1, s1, sv2, c2, t2, s2);
+        put_entry(e2, sc, t1, c1, s1, sv2, c2, t2, s2);
         ready_push(x, e2);
       }
       if (left == 0) {
@@ -881,15 +991,18 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   }
 
   if (code) raise_err(a.err, code);
+  flush_window();
+  flush_decisions();
 
   // ---- save: counters of queued users back to u; the queue itself is recovered next
   // time from the records that have arrived and are still undecided
-  for (int32_t x = 0; x < nX; ++x) {
+  for (int32_t i = 0; i < nX; ++i) {
+    const int32_t x = X.slot(i, nX);
     const int32_t k = X.get_user(x);
     const int64_t uval = slot_u(x);
     if (lane == 0) {
       S.u[k] = uval;
-      S.xslot[k] = -1;
+      if (S.xslot) S.xslot[k] = -1;
     }
   }
   wave_fence();
@@ -971,23 +1084,14 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   };
   const size_t pc = size_t(a.pcap);
   S.pcap = a.pcap;
-  S.e_cost = reinterpret_cast<int64_t *>(take(8 * pc));
-  S.e_scost = reinterpret_cast<int64_t *>(take(8 * pc));
-  S.e_rec = reinterpret_cast<int32_t *>(take(4 * pc));
-  S.e_tok = reinterpret_cast<int32_t *>(take(4 * pc));
-  S.e_succ = reinterpret_cast<int32_t *>(take(4 * pc));
-  S.e_next = reinterpret_cast<int32_t *>(take(4 * pc));
-  S.e_sv = reinterpret_cast<int32_t *>(take(4 * pc));
-  S.e_stok = reinterpret_cast<int32_t *>(take(4 * pc));
-  S.e_ssucc = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.e = reinterpret_cast<Entry *>(take(sizeof(Entry) * pc));
   S.e_free = reinterpret_cast<int32_t *>(take(4 * pc));
+  S.xslot = nullptr;
   if (USERS_LDS) {
     S.u = reinterpret_cast<int64_t *>(take(8 * size_t(a.t.U)));
-    S.xslot = reinterpret_cast<int32_t *>(take(4 * size_t(a.t.U)));
     S.users_global = false;
   } else {
     S.u = reinterpret_cast<int64_t *>(a.state + a.L.u_all) + int64_t(r) * a.t.U;
-    S.xslot = reinterpret_cast<int32_t *>(a.state + a.L.xslot_all) + int64_t(r) * a.t.U;
     S.users_global = true;
   }
   XReg X;
@@ -1021,15 +1125,7 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   X.sb = reinterpret_cast<int32_t *>(st + L.xsb) + off;
   X.rh = reinterpret_cast<int32_t *>(st + L.xrh) + off;
   X.rdy = reinterpret_cast<int32_t *>(st + L.xrdy) + off;
-  S.e_rec = reinterpret_cast<int32_t *>(st + L.e_rec) + off;
-  S.e_tok = reinterpret_cast<int32_t *>(st + L.e_tok) + off;
-  S.e_cost = reinterpret_cast<int64_t *>(st + L.e_cost) + off;
-  S.e_succ = reinterpret_cast<int32_t *>(st + L.e_succ) + off;
-  S.e_next = reinterpret_cast<int32_t *>(st + L.e_next) + off;
-  S.e_sv = reinterpret_cast<int32_t *>(st + L.e_sv) + off;
-  S.e_scost = reinterpret_cast<int64_t *>(st + L.e_scost) + off;
-  S.e_stok = reinterpret_cast<int32_t *>(st + L.e_stok) + off;
-  S.e_ssucc = reinterpret_cast<int32_t *>(st + L.e_ssucc) + off;
+  S.e = reinterpret_cast<Entry *>(st + L.e_all) + off;
   S.e_free = reinterpret_cast<int32_t *>(st + L.e_free) + off;
   S.u = reinterpret_cast<int64_t *>(st + L.u_all) + int64_t(r) * a.t.U;
   S.xslot = reinterpret_cast<int32_t *>(st + L.xslot_all) + int64_t(r) * a.t.U;
@@ -1076,6 +1172,7 @@ __global__ void k_state_records(char *state, StateLayout L, int64_t N) {
        g += int64_t(gridDim.x) * blockDim.x) {
     reinterpret_cast<int8_t *>(state + L.fate)[g] = -1;
     reinterpret_cast<int32_t *>(state + L.succ)[g] = -1;
+    reinterpret_cast<int32_t *>(state + L.emap)[g] = -1;
   }
 }
 
@@ -1158,13 +1255,9 @@ int grid_for(int64_t n, int threads) {
 size_t onchip_lds_bytes(int32_t pcap, int32_t U, bool users_lds) {
   size_t b = 0;
   auto add = [&](size_t x) { b += (x + 15) & ~size_t(15); };
-  add(8 * size_t(pcap));
-  add(8 * size_t(pcap));
-  for (int i = 0; i < 8; ++i) add(4 * size_t(pcap));
-  if (users_lds) {
-    add(8 * size_t(U));
-    add(4 * size_t(U));
-  }
+  add(sizeof(Entry) * size_t(pcap));
+  add(4 * size_t(pcap));
+  if (users_lds) add(8 * size_t(U));
   return b;
 }
 

@@ -1,142 +1,32 @@
-// WSC scheduler steps (Alg. 1, monitoring and execution streams) under the
-// token-budget step engine, one wavefront per trace replica.
+// WSC scheduler steps: the global-memory kernel, the state blob's initialisation
+// and the launcher.
 //
-// Per replica the state is the paper's: service counters u_i, the waiting queue Q
-// (a dictionary from user to queued requests), the last user to leave Q, and the
-// overload measure (tokens queued).  The wave keeps what each decision touches on
-// chip and never waits on HBM inside a decision in the common case:
-//   X table   slots [0, nX) of users with something queued, one slot per lane with
-//             every field in that lane's registers: user id, key (tier << 62 | u) whose
-//             tier is 0 while the user has a ready later call of an incomplete
+// The on-chip kernel (fs_sched_onchip.hip) runs every replica whose backlogged users,
+// queued first calls and ready later calls fit its LDS and register tables.  A
+// replica that would overflow them is handed over here: this kernel keeps the same
+// state as the on-chip one -- service counters u_i, the waiting queue Q (a
+// dictionary from user to queued requests), the last user to leave Q, the overload
+// measure -- with every structure in the state buffer, so its capacities are the
+// trace's own sizes.  It rebuilds the queue from the requests that have arrived and
+// are still undecided and continues exactly where the on-chip kernel stopped,
+// including inside a step's admissions.
+//   X table   slots [0, nX) of users with something queued: key (tier << 62 | u),
+//             whose tier is 0 while the user has a ready later call of an incomplete
 //             interaction, a FIFO of queued first calls and a list of ready later calls.
-//             The argmin over (key, user id) is a DPP wave reduction over registers.
-//   pool      LDS entries of queued requests: record, cost, tokens, next call, link,
-//             and the next call's data when that call has already arrived, so serving
-//             a request releases its successor without touching HBM.
-//   HBM FIFO  first calls beyond the pool go to a per-user segment in the state buffer
-//             (sized by the user's number of first calls) and are refilled into the
-//             pool 64 at a time with one coalesced load.
-//   pending   later calls waiting for their previous call are not stored: their data
-//             is read from the inputs when the previous call enters the pool.
-//   window    the next 64 records, one per lane, with their step, the user's slot and
-//             idle counter, "previous call admitted" and "first call throttled"
-//             prefetched; every state change patches the lanes it affects.
-// Counters of idle users live in LDS when they fit, else in the state buffer.  If an
-// on-chip capacity overflows the wave saves its state and the same code resumes with
-// every structure in global memory (a second launch on the same stream).
-#include "fs_device.h"
-#include "fs_launch.h"
+//   pool      entries of queued requests: record, cost, tokens, next call, link, and
+//             the next call's data when that call has already arrived.
+//   segments  first calls beyond the pool go to a per-user segment (sized by the
+//             user's number of first calls) and are refilled 64 at a time.
+//   window    the next 64 records, one per lane, with their step and the user's
+//             state prefetched; every state change patches the lanes it affects.
+#include "fs_sched_common.h"
 
 namespace fs {
 namespace {
 
-constexpr uint64_t kMagic = 0x32535652'49414646ull;
-constexpr int32_t kVersion = 3;
-constexpr uint64_t kTierShift = 62;
-constexpr uint64_t kValMask = (uint64_t(1) << 62) - 1;
-constexpr uint64_t kEmptyKey = ~uint64_t(0);
-constexpr int kUsersLdsMax = 1024;  // per-user arrays on chip up to this many users
-constexpr int kReserve = 32;         // pool entries first calls leave for later calls
+using namespace sched;
 
-struct RepState {
-  int64_t s, nxt, debt, backlog, seq, gap, last_exit_u, low, s_end;
-  int32_t last_exit, done, overflow, pad;
-  int64_t pad2[5];
-};
-static_assert(sizeof(RepState) == 128, "RepState layout");
-
-struct Header {
-  uint64_t magic;
-  int32_t version, R, U, pad;
-  int64_t N;
-  int64_t pad2[4];
-};
-
-size_t up(size_t x) { return (x + 255) / 256 * 256; }
-
-struct StateLayout {
-  size_t hdr, reps, u_all, xslot_all, fate, succ, seg_start, seg_part, seg_rec, seg_tok, seg_cost,
-      seg_succ;
-  // global-memory scheduler structures (n_r + 1 entries per replica, at rep_off[r] + r)
-  size_t xkey, xuser, xq, xfh, xft, xhh, xht, xsb, xrh, xrdy;
-  size_t e_all, e_free;
-  size_t emap;  // per record: the pool entry it last occupied (checked before use)
-  size_t total;
-};
-
-StateLayout state_layout(int32_t R, int32_t U, int64_t N) {
-  StateLayout L;
-  size_t n = size_t(N > 0 ? N : 1), ru = size_t(R) * size_t(U);
-  size_t nr = size_t(N) + size_t(R) + 1;
-  size_t o = 0;
-  auto take = [&](size_t bytes) {
-    size_t at = o;
-    o += up(bytes);
-    return at;
-  };
-  L.hdr = take(sizeof(Header));
-  L.reps = take(sizeof(RepState) * size_t(R));
-  L.u_all = take(ru * 8);
-  L.xslot_all = take(ru * 4);
-  L.fate = take(n);
-  L.succ = take(n * 4);
-  L.seg_start = take((ru + 1) * 4);
-  L.seg_part = take(scan_partials_bytes(int64_t(ru + 1)));
-  L.seg_rec = take(n * 4);
-  L.seg_tok = take(n * 4);
-  L.seg_cost = take(n * 8);
-  L.seg_succ = take(n * 4);
-  L.xkey = take(nr * 8);
-  L.xuser = take(nr * 4);
-  L.xq = take(nr * 4);
-  L.xfh = take(nr * 4);
-  L.xft = take(nr * 4);
-  L.xhh = take(nr * 4);
-  L.xht = take(nr * 4);
-  L.xsb = take(nr * 4);
-  L.xrh = take(nr * 4);
-  L.xrdy = take(nr * 4);
-  L.e_all = take(nr * 48);
-  L.e_free = take(nr * 4);
-  L.emap = take(n * 4);
-  L.total = o;
-  return L;
-}
-
-struct SchedArgs {
-  DevTrace t;
-  const int64_t *cost;
-  const uint8_t *reason;
-  int64_t tau, cap, theta;
-  int64_t n_steps;
-  bool global_only;
-  int8_t *status;
-  int32_t *admit_step, *admit_seq;
-  int64_t *counter_after, *counter_on_arrival, *counter, *steps, *decisions, *max_gap;
-  int32_t *err;
-  char *state;
-  StateLayout L;
-  int32_t pcap;  // on-chip pool entries
-};
-
-// -------------------------------------------------------------- wave helpers
-
-__device__ inline int32_t rdl(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
-__device__ inline int64_t rdl64(int64_t v, int l) {
-  uint32_t lo = __builtin_amdgcn_readlane(uint32_t(uint64_t(v)), l);
-  uint32_t hi = __builtin_amdgcn_readlane(uint32_t(uint64_t(v) >> 32), l);
-  return int64_t((uint64_t(hi) << 32) | lo);
-}
-__device__ inline int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
-__device__ inline int64_t uni64(int64_t v) { return rdl64(v, 0); }
-
-// Every structure of a replica is read and written by that replica's single wave,
-// so work-group scope is enough for a load to see the wave's own earlier stores.
-template <class T>
-__device__ inline T ld_fresh(const T *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-__device__ inline void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup"); }
+constexpr int kReserve = 32;  // pool entries first calls leave for later calls
 
 template <bool G, class T>
 __device__ inline T RD(const T *p) {
@@ -144,83 +34,6 @@ __device__ inline T RD(const T *p) {
     return ld_fresh(p);
   else
     return *p;
-}
-
-// DPP moves for a full-wave reduction (result in lane 63): swap within pairs, swap
-// pairs, mirror within 8, mirror within 16, then broadcast row ends to later rows.
-template <int CTRL, int ROWS>
-__device__ inline uint32_t dpp(uint32_t v) {
-  return uint32_t(__builtin_amdgcn_update_dpp(int(v), int(v), CTRL, ROWS, 0xF, false));
-}
-
-template <int CTRL, int ROWS>
-__device__ inline void argmin_step(uint64_t &k, uint32_t &us, uint32_t &x) {
-  const uint32_t lo = dpp<CTRL, ROWS>(uint32_t(k)), hi = dpp<CTRL, ROWS>(uint32_t(k >> 32));
-  const uint32_t ous = dpp<CTRL, ROWS>(us), ox = dpp<CTRL, ROWS>(x);
-  const uint64_t ok = (uint64_t(hi) << 32) | lo;
-  const bool take = ok < k || (ok == k && ous < us);
-  k = take ? ok : k;
-  us = take ? ous : us;
-  x = take ? ox : x;
-}
-
-__device__ inline void wave_argmin(uint64_t &k, uint32_t &us, uint32_t &x) {
-  argmin_step<0xB1, 0xF>(k, us, x);
-  argmin_step<0x4E, 0xF>(k, us, x);
-  argmin_step<0x141, 0xF>(k, us, x);
-  argmin_step<0x140, 0xF>(k, us, x);
-  argmin_step<0x142, 0xA>(k, us, x);
-  argmin_step<0x143, 0xC>(k, us, x);
-}
-
-template <int CTRL, int ROWS>
-__device__ inline void minmax_step(uint64_t &lo, uint64_t &hi) {
-  const uint64_t a = (uint64_t(dpp<CTRL, ROWS>(uint32_t(lo >> 32))) << 32) |
-                     dpp<CTRL, ROWS>(uint32_t(lo));
-  const uint64_t b = (uint64_t(dpp<CTRL, ROWS>(uint32_t(hi >> 32))) << 32) |
-                     dpp<CTRL, ROWS>(uint32_t(hi));
-  lo = a < lo ? a : lo;
-  hi = b > hi ? b : hi;
-}
-
-__device__ inline void wave_minmax(uint64_t &lo, uint64_t &hi) {
-  minmax_step<0xB1, 0xF>(lo, hi);
-  minmax_step<0x4E, 0xF>(lo, hi);
-  minmax_step<0x141, 0xF>(lo, hi);
-  minmax_step<0x140, 0xF>(lo, hi);
-  minmax_step<0x142, 0xA>(lo, hi);
-  minmax_step<0x143, 0xC>(lo, hi);
-}
-
-template <int CTRL, int ROWS>
-__device__ inline void min64_step(uint64_t &k) {
-  const uint64_t o = (uint64_t(dpp<CTRL, ROWS>(uint32_t(k >> 32))) << 32) | dpp<CTRL, ROWS>(uint32_t(k));
-  k = o < k ? o : k;
-}
-
-// Wave minimum of a 64-bit value (result in lane 63).
-__device__ inline void wave_min64(uint64_t &k) {
-  min64_step<0xB1, 0xF>(k);
-  min64_step<0x4E, 0xF>(k);
-  min64_step<0x141, 0xF>(k);
-  min64_step<0x140, 0xF>(k);
-  min64_step<0x142, 0xA>(k);
-  min64_step<0x143, 0xC>(k);
-}
-
-template <int CTRL, int ROWS>
-__device__ inline void min32_step(uint32_t &v) {
-  const uint32_t o = dpp<CTRL, ROWS>(v);
-  v = o < v ? o : v;
-}
-
-__device__ inline void wave_min32(uint32_t &v) {
-  min32_step<0xB1, 0xF>(v);
-  min32_step<0x4E, 0xF>(v);
-  min32_step<0x141, 0xF>(v);
-  min32_step<0x140, 0xF>(v);
-  min32_step<0x142, 0xA>(v);
-  min32_step<0x143, 0xC>(v);
 }
 
 // A queued request in the pool: three 16-byte words.
@@ -269,95 +82,6 @@ __device__ inline Entry ld_entry(const Entry *p) {
   v.pad = 0;
   return v;
 }
-
-// The backlogged-user table on chip: one slot per lane, every field in a register of
-// that lane (read with v_readlane, written with a lane select).  Free lanes hold user
-// -1 and the empty key, so a user's slot is one ballot and the argmin needs no mask.
-struct XReg {
-  uint32_t klo, khi;  // key = tier << 62 | counter
-  int32_t user, q, fh, ft, hh, ht, sb, rh, rdy;
-  uint64_t occ;       // lanes in use
-  static constexpr int32_t cap = 64;
-  __device__ void init() {
-    klo = khi = 0xffffffffu;
-    user = -1;
-    q = 0;
-    fh = ft = rh = -1;
-    hh = ht = sb = rdy = 0;
-    occ = 0;
-  }
-  static __device__ int32_t wl(int32_t old, int32_t x, int32_t v) {
-    return int32_t(threadIdx.x) == x ? v : old;
-  }
-  __device__ uint64_t key(int32_t x) const {
-    return (uint64_t(uint32_t(rdl(int32_t(khi), x))) << 32) | uint32_t(rdl(int32_t(klo), x));
-  }
-  __device__ void set_key(int32_t x, uint64_t v) {
-    klo = uint32_t(wl(int32_t(klo), x, int32_t(uint32_t(v))));
-    khi = uint32_t(wl(int32_t(khi), x, int32_t(uint32_t(v >> 32))));
-  }
-#define FS_XREG_FIELD(f)                                              \
-  __device__ int32_t get_##f(int32_t x) const { return rdl(f, x); } \
-  __device__ void set_##f(int32_t x, int32_t v) { f = wl(f, x, v); }
-  FS_XREG_FIELD(user)
-  FS_XREG_FIELD(q)
-  FS_XREG_FIELD(fh)
-  FS_XREG_FIELD(ft)
-  FS_XREG_FIELD(hh)
-  FS_XREG_FIELD(ht)
-  FS_XREG_FIELD(sb)
-  FS_XREG_FIELD(rh)
-  FS_XREG_FIELD(rdy)
-#undef FS_XREG_FIELD
-  __device__ int32_t find(int32_t k, const Store &) const {
-    const uint64_t m = __ballot(user == k);
-    return m ? __ffsll((long long)m) - 1 : -1;
-  }
-  __device__ int32_t alloc(int32_t, int32_t, const Store &) {
-    const int32_t x = __ffsll((long long)~occ) - 1;
-    occ |= uint64_t(1) << x;
-    return x;
-  }
-  __device__ void release(int32_t x, int32_t, int32_t, const Store &) {
-    occ &= ~(uint64_t(1) << x);
-    set_key(x, kEmptyKey);
-    set_user(x, -1);
-  }
-  __device__ int32_t slot(int32_t i, int32_t) const {  // i-th slot in use
-    uint64_t m = occ;
-    for (int32_t j = 0; j < i; ++j) m &= m - 1;
-    return __ffsll((long long)m) - 1;
-  }
-  // Slot of the least (key, user id): a 64-bit DPP minimum, then a ballot of the lanes
-  // holding it; only a tie on the key needs the minimum over user ids.
-  __device__ int32_t argmin(int32_t, uint64_t &bk, int32_t &bu) const {
-    const uint64_t k = (uint64_t(khi) << 32) | klo;
-    uint64_t m = k;
-    wave_min64(m);
-    const uint64_t mn = uint64_t(rdl64(int64_t(m), 63));
-    const uint64_t eq = __ballot(k == mn);
-    int32_t x;
-    if ((eq & (eq - 1)) == 0) {
-      x = __ffsll((long long)eq) - 1;
-    } else {
-      uint32_t us = k == mn ? uint32_t(user) : 0xffffffffu;
-      wave_min32(us);
-      const uint32_t umin = uint32_t(rdl(int32_t(us), 63));
-      x = __ffsll((long long)__ballot(k == mn && uint32_t(user) == umin)) - 1;
-    }
-    bk = mn;
-    bu = rdl(user, x);
-    return x;
-  }
-  __device__ void minmax(int32_t, int64_t &mn, int64_t &mx) const {
-    const bool in = (occ >> threadIdx.x) & 1u;
-    const uint64_t v = ((uint64_t(khi) << 32) | klo) & kValMask;
-    uint64_t lo = in ? v : kEmptyKey, hi = in ? v : 0;
-    wave_minmax(lo, hi);
-    mn = rdl64(int64_t(lo), 63);
-    mx = rdl64(int64_t(hi), 63);
-  }
-};
 
 // The same table in global memory (after an on-chip overflow): slots [0, nX) packed,
 // capacity n_r + 1, with the user -> slot table S.xslot.
@@ -478,6 +202,9 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   else
     s_end = uni64(rs->s_end);  // resuming a launch that overflowed on chip
   const int64_t tau = a.tau, C = a.cap, theta = a.theta;
+  // resuming inside step s: its arrivals are done and its budget is partly spent
+  bool mid = !onchip && uni(rs->mid) != 0;
+  const int64_t mid_budget = uni64(rs->mid_budget);
 
   if (!S.users_global)
     for (int32_t k = lane; k < U; k += 64) S.u[k] = u_all[k];
@@ -882,7 +609,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     if (overflow || code) break;
 
     // execution stream: admit while the step has budget
-    int64_t budget = C + debt;
+    int64_t budget = mid ? mid_budget : C + debt;
+    mid = false;
     while (budget > 0 && nX > 0) {
       uint64_t bk;
       int32_t k;
@@ -1034,6 +762,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     rs->last_exit = last_exit;
     rs->done = drained ? 1 : 0;
     rs->overflow = overflow ? 1 : 0;
+    rs->mid = 0;
     rs->s_end = s_end;
     if (!overflow) {
       a.steps[r] = s;
@@ -1045,57 +774,6 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   if (!overflow)
     for (int32_t k = lane; k < U; k += 64)
       a.counter[int64_t(r) * U + k] = S.users_global ? ld_fresh(u_all + k) : u_all[k];
-}
-
-__device__ inline bool state_header_ok(const SchedArgs &a) {
-  const Header *h = reinterpret_cast<const Header *>(a.state + a.L.hdr);
-  return h->magic == kMagic && h->version == kVersion && h->R == a.t.R && h->U == a.t.U &&
-         h->N == a.t.N;
-}
-
-__device__ inline bool finish_if_done(const SchedArgs &a, int32_t r) {
-  RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
-  if (!rs->done) return false;
-  if (threadIdx.x == 0) {
-    a.steps[r] = rs->s;
-    a.decisions[r] = rs->seq;
-    a.max_gap[r] = rs->gap;
-  }
-  const int64_t *u_all =
-      reinterpret_cast<const int64_t *>(a.state + a.L.u_all) + int64_t(r) * a.t.U;
-  for (int32_t k = threadIdx.x; k < a.t.U; k += 64) a.counter[int64_t(r) * a.t.U + k] = u_all[k];
-  return true;
-}
-
-// On-chip pass: LDS holds the X table and the pool (and the counters when U is small).
-template <bool USERS_LDS>
-__global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
-  extern __shared__ __align__(16) char smem[];
-  const int32_t r = blockIdx.x;
-  if (*a.err) return;
-  if (!state_header_ok(a)) return;
-  if (finish_if_done(a, r)) return;
-  Store S;
-  char *p = smem;
-  auto take = [&](size_t bytes) {
-    char *q = p;
-    p += (bytes + 15) & ~size_t(15);
-    return q;
-  };
-  const size_t pc = size_t(a.pcap);
-  S.pcap = a.pcap;
-  S.e = reinterpret_cast<Entry *>(take(sizeof(Entry) * pc));
-  S.e_free = reinterpret_cast<int32_t *>(take(4 * pc));
-  S.xslot = nullptr;
-  if (USERS_LDS) {
-    S.u = reinterpret_cast<int64_t *>(take(8 * size_t(a.t.U)));
-    S.users_global = false;
-  } else {
-    S.u = reinterpret_cast<int64_t *>(a.state + a.L.u_all) + int64_t(r) * a.t.U;
-    S.users_global = true;
-  }
-  XReg X;
-  run_replica<false>(a, S, X, r, true);
 }
 
 // Global-memory pass: resumes replicas that overflowed on chip (or runs all
@@ -1252,15 +930,6 @@ int grid_for(int64_t n, int threads) {
   return int(b);
 }
 
-size_t onchip_lds_bytes(int32_t pcap, int32_t U, bool users_lds) {
-  size_t b = 0;
-  auto add = [&](size_t x) { b += (x + 15) & ~size_t(15); };
-  add(sizeof(Entry) * size_t(pcap));
-  add(4 * size_t(pcap));
-  if (users_lds) add(8 * size_t(U));
-  return b;
-}
-
 }  // namespace
 
 size_t state_bytes(const fs_trace *t) {
@@ -1313,19 +982,12 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.err = out->err;
   a.state = static_cast<char *>(state);
   a.L = state_layout(t->n_replicas, t->n_users, N);
-  const bool users_lds = t->n_users <= kUsersLdsMax;
-  a.pcap = t->n_users > 512 ? 512 : 1024;
+  a.oc = onchip_config(t->n_replicas, t->n_users);
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
   hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);
   const dim3 grid(t->n_replicas), block(64);
-  if (!a.global_only) {
-    const size_t lds = onchip_lds_bytes(a.pcap, t->n_users, users_lds);
-    if (users_lds)
-      hipLaunchKernelGGL(k_schedule_onchip<true>, grid, block, lds, s, a);
-    else
-      hipLaunchKernelGGL(k_schedule_onchip<false>, grid, block, lds, s, a);
-  }
+  if (!a.global_only) launch_onchip(a, s);
   hipLaunchKernelGGL(k_schedule_global, grid, block, 0, s, a);
   return hipGetLastError();
 }

@@ -1,0 +1,243 @@
+// Scheduler state blob, kernel arguments and wavefront helpers shared by the two
+// scheduler kernels (on-chip: fs_sched_onchip.hip; global memory: fs_sched.hip).
+//
+// The state blob (fs_state_bytes) is what lets fs_schedule_step stop after n steps
+// and resume later, and what lets the on-chip kernel hand a replica over to the
+// global-memory kernel when an on-chip capacity would overflow.  It holds the
+// per-replica scalars, the service counters of every user and the fate of every
+// request; the waiting queue itself is rebuilt on resume from the requests that
+// have arrived and are still undecided, in stream order.
+#pragma once
+#include "fs_device.h"
+#include "fs_launch.h"
+
+namespace fs {
+namespace sched {
+
+constexpr uint64_t kMagic = 0x32535652'49414646ull;
+constexpr int32_t kVersion = 4;
+constexpr uint64_t kTierShift = 62;
+constexpr uint64_t kValMask = (uint64_t(1) << 62) - 1;
+constexpr uint64_t kEmptyKey = ~uint64_t(0);
+
+// Per-replica scalars.  `mid` = 1 when a launch stopped inside the admissions of
+// step s (an on-chip capacity would have overflowed there); `mid_budget` is the
+// budget that step still has.
+struct RepState {
+  int64_t s, nxt, debt, backlog, seq, gap, last_exit_u, low, s_end;
+  int32_t last_exit, done, overflow, mid;
+  int64_t mid_budget;
+  int64_t pad2[4];
+};
+static_assert(sizeof(RepState) == 128, "RepState layout");
+
+struct Header {
+  uint64_t magic;
+  int32_t version, R, U, pad;
+  int64_t N;
+  int64_t pad2[4];
+};
+
+inline size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+struct StateLayout {
+  size_t hdr, reps, u_all, xslot_all, fate, succ, seg_start, seg_part, seg_rec, seg_tok, seg_cost,
+      seg_succ, seg_pk;
+  // global-memory scheduler structures (n_r + 1 entries per replica, at rep_off[r] + r)
+  size_t xkey, xuser, xq, xfh, xft, xhh, xht, xsb, xrh, xrdy;
+  size_t e_all, e_free;
+  size_t emap;  // per record: the pool entry it last occupied (checked before use)
+  size_t total;
+};
+
+inline StateLayout state_layout(int32_t R, int32_t U, int64_t N) {
+  StateLayout L;
+  size_t n = size_t(N > 0 ? N : 1), ru = size_t(R) * size_t(U);
+  size_t nr = size_t(N) + size_t(R) + 1;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o += up256(bytes);
+    return at;
+  };
+  L.hdr = take(sizeof(Header));
+  L.reps = take(sizeof(RepState) * size_t(R));
+  L.u_all = take(ru * 8);
+  L.xslot_all = take(ru * 4);
+  L.fate = take(n);
+  L.succ = take(n * 4);
+  L.seg_start = take((ru + 1) * 4);
+  L.seg_part = take(scan_partials_bytes(int64_t(ru + 1)));
+  L.seg_rec = take(n * 4);
+  L.seg_tok = take(n * 4);
+  L.seg_cost = take(n * 8);
+  L.seg_succ = take(n * 4);
+  L.seg_pk = take(n * 16);
+  L.xkey = take(nr * 8);
+  L.xuser = take(nr * 4);
+  L.xq = take(nr * 4);
+  L.xfh = take(nr * 4);
+  L.xft = take(nr * 4);
+  L.xhh = take(nr * 4);
+  L.xht = take(nr * 4);
+  L.xsb = take(nr * 4);
+  L.xrh = take(nr * 4);
+  L.xrdy = take(nr * 4);
+  L.e_all = take(nr * 48);
+  L.e_free = take(nr * 4);
+  L.emap = take(n * 4);
+  L.total = o;
+  return L;
+}
+
+// LDS layout of the on-chip kernel (sizes chosen on the host from the replica
+// count, so that enough work-groups fit on a CU).
+struct OnchipCfg {
+  int32_t ring;       // first calls kept on chip per backlogged user (power of two)
+  int32_t cache;      // recent arrivals whose data stays on chip (power of two)
+  int32_t users_lds;  // 1: counters of idle users in LDS, 0: in the state buffer
+  int32_t pad;
+  size_t lds_bytes;
+};
+
+struct SchedArgs {
+  DevTrace t;
+  const int64_t *cost;
+  const uint8_t *reason;
+  int64_t tau, cap, theta;
+  int64_t n_steps;
+  bool global_only;
+  int8_t *status;
+  int32_t *admit_step, *admit_seq;
+  int64_t *counter_after, *counter_on_arrival, *counter, *steps, *decisions, *max_gap;
+  int32_t *err;
+  char *state;
+  StateLayout L;
+  OnchipCfg oc;
+};
+
+// ------------------------------------------------------------- wave helpers
+
+__device__ inline int32_t rdl(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ inline uint32_t rdlu(uint32_t v, int l) {
+  return uint32_t(__builtin_amdgcn_readlane(int32_t(v), l));
+}
+__device__ inline int64_t rdl64(int64_t v, int l) {
+  uint32_t lo = __builtin_amdgcn_readlane(uint32_t(uint64_t(v)), l);
+  uint32_t hi = __builtin_amdgcn_readlane(uint32_t(uint64_t(v) >> 32), l);
+  return int64_t((uint64_t(hi) << 32) | lo);
+}
+__device__ inline int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ inline int64_t uni64(int64_t v) { return rdl64(v, 0); }
+
+// Every structure of a replica is read and written by that replica's single wave,
+// so work-group scope is enough for a load to see the wave's own earlier stores.
+template <class T>
+__device__ inline T ld_fresh(const T *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ inline void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup"); }
+
+// DPP moves for a full-wave reduction (result in lane 63): swap within pairs, swap
+// pairs, mirror within 8, mirror within 16, then broadcast row ends to later rows.
+template <int CTRL, int ROWS>
+__device__ inline uint32_t dpp(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(int(v), int(v), CTRL, ROWS, 0xF, false));
+}
+
+template <int CTRL, int ROWS>
+__device__ inline void argmin_step(uint64_t &k, uint32_t &us, uint32_t &x) {
+  const uint32_t lo = dpp<CTRL, ROWS>(uint32_t(k)), hi = dpp<CTRL, ROWS>(uint32_t(k >> 32));
+  const uint32_t ous = dpp<CTRL, ROWS>(us), ox = dpp<CTRL, ROWS>(x);
+  const uint64_t ok = (uint64_t(hi) << 32) | lo;
+  const bool take = ok < k || (ok == k && ous < us);
+  k = take ? ok : k;
+  us = take ? ous : us;
+  x = take ? ox : x;
+}
+
+__device__ inline void wave_argmin(uint64_t &k, uint32_t &us, uint32_t &x) {
+  argmin_step<0xB1, 0xF>(k, us, x);
+  argmin_step<0x4E, 0xF>(k, us, x);
+  argmin_step<0x141, 0xF>(k, us, x);
+  argmin_step<0x140, 0xF>(k, us, x);
+  argmin_step<0x142, 0xA>(k, us, x);
+  argmin_step<0x143, 0xC>(k, us, x);
+}
+
+template <int CTRL, int ROWS>
+__device__ inline void minmax_step(uint64_t &lo, uint64_t &hi) {
+  const uint64_t a = (uint64_t(dpp<CTRL, ROWS>(uint32_t(lo >> 32))) << 32) |
+                     dpp<CTRL, ROWS>(uint32_t(lo));
+  const uint64_t b = (uint64_t(dpp<CTRL, ROWS>(uint32_t(hi >> 32))) << 32) |
+                     dpp<CTRL, ROWS>(uint32_t(hi));
+  lo = a < lo ? a : lo;
+  hi = b > hi ? b : hi;
+}
+
+__device__ inline void wave_minmax(uint64_t &lo, uint64_t &hi) {
+  minmax_step<0xB1, 0xF>(lo, hi);
+  minmax_step<0x4E, 0xF>(lo, hi);
+  minmax_step<0x141, 0xF>(lo, hi);
+  minmax_step<0x140, 0xF>(lo, hi);
+  minmax_step<0x142, 0xA>(lo, hi);
+  minmax_step<0x143, 0xC>(lo, hi);
+}
+
+// 32-bit wave minimum / maximum (result in lane 63).
+template <int CTRL, int ROWS>
+__device__ inline void min32_step(uint32_t &v) {
+  const uint32_t o = dpp<CTRL, ROWS>(v);
+  v = o < v ? o : v;
+}
+template <int CTRL, int ROWS>
+__device__ inline void max32_step(uint32_t &v) {
+  const uint32_t o = dpp<CTRL, ROWS>(v);
+  v = o > v ? o : v;
+}
+__device__ inline uint32_t wave_min32(uint32_t v) {
+  min32_step<0xB1, 0xF>(v);
+  min32_step<0x4E, 0xF>(v);
+  min32_step<0x141, 0xF>(v);
+  min32_step<0x140, 0xF>(v);
+  min32_step<0x142, 0xA>(v);
+  min32_step<0x143, 0xC>(v);
+  return rdlu(v, 63);
+}
+__device__ inline uint32_t wave_max32(uint32_t v) {
+  max32_step<0xB1, 0xF>(v);
+  max32_step<0x4E, 0xF>(v);
+  max32_step<0x141, 0xF>(v);
+  max32_step<0x140, 0xF>(v);
+  max32_step<0x142, 0xA>(v);
+  max32_step<0x143, 0xC>(v);
+  return rdlu(v, 63);
+}
+
+__device__ inline bool state_header_ok(const SchedArgs &a) {
+  const Header *h = reinterpret_cast<const Header *>(a.state + a.L.hdr);
+  return h->magic == kMagic && h->version == kVersion && h->R == a.t.R && h->U == a.t.U &&
+         h->N == a.t.N;
+}
+
+// A replica already drained by an earlier call: republish its results.
+__device__ inline bool finish_if_done(const SchedArgs &a, int32_t r) {
+  RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
+  if (!rs->done) return false;
+  if (threadIdx.x == 0) {
+    a.steps[r] = rs->s;
+    a.decisions[r] = rs->seq;
+    a.max_gap[r] = rs->gap;
+  }
+  const int64_t *u_all =
+      reinterpret_cast<const int64_t *>(a.state + a.L.u_all) + int64_t(r) * a.t.U;
+  for (int32_t k = threadIdx.x; k < a.t.U; k += 64) a.counter[int64_t(r) * a.t.U + k] = u_all[k];
+  return true;
+}
+
+// Host side: the on-chip kernel's LDS layout for this launch and its launcher.
+OnchipCfg onchip_config(int32_t R, int32_t U);
+void launch_onchip(const SchedArgs &a, hipStream_t s);
+
+}  // namespace sched
+}  // namespace fs

@@ -1,0 +1,696 @@
+// WSC scheduler steps (Alg. 1, monitoring and execution streams) under the
+// token-budget step engine: the on-chip kernel, one wavefront per trace replica.
+//
+// A replica is one dependent chain of arrivals and admissions, so its speed is the
+// length of the wave's instruction stream per event.  Everything an event touches
+// stays in registers or LDS, and nothing inside an event waits on HBM in the common
+// case:
+//   slots     one backlogged user per lane (the paper's Q keyed by user): user id,
+//             key = tier << 62 | service counter (tier 0 while the user has a ready
+//             later call of an incomplete interaction), the number of queued calls,
+//             the ordinals of its FIFO of first calls (head, on-chip end, tail), the
+//             head request's data, and its number of ready later calls.  The argmin
+//             over (key, user id) is two 32-bit DPP minimums.  A slot's state changes
+//             in its own lane, under an exec mask, so an update costs no cross-lane
+//             traffic.
+//   ready     one ready later call (previous call admitted) per lane: owning slot,
+//             record, data.  A user's earliest ready call is a masked DPP minimum,
+//             needed only when it has more than one.
+//   ring      per slot, the next first calls of the FIFO in LDS; a FIFO longer than
+//             the ring continues in the user's segment of the state buffer (one entry
+//             per first call of the user) and comes back in coalesced refills.
+//   cache     the data of the most recent arrivals in LDS, by record index, so a
+//             later call that waited for its previous call becomes ready without
+//             reading HBM.
+//   window    the next 64 records, one per lane, with their step, packed request,
+//             flags (first call, raw throttle reason, "head throttled", "previous
+//             call admitted") and the user's counter; state changes patch it.
+// Outputs of arrivals and admissions are collected one per lane and written 64 at a
+// time.  When an on-chip capacity would overflow, the wave stops before the event
+// that needs it, saves the replica's state and the global-memory kernel resumes it.
+#include <stddef.h>
+
+#include "fs_sched_common.h"
+
+namespace fs {
+namespace sched {
+namespace {
+
+constexpr int64_t kPackLimit = int64_t(1) << 40;  // costs that fit a packed request
+constexpr uint64_t kTokMask = (uint64_t(1) << 24) - 1;
+constexpr int kSlots = 64;
+constexpr uint32_t kTier1 = 0x40000000u;  // the tier bit in a key's high word
+constexpr uint32_t kValHi = 0x3fffffffu;  // the counter's bits in a key's high word
+
+// window flags
+constexpr int32_t kFirst = 1;        // first call of its interaction
+constexpr int32_t kReasonShift = 1;  // bits 1-2: raw throttle reason (0 within limits)
+constexpr int32_t kHeadBlk = 8;      // later call whose interaction's first call was throttled
+constexpr int32_t kPrevAdm = 16;     // later call whose previous call has been admitted
+constexpr int32_t kBig = 32;         // cost too large for a packed request
+
+// A queued request on chip: record, its next call (-1: none), (cost << 24) | tokens.
+struct __align__(16) Ent {
+  int32_t rec, succ;
+  uint32_t lo, hi;
+};
+
+__device__ inline Ent mk_ent(int32_t rec, int32_t sc, uint32_t lo, uint32_t hi) {
+  Ent e;
+  e.rec = rec;
+  e.succ = sc;
+  e.lo = lo;
+  e.hi = hi;
+  return e;
+}
+
+__device__ inline int32_t ff1(uint64_t m) { return __ffsll((long long)m) - 1; }
+
+// A field of the kernel's argument block, loaded with a scalar load where it is used
+// instead of being held in a scalar register for the whole kernel.  The block is the
+// kernel's only argument, at the start of the kernarg segment.
+template <class T>
+__device__ __forceinline__ T arg_at(uint32_t off) {
+  __asm__ volatile("" : "+s"(off));
+  const __attribute__((address_space(4))) char *k =
+      (const __attribute__((address_space(4))) char *)__builtin_amdgcn_kernarg_segment_ptr();
+  return *(const __attribute__((address_space(4))) T *)(k + off);
+}
+#define KARG(f) arg_at<decltype(SchedArgs{}.f)>(uint32_t(offsetof(SchedArgs, f)))
+
+#define STATE(T, field) reinterpret_cast<T *>(KARG(state) + KARG(L.field))
+
+__global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  const int32_t r = blockIdx.x;
+  if (*a.err) return;
+  if (!state_header_ok(a)) return;
+  if (finish_if_done(a, r)) return;
+
+  const int lane = threadIdx.x;
+  const int32_t D = a.oc.ring, M = a.oc.cache;
+  const bool ulds = a.oc.users_lds != 0;
+  const int32_t U = a.t.U;
+  Ent *const ring = reinterpret_cast<Ent *>(smem);  // [kSlots][D]
+  Ent *const cache = ring + kSlots * D;             // [M]
+  int64_t *const u_lds = reinterpret_cast<int64_t *>(cache + M);
+  const int64_t base = a.t.rep_off[r];
+  const int32_t n = int32_t(a.t.rep_off[r + 1] - base);
+  RepState *const rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
+  int64_t *const u_all = reinterpret_cast<int64_t *>(a.state + a.L.u_all) + int64_t(r) * U;
+
+  // ---- scalar state of the replica
+  int32_t s = int32_t(uni64(rs->s)), nxt = int32_t(uni64(rs->nxt));
+  int32_t low = int32_t(uni64(rs->low)), seq = int32_t(uni64(rs->seq));
+  int64_t debt = uni64(rs->debt), backlog = uni64(rs->backlog), gap = uni64(rs->gap);
+  int64_t last_exit_u = uni64(rs->last_exit_u);
+  int32_t last_exit = uni(rs->last_exit);
+  const int64_t s_end = a.n_steps < 0 ? INT64_MAX : int64_t(s) + a.n_steps;
+  const int64_t C = a.cap, theta = a.theta;
+  if (uni(rs->mid)) {  // stopped inside a step: only the global-memory kernel resumes that
+    if (lane == 0) {
+      rs->overflow = 1;
+      rs->s_end = s_end;
+    }
+    return;
+  }
+
+  if (ulds)
+    for (int32_t k = lane; k < U; k += 64) u_lds[k] = u_all[k];
+  __syncthreads();
+
+  auto put_u = [&](int32_t k, int64_t v) {
+    if (lane == 0) {
+      if (ulds)
+        u_lds[k] = v;
+      else
+        u_all[k] = v;
+    }
+  };
+
+  // ---- slots: one backlogged user per lane
+  uint32_t kh = 0xffffffffu, kl = 0xffffffffu;  // key (tier << 62 | counter); free = all ones
+  int32_t xu = -1;                              // user id, -1 = free
+  int32_t xq = 0;                               // queued calls (first and later)
+  int32_t xf = 0, xr = 0, xt = 0;               // FIFO ordinals: head, on-chip end, tail
+  uint32_t xsb = 0;                             // the user's segment of first calls
+  int32_t xn = 0;                               // ready later calls
+  int32_t hrec = -1, hsucc = -1;                // FIFO head request
+  uint32_t hlo = 0, hhi = 0;
+  uint64_t occ = 0;
+  int32_t nX = 0;
+  // ---- ready later calls: one per lane
+  int32_t p_x = -1, p_rec = INT32_MAX, p_succ = -1;
+  uint32_t p_lo = 0, p_hi = 0;
+  uint64_t pocc = 0;
+
+  int64_t minX = 0;
+  int32_t code = 0;
+  bool overflow = false, mid = false;
+  int64_t mid_budget = 0;
+
+  // First call (rec, sc, lo, hi) joins the tail of slot x's FIFO: on chip while the
+  // FIFO has no part in HBM and the ring has room, else in the user's segment.
+  auto fifo_push = [&](int32_t x, int32_t rec, int32_t sc, uint32_t lo, uint32_t hi) {
+    if (lane == x) {
+      if (xt == xr && xr - xf < D) {
+        ring[x * D + (xt & (D - 1))] = mk_ent(rec, sc, lo, hi);
+        if (xt == xf) {
+          hrec = rec;
+          hsucc = sc;
+          hlo = lo;
+          hhi = hi;
+        }
+        ++xr;
+      } else {
+        STATE(Ent, seg_pk)[int64_t(xsb) + xt] = mk_ent(rec, sc, lo, hi);
+      }
+      ++xt;
+    }
+  };
+  // Slot x's FIFO runs low on chip while its segment holds more: one coalesced
+  // load moves up to a ring's worth back.
+  auto fifo_refill = [&](int32_t x) {
+    const int32_t f1 = rdl(xf, x) + 1, rr = rdl(xr, x), tt = rdl(xt, x);
+    int32_t m = D - (rr - f1);
+    if (m > tt - rr) m = tt - rr;
+    wave_fence();
+    if (lane < m) {
+      const Ent v = STATE(Ent, seg_pk)[int64_t(rdlu(xsb, x)) + rr + lane];
+      ring[x * D + ((rr + lane) & (D - 1))] = v;
+    }
+    if (lane == x) xr += m;
+  };
+  // Slot x gains ready later call (rec, sc, lo, hi); the caller has checked that a
+  // ready lane is free.
+  auto ready_add = [&](int32_t x, int32_t rec, int32_t sc, uint32_t lo, uint32_t hi) {
+    const int32_t l = ff1(~pocc);
+    pocc |= uint64_t(1) << l;
+    if (lane == l) {
+      p_x = x;
+      p_rec = rec;
+      p_succ = sc;
+      p_lo = lo;
+      p_hi = hi;
+    }
+    if (lane == x) {
+      ++xn;
+      kh &= kValHi;  // tier 0
+    }
+  };
+  // Slot for user k with counter uk (tier 1, nothing queued yet).
+  auto join = [&](int32_t k, int64_t uk, uint32_t sb) -> int32_t {
+    const int32_t x = ff1(~occ);
+    occ |= uint64_t(1) << x;
+    ++nX;
+    if (lane == x) {
+      kh = uint32_t(uint64_t(uk) >> 32) | kTier1;
+      kl = uint32_t(uint64_t(uk));
+      xu = k;
+      xq = 0;
+      xf = xr = xt = 0;
+      xsb = sb;
+      xn = 0;
+    }
+    return x;
+  };
+  // Data of an arrived record read from the inputs (when it is no longer cached).
+  auto load_rec = [&](int32_t i, int32_t &sc, uint32_t &lo, uint32_t &hi) {
+    const int64_t g = base + i;
+    const int32_t *len_sys = KARG(t.len_sys);
+    const int32_t tok =
+        KARG(t.len_in)[g] + KARG(t.len_out)[g] + (len_sys ? len_sys[g] : 0);
+    const uint64_t pk = (uint64_t(KARG(cost)[g]) << 24) | uint32_t(tok);
+    sc = uni(STATE(const int32_t, succ)[base + i]);
+    lo = uint32_t(uni(int32_t(uint32_t(pk))));
+    hi = uint32_t(uni(int32_t(uint32_t(pk >> 32))));
+  };
+
+  // ---- admissions waiting to be written: lane i holds the i-th of nd
+  int32_t d_rec = 0, d_step = 0, nd = 0;
+  int64_t d_cnt = 0;
+  auto flush_decisions = [&]() {
+    if (nd == 0) return;
+    if (lane < nd) {
+      const int64_t g = base + d_rec;
+      STATE(int8_t, fate)[g] = 0;
+      KARG(status)[g] = 0;
+      KARG(admit_step)[g] = d_step;
+      int32_t *const as = KARG(admit_seq);
+      if (as) as[g] = seq - nd + lane;
+      int64_t *const ca = KARG(counter_after);
+      if (ca) ca[g] = d_cnt;
+    }
+    nd = 0;
+  };
+
+  // ---- window of upcoming records, one per lane
+  int32_t wbase = nxt, cache_from = nxt, cache_lo = nxt;
+  int32_t w_step = INT32_MAX, w_user = -1, w_flags = 0, w_head = -1, w_prev = -1, w_succ = -1;
+  uint32_t w_seg = 0, w_lo = 0, w_hi = 0;
+  int64_t c_u = 0;
+  int32_t o_st = 0;
+  int64_t o_coa = 0;
+  auto flush_window = [&]() {
+    const int32_t done = nxt - wbase;
+    if (lane < done) {
+      const int64_t g = base + wbase + lane;
+      if (o_st > 0) {
+        STATE(int8_t, fate)[g] = int8_t(o_st);
+        KARG(status)[g] = int8_t(o_st);
+        KARG(admit_step)[g] = -1;
+        int32_t *const as = KARG(admit_seq);
+        if (as) as[g] = -1;
+        int64_t *const ca = KARG(counter_after);
+        if (ca) ca[g] = -1;
+      }
+      int64_t *const coa = KARG(counter_on_arrival);
+      if (coa) coa[g] = o_coa;
+    }
+    o_st = 0;
+  };
+  auto load_window = [&]() {
+    wave_fence();
+    const int32_t i = wbase + lane;
+    w_step = INT32_MAX;
+    w_user = -1;
+    w_flags = 0;
+    w_head = -1;
+    w_prev = -1;
+    w_succ = -1;
+    w_seg = 0;
+    w_lo = w_hi = 0;
+    c_u = 0;
+    if (i < n) {
+      const int64_t g = base + i;
+      const int32_t *const callp = KARG(t.call);
+      const int32_t call = callp ? callp[g] : 0;
+      const int32_t usr = KARG(t.user)[g];
+      const int64_t ts = KARG(t.ts)[g];
+      const int32_t hd = callp ? KARG(t.head)[g] : i;
+      const int32_t pv = callp ? KARG(t.prev)[g] : -1;
+      const int32_t *len_sys = KARG(t.len_sys);
+      const int32_t tok = KARG(t.len_in)[g] + KARG(t.len_out)[g] + (len_sys ? len_sys[g] : 0);
+      const int64_t cst = KARG(cost)[g];
+      const uint8_t *const reason = KARG(reason);
+      const int32_t why = reason ? reason[g] : 0;
+      const int32_t sc = STATE(const int32_t, succ)[g];
+      const uint32_t sb = STATE(const uint32_t, seg_start)[int64_t(r) * U + usr];
+      const int64_t uu = ulds ? u_lds[usr] : ld_fresh(u_all + usr);
+      int32_t fl = call == 0 ? kFirst : 0;
+      if (call > 0) {
+        const int8_t *const fate = STATE(const int8_t, fate) + base;
+        const int8_t pf = ld_fresh(fate + pv), hf = ld_fresh(fate + hd);
+        fl |= (pf == 0 ? kPrevAdm : 0) | ((hf == 1 || hf == 2) ? kHeadBlk : 0);
+      }
+      fl |= (why << kReasonShift) | (cst >= kPackLimit ? kBig : 0);
+      const int64_t stp = ts / KARG(tau);
+      w_step = stp < INT32_MAX ? int32_t(stp) : INT32_MAX;
+      w_user = usr;
+      w_flags = fl;
+      w_head = hd;
+      w_prev = pv;
+      w_succ = sc;
+      w_seg = sb;
+      const uint64_t pk = (uint64_t(cst) << 24) | uint32_t(tok);
+      w_lo = uint32_t(pk);
+      w_hi = uint32_t(pk >> 32);
+      c_u = uu;
+      cache[i & (M - 1)] = mk_ent(i, sc, w_lo, w_hi);
+    }
+    // every loaded value is in its register from here on: no later wait on HBM
+    __asm__ volatile("" ::"v"(w_step), "v"(w_user), "v"(w_flags), "v"(w_head), "v"(w_prev),
+                     "v"(w_succ), "v"(w_seg), "v"(w_lo), "v"(w_hi), "v"(c_u));
+    const int32_t lo_ = wbase + 64 - M;
+    cache_lo = lo_ > cache_from ? lo_ : cache_from;
+  };
+  auto advance_window = [&]() {
+    flush_window();
+    flush_decisions();
+    wbase = nxt;
+    load_window();
+  };
+
+  // ---- rebuild the queue left by a previous call: arrived records still undecided
+  for (int32_t b0 = low; b0 < nxt && !overflow; b0 += 64) {
+    const int8_t *const fate = STATE(const int8_t, fate) + base;
+    const int32_t i = b0 + lane;
+    const bool q = i < nxt && ld_fresh(fate + i) == -1;
+    uint64_t m = __ballot(q);
+    while (m && !overflow) {
+      const int l = ff1(m);
+      m &= m - 1;
+      const int32_t rec = b0 + l;
+      const int64_t g = base + rec;
+      const int32_t k = uni(KARG(t.user)[g]);
+      const int32_t *const callp = KARG(t.call);
+      const int32_t call = callp ? uni(callp[g]) : 0;
+      int32_t sc;
+      uint32_t lo, hi;
+      load_rec(rec, sc, lo, hi);
+      const bool padm = call > 0 && ld_fresh(fate + uni(KARG(t.prev)[g])) == 0;
+      const uint64_t fm = __ballot(xu == k);
+      const bool big = KARG(cost)[g] >= kPackLimit;
+      if (big || (fm == 0 && nX == kSlots) || (padm && pocc == ~uint64_t(0))) {
+        overflow = true;  // nothing in the state buffer has changed yet
+        break;
+      }
+      int32_t x = ff1(fm);
+      if (fm == 0) {
+        const int64_t uk = uni64(ulds ? u_lds[k] : ld_fresh(u_all + k));
+        const uint32_t sb = uint32_t(uni(int32_t(STATE(const uint32_t, seg_start)[int64_t(r) * U + k])));
+        x = join(k, uk, sb);
+      }
+      if (lane == x) ++xq;
+      if (call == 0)
+        fifo_push(x, rec, sc, lo, hi);
+      else if (padm)
+        ready_add(x, rec, sc, lo, hi);
+    }
+  }
+  if (overflow) {
+    if (lane == 0) {
+      rs->overflow = 1;
+      rs->mid = 0;
+      rs->s_end = s_end;
+    }
+    return;
+  }
+  if (nX > 0) {
+    const bool oc = xu >= 0;
+    const uint32_t uh = kh & kValHi;
+    const uint32_t mh = wave_min32(oc ? uh : 0xffffffffu);
+    const uint32_t ml = wave_min32(oc && uh == mh ? kl : 0xffffffffu);
+    minX = int64_t((uint64_t(mh) << 32) | ml);
+  }
+  if (nxt < n) load_window();
+
+  // ---- steps
+  while (true) {
+    if (s >= s_end) break;
+    if (nxt == n && nX == 0) break;
+    if (nxt < n && nxt - wbase >= 64) advance_window();
+    if (nX == 0 && nxt < n) {
+      // nothing queued: the steps before the next arrival only pay back debt
+      int64_t target = rdl(w_step, nxt - wbase);
+      if (target > s_end) target = s_end;
+      if (target > s) {
+        const int64_t k = target - s;
+        debt = (k >= (-debt + C - 1) / C) ? 0 : debt + k * C;
+        s = int32_t(target);
+        if (s >= s_end) break;
+      }
+    }
+    if (s >= INT32_MAX) {
+      code = FS_E_OVERFLOW;
+      break;
+    }
+
+    // monitoring stream: arrivals of step s in stream order
+    while (nxt < n) {
+      if (nxt - wbase == 64) advance_window();
+      const int j = nxt - wbase;
+      if (rdl(w_step, j) > s) break;
+      const int32_t rec = nxt;
+      const int32_t k = rdl(w_user, j);
+      const int32_t fl = rdl(w_flags, j);
+      const uint64_t fm = __ballot(xu == k);
+      const int32_t xs = ff1(fm);
+      int64_t uk, u_before = 0;
+      if (fm) {
+        uk = int64_t((uint64_t(rdlu(kh, xs) & kValHi) << 32) | rdlu(kl, xs));
+      } else {  // counter lift for a user with nothing queued
+        u_before = rdl64(c_u, j);
+        const int64_t L = nX > 0 ? minX : (last_exit >= 0 ? last_exit_u : 0);
+        uk = u_before > L ? u_before : L;
+      }
+      bool blocked;
+      int32_t why;
+      if (fl & kFirst) {
+        why = (fl >> kReasonShift) & 3;
+        blocked = backlog > theta && why != 0;
+      } else {
+        why = 3;
+        blocked = (fl & kHeadBlk) != 0;
+      }
+      if (blocked) {
+        o_st = lane == j ? why : o_st;
+        if (!fm && uk != u_before) {
+          put_u(k, uk);
+          c_u = (w_user == k) ? uk : c_u;
+        }
+        if (fl & kFirst) w_flags |= (w_head == rec && !(w_flags & kFirst)) ? kHeadBlk : 0;
+      } else {
+        // capacity first: on overflow the state is as before this arrival
+        const bool padm = !(fl & kFirst) && (fl & kPrevAdm);
+        if ((fl & kBig) || (!fm && nX == kSlots) || (padm && pocc == ~uint64_t(0))) {
+          overflow = true;
+          break;
+        }
+        const int32_t x = fm ? xs : join(k, uk, rdlu(w_seg, j));
+        if (!fm && nX == 1) minX = uk;
+        const uint32_t lo = rdlu(w_lo, j), hi = rdlu(w_hi, j);
+        const int32_t sc = rdl(w_succ, j);
+        if (lane == x) ++xq;
+        if (fl & kFirst)
+          fifo_push(x, rec, sc, lo, hi);
+        else if (padm)
+          ready_add(x, rec, sc, lo, hi);
+        backlog += int64_t(lo & uint32_t(kTokMask));
+      }
+      o_coa = lane == j ? uk : o_coa;
+      ++nxt;
+    }
+    if (overflow) break;
+
+    // execution stream: admit while the step has budget
+    int64_t budget = C + debt;
+    while (budget > 0 && nX > 0) {
+      // least (key, user id): the ready tier first, then the least counter
+      const uint32_t mh = wave_min32(kh);
+      const uint32_t ml = wave_min32(kh == mh ? kl : 0xffffffffu);
+      const bool cand = kh == mh && kl == ml;
+      const uint64_t eq = __ballot(cand);
+      int32_t x;
+      if (eq & (eq - 1)) {
+        const uint32_t um = wave_min32(cand ? uint32_t(xu) : 0xffffffffu);
+        x = ff1(__ballot(cand && uint32_t(xu) == um));
+      } else {
+        x = ff1(eq);
+      }
+      const bool tier0 = mh < kTier1;
+      const int64_t uk = int64_t((uint64_t(mh & kValHi) << 32) | ml);
+      int32_t rec, sc, l = -1;
+      uint32_t lo, hi;
+      if (tier0) {  // the user's earliest ready later call
+        const uint64_t pm = __ballot(p_x == x);
+        l = ff1(pm);
+        if (pm & (pm - 1)) {
+          const uint32_t e = wave_min32(p_x == x ? uint32_t(p_rec) : 0xffffffffu);
+          l = ff1(__ballot(p_x == x && uint32_t(p_rec) == e));
+        }
+        rec = rdl(p_rec, l);
+        sc = rdl(p_succ, l);
+        lo = rdlu(p_lo, l);
+        hi = rdlu(p_hi, l);
+      } else {  // the head of the user's FIFO of first calls
+        rec = rdl(hrec, x);
+        sc = rdl(hsucc, x);
+        lo = rdlu(hlo, x);
+        hi = rdlu(hhi, x);
+      }
+      const bool sc_now = sc >= 0 && sc < nxt;  // its next call already arrived
+      if (sc_now && !tier0 && pocc == ~uint64_t(0)) {
+        overflow = mid = true;  // nothing of this admission has happened yet
+        mid_budget = budget;
+        break;
+      }
+      const int32_t tok = int32_t(lo & uint32_t(kTokMask));
+      const int64_t unew = uk + int64_t(((uint64_t(hi) << 32) | lo) >> 24);
+      if (unew >= kValueLimit) {
+        code = FS_E_OVERFLOW;
+        break;
+      }
+      budget -= tok;
+      backlog -= tok;
+      d_rec = lane == nd ? rec : d_rec;
+      d_step = lane == nd ? s : d_step;
+      d_cnt = lane == nd ? unew : d_cnt;
+      ++seq;
+      if (++nd == 64) flush_decisions();
+      w_flags |= (w_prev == rec) ? kPrevAdm : 0;
+      const int32_t q = rdl(xq, x) - 1;
+      if (tier0) {
+        pocc &= ~(uint64_t(1) << l);
+        if (lane == l) p_x = -1;
+        if (lane == x) --xn;
+      } else {
+        const uint64_t low_ring = __ballot(xr < xt && xr - xf - 1 < (D >> 1));
+        if ((low_ring >> x) & 1) fifo_refill(x);
+        if (lane == x) {
+          ++xf;
+          if (xf < xt) {
+            const Ent v = ring[x * D + (xf & (D - 1))];
+            hrec = v.rec;
+            hsucc = v.succ;
+            hlo = v.lo;
+            hhi = v.hi;
+          }
+        }
+      }
+      if (sc_now) {
+        int32_t s2;
+        uint32_t lo2, hi2;
+        if (sc >= cache_lo) {
+          const Ent e = cache[sc & (M - 1)];
+          s2 = uni(e.succ);
+          lo2 = uint32_t(uni(int32_t(e.lo)));
+          hi2 = uint32_t(uni(int32_t(e.hi)));
+        } else {
+          load_rec(sc, s2, lo2, hi2);
+        }
+        ready_add(x, sc, s2, lo2, hi2);
+      }
+      if (q == 0) {  // the user leaves Q
+        const int32_t k = rdl(xu, x);
+        occ &= ~(uint64_t(1) << x);
+        --nX;
+        if (lane == x) {
+          kh = kl = 0xffffffffu;
+          xu = -1;
+          xq = 0;
+        }
+        last_exit = k;
+        last_exit_u = unew;
+        put_u(k, unew);
+        c_u = (w_user == k) ? unew : c_u;
+      } else if (lane == x) {
+        --xq;
+        kh = uint32_t(uint64_t(unew) >> 32) | (xn > 0 ? 0u : kTier1);
+        kl = uint32_t(uint64_t(unew));
+      }
+    }
+    if (overflow || code) break;
+    debt = budget < 0 ? budget : 0;
+    if (nX > 0) {  // the gap sample, and the least counter for the next arrivals
+      const bool oc = xu >= 0;
+      const uint32_t uh = kh & kValHi;
+      const uint32_t mnh = wave_min32(oc ? uh : 0xffffffffu);
+      const uint32_t mxh = wave_max32(oc ? uh : 0u);
+      const uint32_t mnl = wave_min32(oc && uh == mnh ? kl : 0xffffffffu);
+      const uint32_t mxl = wave_max32(oc && uh == mxh ? kl : 0u);
+      const int64_t mn = int64_t((uint64_t(mnh) << 32) | mnl);
+      const int64_t mx = int64_t((uint64_t(mxh) << 32) | mxl);
+      gap = mx - mn > gap ? mx - mn : gap;
+      minX = mn;
+    }
+    ++s;
+  }
+
+  if (code) raise_err(a.err, code);
+  flush_window();
+  flush_decisions();
+
+  // ---- save: counters of queued users back to u; the queue itself is rebuilt from
+  // the records that have arrived and are still undecided
+  while (occ) {
+    const int32_t x = ff1(occ);
+    occ &= occ - 1;
+    put_u(rdl(xu, x), int64_t((uint64_t(rdlu(kh, x) & kValHi) << 32) | rdlu(kl, x)));
+  }
+  wave_fence();
+  __syncthreads();
+  if (ulds)
+    for (int32_t k = lane; k < U; k += 64) u_all[k] = u_lds[k];
+  // lowest record index that may still be queued
+  {
+    const int8_t *const fate = STATE(const int8_t, fate) + base;
+    while (low < nxt) {
+      const int32_t i = low + lane;
+      const bool q = i < nxt && ld_fresh(fate + i) == -1;
+      const uint64_t m = __ballot(q);
+      if (m) {
+        low += ff1(m);
+        break;
+      }
+      low += 64;
+    }
+    if (low > nxt) low = nxt;
+  }
+  const bool drained = nxt == n && nX == 0;
+  if (lane == 0) {
+    rs->s = s;
+    rs->nxt = nxt;
+    rs->debt = debt;
+    rs->backlog = backlog;
+    rs->seq = seq;
+    rs->gap = gap;
+    rs->last_exit_u = last_exit_u;
+    rs->low = low;
+    rs->last_exit = last_exit;
+    rs->done = drained ? 1 : 0;
+    rs->overflow = overflow ? 1 : 0;
+    rs->mid = mid ? 1 : 0;
+    rs->mid_budget = mid_budget;
+    rs->s_end = s_end;
+    if (!overflow) {
+      KARG(steps)[r] = s;
+      KARG(decisions)[r] = seq;
+      KARG(max_gap)[r] = gap;
+    }
+  }
+  wave_fence();
+  if (!overflow) {
+    int64_t *const counter = KARG(counter) + int64_t(r) * U;
+    for (int32_t k = lane; k < U; k += 64) counter[k] = ulds ? u_lds[k] : ld_fresh(u_all + k);
+  }
+}
+
+int max_lds_per_block() {
+  static int cached = 0;
+  if (cached == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+        v <= 0)
+      v = 65536;
+    cached = v;
+  }
+  return cached;
+}
+
+}  // namespace
+
+OnchipCfg onchip_config(int32_t R, int32_t U) {
+  // enough LDS per work-group for all replicas to be resident at once (up to four
+  // work-groups, i.e. one wave per SIMD, on each of the 256 CUs)
+  const int per_cu = R <= 256 ? 1 : R <= 512 ? 2 : R <= 768 ? 3 : 4;
+  size_t budget = size_t(160 * 1024) / per_cu - 1024;
+  const size_t dev_max = size_t(max_lds_per_block());
+  if (budget > dev_max) budget = dev_max;
+  OnchipCfg c;
+  c.pad = 0;
+  c.users_lds = size_t(U) * 8 <= budget / 4 ? 1 : 0;
+  const size_t users = c.users_lds ? size_t(U) * 8 : 0;
+  size_t left = budget - users;
+  // about half for the rings, the rest for the arrival cache
+  int ring = 64;
+  while (ring > 8 && size_t(kSlots) * ring * sizeof(Ent) > left / 2) ring >>= 1;
+  left -= size_t(kSlots) * ring * sizeof(Ent);
+  int cache = 4096;
+  while (cache > 64 && size_t(cache) * sizeof(Ent) > left) cache >>= 1;
+  c.ring = ring;
+  c.cache = cache;
+  c.lds_bytes = size_t(kSlots) * ring * sizeof(Ent) + size_t(cache) * sizeof(Ent) + users;
+  return c;
+}
+
+void launch_onchip(const SchedArgs &a, hipStream_t s) {
+  if (a.oc.lds_bytes > 65536)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&k_schedule_onchip),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, int(a.oc.lds_bytes));
+  hipLaunchKernelGGL(k_schedule_onchip, dim3(a.t.R), dim3(64), a.oc.lds_bytes, s, a);
+}
+
+}  // namespace sched
+}  // namespace fs

@@ -184,34 +184,41 @@ __device__ inline void wave_minmax(uint64_t &lo, uint64_t &hi) {
   minmax_step<0x143, 0xC>(lo, hi);
 }
 
-// 32-bit wave minimum / maximum (result in lane 63).
-template <int CTRL, int ROWS>
-__device__ inline void min32_step(uint32_t &v) {
-  const uint32_t o = dpp<CTRL, ROWS>(v);
-  v = o < v ? o : v;
-}
-template <int CTRL, int ROWS>
-__device__ inline void max32_step(uint32_t &v) {
-  const uint32_t o = dpp<CTRL, ROWS>(v);
-  v = o > v ? o : v;
+// 32-bit wave minimum / maximum, returned in a scalar register.  Four DPP steps
+// leave each 16-lane row's extreme in every lane of the row (with the identity as
+// the DPP "old" value the compiler fuses each move into the min/max instruction),
+// then the four rows' values are read and combined on the scalar unit.
+template <int CTRL>
+__device__ inline uint32_t dpp_id(uint32_t id, uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(int(id), int(v), CTRL, 0xF, 0xF, false));
 }
 __device__ inline uint32_t wave_min32(uint32_t v) {
-  min32_step<0xB1, 0xF>(v);
-  min32_step<0x4E, 0xF>(v);
-  min32_step<0x141, 0xF>(v);
-  min32_step<0x140, 0xF>(v);
-  min32_step<0x142, 0xA>(v);
-  min32_step<0x143, 0xC>(v);
-  return rdlu(v, 63);
+  uint32_t o;
+  o = dpp_id<0xB1>(~0u, v);
+  v = o < v ? o : v;
+  o = dpp_id<0x4E>(~0u, v);
+  v = o < v ? o : v;
+  o = dpp_id<0x141>(~0u, v);
+  v = o < v ? o : v;
+  o = dpp_id<0x140>(~0u, v);
+  v = o < v ? o : v;
+  const uint32_t a = rdlu(v, 15), b = rdlu(v, 31), c = rdlu(v, 47), d = rdlu(v, 63);
+  const uint32_t ab = a < b ? a : b, cd = c < d ? c : d;
+  return ab < cd ? ab : cd;
 }
 __device__ inline uint32_t wave_max32(uint32_t v) {
-  max32_step<0xB1, 0xF>(v);
-  max32_step<0x4E, 0xF>(v);
-  max32_step<0x141, 0xF>(v);
-  max32_step<0x140, 0xF>(v);
-  max32_step<0x142, 0xA>(v);
-  max32_step<0x143, 0xC>(v);
-  return rdlu(v, 63);
+  uint32_t o;
+  o = dpp_id<0xB1>(0u, v);
+  v = o > v ? o : v;
+  o = dpp_id<0x4E>(0u, v);
+  v = o > v ? o : v;
+  o = dpp_id<0x141>(0u, v);
+  v = o > v ? o : v;
+  o = dpp_id<0x140>(0u, v);
+  v = o > v ? o : v;
+  const uint32_t a = rdlu(v, 15), b = rdlu(v, 31), c = rdlu(v, 47), d = rdlu(v, 63);
+  const uint32_t ab = a > b ? a : b, cd = c > d ? c : d;
+  return ab > cd ? ab : cd;
 }
 
 __device__ inline bool state_header_ok(const SchedArgs &a) {

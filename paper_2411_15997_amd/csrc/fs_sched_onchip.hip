@@ -10,7 +10,9 @@
 //             later call of an incomplete interaction), the number of queued calls,
 //             the ordinals of its FIFO of first calls (head, on-chip end, tail), the
 //             head request's data, and its number of ready later calls.  The argmin
-//             over (key, user id) is two 32-bit DPP minimums.  A slot's state changes
+//             over (key, user id) is one 32-bit DPP minimum over tier << 31 | (u - B),
+//             B being the least counter at the last step end, while every u - B fits
+//             31 bits (two minimums over the full key otherwise).  A slot's state changes
 //             in its own lane, under an exec mask, so an update costs no cross-lane
 //             traffic.
 //   ready     one ready later call (previous call admitted) per lane: owning slot,
@@ -41,6 +43,8 @@ constexpr uint64_t kTokMask = (uint64_t(1) << 24) - 1;
 constexpr int kSlots = 64;
 constexpr uint32_t kTier1 = 0x40000000u;  // the tier bit in a key's high word
 constexpr uint32_t kValHi = 0x3fffffffu;  // the counter's bits in a key's high word
+constexpr uint32_t kRelTier1 = 0x80000000u;  // the tier bit of a relative key
+constexpr uint32_t kRelMax = 0x7fffffffu;    // largest relative counter (saturated)
 
 // window flags
 constexpr int32_t kFirst = 1;        // first call of its interaction
@@ -130,6 +134,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
 
   // ---- slots: one backlogged user per lane
   uint32_t kh = 0xffffffffu, kl = 0xffffffffu;  // key (tier << 62 | counter); free = all ones
+  uint32_t k32 = 0xffffffffu;                   // tier << 31 | (counter - B), saturated
   int32_t xu = -1;                              // user id, -1 = free
   int32_t xq = 0;                               // queued calls (first and later)
   int32_t xf = 0, xr = 0, xt = 0;               // FIFO ordinals: head, on-chip end, tail
@@ -145,9 +150,30 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   uint64_t pocc = 0;
 
   int64_t minX = 0;
+  int64_t B = 0;      // base of the relative keys
+  bool wide = false;  // some counter is 2^31 - 1 or more above B: compare full keys
   int32_t code = 0;
   bool overflow = false, mid = false;
   int64_t mid_budget = 0;
+
+  auto rel_of = [&](int64_t u) -> uint32_t {
+    const int64_t d = u - B;
+    if (d < 0 || d >= int64_t(kRelMax)) {
+      wide = true;
+      return kRelMax;
+    }
+    return uint32_t(d);
+  };
+  // Relative keys recomputed from the full keys with base b.
+  auto rebase_full = [&](int64_t b) {
+    B = b;
+    const bool oc = xu >= 0;
+    const int64_t d = int64_t((uint64_t(kh & kValHi) << 32) | kl) - b;
+    const bool sat = oc && (d < 0 || d >= int64_t(kRelMax));
+    const uint32_t rv = sat ? kRelMax : uint32_t(d);
+    k32 = oc ? (((kh & kTier1) << 1) | rv) : 0xffffffffu;
+    wide = __ballot(sat) != 0;
+  };
 
   // First call (rec, sc, lo, hi) joins the tail of slot x's FIFO: on chip while the
   // FIFO has no part in HBM and the ring has room, else in the user's segment.
@@ -196,14 +222,20 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     if (lane == x) {
       ++xn;
       kh &= kValHi;  // tier 0
+      k32 &= kRelMax;
     }
   };
   // Slot for user k with counter uk (tier 1, nothing queued yet).
   auto join = [&](int32_t k, int64_t uk, uint32_t sb) -> int32_t {
     const int32_t x = ff1(~occ);
     occ |= uint64_t(1) << x;
-    ++nX;
+    if (nX++ == 0) {
+      B = uk;
+      wide = false;
+    }
+    const uint32_t rv = rel_of(uk);
     if (lane == x) {
+      k32 = kRelTier1 | rv;
       kh = uint32_t(uint64_t(uk) >> 32) | kTier1;
       kl = uint32_t(uint64_t(uk));
       xu = k;
@@ -231,14 +263,17 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   int64_t d_cnt = 0;
   auto flush_decisions = [&]() {
     if (nd == 0) return;
+    int8_t *const fate = STATE(int8_t, fate);
+    int8_t *const status = KARG(status);
+    int32_t *const astep = KARG(admit_step);
+    int32_t *const as = KARG(admit_seq);
+    int64_t *const ca = KARG(counter_after);
     if (lane < nd) {
       const int64_t g = base + d_rec;
-      STATE(int8_t, fate)[g] = 0;
-      KARG(status)[g] = 0;
-      KARG(admit_step)[g] = d_step;
-      int32_t *const as = KARG(admit_seq);
+      fate[g] = 0;
+      status[g] = 0;
+      astep[g] = d_step;
       if (as) as[g] = seq - nd + lane;
-      int64_t *const ca = KARG(counter_after);
       if (ca) ca[g] = d_cnt;
     }
     nd = 0;
@@ -253,18 +288,21 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   int64_t o_coa = 0;
   auto flush_window = [&]() {
     const int32_t done = nxt - wbase;
+    int8_t *const fate = STATE(int8_t, fate);
+    int8_t *const status = KARG(status);
+    int32_t *const astep = KARG(admit_step);
+    int32_t *const as = KARG(admit_seq);
+    int64_t *const ca = KARG(counter_after);
+    int64_t *const coa = KARG(counter_on_arrival);
     if (lane < done) {
       const int64_t g = base + wbase + lane;
       if (o_st > 0) {
-        STATE(int8_t, fate)[g] = int8_t(o_st);
-        KARG(status)[g] = int8_t(o_st);
-        KARG(admit_step)[g] = -1;
-        int32_t *const as = KARG(admit_seq);
+        fate[g] = int8_t(o_st);
+        status[g] = int8_t(o_st);
+        astep[g] = -1;
         if (as) as[g] = -1;
-        int64_t *const ca = KARG(counter_after);
         if (ca) ca[g] = -1;
       }
-      int64_t *const coa = KARG(counter_on_arrival);
       if (coa) coa[g] = o_coa;
     }
     o_st = 0;
@@ -281,30 +319,38 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     w_seg = 0;
     w_lo = w_hi = 0;
     c_u = 0;
+    // the argument fields first (scalar loads, one wait), then the records
+    struct {
+      const int64_t *ts;
+      const int32_t *user, *call, *head, *prev, *len_in, *len_sys, *len_out;
+    } T = {KARG(t.ts),   KARG(t.user),   KARG(t.call),    KARG(t.head),
+           KARG(t.prev), KARG(t.len_in), KARG(t.len_sys), KARG(t.len_out)};
+    const int64_t *const costp = KARG(cost);
+    const uint8_t *const reason = KARG(reason);
+    const int64_t tau = KARG(tau);
+    char *const st = KARG(state);
+    const size_t o_succ = KARG(L.succ), o_seg = KARG(L.seg_start), o_fate = KARG(L.fate);
     if (i < n) {
       const int64_t g = base + i;
-      const int32_t *const callp = KARG(t.call);
-      const int32_t call = callp ? callp[g] : 0;
-      const int32_t usr = KARG(t.user)[g];
-      const int64_t ts = KARG(t.ts)[g];
-      const int32_t hd = callp ? KARG(t.head)[g] : i;
-      const int32_t pv = callp ? KARG(t.prev)[g] : -1;
-      const int32_t *len_sys = KARG(t.len_sys);
-      const int32_t tok = KARG(t.len_in)[g] + KARG(t.len_out)[g] + (len_sys ? len_sys[g] : 0);
-      const int64_t cst = KARG(cost)[g];
-      const uint8_t *const reason = KARG(reason);
+      const int32_t call = T.call ? T.call[g] : 0;
+      const int32_t usr = T.user[g];
+      const int64_t ts = T.ts[g];
+      const int32_t hd = T.call ? T.head[g] : i;
+      const int32_t pv = T.call ? T.prev[g] : -1;
+      const int32_t tok = T.len_in[g] + T.len_out[g] + (T.len_sys ? T.len_sys[g] : 0);
+      const int64_t cst = costp[g];
       const int32_t why = reason ? reason[g] : 0;
-      const int32_t sc = STATE(const int32_t, succ)[g];
-      const uint32_t sb = STATE(const uint32_t, seg_start)[int64_t(r) * U + usr];
+      const int32_t sc = reinterpret_cast<const int32_t *>(st + o_succ)[g];
+      const uint32_t sb = reinterpret_cast<const uint32_t *>(st + o_seg)[int64_t(r) * U + usr];
       const int64_t uu = ulds ? u_lds[usr] : ld_fresh(u_all + usr);
       int32_t fl = call == 0 ? kFirst : 0;
       if (call > 0) {
-        const int8_t *const fate = STATE(const int8_t, fate) + base;
+        const int8_t *const fate = reinterpret_cast<const int8_t *>(st + o_fate) + base;
         const int8_t pf = ld_fresh(fate + pv), hf = ld_fresh(fate + hd);
         fl |= (pf == 0 ? kPrevAdm : 0) | ((hf == 1 || hf == 2) ? kHeadBlk : 0);
       }
       fl |= (why << kReasonShift) | (cst >= kPackLimit ? kBig : 0);
-      const int64_t stp = ts / KARG(tau);
+      const int64_t stp = ts / tau;
       w_step = stp < INT32_MAX ? int32_t(stp) : INT32_MAX;
       w_user = usr;
       w_flags = fl;
@@ -382,6 +428,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const uint32_t mh = wave_min32(oc ? uh : 0xffffffffu);
     const uint32_t ml = wave_min32(oc && uh == mh ? kl : 0xffffffffu);
     minX = int64_t((uint64_t(mh) << 32) | ml);
+    rebase_full(minX);
   }
   if (nxt < n) load_window();
 
@@ -467,9 +514,20 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     int64_t budget = C + debt;
     while (budget > 0 && nX > 0) {
       // least (key, user id): the ready tier first, then the least counter
-      const uint32_t mh = wave_min32(kh);
-      const uint32_t ml = wave_min32(kh == mh ? kl : 0xffffffffu);
-      const bool cand = kh == mh && kl == ml;
+      bool cand, tier0;
+      int64_t uk;
+      if (!wide) {
+        const uint32_t m = wave_min32(k32);
+        cand = k32 == m;
+        tier0 = m < kRelTier1;
+        uk = B + int64_t(m & kRelMax);
+      } else {
+        const uint32_t mh = wave_min32(kh);
+        const uint32_t ml = wave_min32(kh == mh ? kl : 0xffffffffu);
+        cand = kh == mh && kl == ml;
+        tier0 = mh < kTier1;
+        uk = int64_t((uint64_t(mh & kValHi) << 32) | ml);
+      }
       const uint64_t eq = __ballot(cand);
       int32_t x;
       if (eq & (eq - 1)) {
@@ -478,8 +536,6 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       } else {
         x = ff1(eq);
       }
-      const bool tier0 = mh < kTier1;
-      const int64_t uk = int64_t((uint64_t(mh & kValHi) << 32) | ml);
       int32_t rec, sc, l = -1;
       uint32_t lo, hi;
       if (tier0) {  // the user's earliest ready later call
@@ -556,7 +612,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         occ &= ~(uint64_t(1) << x);
         --nX;
         if (lane == x) {
-          kh = kl = 0xffffffffu;
+          kh = kl = k32 = 0xffffffffu;
           xu = -1;
           xq = 0;
         }
@@ -564,25 +620,40 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         last_exit_u = unew;
         put_u(k, unew);
         c_u = (w_user == k) ? unew : c_u;
-      } else if (lane == x) {
-        --xq;
-        kh = uint32_t(uint64_t(unew) >> 32) | (xn > 0 ? 0u : kTier1);
-        kl = uint32_t(uint64_t(unew));
+      } else {
+        const uint32_t rv = rel_of(unew);
+        if (lane == x) {
+          --xq;
+          kh = uint32_t(uint64_t(unew) >> 32) | (xn > 0 ? 0u : kTier1);
+          kl = uint32_t(uint64_t(unew));
+          k32 = (xn > 0 ? 0u : kRelTier1) | rv;
+        }
       }
     }
     if (overflow || code) break;
     debt = budget < 0 ? budget : 0;
     if (nX > 0) {  // the gap sample, and the least counter for the next arrivals
       const bool oc = xu >= 0;
-      const uint32_t uh = kh & kValHi;
-      const uint32_t mnh = wave_min32(oc ? uh : 0xffffffffu);
-      const uint32_t mxh = wave_max32(oc ? uh : 0u);
-      const uint32_t mnl = wave_min32(oc && uh == mnh ? kl : 0xffffffffu);
-      const uint32_t mxl = wave_max32(oc && uh == mxh ? kl : 0u);
-      const int64_t mn = int64_t((uint64_t(mnh) << 32) | mnl);
-      const int64_t mx = int64_t((uint64_t(mxh) << 32) | mxl);
-      gap = mx - mn > gap ? mx - mn : gap;
-      minX = mn;
+      if (!wide) {
+        const uint32_t rv = k32 & kRelMax;
+        const uint32_t mnr = wave_min32(oc ? rv : kRelMax);
+        const uint32_t mxr = wave_max32(oc ? rv : 0u);
+        gap = int64_t(mxr - mnr) > gap ? int64_t(mxr - mnr) : gap;
+        minX = B + mnr;
+        B = minX;  // rebase: the relative keys only shrink
+        if (oc) k32 -= mnr;
+      } else {
+        const uint32_t uh = kh & kValHi;
+        const uint32_t mnh = wave_min32(oc ? uh : 0xffffffffu);
+        const uint32_t mxh = wave_max32(oc ? uh : 0u);
+        const uint32_t mnl = wave_min32(oc && uh == mnh ? kl : 0xffffffffu);
+        const uint32_t mxl = wave_max32(oc && uh == mxh ? kl : 0u);
+        const int64_t mn = int64_t((uint64_t(mnh) << 32) | mnl);
+        const int64_t mx = int64_t((uint64_t(mxh) << 32) | mxl);
+        gap = mx - mn > gap ? mx - mn : gap;
+        minX = mn;
+        rebase_full(mn);
+      }
     }
     ++s;
   }

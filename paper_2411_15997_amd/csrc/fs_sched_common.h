@@ -221,6 +221,31 @@ __device__ inline uint32_t wave_max32(uint32_t v) {
   return ab > cd ? ab : cd;
 }
 
+// Wave sum of 32-bit values, returned in a scalar register.
+__device__ inline uint32_t wave_sum32(uint32_t v) {
+  v += dpp_id<0xB1>(0u, v);
+  v += dpp_id<0x4E>(0u, v);
+  v += dpp_id<0x141>(0u, v);
+  v += dpp_id<0x140>(0u, v);
+  return rdlu(v, 15) + rdlu(v, 31) + rdlu(v, 47) + rdlu(v, 63);
+}
+
+// Inclusive prefix sum over the wave (lane order): shifts of 1, 2, 4 and 8 within
+// each 16-lane row, then each row's total is carried into the rows after it.
+template <int CTRL, int ROWS>
+__device__ inline uint32_t dpp0(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, ROWS, 0xF, false));
+}
+__device__ inline uint32_t wave_incl_scan32(uint32_t v) {
+  v += dpp0<0x111, 0xF>(v);
+  v += dpp0<0x112, 0xF>(v);
+  v += dpp0<0x114, 0xF>(v);
+  v += dpp0<0x118, 0xF>(v);
+  v += dpp0<0x142, 0xA>(v);
+  v += dpp0<0x143, 0xC>(v);
+  return v;
+}
+
 __device__ inline bool state_header_ok(const SchedArgs &a) {
   const Header *h = reinterpret_cast<const Header *>(a.state + a.L.hdr);
   return h->magic == kMagic && h->version == kVersion && h->R == a.t.R && h->U == a.t.U &&

@@ -377,6 +377,109 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     load_window();
   };
 
+  // First calls of window lanes f (in lane order) join the tail of slot x's FIFO.
+  auto fifo_push_many = [&](int32_t x, uint64_t f) {
+    const int32_t fh = rdl(xf, x), rr = rdl(xr, x), tt = rdl(xt, x);
+    const int32_t cnt = __popcll(f);
+    int32_t ring_n = 0;
+    if (tt == rr) {
+      ring_n = fh + D - rr;
+      if (ring_n > cnt) ring_n = cnt;
+    }
+    if ((f >> lane) & 1) {
+      const int32_t rank = __popcll(f & ((uint64_t(1) << lane) - 1));
+      const int32_t ord = tt + rank;
+      const Ent e = mk_ent(wbase + lane, w_succ, w_lo, w_hi);
+      if (rank < ring_n)
+        ring[x * D + (ord & (D - 1))] = e;
+      else
+        STATE(Ent, seg_pk)[int64_t(rdlu(xsb, x)) + ord] = e;
+    }
+    if (tt == fh) {  // the FIFO was empty: its first entry is the new head
+      const int l0 = ff1(f);
+      const int32_t sc = rdl(w_succ, l0);
+      const uint32_t lo = rdlu(w_lo, l0), hi = rdlu(w_hi, l0);
+      if (lane == x) {
+        hrec = wbase + l0;
+        hsucc = sc;
+        hlo = lo;
+        hhi = hi;
+      }
+    }
+    if (lane == x) {
+      xr += ring_n;
+      xt += cnt;
+    }
+  };
+
+  // All arrivals of the current step in window lanes [j0, j1) at once (X not empty,
+  // so a user outside X is lifted to the least counter in X).  The overload test of
+  // each arrival needs the tokens queued before it: as the queue only grows during
+  // the arrivals, the first arrival that finds it above the threshold is found from
+  // a prefix sum taken as if none were throttled, and every later arrival of the
+  // step finds it above too.  Returns false, having changed nothing, when an
+  // on-chip capacity might not suffice (the arrivals then go one at a time).
+  auto arrive_batch = [&](int32_t j0, int32_t j1) -> bool {
+    const bool inb = lane >= j0 && lane < j1;
+    const bool first = (w_flags & kFirst) != 0;
+    const int32_t why = (w_flags >> kReasonShift) & 3;
+    const uint32_t tok = w_lo & uint32_t(kTokMask);
+    const uint32_t c0 = (inb && (first || !(w_flags & kHeadBlk))) ? tok : 0u;
+    const uint32_t excl = wave_incl_scan32(c0) - c0;
+    const int64_t thr = theta - backlog;  // overloaded at a lane iff excl > thr
+    const bool ovl = thr < 0 ? true : (thr >= int64_t(INT32_MAX) ? false : excl > uint32_t(thr));
+    const bool bf = inb && first && ovl && why != 0;
+    // a later call shares its first call's fate: throttled before the batch or in it
+    const int32_t hl = w_head - wbase;
+    const bool hl_in = hl >= j0 && hl < j1;
+    const int hb_src = __builtin_amdgcn_ds_bpermute((hl_in ? hl : lane) << 2, bf ? 1 : 0);
+    const bool hb_new = !first && w_head >= 0 && hl_in && hb_src != 0;
+    const bool bl = inb && !first && ((w_flags & kHeadBlk) || hb_new);
+    const bool blk = bf || bl;
+    const uint64_t ub = __ballot(inb && !blk);
+    const uint64_t rdym = __ballot(inb && !blk && !first && (w_flags & kPrevAdm));
+    if (__ballot(inb && !blk && (w_flags & kBig)) || __popcll(ub) > kSlots - nX ||
+        __popcll(rdym) > kSlots - __popcll(pocc))
+      return false;
+    w_flags |= hb_new ? kHeadBlk : 0;
+    o_st = inb ? (bf ? why : (bl ? 3 : 0)) : o_st;
+    backlog += int64_t(wave_sum32(inb && !blk ? tok : 0u));
+    const uint64_t firstm = __ballot(first);
+    uint64_t todo = __ballot(inb);
+    while (todo) {  // one user of the batch at a time
+      const int32_t jj = ff1(todo);
+      const int32_t k = rdl(w_user, jj);
+      const uint64_t same = __ballot(w_user == k) & todo;
+      todo &= ~same;
+      const uint64_t fm = __ballot(xu == k);
+      int32_t x = ff1(fm);
+      int64_t uk;
+      if (fm) {
+        uk = int64_t((uint64_t(rdlu(kh, x) & kValHi) << 32) | rdlu(kl, x));
+      } else {  // counter lift
+        const int64_t cu = rdl64(c_u, jj);
+        uk = cu > minX ? cu : minX;
+        if (uk != cu) {
+          put_u(k, uk);
+          c_u = (w_user == k) ? uk : c_u;
+        }
+      }
+      o_coa = ((same >> lane) & 1) ? uk : o_coa;
+      const uint64_t mine = same & ub;
+      if (!mine) continue;
+      if (!fm) x = join(k, uk, rdlu(w_seg, jj));
+      if (lane == x) xq += __popcll(mine);
+      if (mine & firstm) fifo_push_many(x, mine & firstm);
+      uint64_t rm = mine & rdym;
+      while (rm) {
+        const int l = ff1(rm);
+        rm &= rm - 1;
+        ready_add(x, wbase + l, rdl(w_succ, l), rdlu(w_lo, l), rdlu(w_hi, l));
+      }
+    }
+    return true;
+  };
+
   // ---- rebuild the queue left by a previous call: arrived records still undecided
   for (int32_t b0 = low; b0 < nxt && !overflow; b0 += 64) {
     const int8_t *const fate = STATE(const int8_t, fate) + base;
@@ -458,6 +561,14 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (nxt - wbase == 64) advance_window();
       const int j = nxt - wbase;
       if (rdl(w_step, j) > s) break;
+      if (nX > 0) {  // the step's arrivals in this window, together
+        const uint64_t after = __ballot(w_step > s) & (~uint64_t(0) << j);
+        const int32_t j1 = after ? ff1(after) : 64;
+        if (j1 - j > 1 && arrive_batch(j, j1)) {
+          nxt = wbase + j1;
+          continue;
+        }
+      }
       const int32_t rec = nxt;
       const int32_t k = rdl(w_user, j);
       const int32_t fl = rdl(w_flags, j);

@@ -26,18 +26,44 @@ HBM_PEAK_GBS = 8000.0
 #   scheduler ts 8 + user 4 + link 4 + tokens 4 + cost 8 + reason 1/8 + status 1
 #             + admit_step 4 + admit_seq 4                                      = 37.125
 #   metrics   status 1 + admit_step 4 + ts 8 + user 4 + cost 8                  = 25
-ALGO_BYTES = {"cost": 20.0, "throttle": 20.125, "schedule": 37.125, "metrics": 25.0}
-SCHED_SRC = os.path.join(ROOT, "paper_2411_15997_amd", "csrc", "fs_sched.hip")
+ALGO_BYTES = {"cost": 20.0, "throttle": 20.125, "init": 0.0, "schedule": 37.125, "metrics": 25.0}
+CSRC = os.path.join(ROOT, "paper_2411_15997_amd", "csrc")
+STAGE_SRC = {
+    "cost": ["fs_cost.hip"],
+    "throttle": ["fs_throttle.hip"],
+    "schedule": ["fs_sched_onchip.hip", "fs_sched.hip", "fs_sched_common.h"],
+    "metrics": ["fs_metrics.hip"],
+}
 
-# HBM traffic of the dominant kernel measured with rocprofv3 --pmc (FETCH_SIZE and
-# WRITE_SIZE), scaled by the copy-kernel calibration; keyed by workload and the
-# sha256 of the kernel source it was measured on (stale entries are ignored).
-MEASURED_TRAFFIC = {}
+# HBM traffic of a stage's main kernel from rocprofv3 --pmc runs: FETCH_SIZE and
+# WRITE_SIZE (KiB per dispatch), each scaled by bytes / counter of a plain 1 GiB
+# device copy measured in the same run (bench.py --calib-copy).  Keyed by workload
+# and stage; an entry counts only while the stage's sources hash to `src`.
+MEASURED_TRAFFIC = {
+    # k_schedule_onchip on the 64 x 256 x 8 replica workload (6.4M requests)
+    ("c2_replicas", "schedule"): {"src": "531c040bd6da0cf2", "fetch_kib": 147728.5,
+                                  "write_kib": 38757.5625, "fetch_factor": 1.99994,
+                                  "write_factor": 1.0},
+    # every kernel of one fs_throttle call on the 50M-request throttle stream
+    ("c3_throttle", "throttle"): {"src": "001a7871ea775a09", "fetch_kib": 2874819.375,
+                                  "write_kib": 2088836.8125, "fetch_factor": 1.99989,
+                                  "write_factor": 1.0},
+}
 
 
-def src_hash(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def src_hash(stage):
+    h = hashlib.sha256()
+    for name in STAGE_SRC.get(stage, []):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, stage):
+    m = MEASURED_TRAFFIC.get((workload, stage))
+    if not m or m["src"] != src_hash(stage):
+        return None
+    return int(m["fetch_kib"] * 1024 * m["fetch_factor"] + m["write_kib"] * 1024 * m["write_factor"])
 
 
 def main():
@@ -49,6 +75,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--stage-only", default="", help="time only this stage (profiling runs)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="copy 1 GiB on the device first (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the policy's replicas are independent and this "
@@ -84,7 +112,13 @@ def main():
         mws = torch.empty(max(fs.fs_metrics_workspace(dt), 1), dtype=torch.uint8, device=dev)
         metrics = fs.Metrics(dt)
 
-    stages = ["throttle"] if throttle_only else ["cost", "throttle", "schedule", "metrics"]
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    stages = ["throttle"] if throttle_only else ["cost", "throttle", "init", "schedule", "metrics"]
     if args.stage_only:
         stages = [args.stage_only]
 
@@ -97,9 +131,11 @@ def main():
             evs[i].record(); i += 1
             fs.fs_throttle(dt, lim, raw=not throttle_only, ws=tws, err=err, check=False,
                            bitmap=bitmap, reason=reason_buf)
-        if "schedule" in stages:
+        if "init" in stages:
             evs[i].record(); i += 1
             fs.fs_state_init(dt, state)
+        if "schedule" in stages:
+            evs[i].record(); i += 1
             fs.fs_schedule_step(dt, state, cost, reason_buf, eng, out, -1, check=False)
         if "metrics" in stages:
             evs[i].record(); i += 1
@@ -109,6 +145,8 @@ def main():
     # the throttle's raw reasons feed the scheduler (same buffers every step)
     bitmap = torch.empty((N + 31) // 32 + 1, dtype=torch.int32, device=dev)
     reason_buf = None if throttle_only else torch.empty(max(N, 1), dtype=torch.uint8, device=dev)
+    if args.stage_only == "schedule":
+        stages = ["init", "schedule"]
     if args.stage_only in ("schedule", "metrics"):
         fs.fs_cost(dt, w, cost, err)
         fs.fs_throttle(dt, lim, raw=True, ws=tws, err=err, bitmap=bitmap, reason=reason_buf)
@@ -165,13 +203,14 @@ def main():
     dom = max(stage_ms, key=stage_ms.get)
     algo = ALGO_BYTES[dom] * N
     achieved = algo / (stage_ms[dom] / 1000.0) / 1e9
-    tkey = (wl.name, dom, src_hash(SCHED_SRC) if dom == "schedule" else None)
-    traffic = MEASURED_TRAFFIC.get(tkey)
+    traffic = measured_traffic(wl.name, dom)
     result["roofline"] = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2),
                           "peak": HBM_PEAK_GBS, "unit": "GB/s",
                           "frac": round(achieved / HBM_PEAK_GBS, 6),
-                          "algorithmic_bytes": int(algo), "traffic": traffic}
-    all_stage_gbs = {s: round(ALGO_BYTES[s] * N / (stage_ms[s] / 1000.0) / 1e9, 2) for s in stage_ms}
+                          "algorithmic_bytes": int(algo), "traffic": traffic,
+                          "src": src_hash(dom)}
+    all_stage_gbs = {s: round(ALGO_BYTES[s] * N / (stage_ms[s] / 1000.0) / 1e9, 2)
+                     for s in stage_ms if ALGO_BYTES[s] > 0}
     result["stage_gbs"] = all_stage_gbs
 
     if not args.no_cpu_baseline and not args.stage_only:

@@ -184,42 +184,39 @@ __device__ inline void wave_minmax(uint64_t &lo, uint64_t &hi) {
   minmax_step<0x143, 0xC>(lo, hi);
 }
 
-// 32-bit wave minimum / maximum, returned in a scalar register.  Four DPP steps
-// leave each 16-lane row's extreme in every lane of the row (with the identity as
-// the DPP "old" value the compiler fuses each move into the min/max instruction),
-// then the four rows' values are read and combined on the scalar unit.
+// 32-bit wave minimum / maximum, left in every lane.  Four DPP steps leave each
+// 16-lane row's extreme in every lane of the row (with the identity as the DPP "old"
+// value the compiler fuses each move into the min/max instruction); swapping halves
+// and then rows (gfx950 permlane swaps) combines the four rows.
 template <int CTRL>
 __device__ inline uint32_t dpp_id(uint32_t id, uint32_t v) {
   return uint32_t(__builtin_amdgcn_update_dpp(int(id), int(v), CTRL, 0xF, 0xF, false));
 }
-__device__ inline uint32_t wave_min32(uint32_t v) {
-  uint32_t o;
-  o = dpp_id<0xB1>(~0u, v);
-  v = o < v ? o : v;
-  o = dpp_id<0x4E>(~0u, v);
-  v = o < v ? o : v;
-  o = dpp_id<0x141>(~0u, v);
-  v = o < v ? o : v;
-  o = dpp_id<0x140>(~0u, v);
-  v = o < v ? o : v;
-  const uint32_t a = rdlu(v, 15), b = rdlu(v, 31), c = rdlu(v, 47), d = rdlu(v, 63);
-  const uint32_t ab = a < b ? a : b, cd = c < d ? c : d;
-  return ab < cd ? ab : cd;
+__device__ inline uint32_t vmin(uint32_t a, uint32_t b) { return a < b ? a : b; }
+__device__ inline uint32_t vmax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+__device__ inline uint32_t wave_min32v(uint32_t v) {
+  v = vmin(v, dpp_id<0xB1>(~0u, v));
+  v = vmin(v, dpp_id<0x4E>(~0u, v));
+  v = vmin(v, dpp_id<0x141>(~0u, v));
+  v = vmin(v, dpp_id<0x140>(~0u, v));
+  const auto h = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  v = vmin(h[0], h[1]);
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return vmin(r[0], r[1]);
 }
-__device__ inline uint32_t wave_max32(uint32_t v) {
-  uint32_t o;
-  o = dpp_id<0xB1>(0u, v);
-  v = o > v ? o : v;
-  o = dpp_id<0x4E>(0u, v);
-  v = o > v ? o : v;
-  o = dpp_id<0x141>(0u, v);
-  v = o > v ? o : v;
-  o = dpp_id<0x140>(0u, v);
-  v = o > v ? o : v;
-  const uint32_t a = rdlu(v, 15), b = rdlu(v, 31), c = rdlu(v, 47), d = rdlu(v, 63);
-  const uint32_t ab = a > b ? a : b, cd = c > d ? c : d;
-  return ab > cd ? ab : cd;
+__device__ inline uint32_t wave_max32v(uint32_t v) {
+  v = vmax(v, dpp_id<0xB1>(0u, v));
+  v = vmax(v, dpp_id<0x4E>(0u, v));
+  v = vmax(v, dpp_id<0x141>(0u, v));
+  v = vmax(v, dpp_id<0x140>(0u, v));
+  const auto h = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  v = vmax(h[0], h[1]);
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return vmax(r[0], r[1]);
 }
+// The same, returned in a scalar register.
+__device__ inline uint32_t wave_min32(uint32_t v) { return uint32_t(uni(int32_t(wave_min32v(v)))); }
+__device__ inline uint32_t wave_max32(uint32_t v) { return uint32_t(uni(int32_t(wave_max32v(v)))); }
 
 // Wave sum of 32-bit values, returned in a scalar register.
 __device__ inline uint32_t wave_sum32(uint32_t v) {

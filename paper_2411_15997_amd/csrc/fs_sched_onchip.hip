@@ -194,10 +194,10 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       ++xt;
     }
   };
-  // Slot x's FIFO runs low on chip while its segment holds more: one coalesced
-  // load moves up to a ring's worth back.
+  // Slot x's FIFO has nothing left on chip while its segment holds more: one
+  // coalesced load moves up to a ring's worth back.
   auto fifo_refill = [&](int32_t x) {
-    const int32_t f1 = rdl(xf, x) + 1, rr = rdl(xr, x), tt = rdl(xt, x);
+    const int32_t f1 = rdl(xf, x), rr = rdl(xr, x), tt = rdl(xt, x);
     int32_t m = D - (rr - f1);
     if (m > tt - rr) m = tt - rr;
     wave_fence();
@@ -286,6 +286,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   int64_t c_u = 0;
   int32_t o_st = 0;
   int64_t o_coa = 0;
+  bool w_wait = false;  // the window holds later calls whose previous call is not admitted
   auto flush_window = [&]() {
     const int32_t done = nxt - wbase;
     int8_t *const fate = STATE(int8_t, fate);
@@ -369,6 +370,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
                      "v"(w_succ), "v"(w_seg), "v"(w_lo), "v"(w_hi), "v"(c_u));
     const int32_t lo_ = wbase + 64 - M;
     cache_lo = lo_ > cache_from ? lo_ : cache_from;
+    w_wait = __ballot(w_user >= 0 && !(w_flags & (kFirst | kPrevAdm))) != 0;
   };
   auto advance_window = [&]() {
     flush_window();
@@ -628,8 +630,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       bool cand, tier0;
       int64_t uk;
       if (!wide) {
-        const uint32_t m = wave_min32(k32);
-        cand = k32 == m;
+        const uint32_t mv = wave_min32v(k32);
+        cand = k32 == mv;
+        const uint32_t m = uint32_t(uni(int32_t(mv)));
         tier0 = m < kRelTier1;
         uk = B + int64_t(m & kRelMax);
       } else {
@@ -642,7 +645,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       const uint64_t eq = __ballot(cand);
       int32_t x;
       if (eq & (eq - 1)) {
-        const uint32_t um = wave_min32(cand ? uint32_t(xu) : 0xffffffffu);
+        const uint32_t um = wave_min32v(cand ? uint32_t(xu) : 0xffffffffu);
         x = ff1(__ballot(cand && uint32_t(xu) == um));
       } else {
         x = ff1(eq);
@@ -653,7 +656,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         const uint64_t pm = __ballot(p_x == x);
         l = ff1(pm);
         if (pm & (pm - 1)) {
-          const uint32_t e = wave_min32(p_x == x ? uint32_t(p_rec) : 0xffffffffu);
+          const uint32_t e = wave_min32v(p_x == x ? uint32_t(p_rec) : 0xffffffffu);
           l = ff1(__ballot(p_x == x && uint32_t(p_rec) == e));
         }
         rec = rdl(p_rec, l);
@@ -685,24 +688,22 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       d_cnt = lane == nd ? unew : d_cnt;
       ++seq;
       if (++nd == 64) flush_decisions();
-      w_flags |= (w_prev == rec) ? kPrevAdm : 0;
+      if (w_wait) w_flags |= (w_prev == rec) ? kPrevAdm : 0;
       const int32_t q = rdl(xq, x) - 1;
       if (tier0) {
         pocc &= ~(uint64_t(1) << l);
         if (lane == l) p_x = -1;
         if (lane == x) --xn;
       } else {
-        const uint64_t low_ring = __ballot(xr < xt && xr - xf - 1 < (D >> 1));
-        if ((low_ring >> x) & 1) fifo_refill(x);
-        if (lane == x) {
-          ++xf;
-          if (xf < xt) {
-            const Ent v = ring[x * D + (xf & (D - 1))];
-            hrec = v.rec;
-            hsucc = v.succ;
-            hlo = v.lo;
-            hhi = v.hi;
-          }
+        if (lane == x) ++xf;
+        // the on-chip part of the FIFO is used up and its segment holds more: refill
+        if ((__ballot(xf == xr && xr < xt) >> x) & 1) fifo_refill(x);
+        if (lane == x && xf < xt) {
+          const Ent v = ring[x * D + (xf & (D - 1))];
+          hrec = v.rec;
+          hsucc = v.succ;
+          hlo = v.lo;
+          hhi = v.hi;
         }
       }
       if (sc_now) {

@@ -40,7 +40,11 @@ class _Trace(C.Structure):
 
 
 class _Engine(C.Structure):
-    _fields_ = [("step_us", C.c_int64), ("cap_tokens", C.c_int64), ("overload_tokens", C.c_int64)]
+    _fields_ = [("step_us", C.c_int64), ("cap_tokens", C.c_int64), ("overload_tokens", C.c_int64),
+                ("flags", C.c_uint32)]
+
+
+FSO_FCFS, FSO_BLIND = 1, 2
 
 
 class _Outputs(C.Structure):
@@ -174,7 +178,7 @@ class SimResult:
 
 
 def simulate(tr, cost_arr, exceed_reason, step_us, cap_tokens, overload_tokens, max_steps=-1,
-             n_threads=1, check=False):
+             n_threads=1, check=False, flags=0):
     t = _TraceRef(tr)
     R, U, n = tr.n_replicas, tr.n_users, t.n
     cost_arr = np.ascontiguousarray(cost_arr, np.int64)
@@ -185,7 +189,7 @@ def simulate(tr, cost_arr, exceed_reason, step_us, cap_tokens, overload_tokens, 
     o = _Outputs(*(_p(getattr(res, f)) for f in ("status", "admit_step", "admit_seq",
                                                   "counter_after", "counter_on_arrival", "counter",
                                                   "steps", "decisions", "max_gap")))
-    e = _Engine(int(step_us), int(cap_tokens), int(overload_tokens))
+    e = _Engine(int(step_us), int(cap_tokens), int(overload_tokens), int(flags))
     _check(lib().fso_simulate(C.byref(t.s), _p(cost_arr), _p(er), C.byref(e), int(max_steps),
                               int(n_threads), 1 if check else 0, C.byref(o)), "fso_simulate")
     return res

@@ -156,7 +156,10 @@ struct Simulation {
     // X = users with a queued request, T0 = users with a ready later call,
     // both ordered by (counter, user id) so that begin() is the argmin.
     std::set<std::pair<int64_t, int32_t>> X, T0;
-    std::vector<uint8_t> served(n, 0), aborted(n, 0);
+    // Every queued request, by arrival (the first-come, first-served order).
+    std::set<int64_t> arrival_order;
+    const bool fcfs = (e.flags & FSO_FCFS) != 0, blind = (e.flags & FSO_BLIND) != 0;
+    std::vector<uint8_t> served(n, 0), aborted(n, 0), dropped(n, 0);
     std::vector<int64_t> next_call(n, -1);
     if (t->call)
       for (int64_t i = 0; i < n; ++i)
@@ -218,9 +221,13 @@ struct Simulation {
         if (out->counter_on_arrival) out->counter_on_arrival[G(i)] = u[k];
         bool blocked;
         int8_t code;
-        if (!is_first_call(t, G(i))) {
+        if (!is_first_call(t, G(i)) && !blind) {
           // mid-interaction: never limit-checked, dropped only if its interaction was throttled
           blocked = aborted[t->head[G(i)]] != 0;
+          code = 3;
+        } else if (!is_first_call(t, G(i)) && dropped[t->prev[G(i)]]) {
+          // interaction-blind limits: an earlier call was dropped, the interaction is abandoned
+          blocked = true;
           code = 3;
         } else {
           // OIT: limits apply only while the system is overloaded
@@ -231,10 +238,12 @@ struct Simulation {
         }
         if (blocked) {
           out->status[G(i)] = code;
+          dropped[i] = 1;
           if (is_first_call(t, G(i))) aborted[i] = 1;
         } else {
           if (queued[k].empty()) X.insert({u[k], k});
           queued[k].insert(i);
+          arrival_order.insert(i);
           backlog += tokens(t, G(i));
           if (!is_first_call(t, G(i)) && served[t->prev[G(i)]]) make_ready(i);
         }
@@ -246,7 +255,14 @@ struct Simulation {
         bool tier0 = !T0.empty();
         int32_t k;
         int64_t r;
-        if (tier0) {
+        if (fcfs) {
+          // the earliest queued request (a later call waiting for its previous call
+          // cannot be it: that call arrived earlier and is still queued)
+          r = *arrival_order.begin();
+          k = t->user[G(r)];
+          tier0 = ready[k].count(r) != 0;
+          if (check && !tier0 && !is_first_call(t, G(r))) return fail("FCFS picked a waiting call", r);
+        } else if (tier0) {
           k = T0.begin()->second;
           r = *ready[k].begin();
         } else {
@@ -260,6 +276,7 @@ struct Simulation {
           if (ready[k].empty()) T0.erase({u[k], k});
         }
         queued[k].erase(r);
+        arrival_order.erase(r);
         bool emptied = queued[k].empty();
         if (emptied) X.erase({u[k], k});
         if (check && served[r]) return fail("served twice", r);
@@ -273,7 +290,7 @@ struct Simulation {
         if (after >= kValueLimit) return FSO_E_OVERFLOW;
         set_counter(k, after);
         if (check && after < before) return fail("counter decreased", r);
-        if (check && !tier0 && !X.empty() && after - X.begin()->first > cost[G(r)])
+        if (check && !fcfs && !tier0 && !X.empty() && after - X.begin()->first > cost[G(r)])
           return fail("served user ends more than one cost above the minimum", r);
         if (out->admit_step) out->admit_step[G(r)] = int32_t(s);
         if (out->admit_seq) out->admit_seq[G(r)] = int32_t(seq);
@@ -281,7 +298,7 @@ struct Simulation {
         ++seq;
         if (emptied) last_exit = k;
         int64_t nc = next_call[r];
-        if (nc >= 0 && nc < nxt) {
+        if (nc >= 0 && nc < nxt && !dropped[nc]) {  // (interaction-blind limits may drop it)
           if (check && !queued[t->user[G(nc)]].count(nc)) return fail("next call not queued", nc);
           make_ready(nc);
         }
@@ -424,6 +441,7 @@ int fso_simulate(const fso_trace *t, const int64_t *cost, const uint8_t *exceed_
                  fso_outputs *out) {
   if (!e || !out || !out->status || !cost) return FSO_E_ARG;
   if (e->step_us <= 0 || e->cap_tokens <= 0 || e->cap_tokens > kCapLimit) return FSO_E_ARG;
+  if (e->flags & ~uint32_t(FSO_FCFS | FSO_BLIND)) return FSO_E_ARG;
   int code = validate_trace(t, kIds | kOrder | kChain | kLengths);
   if (code != FSO_OK) return code;
   int64_t N = t->rep_off[t->n_replicas];

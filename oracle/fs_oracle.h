@@ -47,7 +47,13 @@ int fso_throttle(const fso_trace *t, int64_t window_us, int32_t t_user, const in
                  const uint8_t *overloaded /* NULL => always */, int32_t raw, uint8_t *reason,
                  uint32_t *bitmap, int32_t *cnt_user, int32_t *cnt_app);
 
-typedef struct fso_engine { int64_t step_us, cap_tokens, overload_tokens; } fso_engine;
+/* flags: FSO_FCFS serves queued requests first come, first served (no service counter
+ * or interaction priority in the choice; counters are still charged); FSO_BLIND checks
+ * every call against the limits (not only first calls) and drops the rest of an
+ * interaction once one of its calls is dropped.  FSO_FCFS | FSO_BLIND with
+ * overload_tokens = -1 is the request-rate-limit (RPM) policy the paper compares with. */
+typedef struct fso_engine { int64_t step_us, cap_tokens, overload_tokens; uint32_t flags; } fso_engine;
+enum { FSO_FCFS = 1, FSO_BLIND = 2 };
 
 typedef struct fso_outputs {
   int8_t *status;             /* [N] 0 admitted, 1/2/3 blocked, -1 not processed (bounded run) */

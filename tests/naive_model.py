@@ -88,7 +88,11 @@ class Result:
     trace_of_counters: list = field(default_factory=list)  # (step, seq, {user: u}) per decision
 
 
-def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_states=False):
+FCFS, BLIND = 1, 2  # engine flags: first come first served; interaction-blind limits
+
+
+def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_states=False,
+             flags=0):
     n_all = tr.n
     res = Result([-1] * n_all, [-1] * n_all, [-1] * n_all, [-1] * n_all, [-1] * n_all,
                  [0] * (tr.n_replicas * tr.n_users), [], [], [])
@@ -100,6 +104,7 @@ def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_sta
         queued: List[int] = []          # replica-local indices, any order
         served = [False] * n
         aborted = [False] * n
+        dropped = [False] * n
         last_exit: Optional[int] = None
         debt = backlog = seq = gap = 0
         nxt = 0
@@ -132,13 +137,16 @@ def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_sta
                     else:
                         u[k] = max(u[k], min(u[x] for x in xs))
                 res.counter_on_arrival[G(i)] = u[k]
-                if not _first(tr, G(i)):
+                if not _first(tr, G(i)) and not flags & BLIND:
                     blocked, code = aborted[int(tr.head[G(i)])], 3
+                elif not _first(tr, G(i)) and dropped[int(tr.prev[G(i)])]:
+                    blocked, code = True, 3
                 else:
                     why = 0 if reason is None else int(reason[G(i)])
                     blocked, code = (backlog > theta and why != 0), why
                 if blocked:
                     res.status[G(i)] = code
+                    dropped[i] = True
                     if _first(tr, G(i)):
                         aborted[i] = True
                 else:
@@ -147,7 +155,11 @@ def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_sta
             budget = cap + debt
             while budget > 0 and queued:
                 ready = ready_calls()
-                if ready:
+                if flags & FCFS:  # the earliest queued request, whoever it belongs to
+                    rcand = min(queued)
+                    k = int(tr.user[G(rcand)])
+                    assert _first(tr, G(rcand)) or rcand in ready
+                elif ready:
                     users = sorted({int(tr.user[G(i)]) for i in ready})
                     k = min(users, key=lambda x: (u[x], x))
                     rcand = min(i for i in ready if int(tr.user[G(i)]) == k)

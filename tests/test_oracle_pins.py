@@ -195,7 +195,7 @@ def test_sliding_window_infinite_window_is_rank_limit():
 # --------------------------------------------------------------- brute force
 
 
-def _run_both(tr, step_us, C, theta, W, t_user, t_app, coef, overloaded=None):
+def _run_both(tr, step_us, C, theta, W, t_user, t_app, coef, overloaded=None, flags=0):
     c = oracle.cost(tr, coef)
     assert c.tolist() == nm.cost(tr, coef)
     th = oracle.throttle(tr, W, t_user, t_app, raw=True)
@@ -204,12 +204,17 @@ def _run_both(tr, step_us, C, theta, W, t_user, t_app, coef, overloaded=None):
     assert th.reason.tolist() == nm.throttle_raw(tr, W, t_user, t_app)
     gated = oracle.throttle(tr, W, t_user, t_app, overloaded=overloaded, raw=False)
     assert gated.reason.tolist() == nm.throttle_gated(tr, W, t_user, t_app, overloaded)
-    r = oracle.simulate(tr, c, th.reason, step_us, C, theta, check=True)
-    n = nm.simulate(tr, c, th.reason, step_us, C, theta)
+    r = oracle.simulate(tr, c, th.reason, step_us, C, theta, check=True, flags=flags)
+    n = nm.simulate(tr, c, th.reason, step_us, C, theta, flags=flags)
     for key in ("status", "admit_step", "admit_seq", "counter_after", "counter_on_arrival",
                 "counter", "steps", "decisions", "max_gap"):
         assert getattr(r, key).tolist() == getattr(n, key), key
     return r
+
+
+# the default policy, first-come first-served order, interaction-blind limits, and both
+# (with overload_tokens = -1 the latter is the request-rate-limit policy)
+POLICY_FLAGS = (0, oracle.FSO_FCFS, oracle.FSO_BLIND, oracle.FSO_FCFS | oracle.FSO_BLIND)
 
 
 def test_naive_equals_oracle_exhaustive_tiny():
@@ -235,9 +240,10 @@ def test_naive_equals_oracle_exhaustive_tiny():
                                np.zeros(n, np.int32), call, head, prev,
                                np.asarray(toks, np.int32), None, np.zeros(n, np.int32))
                     for theta in (-1, 1):
-                        # T_app = 0 makes every first call exceed; T_user = 1 flags repeats
-                        _run_both(tr, 10, 2, theta, 15, 1, [0], coef)
-                        count += 1
+                        for flags in POLICY_FLAGS:
+                            # T_app = 0 makes every first call exceed; T_user = 1 flags repeats
+                            _run_both(tr, 10, 2, theta, 15, 1, [0], coef, flags=flags)
+                            count += 1
     assert count > 100
 
 
@@ -252,7 +258,8 @@ def test_naive_equals_oracle_random(seed):
         ov = rng.integers(0, 2, size=n).astype(np.uint8)
         _run_both(tr, int(rng.integers(1, 30)), int(rng.integers(1, 12)),
                   int(rng.integers(-1, 10)), int(rng.integers(1, 60)), int(rng.integers(0, 4)),
-                  rng.integers(0, 4, size=A).tolist(), coef, overloaded=ov)
+                  rng.integers(0, 4, size=A).tolist(), coef, overloaded=ov,
+                  flags=POLICY_FLAGS[seed % len(POLICY_FLAGS)])
 
 
 def test_naive_equals_oracle_small_workload():
@@ -262,6 +269,67 @@ def test_naive_equals_oracle_small_workload():
     coef, _ = oracle.weights_for(wl, tr)
     _run_both(tr, wl.step_us, wl.cap_tokens, wl.overload_tokens, wl.window_us, wl.t_user,
               wl.t_app, coef)
+
+
+def test_fcfs_serves_in_arrival_order():
+    """First come, first served without throttling: every request is admitted and the
+    admission sequence is the stream order (closed form), whatever the counters say."""
+    rng = np.random.default_rng(31)
+    for _ in range(20):
+        tr = random_trace(rng, int(rng.integers(5, 80)), int(rng.integers(1, 6)), 2,
+                          int(rng.integers(1, 400)), multi=True)
+        c = rng.integers(0, 1000, tr.n).astype(np.int64)
+        r = oracle.simulate(tr, c, None, int(rng.integers(1, 40)), int(rng.integers(1, 10)),
+                            10 ** 9, check=True, flags=oracle.FSO_FCFS)
+        assert (r.status == 0).all()
+        assert r.admit_seq.tolist() == list(range(tr.n))
+        assert (np.diff(r.admit_step) >= 0).all()
+
+
+def _rate_limit_fates(tr, raw):
+    """Interaction-blind limits, always on: a call over a limit is dropped with its
+    reason, and every later call of an interaction with a dropped call is dropped (3)."""
+    out = np.zeros(tr.n, np.int8)
+    for g in range(tr.n):
+        if tr.call is not None and tr.call[g] > 0 and out[int(tr.prev[g])] != 0:
+            out[g] = 3
+        else:
+            out[g] = raw[g]
+    return out
+
+
+def test_rate_limit_policy_fates_closed_form():
+    rng = np.random.default_rng(32)
+    for _ in range(30):
+        tr = random_trace(rng, int(rng.integers(5, 90)), int(rng.integers(1, 5)), 2,
+                          int(rng.integers(1, 300)), multi=True)
+        W, tu, ta = int(rng.integers(1, 100)), int(rng.integers(0, 5)), [2, 3]
+        raw = oracle.throttle(tr, W, tu, ta, raw=True).reason
+        c = np.ones(tr.n, np.int64)
+        for flags in (oracle.FSO_BLIND, oracle.FSO_FCFS | oracle.FSO_BLIND):
+            r = oracle.simulate(tr, c, raw, 10, 4, -1, check=True, flags=flags)
+            assert r.status.tolist() == _rate_limit_fates(tr, raw).tolist()
+
+
+def test_rate_limit_policy_aborts_interactions_midway():
+    """An interaction whose second call goes over the user limit: interaction-blind
+    limits serve its first call and drop the second (an interaction aborted midway,
+    its served tokens wasted); the paper's policy exempts the second call."""
+    # user 0: interaction A = (call 0 at t=0, call 1 at t=10), a single request at t=1
+    tr = Trace(1, 1, 1, np.array([0, 3], np.int64), np.array([0, 1, 10], np.int64),
+               np.zeros(3, np.int32), np.zeros(3, np.int32), np.array([0, 0, 1], np.int32),
+               np.array([0, 1, 0], np.int32), np.array([-1, -1, 0], np.int32),
+               np.array([4, 2, 3], np.int32), None, np.zeros(3, np.int32))
+    raw = oracle.throttle(tr, 100, 1, [100], raw=True).reason
+    assert raw.tolist() == [0, 1, 1]
+    c = np.array([5, 5, 5], np.int64)
+    rpm = oracle.simulate(tr, c, raw, 10, 100, -1, flags=oracle.FSO_FCFS | oracle.FSO_BLIND)
+    fs = oracle.simulate(tr, c, raw, 10, 100, -1)
+    assert rpm.status.tolist() == [0, 1, 1] and fs.status.tolist() == [0, 1, 0]
+    m_rpm = oracle.fairness_metrics(tr, c, rpm.status, rpm.admit_step, rpm.max_gap, 10)
+    m_fs = oracle.fairness_metrics(tr, c, fs.status, fs.admit_step, fs.max_gap, 10)
+    assert m_rpm.aborted_midway[0] == 1 and m_rpm.wasted_tokens[0] == 4
+    assert m_fs.aborted_midway[0] == 0 and m_fs.wasted_tokens[0] == 0
 
 
 def test_bounded_runs_are_prefixes():

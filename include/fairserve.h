@@ -99,16 +99,32 @@ typedef struct fs_limits {
  * positive; overshoot is carried as debt into the next step.  The system counts as
  * overloaded while the queued tokens exceed overload_tokens (-1: always).
  * flags: FS_ENGINE_GLOBAL_ONLY runs the scheduler with all of its state in global
- * memory (the path taken when the on-chip capacities overflow); for testing. */
+ * memory (the path taken when the on-chip capacities overflow); for testing.
+ * The policies the paper compares against (Sec. 2 and Sec. 5: request-rate limits and
+ * the virtual token counter) run on the same kernels:
+ *   FS_ENGINE_FCFS   admit the earliest queued request (first come, first served):
+ *                    neither the service counters nor the interaction priority choose;
+ *                    counters are still lifted and charged, so the metrics compare;
+ *   FS_ENGINE_BLIND  interaction-blind limits: every call, not only an interaction's
+ *                    first, is checked against the raw limit reasons (when overloaded),
+ *                    and once a call is dropped every later call of its interaction is
+ *                    dropped too (status 3), as a client abandons the interaction.
+ * FS_ENGINE_FCFS | FS_ENGINE_BLIND with overload_tokens = -1 is the per-user
+ * request-rate-limit policy (RPM); the virtual token counter is the default policy with
+ * equal coefficients for every app and no limits (t_user = t_app = INT32_MAX); the
+ * paper's WSC-only ablation is the default policy with no limits. */
 typedef struct fs_engine {
   int64_t step_us, cap_tokens, overload_tokens;
   uint32_t flags;
 } fs_engine;
 #define FS_ENGINE_GLOBAL_ONLY 1u
+#define FS_ENGINE_FCFS 2u
+#define FS_ENGINE_BLIND 4u
 
 /* Per-record and per-replica scheduler outputs (device pointers).
  *   status       [N] int8: 0 admitted, 1 throttled by the user limit, 2 by the app limit,
- *                3 dropped because its interaction's first call was throttled,
+ *                3 dropped because its interaction's first call was throttled (or, with
+ *                FS_ENGINE_BLIND, an earlier call of its interaction was dropped),
  *                -1 not yet decided (bounded runs only)
  *   admit_step   [N] int32: step of admission, -1 otherwise
  *   admit_seq    [N] int32 or NULL: global admission order within the replica

@@ -204,6 +204,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   const int64_t tau = a.tau, C = a.cap, theta = a.theta;
   // resuming inside step s: its arrivals are done and its budget is partly spent
   bool mid = !onchip && uni(rs->mid) != 0;
+  int64_t fcfs_lo = low;  // every record below is decided (first-come choice)
   const int64_t mid_budget = uni64(rs->mid_budget);
 
   if (!S.users_global)
@@ -245,7 +246,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   int64_t wbase = nxt;
   int64_t w_cost = 0, c_u = 0, o_coa = 0;
   int32_t w_step = 0, w_user = -1, w_call = 0, w_head = -1, w_prev = -1, w_succ = -1, w_tok = 0,
-          w_reason = 0, w_seg = 0, c_prev_adm = 0, c_head_blk = 0, c_pe = -1, o_st = 0;
+          w_reason = 0, w_seg = 0, c_prev_adm = 0, c_head_blk = 0, c_prev_drop = 0, c_pe = -1,
+          o_st = 0;
   // Arrival outcomes of the window's processed lanes: throttled ones get their status
   // and fate, every one its counter on arrival.
   auto flush_window = [&]() {
@@ -291,6 +293,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     const int32_t pe = call > 0 ? ld_fresh(emap + pv) : -1;
     c_prev_adm = (call > 0 && pf == 0) ? 1 : 0;
     c_head_blk = (call > 0 && (hf == 1 || hf == 2)) ? 1 : 0;
+    c_prev_drop = (call > 0 && pf > 0) ? 1 : 0;
     c_pe = pe;
     o_st = 0;
   };
@@ -578,8 +581,11 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       }
       bool blocked;
       int32_t why;
-      if (call > 0) {
+      if (call > 0 && !a.blind) {
         blocked = rdl(c_head_blk, j) != 0;
+        why = 3;
+      } else if (call > 0 && rdl(c_prev_drop, j) != 0) {
+        blocked = true;  // interaction-blind limits: an earlier call of it was dropped
         why = 3;
       } else {
         why = rdl(w_reason, j);
@@ -602,6 +608,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           c_u = (w_user == k) ? uk : c_u;
         }
         c_head_blk = (call == 0 && w_head == rec && w_call > 0) ? 1 : c_head_blk;
+        c_prev_drop = (w_prev == rec) ? 1 : c_prev_drop;
+        if (lane == 0) fate[rec] = int8_t(why);  // read by the first-come choice
       }
       o_coa = lane == j ? uk : o_coa;
       ++nxt;
@@ -614,7 +622,38 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     while (budget > 0 && nX > 0) {
       uint64_t bk;
       int32_t k;
-      const int32_t x = X.argmin(nX, bk, k);
+      int32_t x;
+      if (!a.fcfs) {
+        x = X.argmin(nX, bk, k);
+      } else {
+        // the earliest queued request: the first arrived record still undecided (a
+        // later call waiting for its previous call cannot be it); its user's FIFO head
+        // or, for a later call, the user's earliest ready call
+        wave_fence();
+        int32_t rec = -1;
+        while (fcfs_lo < nxt) {
+          const int64_t i = fcfs_lo + lane;
+          const uint64_t m = __ballot(i < nxt && ld_fresh(fate + i) == -1);
+          if (m) {
+            rec = int32_t(fcfs_lo + __ffsll((long long)m) - 1);
+            fcfs_lo = rec;
+            break;
+          }
+          fcfs_lo += 64;
+        }
+        if (rec < 0) {
+          code = FS_E_STATE;
+          break;
+        }
+        k = uni(t.user[base + rec]);
+        x = X.find(k, S);
+        if (x < 0) {
+          code = FS_E_STATE;
+          break;
+        }
+        const bool later = t.call && uni(t.call[base + rec]) > 0;
+        bk = (uint64_t(later ? 0 : 1) << kTierShift) | uint64_t(slot_u(x));
+      }
       if (x < 0 || x >= X.cap) {
         code = FS_E_STATE;  // internal bookkeeping error: stop rather than read out of bounds
         break;
@@ -678,12 +717,17 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
         break;
       }
       ++seq;
+      if (lane == 0) fate[v.rec] = 0;  // read by the first-come choice
       d_rec = lane == nd ? v.rec : d_rec;
       d_step = lane == nd ? int32_t(s) : d_step;
       d_cnt = lane == nd ? unew : d_cnt;
       if (++nd == 64) flush_decisions();
       c_prev_adm = (w_prev == v.rec) ? 1 : c_prev_adm;
-      const int32_t sc = v.succ;
+      int32_t sc = v.succ;
+      if (a.blind && sc >= 0 && sc < nxt) {  // interaction-blind limits may have dropped it
+        wave_fence();
+        if (ld_fresh(fate + sc) > 0) sc = -1;
+      }
       if (sc >= 0 && sc < nxt) {
         // the next call arrived while this one was queued: it becomes ready now
         int64_t c1 = v.scost;
@@ -970,6 +1014,8 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.theta = eng->overload_tokens;
   a.n_steps = n_steps;
   a.global_only = (eng->flags & FS_ENGINE_GLOBAL_ONLY) != 0;
+  a.fcfs = (eng->flags & FS_ENGINE_FCFS) != 0;
+  a.blind = (eng->flags & FS_ENGINE_BLIND) != 0;
   a.status = out->status;
   a.admit_step = out->admit_step;
   a.admit_seq = out->admit_seq;

@@ -107,6 +107,8 @@ struct SchedArgs {
   int64_t tau, cap, theta;
   int64_t n_steps;
   bool global_only;
+  bool fcfs;   // first come, first served (FS_ENGINE_FCFS)
+  bool blind;  // interaction-blind limits (FS_ENGINE_BLIND)
   int8_t *status;
   int32_t *admit_step, *admit_seq;
   int64_t *counter_after, *counter_on_arrival, *counter, *steps, *decisions, *max_gap;

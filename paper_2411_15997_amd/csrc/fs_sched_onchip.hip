@@ -52,6 +52,7 @@ constexpr int32_t kReasonShift = 1;  // bits 1-2: raw throttle reason (0 within 
 constexpr int32_t kHeadBlk = 8;      // later call whose interaction's first call was throttled
 constexpr int32_t kPrevAdm = 16;     // later call whose previous call has been admitted
 constexpr int32_t kBig = 32;         // cost too large for a packed request
+constexpr int32_t kPrevDrop = 64;    // later call whose previous call was dropped
 
 // A queued request on chip: record, its next call (-1: none), (cost << 24) | tokens.
 struct __align__(16) Ent {
@@ -111,6 +112,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   int32_t last_exit = uni(rs->last_exit);
   const int64_t s_end = a.n_steps < 0 ? INT64_MAX : int64_t(s) + a.n_steps;
   const int64_t C = a.cap, theta = a.theta;
+  const bool fcfs = a.fcfs, blind = a.blind;
   if (uni(rs->mid)) {  // stopped inside a step: only the global-memory kernel resumes that
     if (lane == 0) {
       rs->overflow = 1;
@@ -348,7 +350,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (call > 0) {
         const int8_t *const fate = reinterpret_cast<const int8_t *>(st + o_fate) + base;
         const int8_t pf = ld_fresh(fate + pv), hf = ld_fresh(fate + hd);
-        fl |= (pf == 0 ? kPrevAdm : 0) | ((hf == 1 || hf == 2) ? kHeadBlk : 0);
+        fl |= (pf == 0 ? kPrevAdm : 0) | ((hf == 1 || hf == 2) ? kHeadBlk : 0) |
+              (pf > 0 ? kPrevDrop : 0);
       }
       fl |= (why << kReasonShift) | (cst >= kPackLimit ? kBig : 0);
       const int64_t stp = ts / tau;
@@ -563,7 +566,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (nxt - wbase == 64) advance_window();
       const int j = nxt - wbase;
       if (rdl(w_step, j) > s) break;
-      if (nX > 0) {  // the step's arrivals in this window, together
+      if (nX > 0 && !blind) {  // the step's arrivals in this window, together
         const uint64_t after = __ballot(w_step > s) & (~uint64_t(0) << j);
         const int32_t j1 = after ? ff1(after) : 64;
         if (j1 - j > 1 && arrive_batch(j, j1)) {
@@ -586,9 +589,12 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       }
       bool blocked;
       int32_t why;
-      if (fl & kFirst) {
+      if ((fl & kFirst) || (blind && !(fl & kPrevDrop))) {
         why = (fl >> kReasonShift) & 3;
         blocked = backlog > theta && why != 0;
+      } else if (blind) {  // interaction-blind limits: an earlier call of it was dropped
+        why = 3;
+        blocked = true;
       } else {
         why = 3;
         blocked = (fl & kHeadBlk) != 0;
@@ -600,6 +606,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
           c_u = (w_user == k) ? uk : c_u;
         }
         if (fl & kFirst) w_flags |= (w_head == rec && !(w_flags & kFirst)) ? kHeadBlk : 0;
+        if (blind) w_flags |= (w_prev == rec) ? kPrevDrop : 0;
       } else {
         // capacity first: on overflow the state is as before this arrival
         const bool padm = !(fl & kFirst) && (fl & kPrevAdm);
@@ -629,33 +636,50 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       // least (key, user id): the ready tier first, then the least counter
       bool cand, tier0;
       int64_t uk;
-      if (!wide) {
-        const uint32_t mv = wave_min32v(k32);
-        cand = k32 == mv;
-        const uint32_t m = uint32_t(uni(int32_t(mv)));
-        tier0 = m < kRelTier1;
-        uk = B + int64_t(m & kRelMax);
+      int32_t x, l = -1;
+      if (fcfs) {
+        // first come, first served: the earliest queued request is a FIFO head or a
+        // ready later call (a later call waiting for its previous call cannot be it)
+        const uint32_t hv = (xu >= 0 && xf < xt) ? uint32_t(hrec) : 0xffffffffu;
+        const uint32_t pv = p_x >= 0 ? uint32_t(p_rec) : 0xffffffffu;
+        const uint32_t mv = wave_min32v(hv < pv ? hv : pv);
+        const uint64_t hm = __ballot(hv == mv);
+        tier0 = hm == 0;
+        if (!tier0) {
+          x = ff1(hm);
+        } else {
+          l = ff1(__ballot(pv == mv));
+          x = rdl(p_x, l);
+        }
+        uk = int64_t((uint64_t(rdlu(kh, x) & kValHi) << 32) | rdlu(kl, x));
       } else {
-        const uint32_t mh = wave_min32(kh);
-        const uint32_t ml = wave_min32(kh == mh ? kl : 0xffffffffu);
-        cand = kh == mh && kl == ml;
-        tier0 = mh < kTier1;
-        uk = int64_t((uint64_t(mh & kValHi) << 32) | ml);
+        if (!wide) {
+          const uint32_t mv = wave_min32v(k32);
+          cand = k32 == mv;
+          const uint32_t m = uint32_t(uni(int32_t(mv)));
+          tier0 = m < kRelTier1;
+          uk = B + int64_t(m & kRelMax);
+        } else {
+          const uint32_t mh = wave_min32(kh);
+          const uint32_t ml = wave_min32(kh == mh ? kl : 0xffffffffu);
+          cand = kh == mh && kl == ml;
+          tier0 = mh < kTier1;
+          uk = int64_t((uint64_t(mh & kValHi) << 32) | ml);
+        }
+        const uint64_t eq = __ballot(cand);
+        if (eq & (eq - 1)) {
+          const uint32_t um = wave_min32v(cand ? uint32_t(xu) : 0xffffffffu);
+          x = ff1(__ballot(cand && uint32_t(xu) == um));
+        } else {
+          x = ff1(eq);
+        }
       }
-      const uint64_t eq = __ballot(cand);
-      int32_t x;
-      if (eq & (eq - 1)) {
-        const uint32_t um = wave_min32v(cand ? uint32_t(xu) : 0xffffffffu);
-        x = ff1(__ballot(cand && uint32_t(xu) == um));
-      } else {
-        x = ff1(eq);
-      }
-      int32_t rec, sc, l = -1;
+      int32_t rec, sc;
       uint32_t lo, hi;
       if (tier0) {  // the user's earliest ready later call
         const uint64_t pm = __ballot(p_x == x);
-        l = ff1(pm);
-        if (pm & (pm - 1)) {
+        if (l < 0) l = ff1(pm);
+        if (!fcfs && (pm & (pm - 1))) {
           const uint32_t e = wave_min32v(p_x == x ? uint32_t(p_rec) : 0xffffffffu);
           l = ff1(__ballot(p_x == x && uint32_t(p_rec) == e));
         }
@@ -669,7 +693,12 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         lo = rdlu(hlo, x);
         hi = rdlu(hhi, x);
       }
-      const bool sc_now = sc >= 0 && sc < nxt;  // its next call already arrived
+      bool sc_now = sc >= 0 && sc < nxt;  // its next call already arrived
+      if (blind && sc_now) {  // interaction-blind limits may have dropped it
+        const int32_t f = sc >= wbase ? rdl(o_st, sc - wbase)
+                                      : int32_t(ld_fresh(STATE(const int8_t, fate) + base + sc));
+        sc_now = f <= 0;
+      }
       if (sc_now && !tier0 && pocc == ~uint64_t(0)) {
         overflow = mid = true;  // nothing of this admission has happened yet
         mid_budget = budget;

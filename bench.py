@@ -66,6 +66,24 @@ def measured_traffic(workload, stage):
     return int(m["fetch_kib"] * 1024 * m["fetch_factor"] + m["write_kib"] * 1024 * m["write_factor"])
 
 
+NO_LIMIT = 2 ** 31 - 1
+
+
+def policy_settings(wl, n_apps, policy):
+    """Limits, engine flags and coefficient choice of a policy (the paper's own, or one
+    it compares with) on a workload: (t_user, t_app, overload_tokens, fcfs, blind,
+    equal_coefficients)."""
+    if policy == "fs":            # FairServe: WSC plus interaction-aware OIT
+        return wl.t_user, list(wl.t_app), wl.overload_tokens, False, False, False
+    if policy == "wsc_only":      # the paper's WSC-only ablation: no limits
+        return NO_LIMIT, [NO_LIMIT] * n_apps, wl.overload_tokens, False, False, False
+    if policy == "vtc":           # virtual token counter: equal token weights, no limits
+        return NO_LIMIT, [NO_LIMIT] * n_apps, wl.overload_tokens, False, False, True
+    if policy == "rpm":           # per-user request limit, always on, interaction-blind, FCFS
+        return wl.t_user, [NO_LIMIT] * n_apps, -1, True, True, False
+    raise ValueError(policy)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -75,6 +93,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--stage-only", default="", help="time only this stage (profiling runs)")
+    ap.add_argument("--policy", default="fs", choices=["fs", "wsc_only", "vtc", "rpm"],
+                    help="the paper's policy (default) or one it compares with")
     ap.add_argument("--calib-copy", action="store_true",
                     help="copy 1 GiB on the device first (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -98,14 +118,17 @@ def main():
     torch.cuda.set_device(dev)
     dt = fs.DeviceTrace(tr, device=dev)
     throttle_only = wl.throttle_only
-    lim = fs.make_limits(wl.window_us, wl.t_user, wl.t_app)
+    t_user, t_app, theta, fcfs, blind, equal = policy_settings(wl, tr.n_apps, args.policy)
+    lim = fs.make_limits(wl.window_us, t_user, t_app)
     N = tr.n
     err = fs.err_word(dev)
     tws = torch.empty(max(fs.fs_throttle_workspace(dt), 1), dtype=torch.uint8, device=dev)
     if not throttle_only:
         coef, per_rep = fs.workload_weights(wl, tr)
+        if equal:
+            coef, per_rep = np.full((1, tr.n_apps, coef.shape[-2], 3), 1 << 16, np.int64), False
         w, keep = fs.make_weights(dt, coef, None, per_rep)
-        eng = fs.make_engine(wl.step_us, wl.cap_tokens, wl.overload_tokens)
+        eng = fs.make_engine(wl.step_us, wl.cap_tokens, theta, fcfs=fcfs, blind=blind)
         out = fs.Outputs(dt, parity=False)
         cost = torch.empty(max(N, 1), dtype=torch.int64, device=dev)
         state = torch.empty(fs.fs_state_bytes(dt), dtype=torch.uint8, device=dev)
@@ -183,7 +206,7 @@ def main():
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64", "data": "synthetic",
-        "config": {"workload": wl.name, "replicas": R, "users": tr.n_users, "apps": tr.n_apps,
+        "config": {"workload": wl.name, "policy": args.policy, "replicas": R, "users": tr.n_users, "apps": tr.n_apps,
                    "requests": N, "trace_sha256": tr.sha256()[:16],
                    "step_us": wl.step_us, "cap_tokens": wl.cap_tokens, "window_us": wl.window_us},
         "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
@@ -213,13 +236,23 @@ def main():
                      for s in stage_ms if ALGO_BYTES[s] > 0}
     result["stage_gbs"] = all_stage_gbs
 
+    if "metrics" in stages:  # the served-experience outcome of the policy (last step's metrics)
+        mh = metrics.host()
+        result["outcome"] = {"throttled": int(mh["throttled"].sum()),
+                             "aborted_midway": int(mh["aborted_midway"].sum()),
+                             "wasted_tokens": int(mh["wasted_tokens"].sum()),
+                             "svc_int_pct": round(float(np.mean(mh["svc_int_pct"])), 3),
+                             "served_users_pct": round(float(np.mean(mh["served_users_pct"])), 3),
+                             "delayed_users_pct": round(float(np.mean(mh["delayed_users_pct"])), 3),
+                             "jain": round(float(np.mean(mh["jain"])), 5)}
     if not args.no_cpu_baseline and not args.stage_only:
-        result["cpu_baseline"] = cpu_baseline(wl, tr, args.cpu_threads, throttle_only)
+        result["cpu_baseline"] = cpu_baseline(wl, tr, args.cpu_threads, throttle_only,
+                                              args.policy)
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(wl, tr, threads, throttle_only):
-    """The CPU oracle (as it stands) on this host, same workload, whole path."""
+def cpu_baseline(wl, tr, threads, throttle_only, policy="fs"):
+    """The CPU oracle (as it stands) on this host, same workload and policy, whole path."""
     import numpy as np
 
     import oracle
@@ -239,7 +272,19 @@ def cpu_baseline(wl, tr, threads, throttle_only):
         return {"value": n / dt, "unit": "throttle evals/s", "cores": 1, "kind": "oracle",
                 "sample": f"first {n} requests of {wl.name}", "seconds": round(dt, 3),
                 "host": platform.processor() or platform.machine()}
-    c, thr, sim, met = oracle.run_workload(wl, tr, n_threads=th)
+    if policy == "fs":
+        c, thr, sim, met = oracle.run_workload(wl, tr, n_threads=th)
+    else:
+        t_user, t_app, theta, fcfs, blind, equal = policy_settings(wl, tr.n_apps, policy)
+        coef, per_rep = oracle.weights_for(wl, tr)
+        if equal:
+            coef, per_rep = np.full((1, tr.n_apps, coef.shape[-2], 3), 1 << 16, np.int64), False
+        c = oracle.cost(tr, coef, coef_per_replica=per_rep)
+        thr = oracle.throttle(tr, wl.window_us, t_user, t_app, raw=True, counts=False)
+        flags = (oracle.FSO_FCFS if fcfs else 0) | (oracle.FSO_BLIND if blind else 0)
+        sim = oracle.simulate(tr, c, thr.reason, wl.step_us, wl.cap_tokens, theta, n_threads=th,
+                              flags=flags)
+        oracle.fairness_metrics(tr, c, sim.status, sim.admit_step, sim.max_gap, wl.step_us)
     dt = time.perf_counter() - t0
     dec = int(sim.decisions.sum())
     return {"value": dec / dt, "unit": "decisions/s", "cores": th, "kind": "oracle",

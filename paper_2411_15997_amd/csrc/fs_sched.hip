@@ -898,23 +898,43 @@ __global__ void k_state_records(char *state, StateLayout L, int64_t N) {
   }
 }
 
-// next-call links (succ[prev] = i) and the number of first calls per (replica, user);
-// links and ids are checked again before the scheduler runs
-__global__ void k_state_links(char *state, StateLayout L, DevTrace t) {
+// next-call links (succ[prev] = i) and the number of requests per (replica, user), the
+// size of the user's segment (a FIFO holds at most all of its user's requests); links
+// and ids are checked again before the scheduler runs.  Each block counts a tile of
+// records in LDS (by user, for the replica the tile starts in) and adds the non-zero
+// counts to global memory; users beyond the LDS table and a tile's records of a later
+// replica are added directly.
+constexpr int kLinkTile = 4096;
+constexpr int kLinkUsers = 8192;
+
+__global__ void __launch_bounds__(256) k_state_links(char *state, StateLayout L, DevTrace t) {
+  __shared__ uint32_t h[kLinkUsers];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(state + L.seg_start);
-  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
-       g += int64_t(gridDim.x) * blockDim.x) {
+  const int64_t g0 = int64_t(blockIdx.x) * kLinkTile;
+  const int32_t nu = t.U < kLinkUsers ? t.U : kLinkUsers;
+  for (int k = threadIdx.x; k < nu; k += 256) h[k] = 0;
+  const int32_t r0 = replica_of(t.rep_off, t.R, g0 < t.N ? g0 : t.N - 1);
+  const int64_t r0_end = t.rep_off[r0 + 1];
+  __syncthreads();
+  for (int64_t g = g0 + threadIdx.x; g < g0 + kLinkTile && g < t.N; g += 256) {
     const int32_t c = t.call ? t.call[g] : 0;
-    const int32_t r = replica_of(t.rep_off, t.R, g);
+    const int32_t r = g < r0_end ? r0 : replica_of(t.rep_off, t.R, g);
     const int64_t b = t.rep_off[r], i = g - b;
     const int32_t u = t.user[g];
-    if (c == 0) {
-      if (u >= 0 && u < t.U) atomicAdd(cnt + int64_t(r) * t.U + u, 1u);
-    } else if (c > 0) {
+    if (u >= 0 && u < t.U) {
+      if (r == r0 && u < nu)
+        atomicAdd(h + u, 1u);
+      else
+        atomicAdd(cnt + int64_t(r) * t.U + u, 1u);
+    }
+    if (c > 0) {
       const int32_t p = t.prev[g];
       if (p >= 0 && p < i) reinterpret_cast<int32_t *>(state + L.succ)[b + p] = int32_t(i);
     }
   }
+  __syncthreads();
+  for (int k = threadIdx.x; k < nu; k += 256)
+    if (h[k]) atomicAdd(cnt + int64_t(r0) * t.U + k, h[k]);
 }
 
 struct CheckArgs {
@@ -991,8 +1011,8 @@ hipError_t launch_state_init(void *state, const fs_trace *t, hipStream_t s) {
   hipLaunchKernelGGL(k_state_users, dim3(grid_for(RU + 1, 256)), dim3(256), 0, s, st, L, RU);
   if (N > 0) {
     hipLaunchKernelGGL(k_state_records, dim3(grid_for(N, 256)), dim3(256), 0, s, st, L, N);
-    hipLaunchKernelGGL(k_state_links, dim3(grid_for(N, 256)), dim3(256), 0, s, st, L,
-                       dev_trace(t));
+    hipLaunchKernelGGL(k_state_links, dim3((N + kLinkTile - 1) / kLinkTile), dim3(256), 0, s, st,
+                       L, dev_trace(t));
   }
   // per-user first-call segments: exclusive prefix of the counts
   hipError_t e = exclusive_scan(reinterpret_cast<uint32_t *>(st + L.seg_start), RU + 1,

@@ -20,7 +20,9 @@
 //             needed only when it has more than one.
 //   ring      per slot, the next first calls of the FIFO in LDS; a FIFO longer than
 //             the ring continues in the user's segment of the state buffer (one entry
-//             per first call of the user) and comes back in coalesced refills.
+//             per request of the user) and comes back in coalesced refills.  First come,
+//             first served keeps every queued call of a user in its FIFO (arrival
+//             order is service order, so nothing needs the ready lanes).
 //   cache     the data of the most recent arrivals in LDS, by record index, so a
 //             later call that waited for its previous call becomes ready without
 //             reading HBM.
@@ -85,6 +87,8 @@ __device__ __forceinline__ T arg_at(uint32_t off) {
 
 #define STATE(T, field) reinterpret_cast<T *>(KARG(state) + KARG(L.field))
 
+// FCFS: first come, first served; BLIND: interaction-blind limits (the engine flags).
+template <bool FCFS, bool BLIND>
 __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int32_t r = blockIdx.x;
@@ -112,7 +116,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   int32_t last_exit = uni(rs->last_exit);
   const int64_t s_end = a.n_steps < 0 ? INT64_MAX : int64_t(s) + a.n_steps;
   const int64_t C = a.cap, theta = a.theta;
-  const bool fcfs = a.fcfs, blind = a.blind;
+  constexpr bool fcfs = FCFS, blind = BLIND;
   if (uni(rs->mid)) {  // stopped inside a step: only the global-memory kernel resumes that
     if (lane == 0) {
       rs->overflow = 1;
@@ -442,7 +446,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const bool bl = inb && !first && ((w_flags & kHeadBlk) || hb_new);
     const bool blk = bf || bl;
     const uint64_t ub = __ballot(inb && !blk);
-    const uint64_t rdym = __ballot(inb && !blk && !first && (w_flags & kPrevAdm));
+    const uint64_t rdym = fcfs ? 0 : __ballot(inb && !blk && !first && (w_flags & kPrevAdm));
     if (__ballot(inb && !blk && (w_flags & kBig)) || __popcll(ub) > kSlots - nX ||
         __popcll(rdym) > kSlots - __popcll(pocc))
       return false;
@@ -474,7 +478,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (!mine) continue;
       if (!fm) x = join(k, uk, rdlu(w_seg, jj));
       if (lane == x) xq += __popcll(mine);
-      if (mine & firstm) fifo_push_many(x, mine & firstm);
+      const uint64_t fifo_m = fcfs ? mine : (mine & firstm);
+      if (fifo_m) fifo_push_many(x, fifo_m);
       uint64_t rm = mine & rdym;
       while (rm) {
         const int l = ff1(rm);
@@ -502,7 +507,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       int32_t sc;
       uint32_t lo, hi;
       load_rec(rec, sc, lo, hi);
-      const bool padm = call > 0 && ld_fresh(fate + uni(KARG(t.prev)[g])) == 0;
+      const bool padm = !fcfs && call > 0 && ld_fresh(fate + uni(KARG(t.prev)[g])) == 0;
       const uint64_t fm = __ballot(xu == k);
       const bool big = KARG(cost)[g] >= kPackLimit;
       if (big || (fm == 0 && nX == kSlots) || (padm && pocc == ~uint64_t(0))) {
@@ -516,7 +521,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         x = join(k, uk, sb);
       }
       if (lane == x) ++xq;
-      if (call == 0)
+      if (call == 0 || fcfs)
         fifo_push(x, rec, sc, lo, hi);
       else if (padm)
         ready_add(x, rec, sc, lo, hi);
@@ -606,10 +611,13 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
           c_u = (w_user == k) ? uk : c_u;
         }
         if (fl & kFirst) w_flags |= (w_head == rec && !(w_flags & kFirst)) ? kHeadBlk : 0;
-        if (blind) w_flags |= (w_prev == rec) ? kPrevDrop : 0;
+        if (blind) {
+          w_flags |= (w_prev == rec) ? kPrevDrop : 0;
+          if (lane == 0) cache[rec & (M - 1)].rec = -1;  // dropped
+        }
       } else {
         // capacity first: on overflow the state is as before this arrival
-        const bool padm = !(fl & kFirst) && (fl & kPrevAdm);
+        const bool padm = !(fl & kFirst) && (fl & kPrevAdm) && !fcfs;
         if ((fl & kBig) || (!fm && nX == kSlots) || (padm && pocc == ~uint64_t(0))) {
           overflow = true;
           break;
@@ -619,7 +627,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         const uint32_t lo = rdlu(w_lo, j), hi = rdlu(w_hi, j);
         const int32_t sc = rdl(w_succ, j);
         if (lane == x) ++xq;
-        if (fl & kFirst)
+        if ((fl & kFirst) || fcfs)
           fifo_push(x, rec, sc, lo, hi);
         else if (padm)
           ready_add(x, rec, sc, lo, hi);
@@ -638,19 +646,11 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       int64_t uk;
       int32_t x, l = -1;
       if (fcfs) {
-        // first come, first served: the earliest queued request is a FIFO head or a
-        // ready later call (a later call waiting for its previous call cannot be it)
+        // first come, first served: the earliest of the FIFO heads (each user's FIFO
+        // holds all of its queued calls in arrival order)
         const uint32_t hv = (xu >= 0 && xf < xt) ? uint32_t(hrec) : 0xffffffffu;
-        const uint32_t pv = p_x >= 0 ? uint32_t(p_rec) : 0xffffffffu;
-        const uint32_t mv = wave_min32v(hv < pv ? hv : pv);
-        const uint64_t hm = __ballot(hv == mv);
-        tier0 = hm == 0;
-        if (!tier0) {
-          x = ff1(hm);
-        } else {
-          l = ff1(__ballot(pv == mv));
-          x = rdl(p_x, l);
-        }
+        x = ff1(__ballot(hv == wave_min32v(hv)));
+        tier0 = false;
         uk = int64_t((uint64_t(rdlu(kh, x) & kValHi) << 32) | rdlu(kl, x));
       } else {
         if (!wide) {
@@ -678,8 +678,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       uint32_t lo, hi;
       if (tier0) {  // the user's earliest ready later call
         const uint64_t pm = __ballot(p_x == x);
-        if (l < 0) l = ff1(pm);
-        if (!fcfs && (pm & (pm - 1))) {
+        l = ff1(pm);
+        if (pm & (pm - 1)) {
           const uint32_t e = wave_min32v(p_x == x ? uint32_t(p_rec) : 0xffffffffu);
           l = ff1(__ballot(p_x == x && uint32_t(p_rec) == e));
         }
@@ -693,11 +693,12 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         lo = rdlu(hlo, x);
         hi = rdlu(hhi, x);
       }
-      bool sc_now = sc >= 0 && sc < nxt;  // its next call already arrived
+      bool sc_now = !fcfs && sc >= 0 && sc < nxt;  // its next call already arrived
       if (blind && sc_now) {  // interaction-blind limits may have dropped it
-        const int32_t f = sc >= wbase ? rdl(o_st, sc - wbase)
-                                      : int32_t(ld_fresh(STATE(const int8_t, fate) + base + sc));
-        sc_now = f <= 0;
+        if (sc >= cache_lo)
+          sc_now = uni(cache[sc & (M - 1)].rec) >= 0;  // a dropped arrival's entry is marked
+        else
+          sc_now = ld_fresh(STATE(const int8_t, fate) + base + sc) <= 0;
       }
       if (sc_now && !tier0 && pocc == ~uint64_t(0)) {
         overflow = mid = true;  // nothing of this admission has happened yet
@@ -897,11 +898,20 @@ OnchipCfg onchip_config(int32_t R, int32_t U) {
   return c;
 }
 
-void launch_onchip(const SchedArgs &a, hipStream_t s) {
+template <bool FCFS, bool BLIND>
+void launch_mode(const SchedArgs &a, hipStream_t s) {
   if (a.oc.lds_bytes > 65536)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&k_schedule_onchip),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&k_schedule_onchip<FCFS, BLIND>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, int(a.oc.lds_bytes));
-  hipLaunchKernelGGL(k_schedule_onchip, dim3(a.t.R), dim3(64), a.oc.lds_bytes, s, a);
+  hipLaunchKernelGGL((k_schedule_onchip<FCFS, BLIND>), dim3(a.t.R), dim3(64), a.oc.lds_bytes, s,
+                     a);
+}
+
+void launch_onchip(const SchedArgs &a, hipStream_t s) {
+  if (a.fcfs)
+    a.blind ? launch_mode<true, true>(a, s) : launch_mode<true, false>(a, s);
+  else
+    a.blind ? launch_mode<false, true>(a, s) : launch_mode<false, false>(a, s);
 }
 
 }  // namespace sched

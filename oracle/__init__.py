@@ -74,6 +74,9 @@ def lib():
                                C.c_void_p, C.c_void_p]
         L.fso_throttle.argtypes = [C.POINTER(_Trace), C.c_int64, C.c_int32, C.c_void_p, C.c_void_p,
                                    C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.fso_throttle_scoped.argtypes = [C.POINTER(_Trace), C.c_int64, C.c_int32, C.c_void_p,
+                                          C.c_int32, C.c_void_p, C.c_int32, C.c_void_p,
+                                          C.c_void_p, C.c_void_p, C.c_void_p]
         L.fso_simulate.argtypes = [C.POINTER(_Trace), C.c_void_p, C.c_void_p, C.POINTER(_Engine),
                                    C.c_int64, C.c_int32, C.c_int32, C.POINTER(_Outputs)]
         L.fso_fairness_metrics.argtypes = [C.POINTER(_Trace), C.c_void_p, C.c_void_p, C.c_void_p,
@@ -150,7 +153,9 @@ class ThrottleResult:
     cnt_app: np.ndarray
 
 
-def throttle(tr, window_us, t_user, t_app, overloaded=None, raw=True, counts=True):
+def throttle(tr, window_us, t_user, t_app, overloaded=None, raw=True, counts=True,
+             app_scope=0):
+    """app_scope 0: the app limit per (user, app); 1: per app over all users."""
     t = _TraceRef(tr)
     t_app = np.ascontiguousarray(t_app, np.int32)
     ov = _c(overloaded, np.uint8)
@@ -158,9 +163,9 @@ def throttle(tr, window_us, t_user, t_app, overloaded=None, raw=True, counts=Tru
     bitmap = np.zeros((t.n + 31) // 32, np.uint32)
     cu = np.zeros(t.n, np.int32) if counts else None
     ca = np.zeros(t.n, np.int32) if counts else None
-    _check(lib().fso_throttle(C.byref(t.s), int(window_us), int(t_user), _p(t_app), _p(ov),
-                              1 if raw else 0, _p(reason), _p(bitmap), _p(cu), _p(ca)),
-           "fso_throttle")
+    _check(lib().fso_throttle_scoped(C.byref(t.s), int(window_us), int(t_user), _p(t_app),
+                                     int(app_scope), _p(ov), 1 if raw else 0, _p(reason),
+                                     _p(bitmap), _p(cu), _p(ca)), "fso_throttle")
     return ThrottleResult(reason, bitmap, cu, ca)
 
 

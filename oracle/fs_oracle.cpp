@@ -392,7 +392,16 @@ int fso_cost(const fso_trace *t, int32_t n_stages, int64_t coef_rep_stride, cons
 int fso_throttle(const fso_trace *t, int64_t window_us, int32_t t_user, const int32_t *t_app,
                  const uint8_t *overloaded, int32_t raw, uint8_t *reason, uint32_t *bitmap,
                  int32_t *cnt_user, int32_t *cnt_app) {
-  if (window_us <= 0 || t_user < 0 || !t_app || !reason) return FSO_E_ARG;
+  return fso_throttle_scoped(t, window_us, t_user, t_app, 0, overloaded, raw, reason, bitmap,
+                             cnt_user, cnt_app);
+}
+
+int fso_throttle_scoped(const fso_trace *t, int64_t window_us, int32_t t_user,
+                        const int32_t *t_app, int32_t app_scope, const uint8_t *overloaded,
+                        int32_t raw, uint8_t *reason, uint32_t *bitmap, int32_t *cnt_user,
+                        int32_t *cnt_app) {
+  if (window_us <= 0 || t_user < 0 || !t_app || !reason || app_scope < 0 || app_scope > 1)
+    return FSO_E_ARG;
   int code = validate_trace(t, kIds | kOrder | (raw ? 0u : unsigned(kChain)));
   if (code == FSO_E_ARG) return code;
   for (int32_t a = 0; a < t->n_apps; ++a)
@@ -401,12 +410,14 @@ int fso_throttle(const fso_trace *t, int64_t window_us, int32_t t_user, const in
   const int64_t A = t->n_apps;
   for (int32_t r = 0; r < t->n_replicas; ++r) {
     Replica rp = replica(t, r);
-    // OIT's dictionaries: user -> arrival times, (user, app) -> arrival times.
+    // OIT's dictionaries: user -> arrival times, (user, app) -> arrival times (or
+    // app -> arrival times for the app-level limit).
     std::unordered_map<int64_t, std::deque<int64_t>> by_user, by_user_app;
     for (int64_t i = 0; i < rp.n; ++i) {
       int64_t g = rp.base + i, ts = t->ts_us[g];
       std::deque<int64_t> &du = by_user[t->user[g]];
-      std::deque<int64_t> &da = by_user_app[int64_t(t->user[g]) * A + t->app[g]];
+      std::deque<int64_t> &da =
+          by_user_app[app_scope ? int64_t(t->app[g]) : int64_t(t->user[g]) * A + t->app[g]];
       du.push_back(ts);  // counted on arrival, whatever the request's fate
       da.push_back(ts);
       while (du.front() <= ts - window_us) du.pop_front();

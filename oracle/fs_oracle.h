@@ -46,6 +46,13 @@ int fso_cost(const fso_trace *t, int32_t n_stages, int64_t coef_rep_stride, cons
 int fso_throttle(const fso_trace *t, int64_t window_us, int32_t t_user, const int32_t *t_app,
                  const uint8_t *overloaded /* NULL => always */, int32_t raw, uint8_t *reason,
                  uint32_t *bitmap, int32_t *cnt_user, int32_t *cnt_app);
+/* The same with the application limit counted per application over all users
+ * (app_scope = 1: the app-level rate limit the paper discusses) instead of per
+ * (user, application) (app_scope = 0, fso_throttle). */
+int fso_throttle_scoped(const fso_trace *t, int64_t window_us, int32_t t_user,
+                        const int32_t *t_app, int32_t app_scope, const uint8_t *overloaded,
+                        int32_t raw, uint8_t *reason, uint32_t *bitmap, int32_t *cnt_user,
+                        int32_t *cnt_app);
 
 /* flags: FSO_FCFS serves queued requests first come, first served (no service counter
  * or interaction priority in the choice; counters are still charged); FSO_BLIND checks

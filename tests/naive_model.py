@@ -36,8 +36,9 @@ def cost(tr, coef, prio=None, coef_per_replica=False):
     return out
 
 
-def window_counts(tr, window_us):
-    """c_user(i), c_app(i): requests j <= i of the same key with ts_j > ts_i - W."""
+def window_counts(tr, window_us, app_scope=0):
+    """c_user(i), c_app(i): requests j <= i of the same key with ts_j > ts_i - W (the app
+    key is (user, app), or the app alone when app_scope is 1)."""
     cu, ca = [], []
     for r in range(tr.n_replicas):
         a0, a1 = int(tr.rep_off[r]), int(tr.rep_off[r + 1])
@@ -45,17 +46,18 @@ def window_counts(tr, window_us):
             lo = int(tr.ts_us[i]) - window_us
             nu = na = 0
             for j in range(a0, i + 1):
-                if int(tr.ts_us[j]) > lo and tr.user[j] == tr.user[i]:
-                    nu += 1
-                    if tr.app[j] == tr.app[i]:
+                if int(tr.ts_us[j]) > lo:
+                    same_user = tr.user[j] == tr.user[i]
+                    nu += 1 if same_user else 0
+                    if tr.app[j] == tr.app[i] and (same_user or app_scope):
                         na += 1
             cu.append(nu)
             ca.append(na)
     return cu, ca
 
 
-def throttle_raw(tr, window_us, t_user, t_app):
-    cu, ca = window_counts(tr, window_us)
+def throttle_raw(tr, window_us, t_user, t_app, app_scope=0):
+    cu, ca = window_counts(tr, window_us, app_scope)
     return [1 if cu[g] > t_user else (2 if ca[g] > t_app[int(tr.app[g])] else 0)
             for g in range(len(cu))]
 

@@ -271,6 +271,27 @@ def test_naive_equals_oracle_small_workload():
               wl.t_app, coef)
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_app_level_limit_brute_force(seed):
+    """The app limit counted per application over all users (the app-level rate limit),
+    against counts by brute force over all earlier requests."""
+    rng = np.random.default_rng(40 + seed)
+    for _ in range(25):
+        A = int(rng.integers(1, 4))
+        tr = random_trace(rng, int(rng.integers(1, 60)), int(rng.integers(1, 5)), A,
+                          int(rng.integers(1, 200)), multi=bool(seed % 2))
+        W, tu = int(rng.integers(1, 80)), int(rng.integers(0, 6))
+        ta = rng.integers(0, 6, size=A).tolist()
+        th = oracle.throttle(tr, W, tu, ta, raw=True, app_scope=1)
+        cu, ca = nm.window_counts(tr, W, app_scope=1)
+        assert th.cnt_user.tolist() == cu and th.cnt_app.tolist() == ca
+        assert th.reason.tolist() == nm.throttle_raw(tr, W, tu, ta, app_scope=1)
+        # with one user the two scopes agree
+        if tr.n_users == 1:
+            th0 = oracle.throttle(tr, W, tu, ta, raw=True)
+            assert th0.reason.tolist() == th.reason.tolist()
+
+
 def test_fcfs_serves_in_arrival_order():
     """First come, first served without throttling: every request is admitted and the
     admission sequence is the stream order (closed form), whatever the counters say."""

@@ -86,11 +86,14 @@ typedef struct fs_weights {
  * (every arrival is counted, whatever its fate).  The user limit is checked first:
  * exceeded if c_user > t_user, else if c_app > t_app_h[app].  t_user = INT32_MAX
  * disables the user limit.  window_us > 0; limits >= 0; t_app_h is a host array
- * [n_apps], n_apps <= 1024. */
+ * [n_apps], n_apps <= 1024.  app_scope = 1 counts c_app over every user of the app
+ * (drop the user_j = user_i term: the app-level rate limit of Sec. 3); 0 is the
+ * per-(user, app) count above. */
 typedef struct fs_limits {
   int64_t window_us;
   int32_t t_user;
   const int32_t *t_app_h;
+  int32_t app_scope;
 } fs_limits;
 
 /* Engine model for the execution stream (the paper leaves the LLM engine's

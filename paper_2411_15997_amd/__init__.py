@@ -46,7 +46,8 @@ class fs_weights(C.Structure):
 
 
 class fs_limits(C.Structure):
-    _fields_ = [("window_us", C.c_int64), ("t_user", C.c_int32), ("t_app_h", C.c_void_p)]
+    _fields_ = [("window_us", C.c_int64), ("t_user", C.c_int32), ("t_app_h", C.c_void_p),
+                ("app_scope", C.c_int32)]
 
 
 class fs_engine(C.Structure):
@@ -207,9 +208,9 @@ def fs_cost(dt: DeviceTrace, weights, cost=None, err=None, check=True):
     return cost
 
 
-def make_limits(window_us, t_user, t_app):
+def make_limits(window_us, t_user, t_app, app_scope=0):
     t_app = np.ascontiguousarray(t_app, np.int32)
-    return fs_limits(int(window_us), int(t_user), t_app.ctypes.data), t_app
+    return fs_limits(int(window_us), int(t_user), t_app.ctypes.data, int(app_scope)), t_app
 
 
 def fs_throttle_workspace(dt: DeviceTrace) -> int:

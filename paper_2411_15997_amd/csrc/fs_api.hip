@@ -51,7 +51,9 @@ fs_status check_weights(const fs_trace *t, const fs_weights *w) {
 }
 
 fs_status check_limits(const fs_trace *t, const fs_limits *l) {
-  if (!l || l->window_us <= 0 || l->t_user < 0 || !l->t_app_h) return FS_E_ARG;
+  if (!l || l->window_us <= 0 || l->t_user < 0 || !l->t_app_h || l->app_scope < 0 ||
+      l->app_scope > 1)
+    return FS_E_ARG;
   for (int32_t a = 0; a < t->n_apps; ++a)
     if (l->t_app_h[a] < 0) return FS_E_ARG;
   return FS_OK;

@@ -479,6 +479,22 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const uint32_t *in,
   }
 }
 
+// ---------------------------------------------------------------- keys
+
+// The key an element is counted under, as an ordered value: its masked key bits, or
+// for the app-level limit (app, replica), the replica being (replica * U + user) / U.
+struct KeySel {
+  uint64_t mask;  // element bits of the key (per-user and per-(user, app) keys)
+  bool app_level;
+  int SK, Bu;
+  uint32_t U;
+};
+__device__ inline uint64_t key_of(uint64_t e, const KeySel &k) {
+  if (!k.app_level) return e & k.mask;
+  const uint64_t ru = (e >> k.SK) & ((uint64_t(1) << k.Bu) - 1);
+  return ((e >> (k.SK + k.Bu)) << 32) | (ru / k.U);
+}
+
 // ---------------------------------------------------------------- app-limit test
 
 // The app limit is tested in (user, app) order and the raw reason goes back to
@@ -489,8 +505,9 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const uint32_t *in,
 constexpr int kUnsortBits = 18;  // stream records per unsort chunk: 2^18, 2 bits each in LDS
 
 struct AppTestArgs {
-  const uint64_t *el;  // (user, app) order, user flag set
+  const uint64_t *el;  // the app key's order (time order within a key), user flag set
   int64_t N;
+  KeySel key;          // the app key
   const int32_t *t_app;
   int32_t A;
   Win win;
@@ -531,7 +548,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_apptest(AppTestArgs a) {
       bool fa = false;
       if (T <= p) {
         const uint64_t eq = a.el[p - T];
-        fa = (ep >> pk.SK) == (eq >> pk.SK) && in_window(ep, eq, win);
+        fa = key_of(ep, a.key) == key_of(eq, a.key) && in_window(ep, eq, win);
       }
       const uint32_t code = (ep & 1u) ? 1u : (fa ? 2u : 0u);
       const uint64_t g = (ep >> pk.SI) & pk.imask;
@@ -613,12 +630,31 @@ __global__ void __launch_bounds__(1024) k_thr_unsort(UnsortArgs a) {
   for (int64_t j = threadIdx.x; j < (n + 15) >> 4; j += 1024) a.rr[(g0 >> 4) + j] = codes[j];
 }
 
+// ---------------------------------------------------------------- app-level limit
+
+// With the app limit counted over all users of an app, the user test runs on the user
+// order and the elements go back to stream order (through their index field) before
+// the app passes, so that each app's records come out in time order.
+__global__ void __launch_bounds__(kThreads) k_thr_user_unsort(ScatterArgs a) {
+  const Win win = load_win(a.win);
+  const Pack &pk = win.pk;
+  for (int64_t p = blockIdx.x * int64_t(kThreads) + threadIdx.x; p < a.N;
+       p += int64_t(gridDim.x) * kThreads) {
+    uint64_t e = a.in[p];
+    if (int64_t(a.t_user) <= p) {
+      const uint64_t eq = a.in[p - a.t_user];
+      if (((e ^ eq) & a.user_mask) == 0 && in_window(e, eq, win)) e |= 1u;
+    }
+    a.out[(e >> pk.SI) & pk.imask] = e;
+  }
+}
+
 // ---------------------------------------------------------------- window counts (optional)
 
 struct CountArgs {
   const uint64_t *el;  // key order in which every compared key is contiguous
   int64_t N;
-  uint64_t key_mask;   // element bits compared
+  KeySel key;
   Win win;
   int32_t *cnt;        // [N] stream order
 };
@@ -630,13 +666,13 @@ __global__ void __launch_bounds__(kThreads) k_thr_count(CountArgs a) {
   for (int64_t p = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; p < a.N;
        p += int64_t(gridDim.x) * blockDim.x) {
     const uint64_t ep = a.el[p];
-    const uint64_t k = ep & a.key_mask;
+    const uint64_t k = key_of(ep, a.key);
     const int64_t gp = int64_t((ep >> pk.SI) & pk.imask);
     const int64_t lo_ts = a.win.ts[gp] - a.win.W;  // window is (ts - W, ts]
     int64_t l = 0, h = p;
     while (l < h) {
       const int64_t m = (l + h) >> 1;
-      if ((a.el[m] & a.key_mask) < k) l = m + 1; else h = m;
+      if (key_of(a.el[m], a.key) < k) l = m + 1; else h = m;
     }
     int64_t h2 = p;
     while (l < h2) {
@@ -767,20 +803,34 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   const Win win{lim->window_us, sh, 0, pk.Bq > 0, pk, dt.ts};
 
   const uint64_t user_mask = ((uint64_t(1) << pk.Bu) - 1) << pk.SK;
+  const bool app_level = lim->app_scope != 0;
   uint64_t *in = A, *out = B;
   for (int k = 0; k < nd; ++k) {
     const uint32_t mask = (1u << dig[k].width) - 1u;
     const int shift = pk.SK + dig[k].shift;
+    if (k == n_user && app_level) {
+      // user test on the user order, then back to stream order for the app passes
+      if (cnt_user) {
+        CountArgs ca{in, L.N, KeySel{user_mask, false, pk.SK, pk.Bu, 1u}, win, cnt_user};
+        hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
+      }
+      ScatterArgs ua{in, out, L.N, 0, 0, nullptr, 0, lim->t_user, user_mask, win};
+      hipLaunchKernelGGL(k_thr_user_unsort, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s,
+                         ua);
+      uint64_t *tmp = in;
+      in = out;
+      out = tmp;
+    }
     if (k > 0)
       hipLaunchKernelGGL(k_radix_hist, dim3(L.tiles), dim3(kThreads), 0, s, in, L.N, shift, mask,
                          hist, L.tiles);
     (void)exclusive_scan(hist, int64_t(mask + 1) * L.tiles, part, s);
-    if (k == n_user && cnt_user) {
-      CountArgs ca{in, L.N, user_mask, win, cnt_user};
+    if (k == n_user && cnt_user && !app_level) {
+      CountArgs ca{in, L.N, KeySel{user_mask, false, pk.SK, pk.Bu, 1u}, win, cnt_user};
       hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
     }
     ScatterArgs sa{in, out, L.N, shift, mask, hist, L.tiles, lim->t_user, user_mask, win};
-    if (k == n_user)
+    if (k == n_user && !app_level)
       hipLaunchKernelGGL(k_radix_scatter<true>, dim3(L.tiles), dim3(kThreads), 0, s, sa);
     else
       hipLaunchKernelGGL(k_radix_scatter<false>, dim3(L.tiles), dim3(kThreads), 0, s, sa);
@@ -797,15 +847,18 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
                        bmask, hist, L.tiles);
     (void)exclusive_scan(hist, int64_t(bmask + 1) * L.tiles, part, s);
     uint32_t *words = reinterpret_cast<uint32_t *>(out);  // the free sort buffer
-    AppTestArgs aa{in, L.N, tapp, t->n_apps, win, bs, bmask, hist, L.tiles, words};
+    const KeySel app_key{((uint64_t(1) << pk.Bk) - 1) << pk.SK, app_level, pk.SK, pk.Bu,
+                         uint32_t(t->n_users)};
+    AppTestArgs aa{in, L.N, app_key, tapp, t->n_apps, win, bs, bmask, hist, L.tiles, words};
     hipLaunchKernelGGL(k_thr_apptest, dim3(L.tiles), dim3(kThreads), 0, s, aa);
     const int chunks = bs > kUnsortBits ? 1 << (bs - kUnsortBits) : 1;
     UnsortArgs ua{words, hist, L.tiles, n_buckets, L.N, bs, chunks, rrw};
     hipLaunchKernelGGL(k_thr_unsort, dim3(n_buckets * chunks), dim3(1024), 0, s, ua);
   }
   if (cnt_app) {
-    const uint64_t key_mask = ((uint64_t(1) << pk.Bk) - 1) << pk.SK;
-    CountArgs ca{in, L.N, key_mask, win, cnt_app};
+    const KeySel app_key{((uint64_t(1) << pk.Bk) - 1) << pk.SK, app_level, pk.SK, pk.Bu,
+                         uint32_t(t->n_users)};
+    CountArgs ca{in, L.N, app_key, win, cnt_app};
     hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
   }
 

@@ -26,11 +26,11 @@ def bits_of(bitmap, n):
     return ((b[idx // 32] >> (idx % 32).astype(np.uint32)) & 1).astype(np.uint8)
 
 
-def gpu_throttle(tr, W, t_user, t_app, overloaded=None, raw=True, counts=True):
+def gpu_throttle(tr, W, t_user, t_app, overloaded=None, raw=True, counts=True, app_scope=0):
     import paper_2411_15997_amd as fs
     dt = fs.DeviceTrace(tr)
-    out = fs.fs_throttle(dt, fs.make_limits(W, t_user, t_app), overloaded=overloaded, raw=raw,
-                         want_reason=True, want_counts=counts)
+    out = fs.fs_throttle(dt, fs.make_limits(W, t_user, t_app, app_scope), overloaded=overloaded,
+                         raw=raw, want_reason=True, want_counts=counts)
     n = tr.n
     res = dict(reason=out.reason.cpu().numpy()[:n], bitmap=out.bitmap.cpu().numpy().view(np.uint32))
     if counts:

@@ -11,9 +11,10 @@ import paper_2411_15997_amd as fs
 pytestmark = pytest.mark.gpu
 
 
-def _check(tr, W, tu, ta, overloaded=None, raw=True, counts=True):
-    g = gpu_throttle(tr, W, tu, ta, overloaded, raw, counts)
-    o = oracle.throttle(tr, W, tu, ta, overloaded=overloaded, raw=raw, counts=counts)
+def _check(tr, W, tu, ta, overloaded=None, raw=True, counts=True, app_scope=0):
+    g = gpu_throttle(tr, W, tu, ta, overloaded, raw, counts, app_scope)
+    o = oracle.throttle(tr, W, tu, ta, overloaded=overloaded, raw=raw, counts=counts,
+                        app_scope=app_scope)
     bad = np.nonzero(g["reason"] != o.reason)[0]
     assert bad.size == 0, f"reason mismatch at {bad[:10]}: gpu {g['reason'][bad[:10]]} oracle {o.reason[bad[:10]]}"
     assert (bits_of(g["bitmap"], tr.n) == bits_of(o.bitmap, tr.n)).all()
@@ -110,3 +111,45 @@ def test_coarse_time_field(jump_bits):
     say("throttle coarse time", jump_bits, int(ts[-1]).bit_length())
     _check(tr, W, 2, [1, 2, 3])
     _check(tr, W, 2**31 - 1, [0, 4, 1], raw=False)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_app_level_limit_random(seed):
+    # The application limit counted per application over all users of a replica.
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(1, 9000))
+    tr = random_trace(rng, n, int(rng.integers(1, 40)), int(rng.integers(1, 6)),
+                      int(rng.integers(1, 20000)), multi=True, n_replicas=int(rng.integers(1, 5)))
+    W = int(rng.integers(1, 5000))
+    tu = int(rng.integers(0, 30)) if seed % 2 else 2 ** 31 - 1
+    ta = rng.integers(0, 60, size=tr.n_apps).tolist()
+    say("throttle app-level random", seed, tr.n)
+    _check(tr, W, tu, ta, app_scope=1)
+    ov = rng.integers(0, 2, size=tr.n).astype(np.uint8)
+    _check(tr, W, tu, ta, overloaded=ov, raw=False, app_scope=1)
+    _check(tr, W, tu, ta, raw=False, counts=False, app_scope=1)
+
+
+def test_app_level_limit_ragged_sizes():
+    rng = np.random.default_rng(13)
+    for n in (1, 2, 33, 64, 65, 4097):
+        tr = random_trace(rng, n, 3, 2, 50, multi=True)
+        _check(tr, 10, 2, [3, 5], app_scope=1)
+        _check(tr, 10, 2**31 - 1, [3, 5], raw=False, counts=False, app_scope=1)
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c3_throttle", dict(records=1_000_003)),
+    ("c5_tenant", dict(records=300_007, users=30_000)),
+])
+def test_app_level_limit_workloads(name, kw):
+    wl, tr = workload_trace(name, **kw)
+    # Per-application limits at the median of each application's window count, so that
+    # the app test refuses a good share of the first calls.
+    big = [2 ** 31 - 1] * tr.n_apps
+    cnt = oracle.throttle(tr, wl.window_us, wl.t_user, big, app_scope=1).cnt_app
+    ta = [int(np.median(cnt[tr.app == a])) if (tr.app == a).any() else 0
+          for a in range(tr.n_apps)]
+    say("throttle app-level", name, tr.n)
+    g, o = _check(tr, wl.window_us, wl.t_user, ta, app_scope=1)
+    assert (o.reason == 2).sum() > tr.n // 100

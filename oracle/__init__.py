@@ -70,6 +70,8 @@ def lib():
         L = C.CDLL(LIB)
         L.fso_coef_from_expectations.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
                                                  C.c_void_p, C.c_int64, C.c_void_p]
+        L.fso_weights_from_history.argtypes = [C.POINTER(_Trace), C.c_int32, C.c_int64,
+                                                C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
         L.fso_cost.argtypes = [C.POINTER(_Trace), C.c_int32, C.c_int64, C.c_void_p, C.c_int64,
                                C.c_void_p, C.c_void_p]
         L.fso_throttle.argtypes = [C.POINTER(_Trace), C.c_int64, C.c_int32, C.c_void_p, C.c_void_p,
@@ -130,6 +132,25 @@ def coef_from_expectations(e_in, e_sys, e_out, K=1024):
     _check(lib().fso_coef_from_expectations(A, J, _p(e_in), _p(e_sys), _p(e_out), K, _p(coef)),
            "fso_coef_from_expectations")
     return coef
+
+
+@dataclass
+class HistoryResult:
+    stats: np.ndarray   # [A][J][5] records, first calls, sum L_I, sum L_S, sum L_O
+    coef: np.ndarray    # [A][J][3] Q16
+    t_app: np.ndarray   # [A]
+
+
+def weights_from_history(tr, n_stages, K=1024, base_limit=30):
+    """Eq. 1 coefficients and per-app limits derived from a historical trace."""
+    t = _TraceRef(tr)
+    A = tr.n_apps
+    res = HistoryResult(np.zeros((A, n_stages, 5), np.int64), np.zeros((A, n_stages, 3), np.int64),
+                        np.zeros(A, np.int32))
+    _check(lib().fso_weights_from_history(C.byref(t.s), int(n_stages), int(K), int(base_limit),
+                                          _p(res.stats), _p(res.coef), _p(res.t_app)),
+           "fso_weights_from_history")
+    return res
 
 
 def cost(tr, coef, prio=None, coef_per_replica=False, prio_per_replica=False):

@@ -3,6 +3,8 @@
 //
 // Written for a reader holding the paper.  Every function follows one passage:
 //   fso_coef_from_expectations  Eq. 1 and the token-class weights (Sec. 4, WSC)
+//   fso_weights_from_history    Eq. 1 from a historical trace's sample means, and the app
+//                               limit scaled by the mean calls per interaction (Sec. 4)
 //   fso_cost                    Eq. 2, one term of the sum (one LLM call), Alg. 1 charge
 //   fso_throttle                Alg. 1 monitoring stream: counting, OIT limit checks, the
 //                               interaction exemption (Sec. 4, OIT)
@@ -349,6 +351,112 @@ int fso_coef_from_expectations(int32_t n_apps, int32_t n_stages, const double *e
       }
     }
   return FSO_OK;
+}
+
+namespace {
+
+// round_half_even(num / den) for den > 0, exact.
+unsigned __int128 div_round_half_even(unsigned __int128 num, unsigned __int128 den) {
+  unsigned __int128 q = num / den, r = num % den;
+  if (2 * r > den || (2 * r == den && (q & 1))) ++q;
+  return q;
+}
+
+}  // namespace
+
+int fso_weights_from_history(const fso_trace *t, int32_t n_stages, int64_t K, int32_t base_limit,
+                             int64_t *stats, int64_t *coef, int32_t *t_app) {
+  if (n_stages < 1 || n_stages > 4096 || K < 1 || K > (int64_t(1) << 20) || base_limit < 0 ||
+      !stats)
+    return FSO_E_ARG;
+  // Only the fields read here are checked: app, call and the token counts.
+  int code = validate_trace(t, kLengths);
+  if (code == FSO_E_ARG) return code;
+  if (t->rep_off[t->n_replicas] >= (int64_t(1) << 36)) return FSO_E_ARG;
+  const int32_t A = t->n_apps, J = n_stages;
+  enum { kN, kFirst, kIn, kSys, kOut };
+  std::vector<int64_t> st(size_t(A) * J * 5, 0);
+  // The history's records per (app, stage): how many, how many first calls, token sums.
+  for (int32_t r = 0; r < t->n_replicas; ++r) {
+    Replica rp = replica(t, r);
+    for (int64_t i = 0; i < rp.n; ++i) {
+      int64_t g = rp.base + i;
+      int32_t a = t->app[g];
+      int64_t li = t->len_in[g], lo = t->len_out[g], ls = t->len_sys ? t->len_sys[g] : 0;
+      bool bad = a < 0 || a >= A || (t->call && t->call[g] < 0) || li < 0 || li >= kLenLimit ||
+                 lo < 0 || lo >= kLenLimit || ls < 0 || ls >= kLenLimit;
+      if (bad) {
+        code = worse(code, FSO_E_RANGE);
+        continue;
+      }
+      int32_t j = t->call ? std::min(t->call[g], J - 1) : 0;
+      int64_t *s = &st[(size_t(a) * J + j) * 5];
+      s[kN] += 1;
+      s[kFirst] += is_first_call(t, g) ? 1 : 0;
+      s[kIn] += li;
+      s[kSys] += ls;
+      s[kOut] += lo;
+    }
+  }
+  std::copy(st.begin(), st.end(), stats);
+  // Eq. 1's weighted token sum D of a group of n records: w = D / n.
+  const int64_t cls[3] = {1, 2, 1};
+  auto D_of = [&](const int64_t *s) { return cls[0] * s[kIn] + cls[1] * s[kSys] + cls[2] * s[kOut]; };
+  int64_t all_n = 0, all_D = 0;
+  std::vector<int64_t> app_n(A, 0), app_D(A, 0), app_first(A, 0);
+  for (int32_t a = 0; a < A; ++a)
+    for (int32_t j = 0; j < J; ++j) {
+      const int64_t *s = &st[(size_t(a) * J + j) * 5];
+      app_n[a] += s[kN];
+      app_D[a] += D_of(s);
+      app_first[a] += s[kFirst];
+    }
+  for (int32_t a = 0; a < A; ++a) {
+    all_n += app_n[a];
+    all_D += app_D[a];
+  }
+  for (int32_t a = 0; a < A; ++a) {
+    for (int32_t j = 0; coef && j < J; ++j) {
+      const int64_t *s = &st[(size_t(a) * J + j) * 5];
+      int64_t n = s[kN], D = D_of(s);
+      if (n == 0 || D == 0) {  // too little history: pool the app's stages, then all apps
+        n = app_n[a];
+        D = app_D[a];
+      }
+      if (n == 0 || D == 0) {
+        n = all_n;
+        D = all_D;
+      }
+      if (n == 0 || D == 0) {  // no tokens anywhere: w_aj = K
+        n = 1;
+        D = K;
+      }
+      for (int x = 0; x < 3; ++x) {
+        unsigned __int128 num = (unsigned __int128)(int64_t(65536) * K * cls[x]) * uint64_t(n);
+        unsigned __int128 c = div_round_half_even(num, uint64_t(D));
+        if (c >= (unsigned __int128)kCoefLimit) {
+          code = worse(code, FSO_E_RANGE);
+          c = 0;
+        }
+        coef[(size_t(a) * J + j) * 3 + x] = int64_t(c);
+      }
+    }
+    if (t_app) {
+      // mean LLM calls per interaction of app a = records / first calls, rounded up
+      int64_t lim = base_limit;
+      if (app_first[a] > 0) {
+        unsigned __int128 num = (unsigned __int128)uint64_t(base_limit) * uint64_t(app_n[a]);
+        unsigned __int128 v = (num + uint64_t(app_first[a]) - 1) / uint64_t(app_first[a]);
+        if (v > (unsigned __int128)INT32_MAX) {
+          code = worse(code, FSO_E_RANGE);
+          v = 0;
+        }
+        lim = int64_t(v);
+      }
+      t_app[a] = int32_t(lim);
+    }
+  }
+  return code;
 }
 
 int fso_cost(const fso_trace *t, int32_t n_stages, int64_t coef_rep_stride, const int64_t *coef,

@@ -35,6 +35,24 @@ int fso_coef_from_expectations(int32_t n_apps, int32_t n_stages, const double *e
                                const double *e_sys, const double *e_out, int64_t K,
                                int64_t *coef /* [A][J][3] */);
 
+/* Offline derivation from a historical trace (Eq. 1 with the expectations taken as
+ * the history's sample means; the OIT app limit scaled by the app's mean number of
+ * LLM calls per interaction).  Over all replicas, with stage j = min(call, J - 1):
+ *   stats[a][j] = {records, first calls, sum L_I, sum L_S, sum L_O}
+ *   coef[a][j][x] = round_half_even(2^16 K x_weight / w_aj), w_aj = D / n, computed
+ *                   exactly as round_half_even(2^16 K x_weight n / D) with
+ *                   n = records, D = sum(1 L_I + 2 L_S + 1 L_O) of the group;
+ *                   a group with n = 0 or D = 0 takes its app's pooled (n, D) over all
+ *                   stages, then the whole history's, and w_aj = K when all are empty;
+ *   t_app[a]     = ceil(base_limit * records_a / first_calls_a), base_limit when the
+ *                   app has no first call.
+ * K in [1, 2^20], base_limit >= 0, fewer than 2^36 records.  coef and t_app may be
+ * NULL.  FSO_E_RANGE for an id or length out of range, a coefficient >= 2^36 or a
+ * limit above INT32_MAX. */
+int fso_weights_from_history(const fso_trace *t, int32_t n_stages, int64_t K, int32_t base_limit,
+                             int64_t *stats /* [A][J][5] */, int64_t *coef /* [A][J][3] */,
+                             int32_t *t_app /* [A] */);
+
 /* Eq. 2, one LLM call: cost = floor(E_u * (c_in*L_I + c_sys*L_S + c_out*L_O) / 2^8). */
 int fso_cost(const fso_trace *t, int32_t n_stages, int64_t coef_rep_stride, const int64_t *coef,
              int64_t prio_rep_stride, const int32_t *prio, int64_t *cost);

@@ -26,13 +26,17 @@ HBM_PEAK_GBS = 8000.0
 #   scheduler ts 8 + user 4 + link 4 + tokens 4 + cost 8 + reason 1/8 + status 1
 #             + admit_step 4 + admit_seq 4                                      = 37.125
 #   metrics   status 1 + admit_step 4 + ts 8 + user 4 + cost 8                  = 25
-ALGO_BYTES = {"cost": 20.0, "throttle": 20.125, "init": 0.0, "schedule": 37.125, "metrics": 25.0}
+#   history   app 4 + call 4 + lengths 8 (+ sys 4) read once (weights from a history;
+#             not part of the step, timed on its own)                         = 16 (20)
+ALGO_BYTES = {"cost": 20.0, "throttle": 20.125, "init": 0.0, "schedule": 37.125, "metrics": 25.0,
+              "history": 16.0}
 CSRC = os.path.join(ROOT, "paper_2411_15997_amd", "csrc")
 STAGE_SRC = {
     "cost": ["fs_cost.hip"],
     "throttle": ["fs_throttle.hip"],
     "schedule": ["fs_sched_onchip.hip", "fs_sched.hip", "fs_sched_common.h"],
     "metrics": ["fs_metrics.hip"],
+    "history": ["fs_history.hip"],
 }
 
 # HBM traffic of a stage's main kernel from rocprofv3 --pmc runs: FETCH_SIZE and
@@ -92,7 +96,8 @@ def main():
     ap.add_argument("--workload", default="c2_replicas")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
-    ap.add_argument("--stage-only", default="", help="time only this stage (profiling runs)")
+    ap.add_argument("--stage-only", default="", help="time only this stage (profiling runs): "
+                    "cost, throttle, schedule, metrics or history")
     ap.add_argument("--policy", default="fs", choices=["fs", "wsc_only", "vtc", "rpm"],
                     help="the paper's policy (default) or one it compares with")
     ap.add_argument("--calib-copy", action="store_true",
@@ -144,6 +149,10 @@ def main():
     stages = ["throttle"] if throttle_only else ["cost", "throttle", "init", "schedule", "metrics"]
     if args.stage_only:
         stages = [args.stage_only]
+    J = wl.n_stages
+    # bytes per record the history pass reads: app, lengths, call and system tokens if present
+    ALGO_BYTES["history"] = 12.0 + (4.0 if tr.call is not None else 0.0) + (
+        4.0 if tr.len_sys is not None else 0.0)
 
     def step(evs):
         i = 0
@@ -163,6 +172,9 @@ def main():
         if "metrics" in stages:
             evs[i].record(); i += 1
             fs.fs_fairness_metrics(dt, cost, out, eng, 0, metrics, mws, check=False)
+        if "history" in stages:
+            evs[i].record(); i += 1
+            fs.fs_weights_from_history(dt, J, K=wl.weight_K, base_limit=30, err=err, check=False)
         evs[i].record()
 
     # the throttle's raw reasons feed the scheduler (same buffers every step)
@@ -215,9 +227,13 @@ def main():
         result["value"] = decisions / (ms_per_step / 1000.0)
         result["unit"] = "decisions/s"
         result["decisions"] = decisions
-    else:
+    elif "throttle" in stage_ms:
         result["value"] = N / (stage_ms["throttle"] / 1000.0)
         result["unit"] = "throttle evals/s"
+    else:  # a profiling run of one other stage
+        only = next(iter(stage_ms))
+        result["value"] = N / (stage_ms[only] / 1000.0)
+        result["unit"] = f"records/s through {only}"
     if "throttle" in stage_ms:
         result["throttle_evals_per_s"] = N / (stage_ms["throttle"] / 1000.0)
     result["requests_per_s"] = N / (ms_per_step / 1000.0)
@@ -245,6 +261,23 @@ def main():
                              "served_users_pct": round(float(np.mean(mh["served_users_pct"])), 3),
                              "delayed_users_pct": round(float(np.mean(mh["delayed_users_pct"])), 3),
                              "jain": round(float(np.mean(mh["jain"])), 5)}
+    if not throttle_only and not args.stage_only:
+        # weights and app limits derived from this trace as a history (timed on its own)
+        hist = []
+        for it in range(args.warmup + args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fs.fs_weights_from_history(dt, J, K=wl.weight_K, base_limit=30, err=err, check=False)
+            e1.record()
+            if it >= args.warmup:
+                hist.append((e0, e1))
+        torch.cuda.synchronize()
+        fs.sync_check(err, "history")
+        hms = float(np.mean([a.elapsed_time(b) for a, b in hist]))
+        hgbs = ALGO_BYTES["history"] * N / (hms / 1000.0) / 1e9
+        result["extra_stages"] = {"history": {"ms": round(hms, 4), "achieved_gbs": round(hgbs, 2),
+                                              "frac": round(hgbs / HBM_PEAK_GBS, 4),
+                                              "bytes_per_record": ALGO_BYTES["history"]}}
     if not args.no_cpu_baseline and not args.stage_only:
         result["cpu_baseline"] = cpu_baseline(wl, tr, args.cpu_threads, throttle_only,
                                               args.policy)

@@ -233,6 +233,31 @@ fs_status fs_coef_from_expectations(int32_t n_apps, int32_t n_stages, const doub
                                     const double *e_sys_h, const double *e_out_h, int64_t K,
                                     int64_t *coef_h);
 
+/* Offline derivation of the weights and app limits from a historical trace (Eq. 1 with
+ * each expectation taken as the history's sample mean; Sec. 4, OIT: the app limit scaled
+ * by the app's mean number of LLM calls per interaction).  Over every record of `hist`
+ * (all replicas pooled), with stage j = min(call, n_stages - 1):
+ *   stats[a][j][5] int64 = {records, first calls (call == 0), sum L_I, sum L_S, sum L_O}
+ *   coef [a][j][3] int64 = round-half-even(2^16 K x / w_aj) for x = 1, 2, 1 (input,
+ *          system, output), w_aj = D / n the group's mean of L_I + 2 L_S + L_O,
+ *          evaluated exactly as round-half-even(2^16 K x n / D).  A group with no
+ *          records or no tokens takes its app's stages pooled, then the whole history,
+ *          and w_aj = K when there are no tokens at all.  The table plugs into
+ *          fs_weights (coef_rep_stride 0, n_stages as here).
+ *   t_app[a] int32 = ceil(base_limit * records_a / first calls_a) (base_limit when app a
+ *          has no first call), usable as fs_limits.t_app_h after a copy to the host.
+ * Device arrays; coef and t_app may be NULL, stats is required (it is cleared by the
+ * call).  ws: device workspace of at least fs_history_workspace(hist, n_stages) bytes,
+ * 256-byte aligned (may be NULL when that size is 0), else FS_E_WORKSPACE.  K in [1, 2^20], base_limit >= 0, n_stages in [1, 4096],
+ * fewer than 2^36 records, else FS_E_ARG.  Device errors (err): FS_E_RANGE for an app,
+ * call or token count out of range (the record is skipped), a coefficient >= 2^36 or a
+ * limit above INT32_MAX.  The trace's ts_us and user are not read. */
+size_t fs_history_workspace(const fs_trace *hist, int32_t n_stages);
+fs_status fs_weights_from_history(const fs_trace *hist, int32_t n_stages, int64_t K,
+                                  int32_t base_limit, int64_t *stats, int64_t *coef,
+                                  int32_t *t_app, void *ws, size_t ws_bytes, int32_t *err,
+                                  hipStream_t stream);
+
 /* Waits for `stream` and returns the device status word `err`. */
 fs_status fs_sync_status(hipStream_t stream, const int32_t *err);
 

@@ -80,6 +80,8 @@ def _lib():
         T = C.POINTER(fs_trace)
         sig = {
             "fs_cost": ([T, C.POINTER(fs_weights), P, P, S], I32),
+            "fs_history_workspace": ([T, I32], SZ),
+            "fs_weights_from_history": ([T, I32, I64, I32, P, P, P, P, SZ, P, S], I32),
             "fs_throttle_workspace": ([T], SZ),
             "fs_throttle": ([T, C.POINTER(fs_limits), P, U32, P, P, P, P, P, SZ, P, S], I32),
             "fs_state_bytes": ([T], SZ),
@@ -103,7 +105,7 @@ def _lib():
     return _LIB
 
 
-EXPORTED = ("fs_cost", "fs_throttle_workspace", "fs_throttle", "fs_state_bytes", "fs_state_init",
+EXPORTED = ("fs_cost", "fs_history_workspace", "fs_weights_from_history", "fs_throttle_workspace", "fs_throttle", "fs_state_bytes", "fs_state_init",
             "fs_schedule_step", "fs_run_trace_workspace", "fs_run_trace", "fs_metrics_workspace",
             "fs_fairness_metrics", "fs_coef_from_expectations", "fs_sync_status",
             "fs_status_string")
@@ -206,6 +208,27 @@ def fs_cost(dt: DeviceTrace, weights, cost=None, err=None, check=True):
     if check:
         sync_check(err, "fs_cost")
     return cost
+
+
+def fs_weights_from_history(dt: DeviceTrace, n_stages, K=1024, base_limit=30, coef=True,
+                            limits=True, err=None, check=True):
+    """Eq. 1 coefficients [A][J][3] and app limits [A] from a historical trace on the
+    device; returns (stats [A][J][5], coef or None, t_app or None) as device tensors."""
+    torch = _torch()
+    A, J = dt.n_apps, int(n_stages)
+    stats = _empty((A, J, 5), torch.int64, dt.device)
+    coef_t = _empty((A, J, 3), torch.int64, dt.device) if coef else None
+    t_app = _empty((A,), torch.int32, dt.device) if limits else None
+    err = err_word(dt.device) if err is None else err
+    wsb = int(_lib().fs_history_workspace(dt.ref, J))
+    ws = _empty((wsb,), torch.uint8, dt.device) if wsb > 0 else None
+    _check(_lib().fs_weights_from_history(dt.ref, J, int(K), int(base_limit), _ptr(stats),
+                                          _ptr(coef_t), _ptr(t_app), _ptr(ws), wsb, _ptr(err),
+                                          _stream()),
+           "fs_weights_from_history")
+    if check:
+        sync_check(err, "fs_weights_from_history")
+    return stats, coef_t, t_app
 
 
 def make_limits(window_us, t_user, t_app, app_scope=0):

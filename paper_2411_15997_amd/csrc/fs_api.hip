@@ -130,6 +130,27 @@ fs_status fs_coef_from_expectations(int32_t n_apps, int32_t n_stages, const doub
   return FS_OK;
 }
 
+size_t fs_history_workspace(const fs_trace *t, int32_t n_stages) {
+  if (check_trace(t, false) != FS_OK || n_stages < 1 || n_stages > 4096) return 0;
+  return history_workspace_bytes(t, n_stages);
+}
+
+fs_status fs_weights_from_history(const fs_trace *t, int32_t n_stages, int64_t K,
+                                  int32_t base_limit, int64_t *stats, int64_t *coef,
+                                  int32_t *t_app, void *ws, size_t ws_bytes, int32_t *err,
+                                  hipStream_t stream) {
+  fs_status s = check_trace(t, true);
+  if (s != FS_OK) return s;
+  if (n_stages < 1 || n_stages > 4096 || K < 1 || K > (int64_t(1) << 20) || base_limit < 0 ||
+      !stats || !err || n_records(t) >= history_max_records())
+    return FS_E_ARG;
+  const size_t need = history_workspace_bytes(t, n_stages);
+  if (need > 0 && (!ws || !aligned(ws) || ws_bytes < need)) return FS_E_WORKSPACE;
+  // the first kernel clears err
+  return hip_status(
+      launch_history(t, n_stages, K, base_limit, stats, coef, t_app, ws, err, stream));
+}
+
 fs_status fs_cost(const fs_trace *t, const fs_weights *w, int64_t *cost, int32_t *err,
                   hipStream_t stream) {
   fs_status s = check_trace(t, true);

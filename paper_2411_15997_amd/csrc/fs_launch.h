@@ -25,6 +25,12 @@ hipError_t launch_metrics(const fs_trace *t, const int64_t *cost, const fs_outpu
                           hipStream_t stream);
 size_t metrics_workspace_bytes(const fs_trace *t);
 
+size_t history_workspace_bytes(const fs_trace *t, int32_t n_stages);
+hipError_t launch_history(const fs_trace *t, int32_t n_stages, int64_t K, int32_t base_limit,
+                          int64_t *stats, int64_t *coef, int32_t *t_app, void *ws, int32_t *err,
+                          hipStream_t stream);
+int64_t history_max_records();
+
 hipError_t launch_zero_i32(int32_t *p, hipStream_t stream);
 
 // Device-wide exclusive prefix sum of n uint32 values in place; `part` needs

@@ -80,3 +80,24 @@ def test_synchronous_argument_errors_need_no_gpu():
     lim2 = fs.fs_limits(1000, 5, t_app2.ctypes.data)
     assert lib.fs_throttle(C.byref(t2), C.byref(lim2), None, 1, 16, None, None, None, 256, 0,
                            16, None) == fs.FS_E_WORKSPACE
+    lim3 = fs.fs_limits(1000, 5, t_app2.ctypes.data, 2)   # app_scope must be 0 or 1
+    assert lib.fs_throttle(C.byref(t2), C.byref(lim3), None, 1, 16, None, None, None, 256,
+                           1 << 20, 16, None) == fs.FS_E_ARG
+
+
+def test_history_arguments_and_workspace_need_no_gpu():
+    lib = fs._lib()
+    rep = np.array([0, 4000], np.int64)
+    t = fs.fs_trace(1, 2, 2, rep.ctypes.data, 16, 16, 16, 16, None, None, None, 16, None, 16)
+    ws = lib.fs_history_workspace(C.byref(t), 3)
+    # one partial table row (2 apps x 3 stages x 5 int64) per work-group of the LDS path
+    assert ws > 0 and ws % (2 * 3 * 5 * 8) == 0
+    assert lib.fs_history_workspace(C.byref(t), 0) == 0
+    assert lib.fs_weights_from_history(C.byref(t), 3, 0, 30, 256, None, None, 256, ws, 16,
+                                       None) == fs.FS_E_ARG          # K = 0
+    assert lib.fs_weights_from_history(C.byref(t), 3, 1024, -1, 256, None, None, 256, ws, 16,
+                                       None) == fs.FS_E_ARG          # negative base limit
+    assert lib.fs_weights_from_history(C.byref(t), 3, 1024, 30, None, None, None, 256, ws, 16,
+                                       None) == fs.FS_E_ARG          # no stats buffer
+    assert lib.fs_weights_from_history(C.byref(t), 3, 1024, 30, 256, None, None, 256, ws - 1,
+                                       16, None) == fs.FS_E_WORKSPACE

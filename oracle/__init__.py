@@ -44,7 +44,7 @@ class _Engine(C.Structure):
                 ("flags", C.c_uint32)]
 
 
-FSO_FCFS, FSO_BLIND = 1, 2
+FSO_FCFS, FSO_BLIND, FSO_LITERAL = 1, 2, 4
 
 
 class _Outputs(C.Structure):

@@ -161,6 +161,16 @@ struct Simulation {
     // Every queued request, by arrival (the first-come, first-served order).
     std::set<int64_t> arrival_order;
     const bool fcfs = (e.flags & FSO_FCFS) != 0, blind = (e.flags & FSO_BLIND) != 0;
+    // Literal engine (Alg. 1 execution stream as written): the batch B of running calls
+    // in admission order with the step of their last output token; each holds its
+    // L_I + L_S + L_O tokens of KV cache from admission to finish, and is charged at
+    // finish.
+    const bool literal = (e.flags & FSO_LITERAL) != 0;
+    struct Running {
+      int64_t rec, fin;
+    };
+    std::vector<Running> batch;
+    int64_t kv_used = 0;
     std::vector<uint8_t> served(n, 0), aborted(n, 0), dropped(n, 0);
     std::vector<int64_t> next_call(n, -1);
     if (t->call)
@@ -195,8 +205,17 @@ struct Simulation {
 
     while (true) {
       if (max_steps >= 0 && s >= max_steps) break;
-      if (nxt == n && X.empty()) break;
-      if (X.empty() && nxt < n) {
+      if (nxt == n && X.empty() && batch.empty()) break;
+      if (X.empty() && literal) {
+        // Nothing queued: nothing happens before the next arrival or the next finish.
+        int64_t target = nxt < n ? t->ts_us[G(nxt)] / tau : INT64_MAX;
+        for (const Running &b : batch) target = std::min(target, b.fin);
+        if (max_steps >= 0 && target > max_steps) target = max_steps;
+        if (target > s) {
+          s = target;
+          if (max_steps >= 0 && s >= max_steps) break;
+        }
+      } else if (X.empty() && nxt < n) {
         // Nothing queued: the steps before the next arrival only pay back debt.
         int64_t target = t->ts_us[G(nxt)] / tau;
         if (max_steps >= 0 && target > max_steps) target = max_steps;
@@ -251,9 +270,11 @@ struct Simulation {
         }
       }
 
-      // Execution stream: admit least-served users while the step has budget.
+      // Execution stream: admit least-served users while the step has budget (literal
+      // engine: while the chosen request's tokens fit in the free KV cache, or nothing
+      // runs at all).
       int64_t budget = C + debt;
-      while (budget > 0 && !X.empty()) {
+      while ((literal || budget > 0) && !X.empty()) {
         bool tier0 = !T0.empty();
         int32_t k;
         int64_t r;
@@ -273,6 +294,7 @@ struct Simulation {
           if (check && !is_first_call(t, G(r))) return fail("queue front is a later call", r);
           if (check && u[k] != X.begin()->first) return fail("argmin key stale", r);
         }
+        if (literal && !batch.empty() && kv_used + tokens(t, G(r)) > C) break;
         if (tier0) {
           ready[k].erase(r);
           if (ready[k].empty()) T0.erase({u[k], k});
@@ -287,16 +309,23 @@ struct Simulation {
         int64_t tok = tokens(t, G(r));
         budget -= tok;
         backlog -= tok;
-        int64_t before = u[k];
-        int64_t after = before + cost[G(r)];
-        if (after >= kValueLimit) return FSO_E_OVERFLOW;
-        set_counter(k, after);
-        if (check && after < before) return fail("counter decreased", r);
-        if (check && !fcfs && !tier0 && !X.empty() && after - X.begin()->first > cost[G(r)])
-          return fail("served user ends more than one cost above the minimum", r);
+        if (literal) {
+          // prefill now (its first output token), one more token per step, charge at finish
+          int64_t lo = t->len_out[G(r)];
+          batch.push_back({r, s + std::max<int64_t>(lo, 1) - 1});
+          kv_used += tok;
+        } else {
+          int64_t before = u[k];
+          int64_t after = before + cost[G(r)];
+          if (after >= kValueLimit) return FSO_E_OVERFLOW;
+          set_counter(k, after);
+          if (check && after < before) return fail("counter decreased", r);
+          if (check && !fcfs && !tier0 && !X.empty() && after - X.begin()->first > cost[G(r)])
+            return fail("served user ends more than one cost above the minimum", r);
+          if (out->counter_after) out->counter_after[G(r)] = after;
+        }
         if (out->admit_step) out->admit_step[G(r)] = int32_t(s);
         if (out->admit_seq) out->admit_seq[G(r)] = int32_t(seq);
-        if (out->counter_after) out->counter_after[G(r)] = after;
         ++seq;
         if (emptied) last_exit = k;
         int64_t nc = next_call[r];
@@ -305,7 +334,27 @@ struct Simulation {
           make_ready(nc);
         }
       }
-      debt = std::min<int64_t>(budget, 0);
+      if (literal) {
+        // Decode: calls whose last output token falls in step s finish, in admission
+        // order; the user is charged the call's service (Eq. 2) and its KV is freed.
+        if (check && kv_used > C && batch.size() > 1) return fail("KV cache over capacity", -1);
+        std::vector<Running> still;
+        for (const Running &b : batch) {
+          if (b.fin != s) {
+            still.push_back(b);
+            continue;
+          }
+          int32_t k = t->user[G(b.rec)];
+          int64_t after = u[k] + cost[G(b.rec)];
+          if (after >= kValueLimit) return FSO_E_OVERFLOW;
+          set_counter(k, after);
+          if (out->counter_after) out->counter_after[G(b.rec)] = after;
+          kv_used -= tokens(t, G(b.rec));
+        }
+        batch.swap(still);
+      } else {
+        debt = std::min<int64_t>(budget, 0);
+      }
       if (!X.empty()) gap = std::max(gap, X.rbegin()->first - X.begin()->first);
       ++s;
     }
@@ -560,7 +609,7 @@ int fso_simulate(const fso_trace *t, const int64_t *cost, const uint8_t *exceed_
                  fso_outputs *out) {
   if (!e || !out || !out->status || !cost) return FSO_E_ARG;
   if (e->step_us <= 0 || e->cap_tokens <= 0 || e->cap_tokens > kCapLimit) return FSO_E_ARG;
-  if (e->flags & ~uint32_t(FSO_FCFS | FSO_BLIND)) return FSO_E_ARG;
+  if (e->flags & ~uint32_t(FSO_FCFS | FSO_BLIND | FSO_LITERAL)) return FSO_E_ARG;
   int code = validate_trace(t, kIds | kOrder | kChain | kLengths);
   if (code != FSO_OK) return code;
   int64_t N = t->rep_off[t->n_replicas];

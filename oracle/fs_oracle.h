@@ -77,8 +77,15 @@ int fso_throttle_scoped(const fso_trace *t, int64_t window_us, int32_t t_user,
  * every call against the limits (not only first calls) and drops the rest of an
  * interaction once one of its calls is dropped.  FSO_FCFS | FSO_BLIND with
  * overload_tokens = -1 is the request-rate-limit (RPM) policy the paper compares with. */
+/* FSO_LITERAL runs the execution stream as Alg. 1 writes it: an admitted call is
+ * prefilled in its admission step (its first output token), decodes one more output
+ * token per step and finishes in step admit + max(L_O, 1) - 1, when its user is charged
+ * the call's cost (Eq. 2); cap_tokens is then the KV-cache capacity: a call holds
+ * L_I + L_S + L_O tokens from admission to the end of its finish step, and the
+ * admissions of a step stop at the first chosen call that does not fit (a call runs
+ * alone when nothing else does).  Counters do not move between admissions. */
 typedef struct fso_engine { int64_t step_us, cap_tokens, overload_tokens; uint32_t flags; } fso_engine;
-enum { FSO_FCFS = 1, FSO_BLIND = 2 };
+enum { FSO_FCFS = 1, FSO_BLIND = 2, FSO_LITERAL = 4 };
 
 typedef struct fso_outputs {
   int8_t *status;             /* [N] 0 admitted, 1/2/3 blocked, -1 not processed (bounded run) */

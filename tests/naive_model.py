@@ -90,7 +90,8 @@ class Result:
     trace_of_counters: list = field(default_factory=list)  # (step, seq, {user: u}) per decision
 
 
-FCFS, BLIND = 1, 2  # engine flags: first come first served; interaction-blind limits
+FCFS, BLIND, LITERAL = 1, 2, 4  # engine flags: first come first served; interaction-blind
+# limits; the literal engine (prefill at admission, one output token per step, charge at finish)
 
 
 def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_states=False,
@@ -109,6 +110,7 @@ def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_sta
         dropped = [False] * n
         last_exit: Optional[int] = None
         debt = backlog = seq = gap = 0
+        running: List[list] = []        # literal engine: [record, last decode step], by admission
         nxt = 0
         s = 0
         G = lambda i: base + i
@@ -124,7 +126,7 @@ def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_sta
         while True:
             if 0 <= max_steps <= s:
                 break
-            if nxt == n and not queued:
+            if nxt == n and not queued and not running:
                 break
             # arrivals of step s (an idle step changes nothing but the debt)
             while nxt < n and int(tr.ts_us[G(nxt)]) // step_us <= s:
@@ -155,7 +157,8 @@ def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_sta
                     queued.append(i)
                     backlog += tok(i)
             budget = cap + debt
-            while budget > 0 and queued:
+            kv = sum(tok(i) for i, _ in running)
+            while (flags & LITERAL or budget > 0) and queued:
                 ready = ready_calls()
                 if flags & FCFS:  # the earliest queued request, whoever it belongs to
                     rcand = min(queued)
@@ -169,23 +172,39 @@ def simulate(tr, cost_arr, reason, step_us, cap, theta, max_steps=-1, record_sta
                     users = X()
                     k = min(users, key=lambda x: (u[x], x))
                     rcand = min(i for i in queued if int(tr.user[G(i)]) == k)
+                if flags & LITERAL and running and kv + tok(rcand) > cap:
+                    break                   # the chosen call does not fit in the KV cache
                 queued.remove(rcand)
                 served[rcand] = True
                 res.status[G(rcand)] = 0
                 budget -= tok(rcand)
                 backlog -= tok(rcand)
-                u[k] += int(cost_arr[G(rcand)])
-                if u[k] >= VALUE_LIMIT:
-                    raise OverflowError("counter overflow")
+                if flags & LITERAL:         # charged when its last output token is decoded
+                    running.append([rcand, s + max(int(tr.len_out[G(rcand)]), 1) - 1])
+                    kv += tok(rcand)
+                else:
+                    u[k] += int(cost_arr[G(rcand)])
+                    if u[k] >= VALUE_LIMIT:
+                        raise OverflowError("counter overflow")
+                    res.counter_after[G(rcand)] = u[k]
                 res.admit_step[G(rcand)] = s
                 res.admit_seq[G(rcand)] = seq
-                res.counter_after[G(rcand)] = u[k]
                 seq += 1
                 if k not in X():
                     last_exit = k
                 if record_states:
                     res.trace_of_counters.append((s, seq - 1, {x: u[x] for x in X()}, bool(ready), k))
-            debt = min(budget, 0)
+            if flags & LITERAL:
+                for rec, fin in running:
+                    if fin == s:
+                        kk = int(tr.user[G(rec)])
+                        u[kk] += int(cost_arr[G(rec)])
+                        if u[kk] >= VALUE_LIMIT:
+                            raise OverflowError("counter overflow")
+                        res.counter_after[G(rec)] = u[kk]
+                running = [x for x in running if x[1] != s]
+            else:
+                debt = min(budget, 0)
             xs = X()
             if xs:
                 gap = max(gap, max(u[x] for x in xs) - min(u[x] for x in xs))

@@ -213,8 +213,10 @@ def _run_both(tr, step_us, C, theta, W, t_user, t_app, coef, overloaded=None, fl
 
 
 # the default policy, first-come first-served order, interaction-blind limits, and both
-# (with overload_tokens = -1 the latter is the request-rate-limit policy)
-POLICY_FLAGS = (0, oracle.FSO_FCFS, oracle.FSO_BLIND, oracle.FSO_FCFS | oracle.FSO_BLIND)
+# (with overload_tokens = -1 the latter is the request-rate-limit policy); then the
+# literal engine under the default policy and under the rate-limit policy
+POLICY_FLAGS = (0, oracle.FSO_FCFS, oracle.FSO_BLIND, oracle.FSO_FCFS | oracle.FSO_BLIND,
+                oracle.FSO_LITERAL, oracle.FSO_LITERAL | oracle.FSO_FCFS | oracle.FSO_BLIND)
 
 
 def test_naive_equals_oracle_exhaustive_tiny():
@@ -245,6 +247,81 @@ def test_naive_equals_oracle_exhaustive_tiny():
                             _run_both(tr, 10, 2, theta, 15, 1, [0], coef, flags=flags)
                             count += 1
     assert count > 100
+
+
+def test_naive_equals_oracle_literal_engine_exhaustive():
+    """The literal engine on every 3-request trace over 2 users, arrival steps {0,1},
+    input tokens {1,3}, output tokens {0,2}, chained or not, at two KV capacities."""
+    coef = np.array([[[[1 << 16, 0, 3 << 16]]]], np.int64)
+    count = 0
+    for users in itertools.product(range(2), repeat=3):
+        for steps in itertools.product(range(2), repeat=3):
+            if list(steps) != sorted(steps):
+                continue
+            for toks in itertools.product((1, 3), repeat=3):
+                for outs in itertools.product((0, 2), repeat=3):
+                    for link in (False, True):
+                        n = 3
+                        call = np.zeros(n, np.int32); head = np.arange(n, dtype=np.int32)
+                        prev = np.full(n, -1, np.int32)
+                        if link and users[2] == users[0]:
+                            call[2], head[2], prev[2] = 1, 0, 0
+                        elif link:
+                            continue
+                        tr = Trace(1, 2, 1, np.array([0, n], np.int64),
+                                   np.asarray(steps, np.int64) * 10, np.asarray(users, np.int32),
+                                   np.zeros(n, np.int32), call, head, prev,
+                                   np.asarray(toks, np.int32), None, np.asarray(outs, np.int32))
+                        for kv in (4, 7):
+                            for flags in (oracle.FSO_LITERAL, oracle.FSO_LITERAL | oracle.FSO_FCFS):
+                                _run_both(tr, 10, kv, 1, 15, 1, [0], coef, flags=flags)
+                                count += 1
+    assert count > 500
+
+
+def test_literal_engine_closed_forms():
+    """Charge at finish (Alg. 1, execution stream): counters do not move between a step's
+    admissions, so the least-served user's whole queue goes first; a call holds its KV
+    tokens until its last output token; an oversized call runs alone."""
+    L = oracle.FSO_LITERAL
+    coef = np.array([[[[1 << 16, 0, 1 << 16]]]], np.int64)
+    # two users, three one-token requests each, all at step 0, ample KV
+    n = 6
+    users = np.array([0, 1, 0, 1, 0, 1], np.int32)
+    tr = Trace(1, 2, 1, np.array([0, n], np.int64), np.zeros(n, np.int64), users,
+               np.zeros(n, np.int32), None, None, None, np.ones(n, np.int32), None,
+               np.zeros(n, np.int32))
+    c = oracle.cost(tr, coef)
+    lit = oracle.simulate(tr, c, None, 10, 100, 10 ** 9, check=True, flags=L)
+    assert lit.admit_seq.tolist() == [0, 3, 1, 4, 2, 5]     # user 0's queue, then user 1's
+    assert lit.counter.tolist() == [3 << 16, 3 << 16]
+    eager = oracle.simulate(tr, c, None, 10, 100, 10 ** 9, check=True)
+    assert eager.admit_seq.tolist() == [0, 1, 2, 3, 4, 5]   # charged at admission: alternate
+    # one user, calls of 1 input + L_O output tokens, KV for one call at a time
+    outs = np.array([3, 1, 2, 5], np.int32)
+    n = 4
+    tr = Trace(1, 1, 1, np.array([0, n], np.int64), np.zeros(n, np.int64), np.zeros(n, np.int32),
+               np.zeros(n, np.int32), None, None, None, np.ones(n, np.int32), None, outs)
+    c = oracle.cost(tr, coef)
+    # KV of 1 token: every call is oversized and runs alone, starting the step after the
+    # previous one decoded its last token
+    r = oracle.simulate(tr, c, None, 10, 1, 10 ** 9, check=True, flags=L)
+    assert r.admit_step.tolist() == [0, 3, 4, 6]
+    assert r.counter_after.tolist() == np.cumsum(c).tolist()
+    assert r.steps.tolist() == [11]                          # the last call decodes in step 10
+    # KV of 6 (footprints 4, 2, 3, 6): calls 0 and 1 fit at step 0; call 1 finishes in
+    # step 0 and call 0 in step 2, so call 2 waits for step 3, call 3 for call 2's finish
+    r = oracle.simulate(tr, c, None, 10, 6, 10 ** 9, check=True, flags=L)
+    assert r.admit_step.tolist() == [0, 0, 3, 5]
+    assert r.counter_after.tolist() == [c[1] + c[0], c[1], c[0] + c[1] + c[2], int(np.sum(c))]
+    assert r.steps.tolist() == [10]
+    # an oversized call (10 tokens > KV 5) runs when nothing else does
+    tr2 = Trace(1, 1, 1, np.array([0, 3], np.int64), np.zeros(3, np.int64), np.zeros(3, np.int32),
+                np.zeros(3, np.int32), None, None, None, np.array([1, 8, 1], np.int32), None,
+                np.array([1, 2, 1], np.int32))
+    c2 = oracle.cost(tr2, coef)
+    r2 = oracle.simulate(tr2, c2, None, 10, 5, 10 ** 9, check=True, flags=L)
+    assert r2.admit_step.tolist() == [0, 1, 3]
 
 
 @pytest.mark.parametrize("seed", range(6))

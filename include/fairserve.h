@@ -115,7 +115,19 @@ typedef struct fs_limits {
  * FS_ENGINE_FCFS | FS_ENGINE_BLIND with overload_tokens = -1 is the per-user
  * request-rate-limit policy (RPM); the virtual token counter is the default policy with
  * equal coefficients for every app and no limits (t_user = t_app = INT32_MAX); the
- * paper's WSC-only ablation is the default policy with no limits. */
+ * paper's WSC-only ablation is the default policy with no limits.
+ *   FS_ENGINE_LITERAL  the execution stream as Alg. 1 writes it: an admitted call is
+ *                    prefilled in its admission step (its first output token), decodes
+ *                    one more output token per step and finishes in step
+ *                    admit + max(L_O, 1) - 1, when its user is charged its cost (charge at
+ *                    finish; counters do not move between a step's admissions).  cap_tokens
+ *                    is then the KV-cache capacity in tokens: a call holds L_I + L_S + L_O
+ *                    tokens from admission to the end of its finish step, and a step's
+ *                    admissions stop at the first chosen call that does not fit (a call
+ *                    runs alone when nothing else runs).  Finishes of a step are charged in
+ *                    admission order after its admissions; counter_after is the counter
+ *                    after the finish charge (-1 while the call runs).  Runs with all
+ *                    state in global memory; combines with FCFS and BLIND. */
 typedef struct fs_engine {
   int64_t step_us, cap_tokens, overload_tokens;
   uint32_t flags;
@@ -123,6 +135,7 @@ typedef struct fs_engine {
 #define FS_ENGINE_GLOBAL_ONLY 1u
 #define FS_ENGINE_FCFS 2u
 #define FS_ENGINE_BLIND 4u
+#define FS_ENGINE_LITERAL 8u
 
 /* Per-record and per-replica scheduler outputs (device pointers).
  *   status       [N] int8: 0 admitted, 1 throttled by the user limit, 2 by the app limit,

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libfairserve.so")
 
 FS_OK, FS_E_ARG, FS_E_ORDER, FS_E_RANGE, FS_E_OVERFLOW, FS_E_WORKSPACE, FS_E_STATE, FS_E_HIP = range(8)
 FS_THROTTLE_RAW = 1
-FS_ENGINE_GLOBAL_ONLY, FS_ENGINE_FCFS, FS_ENGINE_BLIND = 1, 2, 4
+FS_ENGINE_GLOBAL_ONLY, FS_ENGINE_FCFS, FS_ENGINE_BLIND, FS_ENGINE_LITERAL = 1, 2, 4, 8
 ALIGN = 256
 
 
@@ -273,9 +273,11 @@ def fs_throttle(dt: DeviceTrace, limits, overloaded=None, raw=True, want_reason=
     return ThrottleOut(bitmap, reason, cu, ca)
 
 
-def make_engine(step_us, cap_tokens, overload_tokens, global_only=False, fcfs=False, blind=False):
+def make_engine(step_us, cap_tokens, overload_tokens, global_only=False, fcfs=False, blind=False,
+                literal=False):
+    """literal: the literal engine, with cap_tokens the KV-cache capacity in tokens."""
     flags = ((FS_ENGINE_GLOBAL_ONLY if global_only else 0) | (FS_ENGINE_FCFS if fcfs else 0)
-             | (FS_ENGINE_BLIND if blind else 0))
+             | (FS_ENGINE_BLIND if blind else 0) | (FS_ENGINE_LITERAL if literal else 0))
     return fs_engine(int(step_us), int(cap_tokens), int(overload_tokens), flags)
 
 

@@ -61,7 +61,8 @@ fs_status check_limits(const fs_trace *t, const fs_limits *l) {
 
 fs_status check_engine(const fs_engine *e) {
   if (!e || e->step_us <= 0 || e->cap_tokens <= 0 || e->cap_tokens > kCapLimit ||
-      (e->flags & ~(FS_ENGINE_GLOBAL_ONLY | FS_ENGINE_FCFS | FS_ENGINE_BLIND)))
+      (e->flags &
+       ~(FS_ENGINE_GLOBAL_ONLY | FS_ENGINE_FCFS | FS_ENGINE_BLIND | FS_ENGINE_LITERAL)))
     return FS_E_ARG;
   return FS_OK;
 }

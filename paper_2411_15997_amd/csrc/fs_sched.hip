@@ -190,6 +190,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   int64_t *seg_cost = reinterpret_cast<int64_t *>(a.state + a.L.seg_cost);
   int32_t *seg_succ = reinterpret_cast<int32_t *>(a.state + a.L.seg_succ);
   int64_t *u_all = reinterpret_cast<int64_t *>(a.state + a.L.u_all) + int64_t(r) * U;
+  int32_t *run_rec = reinterpret_cast<int32_t *>(a.state + a.L.run_rec) + base + r;
+  int32_t *run_fin = reinterpret_cast<int32_t *>(a.state + a.L.run_fin) + base + r;
 
   // ---- scalar state
   int64_t s = uni64(rs->s), nxt = uni64(rs->nxt), debt = uni64(rs->debt);
@@ -206,6 +208,9 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   bool mid = !onchip && uni(rs->mid) != 0;
   int64_t fcfs_lo = low;  // every record below is decided (first-come choice)
   const int64_t mid_budget = uni64(rs->mid_budget);
+  // literal engine: the running batch (admission order) and the KV tokens it holds
+  const bool literal = a.literal;
+  int64_t kv_used = uni64(rs->kv_used), n_run = uni64(rs->n_run);
 
   if (!S.users_global)
     for (int32_t k = lane; k < U; k += 64) S.u[k] = u_all[k];
@@ -237,7 +242,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       a.status[g] = 0;
       a.admit_step[g] = d_step;
       if (a.admit_seq) a.admit_seq[g] = int32_t(seq - nd + lane);
-      if (a.counter_after) a.counter_after[g] = d_cnt;
+      // (the literal engine writes counter_after when the call finishes)
+      if (a.counter_after && !literal) a.counter_after[g] = d_cnt;
     }
     nd = 0;
   };
@@ -539,12 +545,86 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
   }
   load_window();
 
+  // literal engine: the earliest finish step of the running batch
+  auto batch_min_fin = [&]() -> int64_t {
+    uint32_t mf = 0xffffffffu;
+    for (int64_t b0 = 0; b0 < n_run; b0 += 64) {
+      const int64_t i = b0 + lane;
+      const uint32_t f = i < n_run ? uint32_t(ld_fresh(run_fin + i)) : 0xffffffffu;
+      mf = f < mf ? f : mf;
+    }
+    return n_run > 0 ? int64_t(wave_min32(mf)) : INT64_MAX;
+  };
+  int64_t min_fin = batch_min_fin();
+  // Calls whose last output token is decoded in step s finish, in admission order: each
+  // user is charged its call's cost (Eq. 2) and the call's KV tokens are freed; the
+  // batch is compacted in place.
+  auto finish_calls = [&]() {
+    wave_fence();
+    int64_t kept = 0;
+    uint32_t mf = 0xffffffffu;
+    for (int64_t b0 = 0; b0 < n_run && code == 0; b0 += 64) {
+      const int64_t i = b0 + lane;
+      const bool valid = i < n_run;
+      const int32_t rr = valid ? ld_fresh(run_rec + i) : -1;
+      const int32_t ff = valid ? ld_fresh(run_fin + i) : 0;
+      const bool fin = valid && int64_t(ff) == s;
+      uint64_t dm = __ballot(fin);
+      const uint64_t km = __ballot(valid && !fin);
+      if (valid && !fin) {
+        const int64_t to = kept + __popcll(km & ((uint64_t(1) << lane) - 1));
+        run_rec[to] = rr;
+        run_fin[to] = ff;
+        mf = uint32_t(ff) < mf ? uint32_t(ff) : mf;
+      }
+      kept += __popcll(km);
+      while (dm) {
+        const int l = __ffsll((long long)dm) - 1;
+        dm &= dm - 1;
+        const int32_t rec = rdl(rr, l);
+        const int64_t g = base + rec;
+        const int32_t k = uni(t.user[g]);
+        const int64_t cst = uni64(a.cost[g]);
+        const int32_t xs = X.find(k, S);
+        int64_t unew;
+        if (xs >= 0) {
+          unew = slot_u(xs) + cst;
+          if (unew < kValueLimit) set_key(xs, unew);
+        } else {
+          unew = uni64(get_u(k)) + cst;
+          if (unew < kValueLimit) {
+            if (lane == 0) S.u[k] = unew;
+            c_u = (w_user == k) ? unew : c_u;
+          }
+        }
+        if (unew >= kValueLimit) {
+          code = FS_E_OVERFLOW;
+          break;
+        }
+        if (k == last_exit) last_exit_u = unew;
+        if (lane == 0 && a.counter_after) a.counter_after[g] = unew;
+        kv_used -= uni(tokens_at(rec));
+      }
+    }
+    n_run = kept;
+    min_fin = n_run > 0 ? int64_t(wave_min32(mf)) : INT64_MAX;
+  };
+
   // ---- steps
   while (!overflow && code == 0) {
     if (s >= s_end) break;
-    if (nxt == n && nX == 0) break;
+    if (nxt == n && nX == 0 && n_run == 0) break;
     if (nxt < n && nxt - wbase >= 64) advance_window();
-    if (nX == 0 && nxt < n) {
+    if (literal && nX == 0) {
+      // nothing queued: nothing happens before the next arrival or the next finish
+      int64_t target = nxt < n ? int64_t(rdl(w_step, int(nxt - wbase))) : INT64_MAX;
+      if (min_fin < target) target = min_fin;
+      if (target > s_end) target = s_end;
+      if (target > s) {
+        s = target;
+        if (s >= s_end) break;
+      }
+    } else if (nX == 0 && nxt < n) {
       // nothing queued: the steps before the next arrival only pay back debt
       int64_t target = rdl(w_step, int(nxt - wbase));
       if (target > s_end) target = s_end;
@@ -616,10 +696,11 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     }
     if (overflow || code) break;
 
-    // execution stream: admit while the step has budget
+    // execution stream: admit while the step has budget (literal engine: while the
+    // chosen request fits in the free KV cache, or nothing runs)
     int64_t budget = mid ? mid_budget : C + debt;
     mid = false;
-    while (budget > 0 && nX > 0) {
+    while ((literal || budget > 0) && nX > 0) {
       uint64_t bk;
       int32_t k;
       int32_t x;
@@ -678,6 +759,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           code = FS_E_STATE;
           break;
         }
+        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[be].tok)) > C) break;
         e = be;
         const int32_t nx = uni(RD<G>(&S.e[e].next));
         if (bprev < 0)
@@ -701,6 +783,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           code = FS_E_STATE;
           break;
         }
+        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[e].tok)) > C) break;
         const int32_t nx = uni(RD<G>(&S.e[e].next));
         X.set_fh(x, nx);
         if (nx < 0) X.set_ft(x, -1);
@@ -711,10 +794,27 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       X.set_q(x, left);
       budget -= v.tok;
       backlog -= v.tok;
-      const int64_t unew = uk + v.cost;
+      // literal engine: no charge now; the call runs until its last output token
+      const int64_t unew = literal ? uk : uk + v.cost;
       if (unew >= kValueLimit) {
         code = FS_E_OVERFLOW;
         break;
+      }
+      if (literal) {
+        const int32_t lo = uni(t.len_out[base + v.rec]);
+        const int64_t fin = s + (lo > 1 ? lo : 1) - 1;
+        if (fin >= INT32_MAX) {  // the step count would overflow before it finishes
+          code = FS_E_OVERFLOW;
+          break;
+        }
+        if (lane == 0) {
+          run_rec[n_run] = v.rec;
+          run_fin[n_run] = int32_t(fin);
+          if (a.counter_after) a.counter_after[base + v.rec] = -1;  // until it finishes
+        }
+        ++n_run;
+        kv_used += v.tok;
+        min_fin = fin < min_fin ? fin : min_fin;
       }
       ++seq;
       if (lane == 0) fate[v.rec] = 0;  // read by the first-come choice
@@ -752,7 +852,12 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       }
     }
     if (code || overflow) break;
-    debt = budget < 0 ? budget : 0;
+    if (literal) {
+      if (min_fin <= s) finish_calls();
+      if (code) break;
+    } else {
+      debt = budget < 0 ? budget : 0;
+    }
     if (nX > 0) {
       int64_t mn, mx;
       X.minmax(nX, mn, mx);
@@ -793,7 +898,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     low += 64;
   }
   if (low > nxt) low = nxt;
-  const bool drained = nxt == n && nX == 0;
+  const bool drained = nxt == n && nX == 0 && n_run == 0;
   if (lane == 0) {
     rs->s = s;
     rs->nxt = nxt;
@@ -808,6 +913,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     rs->overflow = overflow ? 1 : 0;
     rs->mid = 0;
     rs->s_end = s_end;
+    rs->kv_used = kv_used;
+    rs->n_run = n_run;
     if (!overflow) {
       a.steps[r] = s;
       a.decisions[r] = seq;
@@ -1036,6 +1143,9 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.global_only = (eng->flags & FS_ENGINE_GLOBAL_ONLY) != 0;
   a.fcfs = (eng->flags & FS_ENGINE_FCFS) != 0;
   a.blind = (eng->flags & FS_ENGINE_BLIND) != 0;
+  a.literal = (eng->flags & FS_ENGINE_LITERAL) != 0;
+  // the on-chip kernel charges at admission: the literal engine runs in global memory
+  if (a.literal) a.global_only = true;
   a.status = out->status;
   a.admit_step = out->admit_step;
   a.admit_seq = out->admit_seq;

@@ -15,19 +15,22 @@ namespace fs {
 namespace sched {
 
 constexpr uint64_t kMagic = 0x32535652'49414646ull;
-constexpr int32_t kVersion = 4;
+constexpr int32_t kVersion = 5;
 constexpr uint64_t kTierShift = 62;
 constexpr uint64_t kValMask = (uint64_t(1) << 62) - 1;
 constexpr uint64_t kEmptyKey = ~uint64_t(0);
 
 // Per-replica scalars.  `mid` = 1 when a launch stopped inside the admissions of
 // step s (an on-chip capacity would have overflowed there); `mid_budget` is the
-// budget that step still has.
+// budget that step still has.  Literal engine: `n_run` calls are running (their
+// records and finish steps in run_rec / run_fin, in admission order), holding
+// `kv_used` tokens of KV cache.
 struct RepState {
   int64_t s, nxt, debt, backlog, seq, gap, last_exit_u, low, s_end;
   int32_t last_exit, done, overflow, mid;
   int64_t mid_budget;
-  int64_t pad2[4];
+  int64_t kv_used, n_run;
+  int64_t pad2[2];
 };
 static_assert(sizeof(RepState) == 128, "RepState layout");
 
@@ -47,6 +50,7 @@ struct StateLayout {
   size_t xkey, xuser, xq, xfh, xft, xhh, xht, xsb, xrh, xrdy;
   size_t e_all, e_free;
   size_t emap;  // per record: the pool entry it last occupied (checked before use)
+  size_t run_rec, run_fin;  // literal engine: running calls (n_r + 1 per replica)
   size_t total;
 };
 
@@ -86,6 +90,8 @@ inline StateLayout state_layout(int32_t R, int32_t U, int64_t N) {
   L.e_all = take(nr * 48);
   L.e_free = take(nr * 4);
   L.emap = take(n * 4);
+  L.run_rec = take(nr * 4);
+  L.run_fin = take(nr * 4);
   L.total = o;
   return L;
 }
@@ -109,6 +115,7 @@ struct SchedArgs {
   bool global_only;
   bool fcfs;   // first come, first served (FS_ENGINE_FCFS)
   bool blind;  // interaction-blind limits (FS_ENGINE_BLIND)
+  bool literal;  // the literal engine (FS_ENGINE_LITERAL): charge at finish, KV capacity
   int8_t *status;
   int32_t *admit_step, *admit_seq;
   int64_t *counter_after, *counter_on_arrival, *counter, *steps, *decisions, *max_gap;

@@ -40,14 +40,14 @@ def gpu_throttle(tr, W, t_user, t_app, overloaded=None, raw=True, counts=True, a
 
 
 def gpu_schedule(tr, cost, reason, step_us, cap, theta, n_steps=-1, chunks=None,
-                 global_only=False, parity=True, fcfs=False, blind=False):
+                 global_only=False, parity=True, fcfs=False, blind=False, literal=False):
     """fs_state_init + fs_schedule_step (once, or in chunks of `chunks` steps)."""
     import torch
     import paper_2411_15997_amd as fs
     dt = fs.DeviceTrace(tr)
     c = torch.as_tensor(np.ascontiguousarray(cost, np.int64)).cuda()
     rz = None if reason is None else torch.as_tensor(np.ascontiguousarray(reason, np.uint8)).cuda()
-    eng = fs.make_engine(step_us, cap, theta, global_only, fcfs=fcfs, blind=blind)
+    eng = fs.make_engine(step_us, cap, theta, global_only, fcfs=fcfs, blind=blind, literal=literal)
     out = fs.Outputs(dt, parity=parity)
     st = fs.fs_state_init(dt)
     if chunks is None:

@@ -100,6 +100,14 @@ def main():
                     "cost, throttle, schedule, metrics or history")
     ap.add_argument("--policy", default="fs", choices=["fs", "wsc_only", "vtc", "rpm"],
                     help="the paper's policy (default) or one it compares with")
+    ap.add_argument("--engine", default="step", choices=["step", "literal"],
+                    help="step: token budget per step, charge at admission; literal: prefill at "
+                         "admission, one output token per decode step, KV-cache capacity, "
+                         "charge at finish")
+    ap.add_argument("--decode-step-us", type=int, default=20_000,
+                    help="literal engine: duration of one decode step")
+    ap.add_argument("--kv-tokens", type=int, default=1 << 20,
+                    help="literal engine: KV-cache capacity per replica, in tokens")
     ap.add_argument("--calib-copy", action="store_true",
                     help="copy 1 GiB on the device first (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -133,7 +141,10 @@ def main():
         if equal:
             coef, per_rep = np.full((1, tr.n_apps, coef.shape[-2], 3), 1 << 16, np.int64), False
         w, keep = fs.make_weights(dt, coef, None, per_rep)
-        eng = fs.make_engine(wl.step_us, wl.cap_tokens, theta, fcfs=fcfs, blind=blind)
+        literal = args.engine == "literal"
+        eng = fs.make_engine(args.decode_step_us if literal else wl.step_us,
+                             args.kv_tokens if literal else wl.cap_tokens, theta, fcfs=fcfs,
+                             blind=blind, literal=literal)
         out = fs.Outputs(dt, parity=False)
         cost = torch.empty(max(N, 1), dtype=torch.int64, device=dev)
         state = torch.empty(fs.fs_state_bytes(dt), dtype=torch.uint8, device=dev)
@@ -218,9 +229,12 @@ def main():
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64", "data": "synthetic",
-        "config": {"workload": wl.name, "policy": args.policy, "replicas": R, "users": tr.n_users, "apps": tr.n_apps,
+        "config": {"workload": wl.name, "policy": args.policy, "engine": args.engine,
+                   "replicas": R, "users": tr.n_users, "apps": tr.n_apps,
                    "requests": N, "trace_sha256": tr.sha256()[:16],
-                   "step_us": wl.step_us, "cap_tokens": wl.cap_tokens, "window_us": wl.window_us},
+                   "step_us": int(eng.step_us) if not throttle_only else wl.step_us,
+                   "cap_tokens": int(eng.cap_tokens) if not throttle_only else wl.cap_tokens,
+                   "window_us": wl.window_us},
         "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
     }
     if "schedule" in stages:
@@ -279,13 +293,15 @@ def main():
                                               "frac": round(hgbs / HBM_PEAK_GBS, 4),
                                               "bytes_per_record": ALGO_BYTES["history"]}}
     if not args.no_cpu_baseline and not args.stage_only:
-        result["cpu_baseline"] = cpu_baseline(wl, tr, args.cpu_threads, throttle_only,
-                                              args.policy)
+        result["cpu_baseline"] = cpu_baseline(
+            wl, tr, args.cpu_threads, throttle_only, args.policy,
+            (args.decode_step_us, args.kv_tokens) if args.engine == "literal" else None)
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(wl, tr, threads, throttle_only, policy="fs"):
-    """The CPU oracle (as it stands) on this host, same workload and policy, whole path."""
+def cpu_baseline(wl, tr, threads, throttle_only, policy="fs", literal=None):
+    """The CPU oracle (as it stands) on this host, same workload, policy and engine
+    (literal: (decode step, KV tokens) of the literal engine), whole path."""
     import numpy as np
 
     import oracle
@@ -305,7 +321,7 @@ def cpu_baseline(wl, tr, threads, throttle_only, policy="fs"):
         return {"value": n / dt, "unit": "throttle evals/s", "cores": 1, "kind": "oracle",
                 "sample": f"first {n} requests of {wl.name}", "seconds": round(dt, 3),
                 "host": platform.processor() or platform.machine()}
-    if policy == "fs":
+    if policy == "fs" and literal is None:
         c, thr, sim, met = oracle.run_workload(wl, tr, n_threads=th)
     else:
         t_user, t_app, theta, fcfs, blind, equal = policy_settings(wl, tr.n_apps, policy)
@@ -315,9 +331,12 @@ def cpu_baseline(wl, tr, threads, throttle_only, policy="fs"):
         c = oracle.cost(tr, coef, coef_per_replica=per_rep)
         thr = oracle.throttle(tr, wl.window_us, t_user, t_app, raw=True, counts=False)
         flags = (oracle.FSO_FCFS if fcfs else 0) | (oracle.FSO_BLIND if blind else 0)
-        sim = oracle.simulate(tr, c, thr.reason, wl.step_us, wl.cap_tokens, theta, n_threads=th,
-                              flags=flags)
-        oracle.fairness_metrics(tr, c, sim.status, sim.admit_step, sim.max_gap, wl.step_us)
+        step_us, cap = wl.step_us, wl.cap_tokens
+        if literal is not None:
+            flags |= oracle.FSO_LITERAL
+            step_us, cap = literal
+        sim = oracle.simulate(tr, c, thr.reason, step_us, cap, theta, n_threads=th, flags=flags)
+        oracle.fairness_metrics(tr, c, sim.status, sim.admit_step, sim.max_gap, step_us)
     dt = time.perf_counter() - t0
     dec = int(sim.decisions.sum())
     return {"value": dec / dt, "unit": "decisions/s", "cores": th, "kind": "oracle",

@@ -556,6 +556,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     return n_run > 0 ? int64_t(wave_min32(mf)) : INT64_MAX;
   };
   int64_t min_fin = batch_min_fin();
+  // literal engine: the last admission attempt found the chosen call too large for the
+  // free KV cache and nothing has changed since (no arrival, no finish): every step
+  // until the next arrival or finish would repeat it, so those steps are skipped
+  bool stalled = false;
   // Calls whose last output token is decoded in step s finish, in admission order: each
   // user is charged its call's cost (Eq. 2) and the call's KV tokens are freed; the
   // batch is compacted in place.
@@ -615,8 +619,9 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     if (s >= s_end) break;
     if (nxt == n && nX == 0 && n_run == 0) break;
     if (nxt < n && nxt - wbase >= 64) advance_window();
-    if (literal && nX == 0) {
-      // nothing queued: nothing happens before the next arrival or the next finish
+    if (literal && (nX == 0 || stalled)) {
+      // nothing queued, or the queue waits for KV: nothing happens before the next
+      // arrival or the next finish
       int64_t target = nxt < n ? int64_t(rdl(w_step, int(nxt - wbase))) : INT64_MAX;
       if (min_fin < target) target = min_fin;
       if (target > s_end) target = s_end;
@@ -645,6 +650,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       if (nxt - wbase == 64) advance_window();
       const int j = int(nxt - wbase);
       if (rdl(w_step, j) > s) break;
+      stalled = false;
       const int32_t rec = int32_t(nxt);
       const int32_t k = rdl(w_user, j);
       const int32_t call = rdl(w_call, j);
@@ -759,7 +765,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           code = FS_E_STATE;
           break;
         }
-        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[be].tok)) > C) break;
+        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[be].tok)) > C) {
+          stalled = true;
+          break;
+        }
         e = be;
         const int32_t nx = uni(RD<G>(&S.e[e].next));
         if (bprev < 0)
@@ -783,7 +792,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
           code = FS_E_STATE;
           break;
         }
-        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[e].tok)) > C) break;
+        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[e].tok)) > C) {
+          stalled = true;
+          break;
+        }
         const int32_t nx = uni(RD<G>(&S.e[e].next));
         X.set_fh(x, nx);
         if (nx < 0) X.set_ft(x, -1);
@@ -853,7 +865,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     }
     if (code || overflow) break;
     if (literal) {
-      if (min_fin <= s) finish_calls();
+      if (min_fin <= s) {
+        finish_calls();
+        stalled = false;
+      }
       if (code) break;
     } else {
       debt = budget < 0 ? budget : 0;

@@ -125,6 +125,9 @@ struct SchedArgs {
   OnchipCfg oc;
 };
 
+// A condition that is rarely true (laid out off the straight-line path).
+#define FS_RARE(x) __builtin_expect(!!(x), 0)
+
 // ------------------------------------------------------------- wave helpers
 
 __device__ inline int32_t rdl(int32_t v, int l) { return __builtin_amdgcn_readlane(v, l); }

@@ -618,7 +618,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       } else {
         // capacity first: on overflow the state is as before this arrival
         const bool padm = !(fl & kFirst) && (fl & kPrevAdm) && !fcfs;
-        if ((fl & kBig) || (!fm && nX == kSlots) || (padm && pocc == ~uint64_t(0))) {
+        if (FS_RARE((fl & kBig) || (!fm && nX == kSlots) || (padm && pocc == ~uint64_t(0)))) {
           overflow = true;
           break;
         }
@@ -636,7 +636,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       o_coa = lane == j ? uk : o_coa;
       ++nxt;
     }
-    if (overflow) break;
+    if (FS_RARE(overflow)) break;
 
     // execution stream: admit while the step has budget
     int64_t budget = C + debt;
@@ -667,7 +667,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
           uk = int64_t((uint64_t(mh & kValHi) << 32) | ml);
         }
         const uint64_t eq = __ballot(cand);
-        if (eq & (eq - 1)) {
+        if (FS_RARE(eq & (eq - 1))) {
           const uint32_t um = wave_min32v(cand ? uint32_t(xu) : 0xffffffffu);
           x = ff1(__ballot(cand && uint32_t(xu) == um));
         } else {
@@ -679,7 +679,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (tier0) {  // the user's earliest ready later call
         const uint64_t pm = __ballot(p_x == x);
         l = ff1(pm);
-        if (pm & (pm - 1)) {
+        if (FS_RARE(pm & (pm - 1))) {
           const uint32_t e = wave_min32v(p_x == x ? uint32_t(p_rec) : 0xffffffffu);
           l = ff1(__ballot(p_x == x && uint32_t(p_rec) == e));
         }
@@ -700,14 +700,14 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         else
           sc_now = ld_fresh(STATE(const int8_t, fate) + base + sc) <= 0;
       }
-      if (sc_now && !tier0 && pocc == ~uint64_t(0)) {
+      if (FS_RARE(sc_now && !tier0 && pocc == ~uint64_t(0))) {
         overflow = mid = true;  // nothing of this admission has happened yet
         mid_budget = budget;
         break;
       }
       const int32_t tok = int32_t(lo & uint32_t(kTokMask));
       const int64_t unew = uk + int64_t(((uint64_t(hi) << 32) | lo) >> 24);
-      if (unew >= kValueLimit) {
+      if (FS_RARE(unew >= kValueLimit)) {
         code = FS_E_OVERFLOW;
         break;
       }
@@ -717,7 +717,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       d_step = lane == nd ? s : d_step;
       d_cnt = lane == nd ? unew : d_cnt;
       ++seq;
-      if (++nd == 64) flush_decisions();
+      if (FS_RARE(++nd == 64)) flush_decisions();
       if (w_wait) w_flags |= (w_prev == rec) ? kPrevAdm : 0;
       const int32_t q = rdl(xq, x) - 1;
       if (tier0) {
@@ -727,7 +727,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       } else {
         if (lane == x) ++xf;
         // the on-chip part of the FIFO is used up and its segment holds more: refill
-        if ((__ballot(xf == xr && xr < xt) >> x) & 1) fifo_refill(x);
+        if (FS_RARE((__ballot(xf == xr && xr < xt) >> x) & 1)) fifo_refill(x);
         if (lane == x && xf < xt) {
           const Ent v = ring[x * D + (xf & (D - 1))];
           hrec = v.rec;
@@ -772,7 +772,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         }
       }
     }
-    if (overflow || code) break;
+    if (FS_RARE(overflow || code)) break;
     debt = budget < 0 ? budget : 0;
     if (nX > 0) {  // the gap sample, and the least counter for the next arrivals
       const bool oc = xu >= 0;

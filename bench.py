@@ -45,12 +45,16 @@ STAGE_SRC = {
 # and stage; an entry counts only while the stage's sources hash to `src`.
 MEASURED_TRAFFIC = {
     # k_schedule_onchip on the 64 x 256 x 8 replica workload (6.4M requests)
-    ("c2_replicas", "schedule"): {"src": "531c040bd6da0cf2", "fetch_kib": 147728.5,
-                                  "write_kib": 38757.5625, "fetch_factor": 1.99994,
+    ("c2_replicas", "schedule"): {"src": "676c21abd35a1afe", "fetch_kib": 147701.5,
+                                  "write_kib": 38822.0, "fetch_factor": 1.99993,
                                   "write_factor": 1.0},
+    # k_schedule_onchip on the 1,024-replica weight sweep (20.48M requests)
+    ("c4_sweep", "schedule"): {"src": "676c21abd35a1afe", "fetch_kib": 353986.375,
+                               "write_kib": 137718.90625, "fetch_factor": 1.99988,
+                               "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
-    ("c3_throttle", "throttle"): {"src": "001a7871ea775a09", "fetch_kib": 2874819.375,
-                                  "write_kib": 2088836.8125, "fetch_factor": 1.99989,
+    ("c3_throttle", "throttle"): {"src": "c43624ae842af9d7", "fetch_kib": 2873445.125,
+                                  "write_kib": 2088911.5625, "fetch_factor": 1.99992,
                                   "write_factor": 1.0},
 }
 

@@ -160,7 +160,12 @@ __global__ void __launch_bounds__(256) k_m_interactions(MArgs a) {
     const uint32_t f = ok ? a.iflags[g] : 0u;
     const bool full = ok && !(f & I_UNSERVED);
     const bool aborted = ok && (f & I_SERVED) && (f & I_UNSERVED);
-    if (full) atomicOr(a.uflags + int64_t(r) * t.U + k, U_FULL);
+    if (full) {
+      // a heavy user has many fully served interactions: skip the atomic once its flag
+      // is visible (a stale read only costs an atomic that changes nothing)
+      uint32_t *uf = a.uflags + int64_t(r) * t.U + k;
+      if (!(*uf & U_FULL)) atomicOr(uf, U_FULL);
+    }
     wave_add_by_key(ok, int64_t(r) * C_NUM + C_FULL, full ? 1ull : 0ull, a.counters, 0, nullptr);
     wave_add_by_key(ok, int64_t(r) * C_NUM + C_ABORTED, aborted ? 1ull : 0ull, a.counters, 0,
                     nullptr);

@@ -1023,18 +1023,21 @@ __global__ void k_state_records(char *state, StateLayout L, int64_t N) {
 // next-call links (succ[prev] = i) and the number of requests per (replica, user), the
 // size of the user's segment (a FIFO holds at most all of its user's requests); links
 // and ids are checked again before the scheduler runs.  Each block counts a tile of
-// records in LDS (by user, for the replica the tile starts in) and adds the non-zero
-// counts to global memory; users beyond the LDS table and a tile's records of a later
-// replica are added directly.
+// records by (replica, user) in an LDS hash table (open addressing, at most half full)
+// and adds each distinct key's count to global memory once, so a heavy user costs one
+// global atomic per tile instead of one per request.
 constexpr int kLinkTile = 4096;
-constexpr int kLinkUsers = 8192;
+constexpr int kLinkSlots = 2 * kLinkTile;
+constexpr uint32_t kLinkEmpty = 0xffffffffu;
 
 __global__ void __launch_bounds__(256) k_state_links(char *state, StateLayout L, DevTrace t) {
-  __shared__ uint32_t h[kLinkUsers];
+  __shared__ uint32_t hk[kLinkSlots], hc[kLinkSlots];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(state + L.seg_start);
   const int64_t g0 = int64_t(blockIdx.x) * kLinkTile;
-  const int32_t nu = t.U < kLinkUsers ? t.U : kLinkUsers;
-  for (int k = threadIdx.x; k < nu; k += 256) h[k] = 0;
+  for (int j = threadIdx.x; j < kLinkSlots; j += 256) {
+    hk[j] = kLinkEmpty;
+    hc[j] = 0;
+  }
   const int32_t r0 = replica_of(t.rep_off, t.R, g0 < t.N ? g0 : t.N - 1);
   const int64_t r0_end = t.rep_off[r0 + 1];
   __syncthreads();
@@ -1044,10 +1047,17 @@ __global__ void __launch_bounds__(256) k_state_links(char *state, StateLayout L,
     const int64_t b = t.rep_off[r], i = g - b;
     const int32_t u = t.user[g];
     if (u >= 0 && u < t.U) {
-      if (r == r0 && u < nu)
-        atomicAdd(h + u, 1u);
-      else
-        atomicAdd(cnt + int64_t(r) * t.U + u, 1u);
+      // (replica, user) < R * U <= 2^31: fits below the empty marker
+      const uint32_t key = uint32_t(int64_t(r) * t.U + u);
+      uint32_t h = (key * 2654435761u) >> 19;  // top 13 bits: a slot in [0, 8192)
+      while (true) {
+        const uint32_t prev = atomicCAS(hk + h, kLinkEmpty, key);
+        if (prev == kLinkEmpty || prev == key) {
+          atomicAdd(hc + h, 1u);
+          break;
+        }
+        h = (h + 1) & (kLinkSlots - 1);
+      }
     }
     if (c > 0) {
       const int32_t p = t.prev[g];
@@ -1055,8 +1065,8 @@ __global__ void __launch_bounds__(256) k_state_links(char *state, StateLayout L,
     }
   }
   __syncthreads();
-  for (int k = threadIdx.x; k < nu; k += 256)
-    if (h[k]) atomicAdd(cnt + int64_t(r0) * t.U + k, h[k]);
+  for (int j = threadIdx.x; j < kLinkSlots; j += 256)
+    if (hk[j] != kLinkEmpty) atomicAdd(cnt + hk[j], hc[j]);
 }
 
 struct CheckArgs {

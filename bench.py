@@ -34,7 +34,8 @@ CSRC = os.path.join(ROOT, "paper_2411_15997_amd", "csrc")
 STAGE_SRC = {
     "cost": ["fs_cost.hip"],
     "throttle": ["fs_throttle.hip"],
-    "schedule": ["fs_sched_onchip.hip", "fs_sched.hip", "fs_sched_common.h"],
+    # the dominant kernel of the stage, k_schedule_onchip, and the header it shares
+    "schedule": ["fs_sched_onchip.hip", "fs_sched_common.h"],
     "metrics": ["fs_metrics.hip"],
     "history": ["fs_history.hip"],
 }
@@ -45,11 +46,11 @@ STAGE_SRC = {
 # and stage; an entry counts only while the stage's sources hash to `src`.
 MEASURED_TRAFFIC = {
     # k_schedule_onchip on the 64 x 256 x 8 replica workload (6.4M requests)
-    ("c2_replicas", "schedule"): {"src": "676c21abd35a1afe", "fetch_kib": 147701.5,
+    ("c2_replicas", "schedule"): {"src": "83896265857a4a28", "fetch_kib": 147701.5,
                                   "write_kib": 38822.0, "fetch_factor": 1.99993,
                                   "write_factor": 1.0},
     # k_schedule_onchip on the 1,024-replica weight sweep (20.48M requests)
-    ("c4_sweep", "schedule"): {"src": "676c21abd35a1afe", "fetch_kib": 353986.375,
+    ("c4_sweep", "schedule"): {"src": "83896265857a4a28", "fetch_kib": 353986.375,
                                "write_kib": 137718.90625, "fetch_factor": 1.99988,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream

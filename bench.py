@@ -111,7 +111,7 @@ def main():
                          "charge at finish")
     ap.add_argument("--decode-step-us", type=int, default=20_000,
                     help="literal engine: duration of one decode step")
-    ap.add_argument("--kv-tokens", type=int, default=1 << 20,
+    ap.add_argument("--kv-tokens", type=int, default=1 << 22,
                     help="literal engine: KV-cache capacity per replica, in tokens")
     ap.add_argument("--calib-copy", action="store_true",
                     help="copy 1 GiB on the device first (calibrates rocprofv3 byte counters)")

@@ -1169,8 +1169,6 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.fcfs = (eng->flags & FS_ENGINE_FCFS) != 0;
   a.blind = (eng->flags & FS_ENGINE_BLIND) != 0;
   a.literal = (eng->flags & FS_ENGINE_LITERAL) != 0;
-  // the on-chip kernel charges at admission: the literal engine runs in global memory
-  if (a.literal) a.global_only = true;
   a.status = out->status;
   a.admit_step = out->admit_step;
   a.admit_seq = out->admit_seq;
@@ -1183,7 +1181,7 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.err = out->err;
   a.state = static_cast<char *>(state);
   a.L = state_layout(t->n_replicas, t->n_users, N);
-  a.oc = onchip_config(t->n_replicas, t->n_users);
+  a.oc = onchip_config(t->n_replicas, t->n_users, a.literal);
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
   hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);

@@ -102,7 +102,7 @@ struct OnchipCfg {
   int32_t ring;       // first calls kept on chip per backlogged user (power of two)
   int32_t cache;      // recent arrivals whose data stays on chip (power of two)
   int32_t users_lds;  // 1: counters of idle users in LDS, 0: in the state buffer
-  int32_t pad;
+  int32_t batch;      // literal engine: running calls kept on chip (power of two), else 0
   size_t lds_bytes;
 };
 
@@ -277,7 +277,7 @@ __device__ inline bool finish_if_done(const SchedArgs &a, int32_t r) {
 }
 
 // Host side: the on-chip kernel's LDS layout for this launch and its launcher.
-OnchipCfg onchip_config(int32_t R, int32_t U);
+OnchipCfg onchip_config(int32_t R, int32_t U, bool literal);
 void launch_onchip(const SchedArgs &a, hipStream_t s);
 
 }  // namespace sched

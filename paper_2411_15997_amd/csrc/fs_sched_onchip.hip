@@ -29,6 +29,10 @@
 //   window    the next 64 records, one per lane, with their step, packed request,
 //             flags (first call, raw throttle reason, "head throttled", "previous
 //             call admitted") and the user's counter; state changes patch it.
+//   batch     (literal engine) the running calls in admission order: record, finish
+//             step, packed request and user; a step's finishes are found by a wave scan
+//             when the earliest finish step is due, charged in admission order, and the
+//             batch is compacted in place.
 // Outputs of arrivals and admissions are collected one per lane and written 64 at a
 // time.  When an on-chip capacity would overflow, the wave stops before the event
 // that needs it, saves the replica's state and the global-memory kernel resumes it.
@@ -87,8 +91,9 @@ __device__ __forceinline__ T arg_at(uint32_t off) {
 
 #define STATE(T, field) reinterpret_cast<T *>(KARG(state) + KARG(L.field))
 
-// FCFS: first come, first served; BLIND: interaction-blind limits (the engine flags).
-template <bool FCFS, bool BLIND>
+// FCFS: first come, first served; BLIND: interaction-blind limits; LITERAL: the literal
+// engine (the engine flags).
+template <bool FCFS, bool BLIND, bool LITERAL>
 __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int32_t r = blockIdx.x;
@@ -100,9 +105,12 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   const int32_t D = a.oc.ring, M = a.oc.cache;
   const bool ulds = a.oc.users_lds != 0;
   const int32_t U = a.t.U;
+  const int32_t BQ = LITERAL ? a.oc.batch : 0;
   Ent *const ring = reinterpret_cast<Ent *>(smem);  // [kSlots][D]
   Ent *const cache = ring + kSlots * D;             // [M]
-  int64_t *const u_lds = reinterpret_cast<int64_t *>(cache + M);
+  Ent *const bat = cache + M;                       // [BQ] rec, finish step, lo, hi
+  int32_t *const bat_u = reinterpret_cast<int32_t *>(bat + BQ);  // [BQ] user
+  int64_t *const u_lds = reinterpret_cast<int64_t *>(bat_u + BQ);
   const int64_t base = a.t.rep_off[r];
   const int32_t n = int32_t(a.t.rep_off[r + 1] - base);
   RepState *const rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
@@ -117,7 +125,12 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   const int64_t s_end = a.n_steps < 0 ? INT64_MAX : int64_t(s) + a.n_steps;
   const int64_t C = a.cap, theta = a.theta;
   constexpr bool fcfs = FCFS, blind = BLIND;
-  if (uni(rs->mid)) {  // stopped inside a step: only the global-memory kernel resumes that
+  // literal engine: the running batch and the KV tokens it holds
+  int64_t kv_used = LITERAL ? uni64(rs->kv_used) : 0;
+  int32_t n_run = LITERAL ? int32_t(uni64(rs->n_run)) : 0;
+  // stopped inside a step, or a batch larger than the LDS one: only the global-memory
+  // kernel resumes that
+  if (uni(rs->mid) || n_run > BQ) {
     if (lane == 0) {
       rs->overflow = 1;
       rs->s_end = s_end;
@@ -127,6 +140,31 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
 
   if (ulds)
     for (int32_t k = lane; k < U; k += 64) u_lds[k] = u_all[k];
+  int64_t min_fin = INT64_MAX;  // literal engine: the batch's earliest finish step
+  int32_t nb0 = n_run;          // batch entries [nb0, n_run) still wait for their finish step
+  bool stalled = false;  // the last admission found no room in the KV cache, nothing changed since
+  if (LITERAL && n_run > 0) {
+    const int32_t *const rr_ = STATE(const int32_t, run_rec) + base + r;
+    const int32_t *const rf_ = STATE(const int32_t, run_fin) + base + r;
+    const int32_t *const len_sys = KARG(t.len_sys);
+    const int32_t *const len_in = KARG(t.len_in), *const len_out = KARG(t.len_out);
+    const int32_t *const user = KARG(t.user);
+    const int64_t *const costp = KARG(cost);
+    uint32_t mf = 0xffffffffu;
+    for (int32_t b0 = 0; b0 < n_run; b0 += 64) {
+      const int32_t i = b0 + lane;
+      if (i < n_run) {
+        const int32_t rec = rr_[i], fin = rf_[i];
+        const int64_t g = base + rec;
+        const int32_t tok = len_in[g] + len_out[g] + (len_sys ? len_sys[g] : 0);
+        const uint64_t pk = (uint64_t(costp[g]) << 24) | uint32_t(tok);
+        bat[i] = mk_ent(rec, fin, uint32_t(pk), uint32_t(pk >> 32));
+        bat_u[i] = user[g];
+        mf = uint32_t(fin) < mf ? uint32_t(fin) : mf;
+      }
+    }
+    min_fin = int64_t(wave_min32(mf));
+  }
   __syncthreads();
 
   auto put_u = [&](int32_t k, int64_t v) {
@@ -280,7 +318,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       status[g] = 0;
       astep[g] = d_step;
       if (as) as[g] = seq - nd + lane;
-      if (ca) ca[g] = d_cnt;
+      if (ca && !LITERAL) ca[g] = d_cnt;  // (the literal engine writes it at finish)
     }
     nd = 0;
   };
@@ -548,9 +586,21 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   // ---- steps
   while (true) {
     if (s >= s_end) break;
-    if (nxt == n && nX == 0) break;
+    if (nxt == n && nX == 0 && n_run == 0) break;
     if (nxt < n && nxt - wbase >= 64) advance_window();
-    if (nX == 0 && nxt < n) {
+    if (LITERAL) {
+      if (nX == 0 || stalled) {
+        // nothing queued, or the queue waits for KV: nothing happens before the next
+        // arrival or the next finish
+        int64_t target = nxt < n ? int64_t(rdl(w_step, nxt - wbase)) : INT64_MAX;
+        if (min_fin < target) target = min_fin;
+        if (target > s_end) target = s_end;
+        if (target > s) {
+          s = target >= int64_t(INT32_MAX) ? INT32_MAX : int32_t(target);
+          if (s >= s_end) break;
+        }
+      }
+    } else if (nX == 0 && nxt < n) {
       // nothing queued: the steps before the next arrival only pay back debt
       int64_t target = rdl(w_step, nxt - wbase);
       if (target > s_end) target = s_end;
@@ -571,6 +621,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (nxt - wbase == 64) advance_window();
       const int j = nxt - wbase;
       if (rdl(w_step, j) > s) break;
+      if (LITERAL) stalled = false;
       if (nX > 0 && !blind) {  // the step's arrivals in this window, together
         const uint64_t after = __ballot(w_step > s) & (~uint64_t(0) << j);
         const int32_t j1 = after ? ff1(after) : 64;
@@ -638,9 +689,10 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     }
     if (FS_RARE(overflow)) break;
 
-    // execution stream: admit while the step has budget
+    // execution stream: admit while the step has budget (literal engine: while the
+    // chosen call fits in the free KV cache, or nothing runs)
     int64_t budget = C + debt;
-    while (budget > 0 && nX > 0) {
+    while ((LITERAL || budget > 0) && nX > 0) {
       // least (key, user id): the ready tier first, then the least counter
       bool cand, tier0;
       int64_t uk;
@@ -700,13 +752,25 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         else
           sc_now = ld_fresh(STATE(const int8_t, fate) + base + sc) <= 0;
       }
+      if (LITERAL) {
+        if (n_run > 0 && kv_used + int64_t(lo & uint32_t(kTokMask)) > C) {
+          stalled = true;  // nothing of this admission has happened
+          break;
+        }
+        if (FS_RARE(n_run == BQ)) {
+          overflow = mid = true;  // the batch is full on chip: continue in global memory
+          mid_budget = budget;
+          break;
+        }
+      }
       if (FS_RARE(sc_now && !tier0 && pocc == ~uint64_t(0))) {
         overflow = mid = true;  // nothing of this admission has happened yet
         mid_budget = budget;
         break;
       }
       const int32_t tok = int32_t(lo & uint32_t(kTokMask));
-      const int64_t unew = uk + int64_t(((uint64_t(hi) << 32) | lo) >> 24);
+      // (literal engine: no charge now; the call runs until its last output token)
+      const int64_t unew = LITERAL ? uk : uk + int64_t(((uint64_t(hi) << 32) | lo) >> 24);
       if (FS_RARE(unew >= kValueLimit)) {
         code = FS_E_OVERFLOW;
         break;
@@ -717,6 +781,18 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       d_step = lane == nd ? s : d_step;
       d_cnt = lane == nd ? unew : d_cnt;
       ++seq;
+      if (LITERAL) {
+        // join the batch; its finish step is resolved after the step's admissions
+        const int32_t ku = rdl(xu, x);
+        if (lane == 0) {
+          bat[n_run] = mk_ent(rec, s, lo, hi);
+          bat_u[n_run] = ku;
+          int64_t *const ca = KARG(counter_after);
+          if (ca) ca[base + rec] = -1;  // until it finishes
+        }
+        ++n_run;
+        kv_used += tok;
+      }
       if (FS_RARE(++nd == 64)) flush_decisions();
       if (w_wait) w_flags |= (w_prev == rec) ? kPrevAdm : 0;
       const int32_t q = rdl(xq, x) - 1;
@@ -772,8 +848,94 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         }
       }
     }
+    if (LITERAL && nb0 < n_run) {
+      // finish steps of this step's admissions (also before a hand-over in the middle
+      // of the admissions): one read of their output lengths
+      const int32_t *const len_out = KARG(t.len_out);
+      uint32_t mf = 0xffffffffu;
+      bool big = false;
+      for (int32_t b0 = nb0; b0 < n_run; b0 += 64) {
+        const int32_t i = b0 + lane;
+        if (i < n_run) {
+          const int32_t lout = len_out[base + bat[i].rec];
+          const int64_t fin = int64_t(s) + (lout > 1 ? lout : 1) - 1;
+          big = big || fin >= int64_t(INT32_MAX);
+          bat[i].succ = int32_t(fin);
+          mf = uint32_t(fin) < mf ? uint32_t(fin) : mf;
+        }
+      }
+      nb0 = n_run;
+      if (FS_RARE(__ballot(big) != 0)) code = FS_E_OVERFLOW;  // the step count would overflow
+      const int64_t m = int64_t(wave_min32(mf));
+      min_fin = m < min_fin ? m : min_fin;
+    }
     if (FS_RARE(overflow || code)) break;
-    debt = budget < 0 ? budget : 0;
+    if (LITERAL) {
+      // decode: calls whose last output token falls in step s finish in admission
+      // order; each user is charged its call's cost and the call's KV is freed
+      if (min_fin <= s) {
+        stalled = false;
+        int64_t *const ca = KARG(counter_after);
+        int32_t kept = 0;
+        uint32_t mk = 0xffffffffu;
+        const uint64_t lt = (uint64_t(1) << lane) - 1;
+        for (int32_t b0 = 0; b0 < n_run && !code; b0 += 64) {
+          const int32_t i = b0 + lane;
+          const bool valid = i < n_run;
+          const Ent e = valid ? bat[i] : mk_ent(-1, -1, 0, 0);
+          const int32_t ku = valid ? bat_u[i] : -1;
+          const bool done = valid && e.succ == s;
+          uint64_t dm = __ballot(done);
+          const uint64_t km = __ballot(valid && !done);
+          if (valid && !done) {
+            const int32_t to = kept + __popcll(km & lt);
+            bat[to] = e;
+            bat_u[to] = ku;
+            mk = uint32_t(e.succ) < mk ? uint32_t(e.succ) : mk;
+          }
+          kept += __popcll(km);
+          while (dm) {
+            const int l = ff1(dm);
+            dm &= dm - 1;
+            const int32_t rec = rdl(e.rec, l), k = rdl(ku, l);
+            const uint32_t elo = rdlu(e.lo, l), ehi = rdlu(e.hi, l);
+            const int64_t cst = int64_t(((uint64_t(ehi) << 32) | elo) >> 24);
+            const uint64_t fm = __ballot(xu == k);
+            int64_t uc;
+            if (fm) {  // a queued user: its key moves, its tier stays
+              const int32_t xx = ff1(fm);
+              uc = int64_t((uint64_t(rdlu(kh, xx) & kValHi) << 32) | rdlu(kl, xx)) + cst;
+              if (FS_RARE(uc >= kValueLimit)) {
+                code = FS_E_OVERFLOW;
+                break;
+              }
+              const uint32_t rv = rel_of(uc);
+              if (lane == xx) {
+                kh = uint32_t(uint64_t(uc) >> 32) | (xn > 0 ? 0u : kTier1);
+                kl = uint32_t(uint64_t(uc));
+                k32 = (xn > 0 ? 0u : kRelTier1) | rv;
+              }
+            } else {
+              uc = uni64(ulds ? u_lds[k] : ld_fresh(u_all + k)) + cst;
+              if (FS_RARE(uc >= kValueLimit)) {
+                code = FS_E_OVERFLOW;
+                break;
+              }
+              put_u(k, uc);
+              c_u = (w_user == k) ? uc : c_u;
+            }
+            if (k == last_exit) last_exit_u = uc;
+            if (lane == 0 && ca) ca[base + rec] = uc;
+            kv_used -= int64_t(elo & uint32_t(kTokMask));
+          }
+        }
+        if (code) break;
+        n_run = nb0 = kept;
+        min_fin = kept > 0 ? int64_t(wave_min32(mk)) : INT64_MAX;
+      }
+    } else {
+      debt = budget < 0 ? budget : 0;
+    }
     if (nX > 0) {  // the gap sample, and the least counter for the next arrivals
       const bool oc = xu >= 0;
       if (!wide) {
@@ -830,8 +992,18 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     }
     if (low > nxt) low = nxt;
   }
-  const bool drained = nxt == n && nX == 0;
+  if (LITERAL) {  // the running batch goes to the state buffer
+    int32_t *const rr_ = STATE(int32_t, run_rec) + base + r;
+    int32_t *const rf_ = STATE(int32_t, run_fin) + base + r;
+    for (int32_t i = lane; i < n_run; i += 64) {
+      rr_[i] = bat[i].rec;
+      rf_[i] = bat[i].succ;
+    }
+  }
+  const bool drained = nxt == n && nX == 0 && n_run == 0;
   if (lane == 0) {
+    rs->kv_used = kv_used;
+    rs->n_run = n_run;
     rs->s = s;
     rs->nxt = nxt;
     rs->debt = debt;
@@ -874,7 +1046,7 @@ int max_lds_per_block() {
 
 }  // namespace
 
-OnchipCfg onchip_config(int32_t R, int32_t U) {
+OnchipCfg onchip_config(int32_t R, int32_t U, bool literal) {
   // enough LDS per work-group for all replicas to be resident at once (up to four
   // work-groups, i.e. one wave per SIMD, on each of the 256 CUs)
   const int per_cu = R <= 256 ? 1 : R <= 512 ? 2 : R <= 768 ? 3 : 4;
@@ -882,10 +1054,17 @@ OnchipCfg onchip_config(int32_t R, int32_t U) {
   const size_t dev_max = size_t(max_lds_per_block());
   if (budget > dev_max) budget = dev_max;
   OnchipCfg c;
-  c.pad = 0;
+  // literal engine: a quarter for the running batch (20 bytes a call), at most 4096
+  int batch = 0;
+  if (literal) {
+    batch = 4096;
+    while (batch > 64 && size_t(batch) * (sizeof(Ent) + 4) > budget / 4) batch >>= 1;
+  }
+  c.batch = batch;
+  const size_t bat_bytes = size_t(batch) * (sizeof(Ent) + 4);
   c.users_lds = size_t(U) * 8 <= budget / 4 ? 1 : 0;
   const size_t users = c.users_lds ? size_t(U) * 8 : 0;
-  size_t left = budget - users;
+  size_t left = budget - users - bat_bytes;
   // about half for the rings, the rest for the arrival cache
   int ring = 64;
   while (ring > 8 && size_t(kSlots) * ring * sizeof(Ent) > left / 2) ring >>= 1;
@@ -894,24 +1073,29 @@ OnchipCfg onchip_config(int32_t R, int32_t U) {
   while (cache > 64 && size_t(cache) * sizeof(Ent) > left) cache >>= 1;
   c.ring = ring;
   c.cache = cache;
-  c.lds_bytes = size_t(kSlots) * ring * sizeof(Ent) + size_t(cache) * sizeof(Ent) + users;
+  c.lds_bytes = size_t(kSlots) * ring * sizeof(Ent) + size_t(cache) * sizeof(Ent) + bat_bytes + users;
   return c;
 }
 
-template <bool FCFS, bool BLIND>
+template <bool FCFS, bool BLIND, bool LITERAL>
 void launch_mode(const SchedArgs &a, hipStream_t s) {
+  const void *k = reinterpret_cast<const void *>(&k_schedule_onchip<FCFS, BLIND, LITERAL>);
   if (a.oc.lds_bytes > 65536)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&k_schedule_onchip<FCFS, BLIND>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, int(a.oc.lds_bytes));
-  hipLaunchKernelGGL((k_schedule_onchip<FCFS, BLIND>), dim3(a.t.R), dim3(64), a.oc.lds_bytes, s,
-                     a);
+    (void)hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(a.oc.lds_bytes));
+  hipLaunchKernelGGL((k_schedule_onchip<FCFS, BLIND, LITERAL>), dim3(a.t.R), dim3(64),
+                     a.oc.lds_bytes, s, a);
+}
+
+template <bool LITERAL>
+void launch_engine(const SchedArgs &a, hipStream_t s) {
+  if (a.fcfs)
+    a.blind ? launch_mode<true, true, LITERAL>(a, s) : launch_mode<true, false, LITERAL>(a, s);
+  else
+    a.blind ? launch_mode<false, true, LITERAL>(a, s) : launch_mode<false, false, LITERAL>(a, s);
 }
 
 void launch_onchip(const SchedArgs &a, hipStream_t s) {
-  if (a.fcfs)
-    a.blind ? launch_mode<true, true>(a, s) : launch_mode<true, false>(a, s);
-  else
-    a.blind ? launch_mode<false, true>(a, s) : launch_mode<false, false>(a, s);
+  a.literal ? launch_engine<true>(a, s) : launch_engine<false>(a, s);
 }
 
 }  // namespace sched

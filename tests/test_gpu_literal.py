@@ -25,8 +25,9 @@ def _run(tr, cost, reason, step, kv, theta, flags, **kw):
     return g, o
 
 
+@pytest.mark.parametrize("global_only", [False, True])
 @pytest.mark.parametrize("mode", list(MODES))
-def test_many_tiny_replicas(mode):
+def test_many_tiny_replicas(mode, global_only):
     rng = np.random.default_rng(80 + len(mode))
     reps = [random_trace(rng, int(rng.integers(1, 40)), int(rng.integers(1, 5)), 2,
                          int(rng.integers(1, 300)), multi=True, max_tok=6) for _ in range(300)]
@@ -34,8 +35,29 @@ def test_many_tiny_replicas(mode):
     cost = rng.integers(0, 50, tr.n).astype(np.int64)
     reason = rng.integers(0, 3, tr.n).astype(np.uint8)
     for kv, theta in ((4, -1), (9, 4), (40, 10 ** 9)):
-        say("literal tiny", mode, kv, theta, tr.n)
-        _run(tr, cost, reason, 20, kv, theta, MODES[mode])
+        say("literal tiny", mode, global_only, kv, theta, tr.n)
+        _run(tr, cost, reason, 20, kv, theta, MODES[mode], global_only=global_only)
+
+
+@pytest.mark.parametrize("chunks", [None, 3])
+def test_running_batch_larger_than_on_chip(chunks):
+    """Thousands of calls running at once: the on-chip batch fills and the replica
+    continues in global memory, in the middle of a step's admissions (and, in chunks,
+    resumes from the saved batch)."""
+    rng = np.random.default_rng(91)
+    reps = []
+    for _ in range(3):
+        n = 5000
+        ts = np.sort(rng.integers(0, 40, size=n)).astype(np.int64)
+        user = rng.integers(0, 30, size=n).astype(np.int32)
+        reps.append(tg.Trace(1, 30, 1, np.array([0, n], np.int64), ts, user,
+                             np.zeros(n, np.int32), None, None, None,
+                             rng.integers(1, 20, n).astype(np.int32), None,
+                             rng.integers(30, 120, n).astype(np.int32)))
+    tr = tg.concat(reps)
+    cost = rng.integers(1, 1 << 20, tr.n).astype(np.int64)
+    say("literal big batch", tr.n, chunks)
+    _run(tr, cost, None, 10, 10 ** 9, 10 ** 9, L, chunks=chunks)
 
 
 def test_oversized_calls_and_zero_output():

@@ -140,8 +140,15 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
 
   if (ulds)
     for (int32_t k = lane; k < U; k += 64) u_lds[k] = u_all[k];
-  int64_t min_fin = INT64_MAX;  // literal engine: the batch's earliest finish step
-  int32_t nb0 = n_run;          // batch entries [nb0, n_run) still wait for their finish step
+  // Literal engine: the batch is an array in admission order, [0, n_run), whose finished
+  // entries are marked dead (finish step kDeadFin) and removed only when the array is
+  // full or saved; n_live entries are alive.  Lane c holds the least finish step of the
+  // live entries of chunk c (entries [64c, 64c + 64)), so a step visits only the chunks
+  // with a finish due.
+  constexpr uint32_t kDeadFin = 0x7fffffffu;
+  uint32_t cmin = 0xffffffffu;
+  int32_t n_live = n_run;
+  int32_t nb0 = n_run;  // entries [nb0, n_run) still wait for their finish step
   bool stalled = false;  // the last admission found no room in the KV cache, nothing changed since
   if (LITERAL && n_run > 0) {
     const int32_t *const rr_ = STATE(const int32_t, run_rec) + base + r;
@@ -150,9 +157,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const int32_t *const len_in = KARG(t.len_in), *const len_out = KARG(t.len_out);
     const int32_t *const user = KARG(t.user);
     const int64_t *const costp = KARG(cost);
-    uint32_t mf = 0xffffffffu;
     for (int32_t b0 = 0; b0 < n_run; b0 += 64) {
       const int32_t i = b0 + lane;
+      uint32_t mf = 0xffffffffu;
       if (i < n_run) {
         const int32_t rec = rr_[i], fin = rf_[i];
         const int64_t g = base + rec;
@@ -160,12 +167,43 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         const uint64_t pk = (uint64_t(costp[g]) << 24) | uint32_t(tok);
         bat[i] = mk_ent(rec, fin, uint32_t(pk), uint32_t(pk >> 32));
         bat_u[i] = user[g];
-        mf = uint32_t(fin) < mf ? uint32_t(fin) : mf;
+        mf = uint32_t(fin);
       }
+      const uint32_t m = wave_min32(mf);
+      if (lane == (b0 >> 6)) cmin = m;
     }
-    min_fin = int64_t(wave_min32(mf));
   }
   __syncthreads();
+  // least live finish step of chunk c, into lane c
+  auto chunk_min = [&](int32_t c) {
+    const int32_t i = c * 64 + lane;
+    const uint32_t f = i < n_run ? uint32_t(bat[i].succ) : 0xffffffffu;
+    const uint32_t m = wave_min32(f == kDeadFin ? 0xffffffffu : f);
+    if (lane == c) cmin = m;
+  };
+  // removes the dead entries, keeping the admission order
+  auto compact = [&]() {
+    const uint64_t lt = (uint64_t(1) << lane) - 1;
+    int32_t kept = 0;
+    for (int32_t b0 = 0; b0 < n_run; b0 += 64) {
+      const int32_t i = b0 + lane;
+      const bool valid = i < n_run;
+      const Ent e = valid ? bat[i] : mk_ent(-1, int32_t(kDeadFin), 0, 0);
+      const int32_t ku = valid ? bat_u[i] : -1;
+      const bool live = valid && uint32_t(e.succ) != kDeadFin;
+      const uint64_t km = __ballot(live);
+      if (live) {
+        const int32_t to = kept + __popcll(km & lt);
+        bat[to] = e;
+        bat_u[to] = ku;
+      }
+      kept += __popcll(km);
+    }
+    nb0 -= n_run - kept;  // the entries still waiting for their finish step are the last ones
+    n_run = kept;
+    cmin = 0xffffffffu;
+    for (int32_t c = 0; c * 64 < n_run; ++c) chunk_min(c);
+  };
 
   auto put_u = [&](int32_t k, int64_t v) {
     if (lane == 0) {
@@ -586,14 +624,15 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   // ---- steps
   while (true) {
     if (s >= s_end) break;
-    if (nxt == n && nX == 0 && n_run == 0) break;
+    if (nxt == n && nX == 0 && n_live == 0) break;
     if (nxt < n && nxt - wbase >= 64) advance_window();
     if (LITERAL) {
       if (nX == 0 || stalled) {
         // nothing queued, or the queue waits for KV: nothing happens before the next
         // arrival or the next finish
         int64_t target = nxt < n ? int64_t(rdl(w_step, nxt - wbase)) : INT64_MAX;
-        if (min_fin < target) target = min_fin;
+        const uint32_t mf = wave_min32(cmin);
+        if (n_live > 0 && int64_t(mf) < target) target = int64_t(mf);
         if (target > s_end) target = s_end;
         if (target > s) {
           s = target >= int64_t(INT32_MAX) ? INT32_MAX : int32_t(target);
@@ -753,14 +792,17 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
           sc_now = ld_fresh(STATE(const int8_t, fate) + base + sc) <= 0;
       }
       if (LITERAL) {
-        if (n_run > 0 && kv_used + int64_t(lo & uint32_t(kTokMask)) > C) {
+        if (n_live > 0 && kv_used + int64_t(lo & uint32_t(kTokMask)) > C) {
           stalled = true;  // nothing of this admission has happened
           break;
         }
         if (FS_RARE(n_run == BQ)) {
-          overflow = mid = true;  // the batch is full on chip: continue in global memory
-          mid_budget = budget;
-          break;
+          compact();
+          if (n_run == BQ) {
+            overflow = mid = true;  // the batch is full on chip: continue in global memory
+            mid_budget = budget;
+            break;
+          }
         }
       }
       if (FS_RARE(sc_now && !tier0 && pocc == ~uint64_t(0))) {
@@ -791,6 +833,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
           if (ca) ca[base + rec] = -1;  // until it finishes
         }
         ++n_run;
+        ++n_live;
         kv_used += tok;
       }
       if (FS_RARE(++nd == 64)) flush_decisions();
@@ -852,86 +895,78 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       // finish steps of this step's admissions (also before a hand-over in the middle
       // of the admissions): one read of their output lengths
       const int32_t *const len_out = KARG(t.len_out);
-      uint32_t mf = 0xffffffffu;
       bool big = false;
       for (int32_t b0 = nb0; b0 < n_run; b0 += 64) {
         const int32_t i = b0 + lane;
         if (i < n_run) {
           const int32_t lout = len_out[base + bat[i].rec];
           const int64_t fin = int64_t(s) + (lout > 1 ? lout : 1) - 1;
-          big = big || fin >= int64_t(INT32_MAX);
+          big = big || fin >= int64_t(kDeadFin);
           bat[i].succ = int32_t(fin);
-          mf = uint32_t(fin) < mf ? uint32_t(fin) : mf;
         }
       }
+      for (int32_t c = nb0 >> 6; c * 64 < n_run; ++c) chunk_min(c);
       nb0 = n_run;
       if (FS_RARE(__ballot(big) != 0)) code = FS_E_OVERFLOW;  // the step count would overflow
-      const int64_t m = int64_t(wave_min32(mf));
-      min_fin = m < min_fin ? m : min_fin;
     }
     if (FS_RARE(overflow || code)) break;
     if (LITERAL) {
       // decode: calls whose last output token falls in step s finish in admission
       // order; each user is charged its call's cost and the call's KV is freed
-      if (min_fin <= s) {
-        stalled = false;
-        int64_t *const ca = KARG(counter_after);
-        int32_t kept = 0;
-        uint32_t mk = 0xffffffffu;
-        const uint64_t lt = (uint64_t(1) << lane) - 1;
-        for (int32_t b0 = 0; b0 < n_run && !code; b0 += 64) {
-          const int32_t i = b0 + lane;
-          const bool valid = i < n_run;
-          const Ent e = valid ? bat[i] : mk_ent(-1, -1, 0, 0);
-          const int32_t ku = valid ? bat_u[i] : -1;
-          const bool done = valid && e.succ == s;
-          uint64_t dm = __ballot(done);
-          const uint64_t km = __ballot(valid && !done);
-          if (valid && !done) {
-            const int32_t to = kept + __popcll(km & lt);
-            bat[to] = e;
-            bat_u[to] = ku;
-            mk = uint32_t(e.succ) < mk ? uint32_t(e.succ) : mk;
-          }
-          kept += __popcll(km);
-          while (dm) {
-            const int l = ff1(dm);
-            dm &= dm - 1;
-            const int32_t rec = rdl(e.rec, l), k = rdl(ku, l);
-            const uint32_t elo = rdlu(e.lo, l), ehi = rdlu(e.hi, l);
-            const int64_t cst = int64_t(((uint64_t(ehi) << 32) | elo) >> 24);
-            const uint64_t fm = __ballot(xu == k);
-            int64_t uc;
-            if (fm) {  // a queued user: its key moves, its tier stays
-              const int32_t xx = ff1(fm);
-              uc = int64_t((uint64_t(rdlu(kh, xx) & kValHi) << 32) | rdlu(kl, xx)) + cst;
-              if (FS_RARE(uc >= kValueLimit)) {
-                code = FS_E_OVERFLOW;
-                break;
-              }
-              const uint32_t rv = rel_of(uc);
-              if (lane == xx) {
-                kh = uint32_t(uint64_t(uc) >> 32) | (xn > 0 ? 0u : kTier1);
-                kl = uint32_t(uint64_t(uc));
-                k32 = (xn > 0 ? 0u : kRelTier1) | rv;
-              }
-            } else {
-              uc = uni64(ulds ? u_lds[k] : ld_fresh(u_all + k)) + cst;
-              if (FS_RARE(uc >= kValueLimit)) {
-                code = FS_E_OVERFLOW;
-                break;
-              }
-              put_u(k, uc);
-              c_u = (w_user == k) ? uc : c_u;
+      uint64_t due = __ballot(cmin <= uint32_t(s));
+      if (due) stalled = false;
+      int64_t *const ca = KARG(counter_after);
+      while (due && !code) {
+        const int32_t c = ff1(due);
+        due &= due - 1;
+        const int32_t i = c * 64 + lane;
+        const bool valid = i < n_run;
+        const Ent e = valid ? bat[i] : mk_ent(-1, int32_t(kDeadFin), 0, 0);
+        const int32_t ku = valid ? bat_u[i] : -1;
+        const bool done = valid && e.succ == s;
+        if (done) bat[i].succ = int32_t(kDeadFin);
+        uint64_t dm = __ballot(done);
+        n_live -= __popcll(dm);
+        while (dm) {
+          const int l = ff1(dm);
+          dm &= dm - 1;
+          const int32_t rec = rdl(e.rec, l), k = rdl(ku, l);
+          const uint32_t elo = rdlu(e.lo, l), ehi = rdlu(e.hi, l);
+          const int64_t cst = int64_t(((uint64_t(ehi) << 32) | elo) >> 24);
+          const uint64_t fm = __ballot(xu == k);
+          int64_t uc;
+          if (fm) {  // a queued user: its key moves, its tier stays
+            const int32_t xx = ff1(fm);
+            uc = int64_t((uint64_t(rdlu(kh, xx) & kValHi) << 32) | rdlu(kl, xx)) + cst;
+            if (FS_RARE(uc >= kValueLimit)) {
+              code = FS_E_OVERFLOW;
+              break;
             }
-            if (k == last_exit) last_exit_u = uc;
-            if (lane == 0 && ca) ca[base + rec] = uc;
-            kv_used -= int64_t(elo & uint32_t(kTokMask));
+            const uint32_t rv = rel_of(uc);
+            if (lane == xx) {
+              kh = uint32_t(uint64_t(uc) >> 32) | (xn > 0 ? 0u : kTier1);
+              kl = uint32_t(uint64_t(uc));
+              k32 = (xn > 0 ? 0u : kRelTier1) | rv;
+            }
+          } else {
+            uc = uni64(ulds ? u_lds[k] : ld_fresh(u_all + k)) + cst;
+            if (FS_RARE(uc >= kValueLimit)) {
+              code = FS_E_OVERFLOW;
+              break;
+            }
+            put_u(k, uc);
+            c_u = (w_user == k) ? uc : c_u;
           }
+          if (k == last_exit) last_exit_u = uc;
+          if (lane == 0 && ca) ca[base + rec] = uc;
+          kv_used -= int64_t(elo & uint32_t(kTokMask));
         }
-        if (code) break;
-        n_run = nb0 = kept;
-        min_fin = kept > 0 ? int64_t(wave_min32(mk)) : INT64_MAX;
+        chunk_min(c);
+      }
+      if (code) break;
+      if (n_live == 0) {  // nothing runs: start the array afresh
+        n_run = nb0 = 0;
+        cmin = 0xffffffffu;
       }
     } else {
       debt = budget < 0 ? budget : 0;
@@ -993,6 +1028,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     if (low > nxt) low = nxt;
   }
   if (LITERAL) {  // the running batch goes to the state buffer
+    compact();
     int32_t *const rr_ = STATE(int32_t, run_rec) + base + r;
     int32_t *const rf_ = STATE(int32_t, run_fin) + base + r;
     for (int32_t i = lane; i < n_run; i += 64) {
@@ -1000,7 +1036,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       rf_[i] = bat[i].succ;
     }
   }
-  const bool drained = nxt == n && nX == 0 && n_run == 0;
+  const bool drained = nxt == n && nX == 0 && n_live == 0;
   if (lane == 0) {
     rs->kv_used = kv_used;
     rs->n_run = n_run;

@@ -145,8 +145,16 @@ __host__ __device__ inline int mask_width(uint32_t mask) {
   return w;
 }
 
-// Adds one item row to the tile histogram in LDS (equal digits aggregated per wave).
+// Adds one item row to the tile histogram in LDS.  Narrow digits (few bins, so many
+// lanes of a wave share one) are aggregated per wave first; wide digits go straight to
+// LDS atomics, whose same-address conflicts are then rare and cheaper than the
+// aggregation's ballots.
+constexpr int kPlainHistWidth = 6;
 __device__ inline void hist_add(uint32_t *h, uint32_t d, bool valid, int width) {
+  if (width >= kPlainHistWidth) {
+    if (valid) atomicAdd(&h[d], 1u);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const uint64_t peers = digit_peers(d, valid, width);
   if (valid && (peers & ((uint64_t(1) << lane) - 1)) == 0) atomicAdd(&h[d], uint32_t(__popcll(peers)));

@@ -66,6 +66,19 @@ struct __align__(16) Ent {
   uint32_t lo, hi;
 };
 
+// A batch of arrivals, lane-parallel: a user joining Q (its id, counter, segment and
+// its batch lanes) and a ready later call (record, next call, packed request, slot).
+struct __align__(16) JoinEnt {
+  int32_t k;
+  uint32_t seg, ulo, uhi, mlo, mhi, pad[2];
+};
+struct __align__(16) ReadyEnt {
+  int32_t rec, succ;
+  uint32_t lo, hi;
+  int32_t x, pad[3];
+};
+constexpr size_t kArriveBytes = kSlots * (sizeof(JoinEnt) + sizeof(ReadyEnt) + 4);
+
 __device__ inline Ent mk_ent(int32_t rec, int32_t sc, uint32_t lo, uint32_t hi) {
   Ent e;
   e.rec = rec;
@@ -105,12 +118,20 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   const int32_t D = a.oc.ring, M = a.oc.cache;
   const bool ulds = a.oc.users_lds != 0;
   const int32_t U = a.t.U;
+  const int ubits = U > 1 ? 32 - __builtin_clz(uint32_t(U - 1)) : 0;  // bits of a user id
   const int32_t BQ = LITERAL ? a.oc.batch : 0;
-  Ent *const ring = reinterpret_cast<Ent *>(smem);  // [kSlots][D]
+  JoinEnt *const a_join = reinterpret_cast<JoinEnt *>(smem);              // [kSlots]
+  ReadyEnt *const a_rdy = reinterpret_cast<ReadyEnt *>(a_join + kSlots);  // [kSlots]
+  int32_t *const a_free = reinterpret_cast<int32_t *>(a_rdy + kSlots);    // [kSlots]
+  Ent *const ring = reinterpret_cast<Ent *>(smem + kArriveBytes);  // [kSlots][D]
   Ent *const cache = ring + kSlots * D;             // [M]
   Ent *const bat = cache + M;                       // [BQ] rec, finish step, lo, hi
   int32_t *const bat_u = reinterpret_cast<int32_t *>(bat + BQ);  // [BQ] user
   int64_t *const u_lds = reinterpret_cast<int64_t *>(bat_u + BQ);
+  // two bytes per user (by the user's low bits) for matching a batch of arrivals
+  const int32_t u_tab = a.oc.user_tab;
+  uint8_t *const u_rep = reinterpret_cast<uint8_t *>(u_lds + (ulds ? U : 0));
+  uint8_t *const u_slot = u_rep + u_tab;
   const int64_t base = a.t.rep_off[r];
   const int32_t n = int32_t(a.t.rep_off[r + 1] - base);
   RepState *const rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
@@ -462,41 +483,6 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     load_window();
   };
 
-  // First calls of window lanes f (in lane order) join the tail of slot x's FIFO.
-  auto fifo_push_many = [&](int32_t x, uint64_t f) {
-    const int32_t fh = rdl(xf, x), rr = rdl(xr, x), tt = rdl(xt, x);
-    const int32_t cnt = __popcll(f);
-    int32_t ring_n = 0;
-    if (tt == rr) {
-      ring_n = fh + D - rr;
-      if (ring_n > cnt) ring_n = cnt;
-    }
-    if ((f >> lane) & 1) {
-      const int32_t rank = __popcll(f & ((uint64_t(1) << lane) - 1));
-      const int32_t ord = tt + rank;
-      const Ent e = mk_ent(wbase + lane, w_succ, w_lo, w_hi);
-      if (rank < ring_n)
-        ring[x * D + (ord & (D - 1))] = e;
-      else
-        STATE(Ent, seg_pk)[int64_t(rdlu(xsb, x)) + ord] = e;
-    }
-    if (tt == fh) {  // the FIFO was empty: its first entry is the new head
-      const int l0 = ff1(f);
-      const int32_t sc = rdl(w_succ, l0);
-      const uint32_t lo = rdlu(w_lo, l0), hi = rdlu(w_hi, l0);
-      if (lane == x) {
-        hrec = wbase + l0;
-        hsucc = sc;
-        hlo = lo;
-        hhi = hi;
-      }
-    }
-    if (lane == x) {
-      xr += ring_n;
-      xt += cnt;
-    }
-  };
-
   // All arrivals of the current step in window lanes [j0, j1) at once (X not empty,
   // so a user outside X is lifted to the least counter in X).  The overload test of
   // each arrival needs the tokens queued before it: as the queue only grows during
@@ -529,38 +515,192 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     w_flags |= hb_new ? kHeadBlk : 0;
     o_st = inb ? (bf ? why : (bl ? 3 : 0)) : o_st;
     backlog += int64_t(wave_sum32(inb && !blk ? tok : 0u));
-    const uint64_t firstm = __ballot(first);
-    uint64_t todo = __ballot(inb);
-    while (todo) {  // one user of the batch at a time
-      const int32_t jj = ff1(todo);
-      const int32_t k = rdl(w_user, jj);
-      const uint64_t same = __ballot(w_user == k) & todo;
-      todo &= ~same;
-      const uint64_t fm = __ballot(xu == k);
-      int32_t x = ff1(fm);
-      int64_t uk;
-      if (fm) {
-        uk = int64_t((uint64_t(rdlu(kh, x) & kValHi) << 32) | rdlu(kl, x));
-      } else {  // counter lift
-        const int64_t cu = rdl64(c_u, jj);
-        uk = cu > minX ? cu : minX;
-        if (uk != cu) {
-          put_u(k, uk);
-          c_u = (w_user == k) ? uk : c_u;
+    // same: batch lanes with this lane's user; x0: the slot holding this lane's user;
+    // mx: batch lanes with this slot's user
+    const uint64_t lt = (uint64_t(1) << lane) - 1;
+    const uint64_t inbm = __ballot(inb);
+    uint64_t same = inbm, mx = inbm;
+    int32_t x0 = -1;
+    bool matched = false;
+    {
+      // per-user tables in LDS, indexed by the user's low bits: a representative batch
+      // lane (any lane of the user) and the slot.  Entries of other users are stale or
+      // taken by a colliding user and are rejected by the checks below; a user who lost
+      // its entry to a collision sends the batch to the matching bit by bit.
+      const int32_t hw = w_user & (u_tab - 1), hx = xu & (u_tab - 1);
+      if (inb) u_rep[hw] = uint8_t(lane);
+      if (xu >= 0) u_slot[hx] = uint8_t(lane);
+      wave_fence();
+      const int32_t rr = w_user >= 0 ? int32_t(u_rep[hw]) : 64;
+      const int32_t xs = w_user >= 0 ? int32_t(u_slot[hw]) : 64;
+      const int32_t rx = xu >= 0 ? int32_t(u_rep[hx]) : 64;
+      const bool lost = xu >= 0 && int32_t(u_slot[hx]) != lane;
+      const int32_t rr_user = __builtin_amdgcn_ds_bpermute((rr & 63) << 2, w_user);
+      const int32_t xs_user = __builtin_amdgcn_ds_bpermute((xs & 63) << 2, xu);
+      const int32_t rx_user = __builtin_amdgcn_ds_bpermute((rx & 63) << 2, w_user);
+      const int32_t rp = (rr < 64 && ((inbm >> rr) & 1) && rr_user == w_user) ? rr : 64;
+      const int32_t rxv = (rx < 64 && ((inbm >> rx) & 1) && rx_user == xu) ? rx : 64;
+      if (!__ballot(lost || (inb && rp == 64))) {
+        matched = true;
+        x0 = (xs < 64 && ((occ >> xs) & 1) && xs_user == w_user) ? xs : -1;
+        // a user with one batch lane is its own representative; the batch lanes of a
+        // user with several are gathered one such user at a time
+        same = rp < 64 ? uint64_t(1) << rp : 0;
+        mx = rxv < 64 ? uint64_t(1) << rxv : 0;
+        for (uint64_t dm = __ballot(inb && rp != lane); dm;) {
+          const int32_t rq = rdl(rp, ff1(dm));
+          const uint64_t m = __ballot(inb && rp == rq);
+          dm &= ~m;
+          if (rp == rq) same = m;
+          if (rxv == rq) mx = m;
         }
       }
-      o_coa = ((same >> lane) & 1) ? uk : o_coa;
-      const uint64_t mine = same & ub;
-      if (!mine) continue;
-      if (!fm) x = join(k, uk, rdlu(w_seg, jj));
-      if (lane == x) xq += __popcll(mine);
-      const uint64_t fifo_m = fcfs ? mine : (mine & firstm);
-      if (fifo_m) fifo_push_many(x, fifo_m);
-      uint64_t rm = mine & rdym;
-      while (rm) {
-        const int l = ff1(rm);
-        rm &= rm - 1;
-        ready_add(x, wbase + l, rdl(w_succ, l), rdlu(w_lo, l), rdlu(w_hi, l));
+    }
+    if (FS_RARE(!matched)) {
+      // users matched bit by bit: W = batch lanes whose user has bit b set, S = slots
+      // whose user has it
+      uint64_t sm = occ;
+      for (int b = 0; b < ubits; ++b) {
+        const bool wb = (uint32_t(w_user) >> b) & 1u, xb = (uint32_t(xu) >> b) & 1u;
+        const uint64_t W = __ballot(inb && wb), S = __ballot(xu >= 0 && xb);
+        same &= wb ? W : ~W;
+        sm &= wb ? S : ~S;
+        mx &= xb ? W : ~W;
+      }
+      x0 = sm ? ff1(sm) : -1;
+    }
+    const int32_t lead = ff1(same);  // the user's first lane in the batch
+    const uint64_t newm = __ballot(inb && x0 < 0);
+    // users outside Q are lifted to the least counter in Q, on every arrival
+    const int64_t lifted = c_u > minX ? c_u : minX;
+    const bool is_lead = inb && lane == lead;
+    if (is_lead && x0 < 0 && lifted != c_u) {
+      if (ulds)
+        u_lds[w_user] = lifted;
+      else
+        u_all[w_user] = lifted;
+    }
+    {
+      const int src = (x0 >= 0 ? x0 : lane) << 2;
+      const uint32_t sh = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(kh & kValHi)));
+      const uint32_t sl = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(kl)));
+      const int64_t us = int64_t((uint64_t(sh) << 32) | sl);
+      if (inb) o_coa = x0 >= 0 ? us : lifted;
+    }
+    if (w_user >= 0 && (same & newm)) c_u = lifted;
+    // users joining Q, at their first batch lane: the i-th takes the i-th free slot
+    const bool jl = is_lead && x0 < 0 && (same & ub) != 0;
+    const uint64_t jm = __ballot(jl);
+    int32_t xj = x0;
+    if (jm) {
+      const int32_t J = __popcll(jm);
+      const bool fr = !((occ >> lane) & 1);
+      const int32_t fi = __popcll(~occ & lt);
+      if (fr) a_free[fi] = lane;
+      const int32_t ji = __popcll(jm & lt);
+      if (jl) {
+        JoinEnt e;
+        e.k = w_user;
+        e.seg = w_seg;
+        e.ulo = uint32_t(uint64_t(lifted));
+        e.uhi = uint32_t(uint64_t(lifted) >> 32);
+        e.mlo = uint32_t(same);
+        e.mhi = uint32_t(same >> 32);
+        a_join[ji] = e;
+      }
+      wave_fence();
+      if (jl) xj = a_free[ji];
+      const bool ns = fr && fi < J;  // a slot taken now
+      bool sat = false;
+      if (ns) {
+        const JoinEnt e = a_join[fi];
+        const int64_t uk = int64_t((uint64_t(e.uhi) << 32) | e.ulo);
+        const int64_t d = uk - B;
+        sat = d < 0 || d >= int64_t(kRelMax);
+        k32 = kRelTier1 | (sat ? kRelMax : uint32_t(d));
+        kh = e.uhi | kTier1;
+        kl = e.ulo;
+        xu = e.k;
+        xq = 0;
+        xf = xr = xt = 0;
+        xsb = e.seg;
+        xn = 0;
+        mx = (uint64_t(e.mhi) << 32) | e.mlo;
+      }
+      if (__ballot(sat)) wide = true;
+      occ |= __ballot(ns);
+      nX += J;
+      // the other batch lanes of a joining user take its slot from its first lane
+      const int32_t xl = __builtin_amdgcn_ds_bpermute((inb ? lead : lane) << 2, xj);
+      if (inb && x0 < 0) xj = xl;
+    }
+    // per slot: queued calls, first calls for its FIFO (in lane order), ready calls
+    const uint64_t F = ub & (fcfs ? ~uint64_t(0) : __ballot(first));
+    const bool oc = xu >= 0;
+    const uint64_t mF = oc ? (mx & F) : 0, mR = oc ? (mx & rdym) : 0, mU = oc ? (mx & ub) : 0;
+    const int32_t cF = __popcll(mF), cR = __popcll(mR), cU = __popcll(mU);
+    int32_t ring_n = 0;
+    if (cF > 0 && xt == xr) {
+      ring_n = xf + D - xr;
+      if (ring_n > cF) ring_n = cF;
+    }
+    if (F) {
+      const int src = (((F >> lane) & 1) ? xj : lane) << 2;
+      const int32_t tt = __builtin_amdgcn_ds_bpermute(src, xt);
+      const uint32_t sb = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(xsb)));
+      const int32_t rn = __builtin_amdgcn_ds_bpermute(src, ring_n);
+      // the head of a FIFO that was empty: its first pushed call
+      const int l0 = mF ? ff1(mF) : lane;
+      const int32_t hs = __builtin_amdgcn_ds_bpermute(l0 << 2, w_succ);
+      const uint32_t hl = uint32_t(__builtin_amdgcn_ds_bpermute(l0 << 2, int(w_lo)));
+      const uint32_t hh = uint32_t(__builtin_amdgcn_ds_bpermute(l0 << 2, int(w_hi)));
+      if ((F >> lane) & 1) {
+        const int32_t rank = __popcll(same & F & lt);
+        const int32_t ord = tt + rank;
+        const Ent e = mk_ent(wbase + lane, w_succ, w_lo, w_hi);
+        if (rank < rn)
+          ring[xj * D + (ord & (D - 1))] = e;
+        else
+          STATE(Ent, seg_pk)[int64_t(sb) + ord] = e;
+      }
+      if (cF > 0 && xt == xf) {
+        hrec = wbase + l0;
+        hsucc = hs;
+        hlo = hl;
+        hhi = hh;
+      }
+      xr += ring_n;
+      xt += cF;
+    }
+    xq += cU;
+    if (rdym) {  // ready later calls: the i-th takes the i-th free ready lane
+      const int32_t NR = __popcll(rdym);
+      const bool pf = !((pocc >> lane) & 1);
+      const int32_t pi = __popcll(~pocc & lt);
+      if ((rdym >> lane) & 1) {
+        ReadyEnt e;
+        e.rec = wbase + lane;
+        e.succ = w_succ;
+        e.lo = w_lo;
+        e.hi = w_hi;
+        e.x = xj;
+        a_rdy[__popcll(rdym & lt)] = e;
+      }
+      wave_fence();
+      const bool np = pf && pi < NR;
+      if (np) {
+        const ReadyEnt e = a_rdy[pi];
+        p_x = e.x;
+        p_rec = e.rec;
+        p_succ = e.succ;
+        p_lo = e.lo;
+        p_hi = e.hi;
+      }
+      pocc |= __ballot(np);
+      if (cR > 0) {
+        xn += cR;
+        kh &= kValHi;  // tier 0
+        k32 &= kRelMax;
       }
     }
     return true;
@@ -1100,7 +1240,11 @@ OnchipCfg onchip_config(int32_t R, int32_t U, bool literal) {
   const size_t bat_bytes = size_t(batch) * (sizeof(Ent) + 4);
   c.users_lds = size_t(U) * 8 <= budget / 4 ? 1 : 0;
   const size_t users = c.users_lds ? size_t(U) * 8 : 0;
-  size_t left = budget - users - bat_bytes;
+  int tab_n = 64;  // power of two, at least U up to 4096
+  while (tab_n < U && tab_n < 4096) tab_n <<= 1;
+  c.user_tab = tab_n;
+  const size_t tab = size_t(tab_n) * 2;
+  size_t left = budget - kArriveBytes - users - bat_bytes - tab;
   // about half for the rings, the rest for the arrival cache
   int ring = 64;
   while (ring > 8 && size_t(kSlots) * ring * sizeof(Ent) > left / 2) ring >>= 1;
@@ -1109,7 +1253,8 @@ OnchipCfg onchip_config(int32_t R, int32_t U, bool literal) {
   while (cache > 64 && size_t(cache) * sizeof(Ent) > left) cache >>= 1;
   c.ring = ring;
   c.cache = cache;
-  c.lds_bytes = size_t(kSlots) * ring * sizeof(Ent) + size_t(cache) * sizeof(Ent) + bat_bytes + users;
+  c.lds_bytes = kArriveBytes + size_t(kSlots) * ring * sizeof(Ent) + size_t(cache) * sizeof(Ent) +
+                bat_bytes + users + tab;
   return c;
 }
 

@@ -69,6 +69,20 @@ def test_workloads_schedule(name, kw):
     compare_sim(g, o)
 
 
+def test_users_sharing_low_bits():
+    """User ids spread so that groups of users share their low 12 bits: the on-chip
+    kernel's per-user tables for a batch of arrivals collide often (and then match users
+    bit by bit), and must give the same schedule."""
+    wl, tr = workload_trace("c2_replicas", replicas=4, records=15000)
+    spread = (tr.user % 3) + 4096 * (tr.user // 3)
+    tr = tg.Trace(**{**tr.__dict__, "user": spread.astype(np.int32),
+                     "n_users": int(spread.max()) + 1})
+    say("sched colliding users", tr.n, tr.n_users)
+    g, o, _, _ = _run_workload(wl, tr)
+    compare_sim(g, o)
+    assert (o.status == 0).any() and (o.status > 0).any()
+
+
 def test_global_memory_path_matches():
     wl, tr = workload_trace("c2_replicas", replicas=2, records=20000)
     g, o, _, _ = _run_workload(wl, tr, global_only=True)

@@ -588,11 +588,32 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (inb) o_coa = x0 >= 0 ? us : lifted;
     }
     if (w_user >= 0 && (same & newm)) c_u = lifted;
-    // users joining Q, at their first batch lane: the i-th takes the i-th free slot
+    // users joining Q, at their first batch lane.  Which slot a user holds changes no
+    // result (ties go by user id), so each takes the slot of its own lane when all of
+    // those are free, else the i-th takes the i-th free slot.
     const bool jl = is_lead && x0 < 0 && (same & ub) != 0;
     const uint64_t jm = __ballot(jl);
     int32_t xj = x0;
-    if (jm) {
+    if (jm && !(jm & occ)) {
+      bool sat = false;
+      if (jl) {
+        const int64_t d = lifted - B;
+        sat = d < 0 || d >= int64_t(kRelMax);
+        k32 = kRelTier1 | (sat ? kRelMax : uint32_t(d));
+        kh = uint32_t(uint64_t(lifted) >> 32) | kTier1;
+        kl = uint32_t(uint64_t(lifted));
+        xu = w_user;
+        xq = 0;
+        xf = xr = xt = 0;
+        xsb = w_seg;
+        xn = 0;
+        mx = same;
+      }
+      if (__ballot(sat)) wide = true;
+      occ |= jm;
+      nX += __popcll(jm);
+      if (inb && x0 < 0) xj = ((jm >> lead) & 1) ? lead : -1;
+    } else if (jm) {
       const int32_t J = __popcll(jm);
       const bool fr = !((occ >> lane) & 1);
       const int32_t fi = __popcll(~occ & lt);
@@ -673,7 +694,21 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       xt += cF;
     }
     xq += cU;
-    if (rdym) {  // ready later calls: the i-th takes the i-th free ready lane
+    if (rdym && !(rdym & pocc)) {  // ready later calls, each in the ready lane of its lane
+      if ((rdym >> lane) & 1) {
+        p_x = xj;
+        p_rec = wbase + lane;
+        p_succ = w_succ;
+        p_lo = w_lo;
+        p_hi = w_hi;
+      }
+      pocc |= rdym;
+      if (cR > 0) {
+        xn += cR;
+        kh &= kValHi;  // tier 0
+        k32 &= kRelMax;
+      }
+    } else if (rdym) {  // or the i-th takes the i-th free ready lane
       const int32_t NR = __popcll(rdym);
       const bool pf = !((pocc >> lane) & 1);
       const int32_t pi = __popcll(~pocc & lt);

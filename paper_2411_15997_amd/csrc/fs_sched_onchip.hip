@@ -119,6 +119,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   const bool ulds = a.oc.users_lds != 0;
   const int32_t U = a.t.U;
   const int ubits = U > 1 ? 32 - __builtin_clz(uint32_t(U - 1)) : 0;  // bits of a user id
+  const bool want_coa = a.counter_on_arrival != nullptr;
   const int32_t BQ = LITERAL ? a.oc.batch : 0;
   JoinEnt *const a_join = reinterpret_cast<JoinEnt *>(smem);              // [kSlots]
   ReadyEnt *const a_rdy = reinterpret_cast<ReadyEnt *>(a_join + kSlots);  // [kSlots]
@@ -495,16 +496,23 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const bool first = (w_flags & kFirst) != 0;
     const int32_t why = (w_flags >> kReasonShift) & 3;
     const uint32_t tok = w_lo & uint32_t(kTokMask);
-    const uint32_t c0 = (inb && (first || !(w_flags & kHeadBlk))) ? tok : 0u;
-    const uint32_t excl = wave_incl_scan32(c0) - c0;
-    const int64_t thr = theta - backlog;  // overloaded at a lane iff excl > thr
-    const bool ovl = thr < 0 ? true : (thr >= int64_t(INT32_MAX) ? false : excl > uint32_t(thr));
-    const bool bf = inb && first && ovl && why != 0;
+    bool bf = false;  // a first call throttled (over a limit while the system is overloaded)
+    if (__ballot(inb && first && why != 0)) {
+      const uint32_t c0 = (inb && (first || !(w_flags & kHeadBlk))) ? tok : 0u;
+      const uint32_t excl = wave_incl_scan32(c0) - c0;
+      const int64_t thr = theta - backlog;  // overloaded at a lane iff excl > thr
+      const bool ovl =
+          thr < 0 ? true : (thr >= int64_t(INT32_MAX) ? false : excl > uint32_t(thr));
+      bf = inb && first && ovl && why != 0;
+    }
     // a later call shares its first call's fate: throttled before the batch or in it
-    const int32_t hl = w_head - wbase;
-    const bool hl_in = hl >= j0 && hl < j1;
-    const int hb_src = __builtin_amdgcn_ds_bpermute((hl_in ? hl : lane) << 2, bf ? 1 : 0);
-    const bool hb_new = !first && w_head >= 0 && hl_in && hb_src != 0;
+    bool hb_new = false;
+    if (__ballot(bf)) {
+      const int32_t hl = w_head - wbase;
+      const bool hl_in = hl >= j0 && hl < j1;
+      const int hb_src = __builtin_amdgcn_ds_bpermute((hl_in ? hl : lane) << 2, bf ? 1 : 0);
+      hb_new = !first && w_head >= 0 && hl_in && hb_src != 0;
+    }
     const bool bl = inb && !first && ((w_flags & kHeadBlk) || hb_new);
     const bool blk = bf || bl;
     const uint64_t ub = __ballot(inb && !blk);
@@ -580,7 +588,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       else
         u_all[w_user] = lifted;
     }
-    {
+    if (want_coa) {  // (an optional output)
       const int src = (x0 >= 0 ? x0 : lane) << 2;
       const uint32_t sh = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(kh & kValHi)));
       const uint32_t sl = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(kl)));

@@ -100,6 +100,13 @@ def test_replica_workload(chunks):
     assert (o.status > 0).any() and (o.status == 0).any()
 
 
+def test_without_optional_outputs():
+    wl, tr, c = _workload("c2_replicas", replicas=4, records=15000)
+    raw = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False).reason
+    say("literal no optional outputs", tr.n)
+    _run(tr, c, raw, 20_000, 1 << 20, 1 << 20, L, parity=False)
+
+
 def test_bounded_run_is_a_prefix():
     wl, tr, c = _workload("c2_replicas", replicas=2, records=8000)
     raw = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False).reason

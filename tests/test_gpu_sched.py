@@ -83,6 +83,24 @@ def test_users_sharing_low_bits():
     assert (o.status == 0).any() and (o.status > 0).any()
 
 
+@pytest.mark.parametrize("name,kw", [("c2_replicas", dict(replicas=4, records=15000)),
+                                     ("c4_sweep", dict(replicas=16))])
+def test_without_optional_outputs(name, kw):
+    """Without admit_seq, counter_after and counter_on_arrival (the kernel then skips
+    the work that only feeds them) the remaining outputs are unchanged."""
+    wl, tr = workload_trace(name, **kw)
+    coef, per_rep = fs.workload_weights(wl, tr)
+    c = oracle.cost(tr, coef, coef_per_replica=per_rep)
+    th = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
+    o = oracle.simulate(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens,
+                        n_threads=8)
+    say("sched no optional outputs", name, tr.n)
+    g = gpu_schedule(tr, c, th.reason, wl.step_us, wl.cap_tokens, wl.overload_tokens,
+                     parity=False)
+    assert g["admit_seq"] is None and g["counter_on_arrival"] is None
+    compare_sim(g, o)
+
+
 def test_global_memory_path_matches():
     wl, tr = workload_trace("c2_replicas", replicas=2, records=20000)
     g, o, _, _ = _run_workload(wl, tr, global_only=True)

@@ -329,6 +329,18 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       k32 &= kRelMax;
     }
   };
+  // ---- window of upcoming records, one per lane
+  int32_t wbase = nxt, cache_from = nxt, cache_lo = nxt;
+  int32_t w_step = INT32_MAX, w_user = -1, w_flags = 0, w_head = -1, w_prev = -1, w_succ = -1;
+  uint32_t w_seg = 0, w_lo = 0, w_hi = 0;
+  int64_t c_u = 0;
+  int32_t o_st = 0;
+  int64_t o_coa = 0;
+  bool w_wait = false;  // the window holds later calls whose previous call is not admitted
+  // window lanes: the slot holding the lane's user (-1: none) and the window lanes of
+  // the same user; slots: the window lanes of the slot's user
+  int32_t w_slot = -1;
+  uint64_t w_gm = 0, xwm = 0;
   // Slot for user k with counter uk (tier 1, nothing queued yet).
   auto join = [&](int32_t k, int64_t uk, uint32_t sb) -> int32_t {
     const int32_t x = ff1(~occ);
@@ -348,6 +360,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       xsb = sb;
       xn = 0;
     }
+    const uint64_t km = __ballot(w_user == k);
+    w_slot = (w_user == k) ? x : w_slot;
+    xwm = lane == x ? km : xwm;
     return x;
   };
   // Data of an arrived record read from the inputs (when it is no longer cached).
@@ -383,14 +398,6 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     nd = 0;
   };
 
-  // ---- window of upcoming records, one per lane
-  int32_t wbase = nxt, cache_from = nxt, cache_lo = nxt;
-  int32_t w_step = INT32_MAX, w_user = -1, w_flags = 0, w_head = -1, w_prev = -1, w_succ = -1;
-  uint32_t w_seg = 0, w_lo = 0, w_hi = 0;
-  int64_t c_u = 0;
-  int32_t o_st = 0;
-  int64_t o_coa = 0;
-  bool w_wait = false;  // the window holds later calls whose previous call is not admitted
   auto flush_window = [&]() {
     const int32_t done = nxt - wbase;
     int8_t *const fate = STATE(int8_t, fate);
@@ -411,6 +418,49 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       if (coa) coa[g] = o_coa;
     }
     o_st = 0;
+  };
+  // The window's users matched once per window: per-user tables in LDS, indexed by the
+  // user's low bits, give a representative window lane (any lane of the user) and the
+  // slot.  Entries taken by a colliding user are rejected by the checks below; a user
+  // who lost its entry sends the window to the matching bit by bit.
+  auto match_window = [&]() {
+    const bool wv = w_user >= 0;
+    const uint64_t wvm = __ballot(wv);
+    const int32_t hw = w_user & (u_tab - 1), hx = xu & (u_tab - 1);
+    if (wv) u_rep[hw] = uint8_t(lane);
+    if (xu >= 0) u_slot[hx] = uint8_t(lane);
+    wave_fence();
+    const int32_t rr = wv ? int32_t(u_rep[hw]) : 64;
+    const int32_t xs = wv ? int32_t(u_slot[hw]) : 64;
+    const int32_t rx = xu >= 0 ? int32_t(u_rep[hx]) : 64;
+    const bool lost = xu >= 0 && int32_t(u_slot[hx]) != lane;
+    const int32_t rr_user = __builtin_amdgcn_ds_bpermute((rr & 63) << 2, w_user);
+    const int32_t xs_user = __builtin_amdgcn_ds_bpermute((xs & 63) << 2, xu);
+    const int32_t rx_user = __builtin_amdgcn_ds_bpermute((rx & 63) << 2, w_user);
+    const int32_t rp = (wv && rr < 64 && rr_user == w_user) ? rr : 64;
+    const int32_t rxv = (xu >= 0 && rx < 64 && rx_user == xu) ? rx : 64;
+    uint64_t g = wvm, m = wvm;
+    if (!__ballot(lost || (wv && rp == 64))) {
+      w_slot = (wv && xs < 64 && ((occ >> xs) & 1) && xs_user == w_user) ? xs : -1;
+      for (int b = 0; b < 6; ++b) {  // lanes match on their representative's bits
+        const uint64_t W = __ballot(wv && ((rp >> b) & 1));
+        g &= ((rp >> b) & 1) ? W : ~W;
+        m &= ((rxv >> b) & 1) ? W : ~W;
+      }
+      xwm = (xu >= 0 && rxv < 64) ? m : 0;
+    } else {
+      uint64_t sm = occ;
+      for (int b = 0; b < ubits; ++b) {
+        const bool wb = (uint32_t(w_user) >> b) & 1u, xb = (uint32_t(xu) >> b) & 1u;
+        const uint64_t W = __ballot(wv && wb), S = __ballot(xu >= 0 && xb);
+        g &= wb ? W : ~W;
+        sm &= wb ? S : ~S;
+        m &= xb ? W : ~W;
+      }
+      w_slot = (wv && sm) ? ff1(sm) : -1;
+      xwm = xu >= 0 ? m : 0;
+    }
+    w_gm = wv ? g : 0;
   };
   auto load_window = [&]() {
     wave_fence();
@@ -476,6 +526,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const int32_t lo_ = wbase + 64 - M;
     cache_lo = lo_ > cache_from ? lo_ : cache_from;
     w_wait = __ballot(w_user >= 0 && !(w_flags & (kFirst | kPrevAdm))) != 0;
+    match_window();
   };
   auto advance_window = [&]() {
     flush_window();
@@ -527,56 +578,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     // mx: batch lanes with this slot's user
     const uint64_t lt = (uint64_t(1) << lane) - 1;
     const uint64_t inbm = __ballot(inb);
-    uint64_t same = inbm, mx = inbm;
-    int32_t x0 = -1;
-    bool matched = false;
-    {
-      // per-user tables in LDS, indexed by the user's low bits: a representative batch
-      // lane (any lane of the user) and the slot.  Entries of other users are stale or
-      // taken by a colliding user and are rejected by the checks below; a user who lost
-      // its entry to a collision sends the batch to the matching bit by bit.
-      const int32_t hw = w_user & (u_tab - 1), hx = xu & (u_tab - 1);
-      if (inb) u_rep[hw] = uint8_t(lane);
-      if (xu >= 0) u_slot[hx] = uint8_t(lane);
-      wave_fence();
-      const int32_t rr = w_user >= 0 ? int32_t(u_rep[hw]) : 64;
-      const int32_t xs = w_user >= 0 ? int32_t(u_slot[hw]) : 64;
-      const int32_t rx = xu >= 0 ? int32_t(u_rep[hx]) : 64;
-      const bool lost = xu >= 0 && int32_t(u_slot[hx]) != lane;
-      const int32_t rr_user = __builtin_amdgcn_ds_bpermute((rr & 63) << 2, w_user);
-      const int32_t xs_user = __builtin_amdgcn_ds_bpermute((xs & 63) << 2, xu);
-      const int32_t rx_user = __builtin_amdgcn_ds_bpermute((rx & 63) << 2, w_user);
-      const int32_t rp = (rr < 64 && ((inbm >> rr) & 1) && rr_user == w_user) ? rr : 64;
-      const int32_t rxv = (rx < 64 && ((inbm >> rx) & 1) && rx_user == xu) ? rx : 64;
-      if (!__ballot(lost || (inb && rp == 64))) {
-        matched = true;
-        x0 = (xs < 64 && ((occ >> xs) & 1) && xs_user == w_user) ? xs : -1;
-        // a user with one batch lane is its own representative; the batch lanes of a
-        // user with several are gathered one such user at a time
-        same = rp < 64 ? uint64_t(1) << rp : 0;
-        mx = rxv < 64 ? uint64_t(1) << rxv : 0;
-        for (uint64_t dm = __ballot(inb && rp != lane); dm;) {
-          const int32_t rq = rdl(rp, ff1(dm));
-          const uint64_t m = __ballot(inb && rp == rq);
-          dm &= ~m;
-          if (rp == rq) same = m;
-          if (rxv == rq) mx = m;
-        }
-      }
-    }
-    if (FS_RARE(!matched)) {
-      // users matched bit by bit: W = batch lanes whose user has bit b set, S = slots
-      // whose user has it
-      uint64_t sm = occ;
-      for (int b = 0; b < ubits; ++b) {
-        const bool wb = (uint32_t(w_user) >> b) & 1u, xb = (uint32_t(xu) >> b) & 1u;
-        const uint64_t W = __ballot(inb && wb), S = __ballot(xu >= 0 && xb);
-        same &= wb ? W : ~W;
-        sm &= wb ? S : ~S;
-        mx &= xb ? W : ~W;
-      }
-      x0 = sm ? ff1(sm) : -1;
-    }
+    const uint64_t same = w_gm & inbm;
+    uint64_t mx = xwm & inbm;
+    const int32_t x0 = w_slot;
     const int32_t lead = ff1(same);  // the user's first lane in the batch
     const uint64_t newm = __ballot(inb && x0 < 0);
     // users outside Q are lifted to the least counter in Q, on every arrival
@@ -616,11 +620,16 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         xsb = w_seg;
         xn = 0;
         mx = same;
+        xwm = w_gm;
       }
       if (__ballot(sat)) wide = true;
       occ |= jm;
       nX += __popcll(jm);
-      if (inb && x0 < 0) xj = ((jm >> lead) & 1) ? lead : -1;
+      // every window lane of a joining user: the slot is its first batch lane
+      if (lead >= 0 && ((jm >> lead) & 1)) {
+        w_slot = lead;
+        xj = lead;
+      }
     } else if (jm) {
       const int32_t J = __popcll(jm);
       const bool fr = !((occ >> lane) & 1);
@@ -633,8 +642,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         e.seg = w_seg;
         e.ulo = uint32_t(uint64_t(lifted));
         e.uhi = uint32_t(uint64_t(lifted) >> 32);
-        e.mlo = uint32_t(same);
-        e.mhi = uint32_t(same >> 32);
+        e.mlo = uint32_t(w_gm);
+        e.mhi = uint32_t(w_gm >> 32);
         a_join[ji] = e;
       }
       wave_fence();
@@ -654,14 +663,18 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         xf = xr = xt = 0;
         xsb = e.seg;
         xn = 0;
-        mx = (uint64_t(e.mhi) << 32) | e.mlo;
+        xwm = (uint64_t(e.mhi) << 32) | e.mlo;
+        mx = xwm & inbm;
       }
       if (__ballot(sat)) wide = true;
       occ |= __ballot(ns);
       nX += J;
-      // the other batch lanes of a joining user take its slot from its first lane
-      const int32_t xl = __builtin_amdgcn_ds_bpermute((inb ? lead : lane) << 2, xj);
-      if (inb && x0 < 0) xj = xl;
+      // every window lane of a joining user takes its slot from its first batch lane
+      const int32_t xl = __builtin_amdgcn_ds_bpermute((lead >= 0 ? lead : lane) << 2, xj);
+      if (lead >= 0 && ((jm >> lead) & 1)) {
+        w_slot = xl;
+        xj = xl;
+      }
     }
     // per slot: queued calls, first calls for its FIFO (in lane order), ready calls
     const uint64_t F = ub & (fcfs ? ~uint64_t(0) : __ballot(first));
@@ -1064,6 +1077,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         last_exit_u = unew;
         put_u(k, unew);
         c_u = (w_user == k) ? unew : c_u;
+        w_slot = (w_user == k) ? -1 : w_slot;
       } else {
         const uint32_t rv = rel_of(unew);
         if (lane == x) {

@@ -46,12 +46,12 @@ STAGE_SRC = {
 # and stage; an entry counts only while the stage's sources hash to `src`.
 MEASURED_TRAFFIC = {
     # k_schedule_onchip on the 64 x 256 x 8 replica workload (6.4M requests)
-    ("c2_replicas", "schedule"): {"src": "ac34baed908274ec", "fetch_kib": 147741.0625,
-                                  "write_kib": 38757.34375, "fetch_factor": 1.99993,
+    ("c2_replicas", "schedule"): {"src": "f135e02d3147922f", "fetch_kib": 147799.9375,
+                                  "write_kib": 38770.25, "fetch_factor": 1.99993,
                                   "write_factor": 1.0},
     # k_schedule_onchip on the 1,024-replica weight sweep (20.48M requests)
-    ("c4_sweep", "schedule"): {"src": "ac34baed908274ec", "fetch_kib": 353937.5625,
-                               "write_kib": 137777.09375, "fetch_factor": 1.99987,
+    ("c4_sweep", "schedule"): {"src": "f135e02d3147922f", "fetch_kib": 353946.5,
+                               "write_kib": 137780.4375, "fetch_factor": 1.99988,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
     ("c3_throttle", "throttle"): {"src": "c204dcaa8544790f", "fetch_kib": 2874968.3125,

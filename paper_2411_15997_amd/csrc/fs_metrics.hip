@@ -98,8 +98,87 @@ __device__ inline void wave_add_by_key(bool active, int64_t key, unsigned long l
   }
 }
 
+// The same for keys that are mostly distinct within a wave (users): lanes of one key
+// find a representative lane through a per-wave hash table in LDS (any lane of the key
+// wins the slot), add into its LDS accumulator, and the representative issues one
+// atomic.  A lane whose key lost its slot to another key updates its own key.
+constexpr int kKeyTab = 1024;  // hash slots per wave
+struct KeyScratch {
+  uint8_t tab[kKeyTab];
+  unsigned long long acc[64];
+  uint32_t accf[64];
+};
+// (skip_set: read the flags first and skip the atomic when they are already set.)
+__device__ inline void wave_add_by_key_hashed(bool active, int64_t key, unsigned long long v,
+                                              unsigned long long *sum_base, uint32_t f,
+                                              uint32_t *or_base, KeyScratch &ks,
+                                              bool skip_set = false) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t h = (uint32_t(uint64_t(key)) * 2654435761u) >> 22;  // 10 bits
+  if (active) ks.tab[h] = uint8_t(lane);
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  const int rp = active ? int(ks.tab[h]) : lane;
+  const int64_t rk = __shfl(key, rp, 64);
+  const bool own = active && rk == key;
+  const bool lead = own && rp == lane;
+  if (lead) {
+    ks.acc[lane] = 0;
+    ks.accf[lane] = 0;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  if (own) {
+    if (v) atomicAdd(&ks.acc[rp], v);
+    if (or_base && f) atomicOr(&ks.accf[rp], f);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  if (lead) {
+    const unsigned long long t = ks.acc[lane];
+    const uint32_t fl = ks.accf[lane];
+    if (t) atomicAdd(sum_base + key, t);
+    if (or_base && fl && !(skip_set && (or_base[key] & fl) == fl)) atomicOr(or_base + key, fl);
+  } else if (active && !own) {
+    if (v) atomicAdd(sum_base + key, v);
+    if (or_base && f && !(skip_set && (or_base[key] & f) == f)) atomicOr(or_base + key, f);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
+
+// Up to three small per-replica counts (each below 2^16 in a wave) in one reduction:
+// counters[r * C_NUM + c_i] += x_i for each distinct replica r of the active lanes.
+__device__ inline void wave_count3(bool active, int32_t r, unsigned long long *counters,
+                                   int c0, uint32_t x0, int c1, uint32_t x1, int c2, uint32_t x2) {
+  const int lane = threadIdx.x & 63;
+  uint64_t pending = __ballot(active);
+  while (pending) {
+    const int leader = __ffsll((long long)pending) - 1;
+    const int32_t rl = __shfl(r, leader, 64);
+    const bool mine = active && r == rl;
+    const unsigned long long packed =
+        mine ? (uint64_t(x0) | (uint64_t(x1) << 16) | (uint64_t(x2) << 32)) : 0ull;
+    const unsigned long long total = wave_sum(packed);
+    if (lane == leader) {
+      unsigned long long *cr = counters + int64_t(rl) * C_NUM;
+      const unsigned long long t0 = total & 0xffffu, t1 = (total >> 16) & 0xffffu,
+                               t2 = (total >> 32) & 0xffffu;
+      if (c0 >= 0 && t0) atomicAdd(cr + c0, t0);
+      if (c1 >= 0 && t1) atomicAdd(cr + c1, t1);
+      if (c2 >= 0 && t2) atomicAdd(cr + c2, t2);
+    }
+    pending &= ~__ballot(mine);
+  }
+}
+
+// The replica of record g, walking forward from the replica of the block's first
+// record (records of a replica are contiguous, so a block spans few of them).
+__device__ inline int32_t replica_from(const int64_t *rep_off, int32_t r0, int64_t g) {
+  int32_t r = r0;
+  while (__ldg(rep_off + r + 1) <= g) ++r;
+  return r;
+}
+
 // Pass 1: per record -- validity, user flags, charged service, interaction flags.
 __global__ void __launch_bounds__(256) k_m_records(MArgs a) {
+  __shared__ KeyScratch ks[4];
   const DevTrace &t = a.t;
   int32_t code = 0;
   // grid-stride over whole waves so that every lane takes part in the wave reductions
@@ -109,8 +188,9 @@ __global__ void __launch_bounds__(256) k_m_records(MArgs a) {
     bool ok = g < t.N;
     int32_t r = 0, k = 0;
     int64_t base = 0, i = 0, h = 0;
+    const int32_t r0 = replica_of(t.rep_off, t.R, base0);  // (a uniform search)
     if (ok) {
-      r = replica_of(t.rep_off, t.R, g);
+      r = replica_from(t.rep_off, r0, g);
       base = t.rep_off[r];
       i = g - base;
       k = t.user[g];
@@ -135,20 +215,17 @@ __global__ void __launch_bounds__(256) k_m_records(MArgs a) {
     if (served && int64_t(a.admit_step[g]) - t.ts[g] / a.tau > a.D) uf |= U_DELAYED;
     if (ok) atomicOr(a.iflags + base + h, served ? I_SERVED : I_UNSERVED);
     const int64_t uk = int64_t(r) * t.U + k;
-    wave_add_by_key(ok, uk, served ? (unsigned long long)a.cost[g] : 0ull, a.charged, uf,
-                    a.uflags);
-    wave_add_by_key(ok, int64_t(r) * C_NUM + C_ADMITTED, served ? 1ull : 0ull, a.counters, 0,
-                    nullptr);
-    wave_add_by_key(ok, int64_t(r) * C_NUM + C_THROTTLED, (ok && st > 0) ? 1ull : 0ull,
-                    a.counters, 0, nullptr);
-    wave_add_by_key(ok, int64_t(r) * C_NUM + C_INTERACTIONS,
-                    (ok && first_call(t, g)) ? 1ull : 0ull, a.counters, 0, nullptr);
+    wave_add_by_key_hashed(ok, uk, served ? (unsigned long long)a.cost[g] : 0ull, a.charged, uf,
+                           a.uflags, ks[threadIdx.x >> 6]);
+    wave_count3(ok, r, a.counters, C_ADMITTED, served ? 1u : 0u, C_THROTTLED,
+                (ok && st > 0) ? 1u : 0u, C_INTERACTIONS, (ok && first_call(t, g)) ? 1u : 0u);
   }
   if (code) raise_err(a.err, code);
 }
 
 // Pass 2: per interaction (first call) -- fully served, aborted midway.
 __global__ void __launch_bounds__(256) k_m_interactions(MArgs a) {
+  __shared__ KeyScratch ks[4];
   const DevTrace &t = a.t;
   for (int64_t base0 = blockIdx.x * int64_t(blockDim.x); base0 < t.N;
        base0 += int64_t(gridDim.x) * blockDim.x) {
@@ -156,19 +233,17 @@ __global__ void __launch_bounds__(256) k_m_interactions(MArgs a) {
     bool ok = g < t.N && first_call(t, g);
     int32_t k = ok ? t.user[g] : 0;
     ok = ok && k >= 0 && k < t.U;
-    const int32_t r = ok ? replica_of(t.rep_off, t.R, g) : 0;
+    const int32_t r0 = replica_of(t.rep_off, t.R, base0);
+    const int32_t r = ok ? replica_from(t.rep_off, r0, g) : 0;
     const uint32_t f = ok ? a.iflags[g] : 0u;
     const bool full = ok && !(f & I_UNSERVED);
     const bool aborted = ok && (f & I_SERVED) && (f & I_UNSERVED);
-    if (full) {
-      // a heavy user has many fully served interactions: skip the atomic once its flag
-      // is visible (a stale read only costs an atomic that changes nothing)
-      uint32_t *uf = a.uflags + int64_t(r) * t.U + k;
-      if (!(*uf & U_FULL)) atomicOr(uf, U_FULL);
-    }
-    wave_add_by_key(ok, int64_t(r) * C_NUM + C_FULL, full ? 1ull : 0ull, a.counters, 0, nullptr);
-    wave_add_by_key(ok, int64_t(r) * C_NUM + C_ABORTED, aborted ? 1ull : 0ull, a.counters, 0,
-                    nullptr);
+    // one flag per user and wave; a heavy user has many fully served interactions, so
+    // the atomic is skipped once its flag is visible (a stale read only costs an atomic
+    // that changes nothing)
+    wave_add_by_key_hashed(full, int64_t(r) * t.U + k, 0ull, nullptr, U_FULL, a.uflags,
+                           ks[threadIdx.x >> 6], true);
+    wave_count3(ok, r, a.counters, C_FULL, full ? 1u : 0u, C_ABORTED, aborted ? 1u : 0u, -1, 0u);
   }
 }
 
@@ -181,8 +256,9 @@ __global__ void __launch_bounds__(256) k_m_wasted(MArgs a) {
     bool ok = g < t.N && a.status[g] == 0;
     int32_t r = 0;
     unsigned long long w = 0;
+    const int32_t r0 = replica_of(t.rep_off, t.R, base0);
     if (ok) {
-      r = replica_of(t.rep_off, t.R, g);
+      r = replica_from(t.rep_off, r0, g);
       const int64_t base = t.rep_off[r], i = g - base;
       const int64_t h = first_call(t, g) ? i : t.head[g];
       ok = h >= 0 && h <= i;

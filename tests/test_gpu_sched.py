@@ -69,16 +69,29 @@ def test_workloads_schedule(name, kw):
     compare_sim(g, o)
 
 
-def test_users_sharing_low_bits():
+@pytest.mark.parametrize("mode", ["fs", "fcfs", "blind", "literal"])
+def test_users_sharing_low_bits(mode):
     """User ids spread so that groups of users share their low 12 bits: the on-chip
-    kernel's per-user tables for a batch of arrivals collide often (and then match users
-    bit by bit), and must give the same schedule."""
+    kernel's per-user tables for matching the arrival window collide often (and then
+    match users bit by bit), and must give the same schedule in every engine mode."""
     wl, tr = workload_trace("c2_replicas", replicas=4, records=15000)
     spread = (tr.user % 3) + 4096 * (tr.user // 3)
     tr = tg.Trace(**{**tr.__dict__, "user": spread.astype(np.int32),
                      "n_users": int(spread.max()) + 1})
-    say("sched colliding users", tr.n, tr.n_users)
-    g, o, _, _ = _run_workload(wl, tr)
+    say("sched colliding users", mode, tr.n, tr.n_users)
+    if mode == "fs":
+        g, o, _, _ = _run_workload(wl, tr)
+    else:
+        coef, per_rep = fs.workload_weights(wl, tr)
+        c = oracle.cost(tr, coef, coef_per_replica=per_rep)
+        th = oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, counts=False)
+        flags = {"fcfs": oracle.FSO_FCFS, "blind": oracle.FSO_BLIND | oracle.FSO_FCFS,
+                 "literal": oracle.FSO_LITERAL}[mode]
+        step, cap = (20_000, 1 << 20) if mode == "literal" else (wl.step_us, wl.cap_tokens)
+        o = oracle.simulate(tr, c, th.reason, step, cap, wl.overload_tokens, flags=flags)
+        g = gpu_schedule(tr, c, th.reason, step, cap, wl.overload_tokens,
+                         fcfs=bool(flags & oracle.FSO_FCFS), blind=bool(flags & oracle.FSO_BLIND),
+                         literal=mode == "literal")
     compare_sim(g, o)
     assert (o.status == 0).any() and (o.status > 0).any()
 

@@ -267,6 +267,11 @@ def main():
                           "frac": round(achieved / HBM_PEAK_GBS, 6),
                           "algorithmic_bytes": int(algo), "traffic": traffic,
                           "src": src_hash(dom)}
+    if dom == "schedule":
+        # what limits it instead of bytes (measured with rocprofv3's SQ counters)
+        result["roofline"]["limiter"] = (
+            "latency of each replica's dependent decision chain: one wave per replica, "
+            f"{wl.n_replicas} waves on 1,024 SIMDs")
     all_stage_gbs = {s: round(ALGO_BYTES[s] * N / (stage_ms[s] / 1000.0) / 1e9, 2)
                      for s in stage_ms if ALGO_BYTES[s] > 0}
     result["stage_gbs"] = all_stage_gbs

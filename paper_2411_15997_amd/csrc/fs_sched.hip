@@ -167,6 +167,97 @@ struct XMem {
   }
 };
 
+// The same table in LDS when the replica's users fit (one slot per user, so capacity U),
+// with its own user -> slot table: every read of a decision's bookkeeping then stays
+// on chip and only the pool of queued requests is in global memory.
+struct XLds {
+  uint64_t *k;
+  int32_t *user, *q, *fh, *ft, *hh, *ht, *sb, *rh, *rdy, *xs;
+  int32_t cap;
+  __device__ void init() {
+    for (int32_t i = threadIdx.x; i < cap; i += 64) {
+      xs[i] = -1;
+      k[i] = kEmptyKey;
+    }
+  }
+  __device__ uint64_t key(int32_t x) const { return uint64_t(uni64(int64_t(k[x]))); }
+  __device__ void set_key(int32_t x, uint64_t v) {
+    if (threadIdx.x == 0) k[x] = v;
+  }
+#define FS_XLDS_FIELD(f)                                                 \
+  __device__ int32_t get_##f(int32_t x) const { return uni(f[x]); } \
+  __device__ void set_##f(int32_t x, int32_t v) {                        \
+    if (threadIdx.x == 0) f[x] = v;                                      \
+  }
+  FS_XLDS_FIELD(user)
+  FS_XLDS_FIELD(q)
+  FS_XLDS_FIELD(fh)
+  FS_XLDS_FIELD(ft)
+  FS_XLDS_FIELD(hh)
+  FS_XLDS_FIELD(ht)
+  FS_XLDS_FIELD(sb)
+  FS_XLDS_FIELD(rh)
+  FS_XLDS_FIELD(rdy)
+#undef FS_XLDS_FIELD
+  __device__ void copy(int32_t from, int32_t to) {
+    set_key(to, key(from));
+    set_user(to, get_user(from));
+    set_q(to, get_q(from));
+    set_fh(to, get_fh(from));
+    set_ft(to, get_ft(from));
+    set_hh(to, get_hh(from));
+    set_ht(to, get_ht(from));
+    set_sb(to, get_sb(from));
+    set_rh(to, get_rh(from));
+    set_rdy(to, get_rdy(from));
+  }
+  __device__ int32_t find(int32_t kk, const Store &) const { return uni(xs[kk]); }
+  __device__ int32_t alloc(int32_t kk, int32_t nX, const Store &) {
+    if (threadIdx.x == 0) xs[kk] = nX;
+    return nX;
+  }
+  // Moves the last slot into the freed one.
+  __device__ void release(int32_t x, int32_t kk, int32_t nX, const Store &) {
+    const int32_t last = nX - 1;
+    if (threadIdx.x == 0) xs[kk] = -1;
+    if (x != last) {
+      const int32_t k2 = get_user(last);
+      copy(last, x);
+      if (threadIdx.x == 0) xs[k2] = x;
+    }
+    set_key(last, kEmptyKey);
+  }
+  __device__ int32_t slot(int32_t i, int32_t) const { return i; }
+  __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
+    uint64_t kk = kEmptyKey;
+    uint32_t us = 0xffffffffu, bx = 0xffffffffu;
+    for (int32_t x = threadIdx.x; x < nX; x += 64) {
+      const uint64_t a = k[x];
+      const uint32_t b = uint32_t(user[x]);
+      const bool take = a < kk || (a == kk && b < us);
+      kk = take ? a : kk;
+      us = take ? b : us;
+      bx = take ? uint32_t(x) : bx;
+    }
+    wave_argmin(kk, us, bx);
+    bk = uint64_t(rdl64(int64_t(kk), 63));
+    bu = rdl(int32_t(us), 63);
+    return rdl(int32_t(bx), 63);
+  }
+  __device__ void minmax(int32_t nX, int64_t &mn, int64_t &mx) const {
+    uint64_t lo = kEmptyKey, hi = 0;
+    for (int32_t x = threadIdx.x; x < nX; x += 64) {
+      const uint64_t v = k[x] & kValMask;
+      lo = v < lo ? v : lo;
+      hi = v > hi ? v : hi;
+    }
+    wave_minmax(lo, hi);
+    mn = rdl64(int64_t(lo), 63);
+    mx = rdl64(int64_t(hi), 63);
+  }
+};
+constexpr size_t kXLdsBytesPerUser = 8 + 8 + 10 * 4;  // counter, key, nine fields and xs
+
 // ---------------------------------------------------------------------------
 // The scheduler body.  All control flow is wave-uniform; the arrival window holds
 // one record per lane.  Per-record outputs are collected in registers and written
@@ -945,6 +1036,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
 // Global-memory pass: resumes replicas that overflowed on chip (or runs all
 // replicas when the engine asks for global memory only).
 __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
+  extern __shared__ __align__(16) char gsm[];
   const int32_t r = blockIdx.x;
   if (*a.err) return;
   if (!state_header_ok(a)) return;
@@ -957,6 +1049,31 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   const StateLayout &L = a.L;
   Store S;
   S.pcap = cap;
+  S.e = reinterpret_cast<Entry *>(st + L.e_all) + off;
+  S.e_free = reinterpret_cast<int32_t *>(st + L.e_free) + off;
+  if (a.oc.glds) {  // the table and the counters in LDS
+    const int32_t U = a.t.U;
+    XLds X;
+    X.cap = U;
+    S.u = reinterpret_cast<int64_t *>(gsm);
+    X.k = reinterpret_cast<uint64_t *>(S.u + U);
+    int32_t *p = reinterpret_cast<int32_t *>(X.k + U);
+    X.user = p;
+    X.q = p += U;
+    X.fh = p += U;
+    X.ft = p += U;
+    X.hh = p += U;
+    X.ht = p += U;
+    X.sb = p += U;
+    X.rh = p += U;
+    X.rdy = p += U;
+    X.xs = p += U;
+    S.xslot = nullptr;
+    S.users_global = false;
+    run_replica<true>(a, S, X, r, false);
+    if (threadIdx.x == 0) rs->overflow = 0;
+    return;
+  }
   XMem X;
   X.cap = cap;
   X.k = reinterpret_cast<uint64_t *>(st + L.xkey) + off;
@@ -969,8 +1086,6 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   X.sb = reinterpret_cast<int32_t *>(st + L.xsb) + off;
   X.rh = reinterpret_cast<int32_t *>(st + L.xrh) + off;
   X.rdy = reinterpret_cast<int32_t *>(st + L.xrdy) + off;
-  S.e = reinterpret_cast<Entry *>(st + L.e_all) + off;
-  S.e_free = reinterpret_cast<int32_t *>(st + L.e_free) + off;
   S.u = reinterpret_cast<int64_t *>(st + L.u_all) + int64_t(r) * a.t.U;
   S.xslot = reinterpret_cast<int32_t *>(st + L.xslot_all) + int64_t(r) * a.t.U;
   S.users_global = true;
@@ -1182,12 +1297,15 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.state = static_cast<char *>(state);
   a.L = state_layout(t->n_replicas, t->n_users, N);
   a.oc = onchip_config(t->n_replicas, t->n_users, a.literal);
+  // the global-memory kernel keeps its user table in LDS when it fits in 64 KB
+  const size_t glds = size_t(t->n_users) * kXLdsBytesPerUser;
+  a.oc.glds = glds <= 65536 ? 1 : 0;
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
   hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);
   const dim3 grid(t->n_replicas), block(64);
   if (!a.global_only) launch_onchip(a, s);
-  hipLaunchKernelGGL(k_schedule_global, grid, block, 0, s, a);
+  hipLaunchKernelGGL(k_schedule_global, grid, block, a.oc.glds ? glds : 0, s, a);
   return hipGetLastError();
 }
 

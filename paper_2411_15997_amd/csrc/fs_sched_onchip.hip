@@ -1294,6 +1294,7 @@ OnchipCfg onchip_config(int32_t R, int32_t U, bool literal) {
     while (batch > 64 && size_t(batch) * (sizeof(Ent) + 4) > budget / 4) batch >>= 1;
   }
   c.batch = batch;
+  c.glds = 0;
   const size_t bat_bytes = size_t(batch) * (sizeof(Ent) + 4);
   c.users_lds = size_t(U) * 8 <= budget / 4 ? 1 : 0;
   const size_t users = c.users_lds ? size_t(U) * 8 : 0;

@@ -40,6 +40,10 @@ constexpr int kRadix = 1 << kRadixBits;
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 4;
 constexpr int kScanChunk = kScanThreads * kScanItems;
+// Records over the user limit are counted in kFlagSlots counters, one per 64-byte line
+// (a work-group adds to counter blockIdx % kFlagSlots), after the time shift's line.
+constexpr int kFlagSlots = 64;
+constexpr int kFlagStride = 16;
 
 int bits_for(int64_t n_values) {  // bits to represent 0 .. n_values-1 (at least 1)
   int b = 1;
@@ -76,7 +80,7 @@ struct Layout {
   int64_t N;
   int64_t tiles;
   Pack pk;
-  size_t off_a, off_b, off_rr, off_hist, off_part, off_tapp, off_sh;
+  size_t off_a, off_b, off_hist, off_part, off_tapp, off_sh;
   size_t total;
 };
 
@@ -90,11 +94,10 @@ Layout layout(const fs_trace *t) {
   size_t o = 0;
   L.off_a = o; o += up(n * 8);
   L.off_b = o; o += up(n * 8);
-  L.off_rr = o; o += up((n + 15) / 16 * 4);
   L.off_hist = o; o += up(hist_len * 4);
   L.off_part = o; o += up(((hist_len + kScanChunk - 1) / kScanChunk + 1) * 4);
   L.off_tapp = o; o += up(kMaxApps * 4);
-  L.off_sh = o; o += up(4);
+  L.off_sh = o; o += up(4 * kFlagStride * (kFlagSlots + 1));  // time shift, flag counters
   L.total = o;
   return L;
 }
@@ -226,8 +229,9 @@ __global__ void __launch_bounds__(kThreads) k_thr_span(const int64_t *rep_off, c
     int sh = 0;
     if (Bq > 0)
       while (sh < 63 && (uint64_t(s_max[0]) >> sh) >= (uint64_t(1) << Bq)) ++sh;
-    *sh_out = sh;
+    sh_out[0] = sh;
   }
+  if (threadIdx.x < kFlagSlots) sh_out[kFlagStride * (threadIdx.x + 1)] = 0;  // user-test counts
 }
 
 // ---------------------------------------------------------------- element construction
@@ -351,6 +355,7 @@ struct ScatterArgs {
   int32_t t_user;
   uint64_t user_mask;  // element bits of the user part of the key
   Win win;
+  int32_t *n_flag;     // counters of records over the user limit (TEST_USER)
 };
 
 // Stable scatter of one tile.  Wave w owns the contiguous sub-tile
@@ -383,6 +388,7 @@ __global__ void __launch_bounds__(kThreads) k_radix_scatter(ScatterArgs a) {
     k_r[i] = e < a.N ? a.in[e] : 0u;
   }
   if (TEST_USER) {
+    int32_t nf = 0;
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
       const int64_t e = wbase + i * 64 + lane;
@@ -390,7 +396,9 @@ __global__ void __launch_bounds__(kThreads) k_radix_scatter(ScatterArgs a) {
         const uint64_t eq = a.in[e - a.t_user];
         if (((k_r[i] ^ eq) & a.user_mask) == 0 && in_window(k_r[i], eq, win)) k_r[i] |= 1u;
       }
+      nf += __popcll(__ballot(k_r[i] & 1u));
     }
+    if (lane == 0 && nf) atomicAdd(a.n_flag + kFlagStride * (blockIdx.x % kFlagSlots), nf);
   }
   uint32_t rank[kItems];
   const uint64_t lt = (uint64_t(1) << lane) - 1;
@@ -505,12 +513,35 @@ __device__ inline uint64_t key_of(uint64_t e, const KeySel &k) {
 
 // ---------------------------------------------------------------- app-limit test
 
-// The app limit is tested in (user, app) order and the raw reason goes back to
-// stream order in two coalesced steps instead of one random byte store per record:
-// each tile scatters compact words (index low bits << 2 | reason) into buckets by
-// the high bits of the index (a stable radix pass), then one work-group per bucket
-// assembles its contiguous stream range in LDS and writes it out.
-constexpr int kUnsortBits = 18;  // stream records per unsort chunk: 2^18, 2 bits each in LDS
+// The app limit is tested in (user, app) order.  Each record's raw reason (the user
+// flag carried by the element, else the app test) goes to its stream position as one
+// byte.  Those stores are scattered, so the array is first filled with the likelier
+// reason (1 when most records are over the user limit, else 0) in coalesced stores
+// and only the records with another reason are stored one by one.
+// Called by every thread of the block.
+__device__ inline uint8_t background_reason(const int32_t *n_flag, int64_t N) {
+  __shared__ uint8_t s_bg;
+  if (threadIdx.x < 64) {
+    int64_t c = threadIdx.x < kFlagSlots ? n_flag[kFlagStride * threadIdx.x] : 0;
+#pragma unroll
+    for (int d = 32; d > 0; d >>= 1) c += __shfl_xor(c, d, 64);
+    if (threadIdx.x == 0) s_bg = c * 2 > N ? 1 : 0;
+  }
+  __syncthreads();
+  return s_bg;
+}
+
+__global__ void __launch_bounds__(kThreads) k_thr_fill(uint8_t *rb, int64_t N,
+                                                        const int32_t *n_flag) {
+  const uint32_t v = uint32_t(background_reason(n_flag, N)) * 0x01010101u;
+  const uint4 q = make_uint4(v, v, v, v);
+  const int64_t n16 = N >> 4;
+  uint4 *r4 = reinterpret_cast<uint4 *>(rb);
+  for (int64_t i = blockIdx.x * int64_t(kThreads) + threadIdx.x; i < n16;
+       i += int64_t(gridDim.x) * kThreads)
+    r4[i] = q;
+  if (blockIdx.x == 0 && threadIdx.x < (N & 15)) rb[(n16 << 4) + threadIdx.x] = uint8_t(v);
+}
 
 struct AppTestArgs {
   const uint64_t *el;  // the app key's order (time order within a key), user flag set
@@ -519,123 +550,40 @@ struct AppTestArgs {
   const int32_t *t_app;
   int32_t A;
   Win win;
-  int bs;              // bucket = index >> bs
-  uint32_t mask;       // bucket digit mask
-  const uint32_t *offs;
-  int64_t tiles;
-  uint32_t *out;       // [N] words grouped by bucket
+  uint8_t *rb;         // [N] raw reasons in stream order, filled with the background
+  const int32_t *n_flag;
 };
 
 __global__ void __launch_bounds__(kThreads) k_thr_apptest(AppTestArgs a) {
-  __shared__ uint32_t s_w[kTile];
-  __shared__ uint8_t s_d[kTile];
-  __shared__ uint32_t cnt[kWaves][kRadix];
-  __shared__ uint32_t loc[kRadix];
-  __shared__ uint32_t goff[kRadix];
-  __shared__ uint32_t s_waves[kWaves];
   const Win win = load_win(a.win);
   const Pack &pk = win.pk;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int64_t base = blockIdx.x * int64_t(kTile);
-  const int64_t wbase = base + int64_t(wave) * kWaveSpan;
-  goff[t] = t <= int(a.mask) ? a.offs[int64_t(t) * a.tiles + blockIdx.x] : 0u;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) cnt[w][t] = 0;
-  __syncthreads();
-
-  uint32_t wd[kItems], dg[kItems];
+  const uint8_t bg = background_reason(a.n_flag, a.N);
+  const int64_t base = blockIdx.x * int64_t(kTile) + threadIdx.x;
+  uint64_t ep[kItems];
+  int64_t T[kItems];
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
-    const int64_t p = wbase + i * 64 + lane;
-    wd[i] = 0;
-    dg[i] = 0;
-    if (p < a.N) {
-      const uint64_t ep = a.el[p];
-      const uint32_t ap = uint32_t((ep >> pk.SK) >> pk.Bu);
-      const int64_t T = ap < uint32_t(a.A) ? a.t_app[ap] : 0;
-      bool fa = false;
-      if (T <= p) {
-        const uint64_t eq = a.el[p - T];
-        fa = key_of(ep, a.key) == key_of(eq, a.key) && in_window(ep, eq, win);
-      }
-      const uint32_t code = (ep & 1u) ? 1u : (fa ? 2u : 0u);
-      const uint64_t g = (ep >> pk.SI) & pk.imask;
-      wd[i] = (uint32_t(g & ((uint64_t(1) << a.bs) - 1)) << 2) | code;
-      dg[i] = uint32_t(g >> a.bs) & a.mask;
-    }
+    const int64_t p = base + i * kThreads;
+    ep[i] = p < a.N ? a.el[p] : 0u;
   }
-  uint32_t rank[kItems];
-  const uint64_t lt = (uint64_t(1) << lane) - 1;
-  uint32_t *my = cnt[wave];
-  const int width = mask_width(a.mask);
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
-    const bool valid = wbase + i * 64 + lane < a.N;
-    const uint64_t peers = digit_peers(dg[i], valid, width);
-    const uint32_t before = valid ? my[dg[i]] : 0u;
-    rank[i] = valid ? before + uint32_t(__popcll(peers & lt)) : 0xffffffffu;
-    if (valid && (peers & lt) == 0) my[dg[i]] = before + uint32_t(__popcll(peers));
+    const int64_t p = base + i * kThreads;
+    const uint32_t ap = uint32_t((ep[i] >> pk.SK) >> pk.Bu);
+    T[i] = (p < a.N && ap < uint32_t(a.A)) ? a.t_app[ap] : INT64_MAX;
   }
-  __syncthreads();
-  uint32_t tot = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const uint32_t c = cnt[w][t];
-    cnt[w][t] = tot;
-    tot += c;
-  }
-  uint32_t total;
-  const uint32_t incl = block_inclusive_scan(tot, s_waves, total);
-  loc[t] = incl - tot;
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kItems; ++i)
-    if (rank[i] != 0xffffffffu) {
-      const uint32_t pos = loc[dg[i]] + my[dg[i]] + rank[i];
-      s_w[pos] = wd[i];
-      s_d[pos] = uint8_t(dg[i]);
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t p = base + i * kThreads;
+    if (p >= a.N) continue;
+    bool fa = false;
+    if (T[i] <= p) {
+      const uint64_t eq = a.el[p - T[i]];
+      fa = key_of(ep[i], a.key) == key_of(eq, a.key) && in_window(ep[i], eq, win);
     }
-  __syncthreads();
-  const int64_t n_here = a.N - base < kTile ? a.N - base : kTile;
-  for (int j = t; j < n_here; j += kThreads) {
-    const uint32_t d = s_d[j];
-    const uint32_t dst = goff[d] + (uint32_t(j) - loc[d]);
-    if (dst < a.N) a.out[dst] = s_w[j];
+    const uint8_t code = (ep[i] & 1u) ? 1 : (fa ? 2 : 0);
+    if (code != bg) a.rb[(ep[i] >> pk.SI) & pk.imask] = code;
   }
-}
-
-struct UnsortArgs {
-  const uint32_t *words;   // grouped by bucket
-  const uint32_t *offs;    // bucket starts at offs[bucket * tiles]
-  int64_t tiles;
-  int32_t n_buckets;
-  int64_t N;
-  int bs;                  // records per bucket: 2^bs, bs >= 4
-  int chunks;              // chunks of 2^kUnsortBits records per bucket
-  uint32_t *rr;            // [ceil(N/16)] raw reasons in stream order, 2 bits each
-};
-
-__global__ void __launch_bounds__(1024) k_thr_unsort(UnsortArgs a) {
-  __shared__ uint32_t codes[(1 << kUnsortBits) / 16];
-  const int32_t b = blockIdx.x / a.chunks, c = blockIdx.x % a.chunks;
-  const int csh = a.bs > kUnsortBits ? kUnsortBits : a.bs;  // records per chunk: 2^csh
-  for (int j = threadIdx.x; j < (1 << csh) / 16 + 1 && j < (1 << kUnsortBits) / 16; j += 1024)
-    codes[j] = 0;
-  __syncthreads();
-  const int64_t start = a.offs[int64_t(b) * a.tiles];
-  const int64_t stop = b + 1 < a.n_buckets ? int64_t(a.offs[int64_t(b + 1) * a.tiles]) : a.N;
-  for (int64_t k = start + threadIdx.x; k < stop; k += 1024) {
-    const uint32_t w = a.words[k];
-    const uint32_t lo = w >> 2;
-    if (int(lo >> csh) != c) continue;
-    const uint32_t o = lo & ((1u << csh) - 1);
-    atomicOr(&codes[o >> 4], (w & 3u) << ((o & 15) * 2));
-  }
-  __syncthreads();
-  // chunk starts are multiples of 16 records, so whole words belong to one chunk
-  const int64_t g0 = (int64_t(b) << a.bs) + (int64_t(c) << csh);
-  const int64_t n = a.N - g0 < (int64_t(1) << csh) ? a.N - g0 : (int64_t(1) << csh);
-  for (int64_t j = threadIdx.x; j < (n + 15) >> 4; j += 1024) a.rr[(g0 >> 4) + j] = codes[j];
 }
 
 // ---------------------------------------------------------------- app-level limit
@@ -696,7 +644,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_count(CountArgs a) {
 
 struct CombineArgs {
   DevTrace t;
-  const uint32_t *rr;  // 2-bit raw reasons, 16 per word
+  const uint8_t *rb;   // [N] raw reasons in stream order
   const uint8_t *overloaded;
   bool raw;
   uint32_t *bitmap;
@@ -715,7 +663,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_combine(CombineArgs a) {
     const int64_t g = base + threadIdx.x;
     uint8_t code = 0;
     if (g < N) {
-      const uint8_t rr = uint8_t((a.rr[g >> 4] >> ((g & 15) * 2)) & 3u);
+      const uint8_t rr = a.rb[g];
       if (a.raw) {
         code = rr;
       } else if (!a.t.call || a.t.call[g] == 0) {
@@ -727,7 +675,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_combine(CombineArgs a) {
         const int64_t h = lo + a.t.head[g];
         if (h >= lo && h < hi) {
           const bool hover = a.overloaded ? a.overloaded[h] != 0 : true;
-          code = (hover && ((a.rr[h >> 4] >> ((h & 15) * 2)) & 3u) != 0) ? 3 : 0;
+          code = (hover && a.rb[h] != 0) ? 3 : 0;
         }
       }
       if (a.reason) a.reason[g] = code;
@@ -773,7 +721,6 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   char *w = static_cast<char *>(ws);
   uint64_t *A = reinterpret_cast<uint64_t *>(w + L.off_a);
   uint64_t *B = reinterpret_cast<uint64_t *>(w + L.off_b);
-  uint32_t *rrw = reinterpret_cast<uint32_t *>(w + L.off_rr);
   uint32_t *hist = reinterpret_cast<uint32_t *>(w + L.off_hist);
   uint32_t *part = reinterpret_cast<uint32_t *>(w + L.off_part);
   int32_t *tapp = reinterpret_cast<int32_t *>(w + L.off_tapp);
@@ -822,7 +769,8 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
         CountArgs ca{in, L.N, KeySel{user_mask, false, pk.SK, pk.Bu, 1u}, win, cnt_user};
         hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
       }
-      ScatterArgs ua{in, out, L.N, 0, 0, nullptr, 0, lim->t_user, user_mask, win};
+      ScatterArgs ua{in, out, L.N, 0, 0, nullptr, 0, lim->t_user,
+                     user_mask, win, sh + kFlagStride};
       hipLaunchKernelGGL(k_thr_user_unsort, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s,
                          ua);
       uint64_t *tmp = in;
@@ -837,7 +785,8 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
       CountArgs ca{in, L.N, KeySel{user_mask, false, pk.SK, pk.Bu, 1u}, win, cnt_user};
       hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
     }
-    ScatterArgs sa{in, out, L.N, shift, mask, hist, L.tiles, lim->t_user, user_mask, win};
+    ScatterArgs sa{in, out, L.N, shift, mask, hist, L.tiles, lim->t_user,
+                   user_mask, win, sh + kFlagStride};
     if (k == n_user && !app_level)
       hipLaunchKernelGGL(k_radix_scatter<true>, dim3(L.tiles), dim3(kThreads), 0, s, sa);
     else
@@ -846,22 +795,15 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
     in = out;
     out = tmp;
   }
+  // app test in (user, app) order; raw reasons to stream order in the free sort buffer
+  uint8_t *rb = reinterpret_cast<uint8_t *>(out);
   {
-    // app test in (user, app) order, results bucketed by the index's high bits
-    const int bs = pk.Bi - kRadixBits > 4 ? pk.Bi - kRadixBits : 4;
-    const uint32_t bmask = pk.Bi > bs ? (1u << (pk.Bi - bs)) - 1u : 0u;
-    const int32_t n_buckets = int32_t((L.N + (int64_t(1) << bs) - 1) >> bs);
-    hipLaunchKernelGGL(k_radix_hist, dim3(L.tiles), dim3(kThreads), 0, s, in, L.N, pk.SI + bs,
-                       bmask, hist, L.tiles);
-    (void)exclusive_scan(hist, int64_t(bmask + 1) * L.tiles, part, s);
-    uint32_t *words = reinterpret_cast<uint32_t *>(out);  // the free sort buffer
     const KeySel app_key{((uint64_t(1) << pk.Bk) - 1) << pk.SK, app_level, pk.SK, pk.Bu,
                          uint32_t(t->n_users)};
-    AppTestArgs aa{in, L.N, app_key, tapp, t->n_apps, win, bs, bmask, hist, L.tiles, words};
+    hipLaunchKernelGGL(k_thr_fill, dim3(grid_for((L.N >> 4) + 1, kThreads)), dim3(kThreads), 0, s,
+                       rb, L.N, sh + kFlagStride);
+    AppTestArgs aa{in, L.N, app_key, tapp, t->n_apps, win, rb, sh + kFlagStride};
     hipLaunchKernelGGL(k_thr_apptest, dim3(L.tiles), dim3(kThreads), 0, s, aa);
-    const int chunks = bs > kUnsortBits ? 1 << (bs - kUnsortBits) : 1;
-    UnsortArgs ua{words, hist, L.tiles, n_buckets, L.N, bs, chunks, rrw};
-    hipLaunchKernelGGL(k_thr_unsort, dim3(n_buckets * chunks), dim3(1024), 0, s, ua);
   }
   if (cnt_app) {
     const KeySel app_key{((uint64_t(1) << pk.Bk) - 1) << pk.SK, app_level, pk.SK, pk.Bu,
@@ -870,7 +812,7 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
     hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
   }
 
-  CombineArgs ca{dt, rrw, overloaded, raw, bitmap, reason, (L.N + 31) / 32};
+  CombineArgs ca{dt, rb, overloaded, raw, bitmap, reason, (L.N + 31) / 32};
   hipLaunchKernelGGL(k_thr_combine, dim3((L.N + kCombineSpan - 1) / kCombineSpan), dim3(kThreads),
                      0, s, ca);
   return hipGetLastError();

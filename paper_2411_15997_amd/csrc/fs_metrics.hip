@@ -53,14 +53,33 @@ __global__ void k_m_zero(MArgs a, int64_t RU, int64_t N) {
     a.charged[i] = 0;
     a.uflags[i] = 0;
   }
-  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < N; i += stride)
-    a.iflags[i] = 0;
+  if (a.t.call)  // (only later calls add interaction flags)
+    for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < N; i += stride)
+      a.iflags[i] = 0;
   for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < int64_t(a.t.R) * C_NUM;
        i += stride)
     a.counters[i] = 0;
 }
 
 __device__ inline bool first_call(const DevTrace &t, int64_t g) { return !t.call || t.call[g] == 0; }
+
+// An interaction's flags: its later calls OR theirs into iflags[first call]; the first
+// call's own flag comes from its status where it is read, which spares one atomic per
+// interaction.
+__device__ inline uint32_t own_iflag(int8_t st) { return st == 0 ? I_SERVED : I_UNSERVED; }
+
+// The flags that the later calls of the interaction starting at g added (none, and
+// the array is not cleared, when every record is a single-call interaction).
+__device__ inline uint32_t later_iflags(const MArgs &a, int64_t g) {
+  return a.t.call ? a.iflags[g] : 0u;
+}
+
+// admit_step - ts / tau > D.  For ts >= 0 the quotient is a floor, so this holds iff
+// ts < (admit_step - D) * tau, which needs no division while the product fits.
+__device__ inline bool is_delayed(int32_t astep, int64_t ts, int64_t tau, int32_t D) {
+  if (ts >= 0 && tau <= (int64_t(1) << 30)) return ts < (int64_t(astep) - D) * tau;
+  return int64_t(astep) - ts / tau > D;
+}
 
 __device__ inline unsigned long long wave_sum(unsigned long long v) {
 #pragma unroll
@@ -212,8 +231,8 @@ __global__ void __launch_bounds__(256) k_m_records(MArgs a) {
     const int8_t st = ok ? a.status[g] : int8_t(-1);
     const bool served = ok && st == 0;
     uint32_t uf = U_HAS;
-    if (served && int64_t(a.admit_step[g]) - t.ts[g] / a.tau > a.D) uf |= U_DELAYED;
-    if (ok) atomicOr(a.iflags + base + h, served ? I_SERVED : I_UNSERVED);
+    if (served && is_delayed(a.admit_step[g], t.ts[g], a.tau, a.D)) uf |= U_DELAYED;
+    if (ok && h != i) atomicOr(a.iflags + base + h, own_iflag(st));
     const int64_t uk = int64_t(r) * t.U + k;
     wave_add_by_key_hashed(ok, uk, served ? (unsigned long long)a.cost[g] : 0ull, a.charged, uf,
                            a.uflags, ks[threadIdx.x >> 6]);
@@ -235,7 +254,7 @@ __global__ void __launch_bounds__(256) k_m_interactions(MArgs a) {
     ok = ok && k >= 0 && k < t.U;
     const int32_t r0 = replica_of(t.rep_off, t.R, base0);
     const int32_t r = ok ? replica_from(t.rep_off, r0, g) : 0;
-    const uint32_t f = ok ? a.iflags[g] : 0u;
+    const uint32_t f = ok ? (later_iflags(a, g) | own_iflag(a.status[g])) : 0u;
     const bool full = ok && !(f & I_UNSERVED);
     const bool aborted = ok && (f & I_SERVED) && (f & I_UNSERVED);
     // one flag per user and wave; a heavy user has many fully served interactions, so
@@ -247,27 +266,184 @@ __global__ void __launch_bounds__(256) k_m_interactions(MArgs a) {
   }
 }
 
-// Pass 3: per admitted record of an aborted interaction -- wasted tokens.
-__global__ void __launch_bounds__(256) k_m_wasted(MArgs a) {
+// Replicas whose users fit in LDS: a work-group takes kChunk consecutive records and,
+// for each replica segment among them, sums the charged service and ORs the user
+// flags in LDS tables indexed by user, then adds each touched user's values to global
+// memory once.  Per-replica counts are reduced over the work-group.
+constexpr int kChunk = 8192;
+constexpr int kLdsUsers = 4096;
+
+// Sums three per-thread counts over the work-group (256 threads) and adds them to the
+// replica's counters c0, c1, c2 (c < 0: unused).
+__device__ inline void block_count3(uint32_t x0, uint32_t x1, uint32_t x2,
+                                    unsigned long long *cr, int c0, int c1, int c2,
+                                    unsigned long long (*s_red)[4]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long packed =
+      uint64_t(x0) | (uint64_t(x1) << 21) | (uint64_t(x2) << 42);  // each at most kChunk
+  const unsigned long long tw = wave_sum(packed);
+  if (lane == 0) s_red[0][wave] = tw;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned long long t = s_red[0][0] + s_red[0][1] + s_red[0][2] + s_red[0][3];
+    const unsigned long long m = (uint64_t(1) << 21) - 1;
+    if (c0 >= 0 && (t & m)) atomicAdd(cr + c0, t & m);
+    if (c1 >= 0 && ((t >> 21) & m)) atomicAdd(cr + c1, (t >> 21) & m);
+    if (c2 >= 0 && ((t >> 42) & m)) atomicAdd(cr + c2, (t >> 42) & m);
+  }
+}
+
+// Pass 1, LDS tables (U <= kLdsUsers): dynamic LDS of U * 12 bytes.
+constexpr int kRecBatch = 4;  // records per thread whose loads are issued together
+__global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
+  extern __shared__ unsigned long long s_dyn[];
+  __shared__ unsigned long long s_red[1][4];
   const DevTrace &t = a.t;
-  for (int64_t base0 = blockIdx.x * int64_t(blockDim.x); base0 < t.N;
-       base0 += int64_t(gridDim.x) * blockDim.x) {
-    const int64_t g = base0 + threadIdx.x;
-    bool ok = g < t.N && a.status[g] == 0;
-    int32_t r = 0;
-    unsigned long long w = 0;
-    const int32_t r0 = replica_of(t.rep_off, t.R, base0);
-    if (ok) {
-      r = replica_from(t.rep_off, r0, g);
-      const int64_t base = t.rep_off[r], i = g - base;
-      const int64_t h = first_call(t, g) ? i : t.head[g];
-      ok = h >= 0 && h <= i;
-      if (ok) {
-        const uint32_t f = a.iflags[base + h];
-        if ((f & I_SERVED) && (f & I_UNSERVED)) w = (unsigned long long)tokens_of(t, g);
+  unsigned long long *const s_chg = s_dyn;
+  uint32_t *const s_uf = reinterpret_cast<uint32_t *>(s_dyn + t.U);
+  const int64_t c0 = blockIdx.x * int64_t(kChunk);
+  const int64_t c1 = c0 + kChunk < t.N ? c0 + kChunk : t.N;
+  int32_t r = replica_of(t.rep_off, t.R, c0);
+  int32_t code = 0;
+  for (int64_t s0 = c0; s0 < c1; s0 = t.rep_off[r + 1], ++r) {
+    while (t.rep_off[r + 1] <= s0) ++r;  // (empty replicas)
+    const int64_t base = t.rep_off[r];
+    const int64_t s1 = t.rep_off[r + 1] < c1 ? t.rep_off[r + 1] : c1;
+    for (int32_t k = threadIdx.x; k < t.U; k += 256) {
+      s_chg[k] = 0;
+      s_uf[k] = 0;
+    }
+    __syncthreads();
+    uint32_t n_adm = 0, n_thr = 0, n_int = 0;
+    for (int64_t g0 = s0 + threadIdx.x; g0 < s1; g0 += kRecBatch * 256) {
+      int32_t uk[kRecBatch], ap[kRecBatch], cl[kRecBatch], hd[kRecBatch], as[kRecBatch];
+      int8_t st[kRecBatch];
+      int64_t ts[kRecBatch], cs[kRecBatch];
+#pragma unroll
+      for (int j = 0; j < kRecBatch; ++j) {
+        const int64_t g = g0 + j * 256;
+        const bool v = g < s1;
+        uk[j] = v ? t.user[g] : 0;
+        ap[j] = v ? t.app[g] : 0;
+        cl[j] = (v && t.call) ? t.call[g] : 0;
+        hd[j] = (v && t.call) ? t.head[g] : 0;
+        st[j] = v ? a.status[g] : int8_t(-1);
+        as[j] = v ? a.admit_step[g] : 0;
+        ts[j] = v ? t.ts[g] : 0;
+        cs[j] = v ? a.cost[g] : 0;
+      }
+#pragma unroll
+      for (int j = 0; j < kRecBatch; ++j) {
+        const int64_t g = g0 + j * 256;
+        if (g >= s1) continue;
+        const int64_t i = g - base;
+        const int32_t k = uk[j];
+        bool ok = k >= 0 && k < t.U && ap[j] >= 0 && ap[j] < t.A;
+        const bool fc = cl[j] == 0;
+        int64_t h = i;
+        if (ok && !fc) {
+          h = hd[j];
+          ok = h >= 0 && h < i;
+        }
+        if (!ok) {
+          code = int32_t(FS_E_RANGE);
+          continue;
+        }
+        const bool served = st[j] == 0;
+        uint32_t uf = U_HAS;
+        if (served && is_delayed(as[j], ts[j], a.tau, a.D)) uf |= U_DELAYED;
+        if (!fc) atomicOr(a.iflags + base + h, own_iflag(st[j]));
+        if (served) atomicAdd(&s_chg[k], (unsigned long long)cs[j]);
+        atomicOr(&s_uf[k], uf);
+        n_adm += served ? 1u : 0u;
+        n_thr += st[j] > 0 ? 1u : 0u;
+        n_int += fc ? 1u : 0u;
       }
     }
-    wave_add_by_key(ok, int64_t(r) * C_NUM + C_WASTED, w, a.counters, 0, nullptr);
+    __syncthreads();
+    unsigned long long *const chg = a.charged + int64_t(r) * t.U;
+    uint32_t *const ufg = a.uflags + int64_t(r) * t.U;
+    for (int32_t k = threadIdx.x; k < t.U; k += 256) {
+      const uint32_t f = s_uf[k];
+      if (!f) continue;
+      const unsigned long long c = s_chg[k];
+      if (c) atomicAdd(chg + k, c);
+      if ((ufg[k] & f) != f) atomicOr(ufg + k, f);
+    }
+    block_count3(n_adm, n_thr, n_int, a.counters + int64_t(r) * C_NUM, C_ADMITTED, C_THROTTLED,
+                 C_INTERACTIONS, s_red);
+    __syncthreads();
+  }
+  if (code) raise_err(a.err, code);
+}
+
+// Pass 2, LDS tables (U <= kLdsUsers).
+__global__ void __launch_bounds__(256) k_m_interactions_lds(MArgs a) {
+  extern __shared__ unsigned long long s_dyn[];
+  __shared__ unsigned long long s_red[1][4];
+  const DevTrace &t = a.t;
+  uint8_t *const s_full = reinterpret_cast<uint8_t *>(s_dyn);
+  const int64_t c0 = blockIdx.x * int64_t(kChunk);
+  const int64_t c1 = c0 + kChunk < t.N ? c0 + kChunk : t.N;
+  int32_t r = replica_of(t.rep_off, t.R, c0);
+  for (int64_t s0 = c0; s0 < c1; s0 = t.rep_off[r + 1], ++r) {
+    while (t.rep_off[r + 1] <= s0) ++r;
+    const int64_t s1 = t.rep_off[r + 1] < c1 ? t.rep_off[r + 1] : c1;
+    for (int32_t k = threadIdx.x; k < t.U; k += 256) s_full[k] = 0;
+    __syncthreads();
+    uint32_t n_full = 0, n_ab = 0;
+    for (int64_t g = s0 + threadIdx.x; g < s1; g += 256) {
+      if (!first_call(t, g)) continue;
+      const int32_t k = t.user[g];
+      if (k < 0 || k >= t.U) continue;
+      const uint32_t f = later_iflags(a, g) | own_iflag(a.status[g]);
+      const bool full = !(f & I_UNSERVED);
+      if (full) s_full[k] = 1;  // (the same value from every writer)
+      n_full += full ? 1u : 0u;
+      n_ab += ((f & I_SERVED) && (f & I_UNSERVED)) ? 1u : 0u;
+    }
+    __syncthreads();
+    uint32_t *const ufg = a.uflags + int64_t(r) * t.U;
+    for (int32_t k = threadIdx.x; k < t.U; k += 256)
+      if (s_full[k] && !(ufg[k] & U_FULL)) atomicOr(ufg + k, uint32_t(U_FULL));
+    block_count3(n_full, n_ab, 0, a.counters + int64_t(r) * C_NUM, C_FULL, C_ABORTED, -1, s_red);
+    __syncthreads();
+  }
+}
+
+// Pass 3: per admitted record of an aborted interaction -- wasted tokens.  Chunked like
+// the LDS passes; a replica segment without aborted interactions (every replica under
+// the paper's policy) is skipped without reading its records.
+__global__ void __launch_bounds__(256) k_m_wasted(MArgs a) {
+  __shared__ unsigned long long s_red[1][4];
+  const DevTrace &t = a.t;
+  const int64_t c0 = blockIdx.x * int64_t(kChunk);
+  const int64_t c1 = c0 + kChunk < t.N ? c0 + kChunk : t.N;
+  int32_t r = replica_of(t.rep_off, t.R, c0);
+  for (int64_t s0 = c0; s0 < c1; s0 = t.rep_off[r + 1], ++r) {
+    while (t.rep_off[r + 1] <= s0) ++r;
+    const int64_t base = t.rep_off[r];
+    const int64_t s1 = t.rep_off[r + 1] < c1 ? t.rep_off[r + 1] : c1;
+    unsigned long long *const cr = a.counters + int64_t(r) * C_NUM;
+    if (cr[C_ABORTED] == 0) continue;  // (uniform over the work-group)
+    unsigned long long w = 0;
+    for (int64_t g = s0 + threadIdx.x; g < s1; g += 256) {
+      if (a.status[g] != 0) continue;
+      const int64_t i = g - base;
+      const int64_t h = first_call(t, g) ? i : t.head[g];
+      if (h < 0 || h > i) continue;
+      const uint32_t f =
+          later_iflags(a, base + h) | (h == i ? I_SERVED : own_iflag(a.status[base + h]));
+      if ((f & I_SERVED) && (f & I_UNSERVED)) w += (unsigned long long)tokens_of(t, g);
+    }
+    const unsigned long long tw = wave_sum(w);
+    if ((threadIdx.x & 63) == 0) s_red[0][threadIdx.x >> 6] = tw;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const unsigned long long tot = s_red[0][0] + s_red[0][1] + s_red[0][2] + s_red[0][3];
+      if (tot) atomicAdd(cr + C_WASTED, tot);
+    }
+    __syncthreads();
   }
 }
 
@@ -377,9 +553,15 @@ hipError_t launch_metrics(const fs_trace *t, const int64_t *cost, const fs_outpu
   const int64_t N = a.t.N;
   hipLaunchKernelGGL(k_m_zero, dim3(grid_for(RU > N ? RU : N, 256)), dim3(256), 0, s, a, RU, N);
   if (N > 0) {
-    hipLaunchKernelGGL(k_m_records, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_m_interactions, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_m_wasted, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
+    const int64_t chunks = (N + kChunk - 1) / kChunk;
+    if (t->n_users <= kLdsUsers) {
+      hipLaunchKernelGGL(k_m_records_lds, dim3(chunks), dim3(256), size_t(t->n_users) * 12, s, a);
+      hipLaunchKernelGGL(k_m_interactions_lds, dim3(chunks), dim3(256), size_t(t->n_users), s, a);
+    } else {
+      hipLaunchKernelGGL(k_m_records, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(k_m_interactions, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
+    }
+    hipLaunchKernelGGL(k_m_wasted, dim3(chunks), dim3(256), 0, s, a);
   }
   hipLaunchKernelGGL(k_m_finish, dim3(t->n_replicas), dim3(256), 0, s, a);
   return hipGetLastError();

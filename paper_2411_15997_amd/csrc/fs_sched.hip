@@ -1202,9 +1202,13 @@ __global__ void __launch_bounds__(256) k_sched_check(CheckArgs a) {
           h->N == t.N))
       code = FS_E_STATE;
   }
-  for (int64_t g = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; g < t.N;
-       g += int64_t(gridDim.x) * blockDim.x) {
-    const int32_t r = replica_of(t.rep_off, t.R, g);
+  for (int64_t g0 = blockIdx.x * int64_t(blockDim.x); g0 < t.N;
+       g0 += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t g = g0 + threadIdx.x;
+    // one search per work-group row, then a short walk (a row spans few replicas)
+    int32_t r = replica_of(t.rep_off, t.R, g0);
+    if (g >= t.N) continue;
+    while (t.rep_off[r + 1] <= g) ++r;
     const int64_t base = t.rep_off[r], i = g - base;
     const int32_t u = t.user[g], ap = t.app[g];
     const int64_t ts = t.ts[g];

@@ -1301,9 +1301,14 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   a.state = static_cast<char *>(state);
   a.L = state_layout(t->n_replicas, t->n_users, N);
   a.oc = onchip_config(t->n_replicas, t->n_users, a.literal);
-  // the global-memory kernel keeps its user table in LDS when it fits in 64 KB
+  // The global-memory kernel keeps its user table in LDS when it fits in 64 KB and
+  // every replica's work-group can still be resident at once (up to four per CU on
+  // the 256 CUs): a table that left some replicas waiting for a CU made the
+  // 1,024-replica literal runs slower than no table.
   const size_t glds = size_t(t->n_users) * kXLdsBytesPerUser;
-  a.oc.glds = glds <= 65536 ? 1 : 0;
+  const int32_t R = t->n_replicas;
+  const size_t per_cu = R <= 256 ? 1 : R <= 512 ? 2 : R <= 768 ? 3 : 4;
+  a.oc.glds = (glds <= 65536 && glds <= size_t(160 * 1024) / per_cu - 1024) ? 1 : 0;
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
   hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);

@@ -120,6 +120,23 @@ def test_global_memory_path_matches():
     compare_sim(g, o)
 
 
+@pytest.mark.parametrize("literal", [False, True])
+def test_global_memory_path_many_replicas_many_users(literal):
+    """800 replicas of 800 users: the global-memory kernel's user table would not let
+    every replica's work-group be resident at once, so it keeps the table in HBM."""
+    rng = np.random.default_rng(63 + literal)
+    reps = [random_trace(rng, int(rng.integers(1, 30)), 800, 2, 400, multi=True, max_tok=6)
+            for _ in range(800)]
+    tr = tg.concat(reps)
+    cost = rng.integers(0, 100, tr.n).astype(np.int64)
+    reason = rng.integers(0, 3, tr.n).astype(np.uint8)
+    say("global many replicas", literal, tr.n)
+    cap = 40 if literal else 8  # (the literal engine's KV capacity)
+    o = oracle.simulate(tr, cost, reason, 20, cap, 6, flags=oracle.FSO_LITERAL if literal else 0)
+    g = gpu_schedule(tr, cost, reason, 20, cap, 6, global_only=True, literal=literal)
+    compare_sim(g, o)
+
+
 def test_onchip_overflow_resumes_in_global_memory():
     """More backlogged users and queued requests than fit on chip: with no
     throttling and a tiny capacity the queue grows to thousands of requests."""

@@ -149,18 +149,30 @@ __host__ __device__ inline int mask_width(uint32_t mask) {
 }
 
 // Adds one item row to the tile histogram in LDS.  Narrow digits (few bins, so many
-// lanes of a wave share one) are aggregated per wave first; wide digits go straight to
-// LDS atomics, whose same-address conflicts are then rare and cheaper than the
-// aggregation's ballots.
+// lanes of a wave share one) are aggregated per wave first.  Wide digits go straight to
+// LDS atomics on one of kHistCopies copies of the histogram chosen by the lane's low
+// bits: lanes of a heavy key's digit then add to different words in different banks
+// (each copy is padded by one word) instead of stalling on one address.
 constexpr int kPlainHistWidth = 6;
+constexpr int kHistCopies = 8;
+constexpr int kHistStride = kRadix + 1;
+constexpr int kHistWords = kHistCopies * kHistStride;
 __device__ inline void hist_add(uint32_t *h, uint32_t d, bool valid, int width) {
   if (width >= kPlainHistWidth) {
-    if (valid) atomicAdd(&h[d], 1u);
+    if (valid) atomicAdd(&h[(threadIdx.x & (kHistCopies - 1)) * kHistStride + d], 1u);
     return;
   }
   const int lane = threadIdx.x & 63;
   const uint64_t peers = digit_peers(d, valid, width);
   if (valid && (peers & ((uint64_t(1) << lane) - 1)) == 0) atomicAdd(&h[d], uint32_t(__popcll(peers)));
+}
+
+// Bin b of the tile histogram: the sum of its copies (narrow digits use copy 0 only).
+__device__ inline uint32_t hist_total(const uint32_t *h, int b) {
+  uint32_t v = 0;
+#pragma unroll
+  for (int c = 0; c < kHistCopies; ++c) v += h[c * kHistStride + b];
+  return v;
 }
 
 // Work-groups are dealt to the 8 XCDs round robin (block b runs on XCD b % 8).  This
@@ -252,13 +264,13 @@ struct InitArgs {
 // Builds the elements of one tile in stream order, checks the fields the throttle
 // reads, and counts the tile's first radix digit.
 __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
-  __shared__ uint32_t h[kRadix];
+  __shared__ uint32_t h[kHistWords];
   __shared__ int32_t s_r0;
   const int t = threadIdx.x;
   const DevTrace &tr = a.t;
   const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
   const int64_t base = tile * kTile;
-  h[t] = 0;
+  for (int j = t; j < kHistWords; j += kThreads) h[j] = 0;
   if (t == 0) s_r0 = replica_of(tr.rep_off, tr.R, base);
   __syncthreads();
   const int sh = *a.sh;
@@ -318,7 +330,7 @@ __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
   }
   if (code) raise_err(a.err, code);
   __syncthreads();
-  if (t <= int(a.mask)) a.hist[int64_t(t) * a.tiles + tile] = h[t];
+  if (t <= int(a.mask)) a.hist[int64_t(t) * a.tiles + tile] = hist_total(h, t);
 }
 
 // ---------------------------------------------------------------- radix sort pass
@@ -326,9 +338,9 @@ __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
 __global__ void __launch_bounds__(kThreads) k_radix_hist(const uint64_t *el, int64_t N, int shift,
                                                           uint32_t mask, uint32_t *hist,
                                                           int64_t tiles) {
-  __shared__ uint32_t h[kRadix];
+  __shared__ uint32_t h[kHistWords];
   const int t = threadIdx.x;
-  h[t] = 0;
+  for (int j = t; j < kHistWords; j += kThreads) h[j] = 0;
   __syncthreads();
   const int64_t base = blockIdx.x * int64_t(kTile);
   const int width = mask_width(mask);
@@ -340,7 +352,7 @@ __global__ void __launch_bounds__(kThreads) k_radix_hist(const uint64_t *el, int
     hist_add(h, d, valid, width);
   }
   __syncthreads();
-  if (t <= int(mask)) hist[int64_t(t) * tiles + blockIdx.x] = h[t];
+  if (t <= int(mask)) hist[int64_t(t) * tiles + blockIdx.x] = hist_total(h, t);
 }
 
 struct ScatterArgs {

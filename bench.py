@@ -46,18 +46,19 @@ STAGE_SRC = {
 # and stage; an entry counts only while the stage's sources hash to `src`.
 MEASURED_TRAFFIC = {
     # k_schedule_onchip on the 64 x 256 x 8 replica workload (6.4M requests)
-    ("c2_replicas", "schedule"): {"src": "e54b779cc0911a8b", "fetch_kib": 147788.0,
-                                  "write_kib": 38783.9375, "fetch_factor": 1.99993,
+    ("c2_replicas", "schedule"): {"src": "e54b779cc0911a8b", "fetch_kib": 147786.3125,
+                                  "write_kib": 38781.78125, "fetch_factor": 1.99993,
                                   "write_factor": 1.0},
     # k_schedule_onchip on the 1,024-replica weight sweep (20.48M requests)
-    ("c4_sweep", "schedule"): {"src": "e54b779cc0911a8b", "fetch_kib": 353970.4375,
-                               "write_kib": 137772.96875, "fetch_factor": 1.99988,
+    ("c4_sweep", "schedule"): {"src": "e54b779cc0911a8b", "fetch_kib": 353983.4375,
+                               "write_kib": 137776.03125, "fetch_factor": 1.99988,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
-    ("c3_throttle", "throttle"): {"src": "d6467d5ee97b766d", "fetch_kib": 2711446.125,
-                                  "write_kib": 2221909.3125, "fetch_factor": 1.99992,
+    ("c3_throttle", "throttle"): {"src": "e7d650dbb7b01d78", "fetch_kib": 2711800.6875,
+                                  "write_kib": 2219110.96875, "fetch_factor": 1.99993,
                                   "write_factor": 1.0},
 }
+
 
 
 def src_hash(stage):

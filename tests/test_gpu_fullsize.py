@@ -68,3 +68,58 @@ def test_full_throttle_stream():
     nw = (tr.n + 31) // 32
     assert (g["bitmap"][:nw] == o.bitmap[:nw]).all()
     say("  ok:", int((o.reason > 0).sum()), "throttled")
+
+
+NO_LIMIT = 2 ** 31 - 1
+
+
+@pytest.mark.parametrize("policy", ["rpm", "literal"])
+def test_full_replica_workload_policy_and_engine(policy):
+    """The 64 x 256 x 8 replica workload (6.4M requests) as the benchmark runs it with
+    --policy rpm (per-user limit always on, interaction-blind, first come first served)
+    or --engine literal (20 ms decode steps, 2^22 KV tokens per replica), through
+    fs_run_trace and fs_fairness_metrics, bit-exact with the oracle."""
+    wl, tr = workload_trace("c2_replicas")
+    say("full", policy, tr.n)
+    if policy == "rpm":
+        t_user, t_app, theta = wl.t_user, [NO_LIMIT] * tr.n_apps, -1
+        fcfs, blind, literal = True, True, False
+        step_us, cap = wl.step_us, wl.cap_tokens
+    else:
+        t_user, t_app, theta = wl.t_user, list(wl.t_app), wl.overload_tokens
+        fcfs, blind, literal = False, False, True
+        step_us, cap = 20_000, 1 << 22
+    dt = fs.DeviceTrace(tr)
+    coef, per_rep = fs.workload_weights(wl, tr)
+    w, keep = fs.make_weights(dt, coef, None, per_rep)
+    lim = fs.make_limits(wl.window_us, t_user, t_app)
+    eng = fs.make_engine(step_us, cap, theta, fcfs=fcfs, blind=blind, literal=literal)
+    out = fs.Outputs(dt)
+    ws, cost_view, reason_view = fs.run_trace_buffers(dt)
+    fs.fs_run_trace(dt, w, lim, eng, out, ws)
+    m = fs.fs_fairness_metrics(dt, cost_view, out, eng).host()
+    h = out.host()
+    gcost, greason = cost_view.cpu().numpy(), reason_view.cpu().numpy()
+    del ws, out, dt
+    say("  gpu done; oracle")
+    ocoef, oper = oracle.weights_for(wl, tr)
+    c = oracle.cost(tr, ocoef, coef_per_replica=oper)
+    th = oracle.throttle(tr, wl.window_us, t_user, t_app, raw=True, counts=False)
+    flags = ((oracle.FSO_FCFS if fcfs else 0) | (oracle.FSO_BLIND if blind else 0) |
+             (oracle.FSO_LITERAL if literal else 0))
+    sim = oracle.simulate(tr, c, th.reason, step_us, cap, theta, n_threads=16, flags=flags)
+    met = oracle.fairness_metrics(tr, c, sim.status, sim.admit_step, sim.max_gap, step_us)
+    assert (gcost == c).all()
+    assert (greason == th.reason).all()
+    n = tr.n
+    compare_sim({k: (v[:n] if v is not None and k not in ("counter", "steps", "decisions",
+                                                          "max_gap") else v)
+                 for k, v in h.items()}, sim)
+    for k in ("jain", "max_gap_tokens", "svc_req_pct", "svc_int_pct", "served_users_pct",
+              "delayed_users_pct"):
+        np.testing.assert_allclose(m[k], getattr(met, k), rtol=1e-9, atol=0, err_msg=k)
+    for k in ("throttled", "aborted_midway", "wasted_tokens"):
+        assert (m[k] == getattr(met, k)).all(), k
+    if policy == "rpm":
+        assert met.aborted_midway.sum() > 0
+    say("  ok:", int(h["decisions"].sum()), "admissions")

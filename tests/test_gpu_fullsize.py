@@ -47,6 +47,11 @@ def test_full_small():
     _full_path("c1_small")
 
 
+def test_full_replica_workload():
+    """64 replicas x 256 users x 8 apps, 6.4M requests: the benchmark's default line."""
+    _full_path("c2_replicas")
+
+
 def test_full_weight_sweep():
     """1,024 replicas x 1,024 users, 20.48M requests, one weight pair per replica."""
     _full_path("c4_sweep")

@@ -29,6 +29,9 @@
  *   len_in, len_sys, len_out  int32 input / system / output tokens, each in [0, 2^24)
  *   call, head and prev are either all NULL (every record is a single-call
  *   interaction) or all set.  len_sys may be NULL (= 0).
+ *   A trace without requests (rep_off_h[n_replicas] == 0) may leave every per-request
+ *   array NULL, here and in the calls below (cost, reasons, bitmap, per-request
+ *   outputs); the calls then write only their per-replica and per-user outputs.
  */
 #ifndef FAIRSERVE_H
 #define FAIRSERVE_H

@@ -24,22 +24,30 @@ constexpr size_t kAlign = 256;
 bool aligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) == 0; }
 
 // Checks that need no device access: shapes, the host copy of the replica offsets,
-// and which optional arrays are present.
+// and which optional arrays are present.  A trace without requests may leave its
+// per-request arrays NULL (an empty device tensor has no storage).
 fs_status check_trace(const fs_trace *t, bool need_lengths) {
   if (!t || t->n_replicas < 1 || t->n_users < 1 || t->n_apps < 1 || t->n_apps > kMaxApps)
     return FS_E_ARG;
-  if (!t->rep_off_h || !t->rep_off || !t->ts_us || !t->user || !t->app) return FS_E_ARG;
-  bool any = t->call || t->head || t->prev;
-  bool all = t->call && t->head && t->prev;
-  if (any && !all) return FS_E_ARG;
-  if (need_lengths && (!t->len_in || !t->len_out)) return FS_E_ARG;
+  if (!t->rep_off_h || !t->rep_off) return FS_E_ARG;
   if (t->rep_off_h[0] != 0) return FS_E_ARG;
   for (int32_t r = 0; r < t->n_replicas; ++r) {
     int64_t n = t->rep_off_h[r + 1] - t->rep_off_h[r];
     if (n < 0 || n > INT32_MAX - 64) return FS_E_ARG;
   }
   if (int64_t(t->n_replicas) * t->n_users > (int64_t(1) << 31)) return FS_E_ARG;
+  if (t->rep_off_h[t->n_replicas] == 0) return FS_OK;
+  if (!t->ts_us || !t->user || !t->app) return FS_E_ARG;
+  bool any = t->call || t->head || t->prev;
+  bool all = t->call && t->head && t->prev;
+  if (any && !all) return FS_E_ARG;
+  if (need_lengths && (!t->len_in || !t->len_out)) return FS_E_ARG;
   return FS_OK;
+}
+
+// Per-request array p is present, or not needed because the trace has no requests.
+bool per_request(const fs_trace *t, const void *p) {
+  return p != nullptr || t->rep_off_h[t->n_replicas] == 0;
 }
 
 fs_status check_weights(const fs_trace *t, const fs_weights *w) {
@@ -68,8 +76,8 @@ fs_status check_engine(const fs_engine *e) {
 }
 
 fs_status check_outputs(const fs_trace *t, const fs_outputs *o) {
-  if (!o || !o->status || !o->admit_step || !o->counter || !o->steps || !o->decisions ||
-      !o->max_gap || !o->err)
+  if (!o || !per_request(t, o->status) || !per_request(t, o->admit_step) || !o->counter ||
+      !o->steps || !o->decisions || !o->max_gap || !o->err)
     return FS_E_ARG;
   return FS_OK;
 }
@@ -157,7 +165,7 @@ fs_status fs_cost(const fs_trace *t, const fs_weights *w, int64_t *cost, int32_t
   fs_status s = check_trace(t, true);
   if (s == FS_OK) s = check_weights(t, w);
   if (s != FS_OK) return s;
-  if (!cost || !err) return FS_E_ARG;
+  if (!per_request(t, cost) || !err) return FS_E_ARG;
   if (launch_zero_i32(err, stream) != hipSuccess) return FS_E_HIP;
   return hip_status(launch_cost(t, w, cost, err, stream));
 }
@@ -174,7 +182,7 @@ fs_status fs_throttle(const fs_trace *t, const fs_limits *lim, const uint8_t *ov
   fs_status s = check_trace(t, false);
   if (s == FS_OK) s = check_limits(t, lim);
   if (s != FS_OK) return s;
-  if ((flags & ~FS_THROTTLE_RAW) || !bitmap || !err) return FS_E_ARG;
+  if ((flags & ~FS_THROTTLE_RAW) || !per_request(t, bitmap) || !err) return FS_E_ARG;
   if (!ws || !aligned(ws) || ws_bytes < throttle_workspace_bytes(t)) return FS_E_WORKSPACE;
   if (launch_zero_i32(err, stream) != hipSuccess) return FS_E_HIP;
   return hip_status(launch_throttle(t, lim, overloaded, flags, bitmap, reason, cnt_user, cnt_app,
@@ -200,7 +208,7 @@ fs_status fs_schedule_step(void *state, const fs_trace *t, const int64_t *cost,
   if (s == FS_OK) s = check_engine(eng);
   if (s == FS_OK) s = check_outputs(t, out);
   if (s != FS_OK) return s;
-  if (!state || !aligned(state) || !cost) return FS_E_ARG;
+  if (!state || !aligned(state) || !per_request(t, cost)) return FS_E_ARG;
   if (launch_zero_i32(out->err, stream) != hipSuccess) return FS_E_HIP;
   return hip_status(launch_schedule(state, t, cost, exceed_reason, eng, out, n_steps, stream));
 }
@@ -258,8 +266,8 @@ fs_status fs_fairness_metrics(const fs_trace *t, const int64_t *cost, const fs_o
   fs_status s = check_trace(t, true);
   if (s == FS_OK) s = check_engine(eng);
   if (s != FS_OK) return s;
-  if (!cost || !out || !out->status || !out->admit_step || !out->max_gap || !out->err || !m ||
-      delay_steps < 0)
+  if (!per_request(t, cost) || !out || !per_request(t, out->status) ||
+      !per_request(t, out->admit_step) || !out->max_gap || !out->err || !m || delay_steps < 0)
     return FS_E_ARG;
   if (!m->jain || !m->max_gap_tokens || !m->svc_req_pct || !m->svc_int_pct ||
       !m->served_users_pct || !m->delayed_users_pct || !m->throttled || !m->aborted_midway ||

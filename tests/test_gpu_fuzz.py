@@ -1,0 +1,54 @@
+"""Randomised parity sweep: small random traces (several replicas, multi-call
+interactions, random limits, capacities and overload thresholds) through the raw
+throttle and the scheduler in every engine and policy mode, on the on-chip path, the
+global-memory path and in resumed chunks of steps, bit-exact against the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_common import compare_sim, gpu_schedule, gpu_throttle, say
+from tiny import random_trace
+from paper_2411_15997_amd import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(seed):
+    rng = np.random.default_rng(1000 + seed)
+    R = int(rng.integers(1, 7))
+    U = int(rng.choice([1, 3, 17, 64, 65, 200]))
+    A = int(rng.integers(1, 5))
+    multi = bool(rng.integers(0, 2))  # (interaction links are all set or all absent)
+    reps = []
+    for _ in range(R):
+        n = int(rng.choice([0, 1, 50, 700, 2500, 8000]))
+        span = int(rng.integers(1, 4 * max(n, 1) * 10))
+        reps.append(random_trace(rng, n, U, A, span, multi=multi, max_tok=int(rng.integers(1, 40))))
+    tr = tg.concat(reps)
+    W = int(rng.integers(1, 2000))
+    t_user = int(rng.choice([0, 3, 20, 2 ** 31 - 1]))
+    t_app = [int(x) for x in rng.integers(0, 15, A)]
+    step = int(rng.integers(1, 200))
+    literal = bool(rng.integers(0, 3) == 0)
+    cap = int(rng.integers(1, 300)) if not literal else int(rng.integers(40, 2000))
+    theta = int(rng.choice([-1, 0, 50, 10 ** 9]))
+    fcfs, blind = bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+    mode = int(rng.integers(0, 3))  # 0 on chip, 1 global memory only, 2 in chunks of steps
+    cost = rng.integers(0, 5000, tr.n).astype(np.int64)
+    return tr, W, t_user, t_app, step, literal, cap, theta, fcfs, blind, mode, cost, rng
+
+
+@pytest.mark.parametrize("seed", range(300))
+def test_random_throttle_and_schedule(seed):
+    tr, W, t_user, t_app, step, literal, cap, theta, fcfs, blind, mode, cost, rng = _case(seed)
+    say("fuzz", seed, tr.n_replicas, tr.n_users, tr.n, literal, fcfs, blind, mode)
+    o_th = oracle.throttle(tr, W, t_user, t_app, raw=True, counts=False)
+    g_th = gpu_throttle(tr, W, t_user, t_app, raw=True, counts=False)
+    assert (g_th["reason"] == o_th.reason).all()
+    flags = ((oracle.FSO_FCFS if fcfs else 0) | (oracle.FSO_BLIND if blind else 0) |
+             (oracle.FSO_LITERAL if literal else 0))
+    o = oracle.simulate(tr, cost, o_th.reason, step, cap, theta, flags=flags)
+    chunks = int(rng.integers(1, 40)) if mode == 2 else None
+    g = gpu_schedule(tr, cost, o_th.reason, step, cap, theta, chunks=chunks,
+                     global_only=(mode == 1), fcfs=fcfs, blind=blind, literal=literal)
+    compare_sim(g, o)

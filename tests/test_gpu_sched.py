@@ -5,7 +5,7 @@ import torch
 
 import oracle
 import paper_2411_15997_amd as fs
-from gpu_common import compare_sim, gpu_schedule, say, workload_trace
+from gpu_common import compare_sim, gpu_schedule, gpu_throttle, say, workload_trace
 from tiny import load_golden, random_trace, trace_from_case
 from paper_2411_15997_amd import tracegen as tg
 
@@ -259,3 +259,42 @@ def test_full_replica_workload_c2():
     say("sched full c2", tr.n)
     g, o, _, _ = _run_workload(wl, tr)
     compare_sim(g, o)
+
+
+@pytest.mark.parametrize("multi", [False, True])
+def test_empty_trace_every_entry_point(multi):
+    """Replicas without requests (empty device tensors have no storage, so every
+    per-request pointer is NULL): cost, throttle, state init, steps, the whole path and
+    the metrics succeed and give the oracle's per-replica results."""
+    rng = np.random.default_rng(64 + multi)
+    tr = tg.concat([random_trace(rng, 0, 5, 2, 10, multi=multi) for _ in range(3)])
+    assert tr.n == 0
+    cost = np.zeros(0, np.int64)
+    reason = np.zeros(0, np.uint8)
+    for literal in (False, True):
+        o = oracle.simulate(tr, cost, reason, 10, 50, 5,
+                            flags=oracle.FSO_LITERAL if literal else 0)
+        g = gpu_schedule(tr, cost, reason, 10, 50, 5, literal=literal)
+        compare_sim(g, o)
+    dt = fs.DeviceTrace(tr)
+    coef = np.full((1, 2, 1, 3), 1 << 16, np.int64)
+    w, keep = fs.make_weights(dt, coef, None, False)
+    lim = fs.make_limits(100, 3, [2, 2])
+    eng = fs.make_engine(10, 50, 5)
+    empty_cost = torch.zeros(0, dtype=torch.int64, device=dt.device)
+    fs.fs_cost(dt, w, cost=empty_cost)
+    out = fs.Outputs(dt)
+    ws, cost_view, reason_view = fs.run_trace_buffers(dt)
+    fs.fs_run_trace(dt, w, lim, eng, out, ws)
+    h = out.host()
+    assert (h["steps"] == 0).all() and (h["decisions"] == 0).all() and (h["counter"] == 0).all()
+    m = fs.fs_fairness_metrics(dt, empty_cost, out, eng).host()
+    mo = oracle.fairness_metrics(tr, cost, np.zeros(0, np.int8), np.zeros(0, np.int32),
+                                 h["max_gap"], 10)
+    for k in ("jain", "svc_req_pct", "svc_int_pct", "served_users_pct", "delayed_users_pct"):
+        np.testing.assert_allclose(m[k], getattr(mo, k), rtol=1e-9, atol=0, err_msg=k)
+    for k in ("throttled", "aborted_midway", "wasted_tokens"):
+        assert (m[k] == getattr(mo, k)).all(), k
+    for raw in (True, False):
+        gt = gpu_throttle(tr, 100, 3, [2, 2], raw=raw, counts=True)
+        assert gt["reason"].size == 0

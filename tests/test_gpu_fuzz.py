@@ -52,3 +52,44 @@ def test_random_throttle_and_schedule(seed):
     g = gpu_schedule(tr, cost, o_th.reason, step, cap, theta, chunks=chunks,
                      global_only=(mode == 1), fcfs=fcfs, blind=blind, literal=literal)
     compare_sim(g, o)
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_random_throttle_modes(seed):
+    """Gated (random overload flags or always overloaded) and raw, per-(user, app) and
+    app-level limits, with the window counts."""
+    from gpu_common import bits_of
+    tr, W, t_user, t_app, *_, rng = _case(5000 + seed)
+    raw = bool(rng.integers(0, 2))
+    scope = int(rng.integers(0, 2))
+    ov = None if rng.integers(0, 2) else rng.integers(0, 2, tr.n).astype(np.uint8)
+    say("fuzz throttle", seed, tr.n, raw, scope, ov is None)
+    o = oracle.throttle(tr, W, t_user, t_app, overloaded=ov, raw=raw, counts=True,
+                        app_scope=scope)
+    g = gpu_throttle(tr, W, t_user, t_app, ov, raw, True, scope)
+    assert (g["reason"] == o.reason).all()
+    assert (bits_of(g["bitmap"], tr.n) == bits_of(o.bitmap, tr.n)).all()
+    assert (g["cnt_user"] == o.cnt_user).all() and (g["cnt_app"] == o.cnt_app).all()
+
+
+@pytest.mark.parametrize("seed", range(100))
+def test_random_cost(seed):
+    """Random Q16 coefficient tables (shared or per replica, 1 to 20 stages) and Q8
+    priorities (none, shared or per replica)."""
+    import torch
+    import paper_2411_15997_amd as fs
+    tr, *_, rng = _case(9000 + seed)
+    R, A, U = tr.n_replicas, tr.n_apps, tr.n_users
+    J = int(rng.choice([1, 2, 20]))
+    per_rep = bool(rng.integers(0, 2))
+    coef = rng.integers(0, 1 << int(rng.choice([8, 17, 30])), (R if per_rep else 1, A, J, 3))
+    pmode = int(rng.integers(0, 3))  # 0 none, 1 shared, 2 per replica
+    prio = (None if pmode == 0 else
+            rng.integers(0, 1 << 12, (R if pmode == 2 else 1, U)).astype(np.int32))
+    say("fuzz cost", seed, tr.n, J, per_rep, pmode)
+    o = oracle.cost(tr, coef, prio if pmode else None, coef_per_replica=per_rep,
+                    prio_per_replica=pmode == 2)
+    dt = fs.DeviceTrace(tr)
+    w, keep = fs.make_weights(dt, coef, prio if pmode else None, per_rep, pmode == 2)
+    c = fs.fs_cost(dt, w, cost=torch.empty(tr.n, dtype=torch.int64, device=dt.device))
+    assert (c.cpu().numpy() == o).all()

@@ -93,3 +93,55 @@ def test_random_cost(seed):
     w, keep = fs.make_weights(dt, coef, prio if pmode else None, per_rep, pmode == 2)
     c = fs.fs_cost(dt, w, cost=torch.empty(tr.n, dtype=torch.int64, device=dt.device))
     assert (c.cpu().numpy() == o).all()
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_history(seed):
+    """fs_weights_from_history on random histories (several replicas pooled, 1 to 20
+    stages, random K and base limit)."""
+    import paper_2411_15997_amd as fs
+    tr, *_, rng = _case(12000 + seed)
+    J = int(rng.choice([1, 3, 20]))
+    K = int(rng.integers(1, 1 << 20))
+    base = int(rng.integers(0, 200))
+    say("fuzz history", seed, tr.n, J, K, base)
+    o = oracle.weights_from_history(tr, J, K=K, base_limit=base)
+    dt = fs.DeviceTrace(tr)
+    st, c, t = fs.fs_weights_from_history(dt, J, K=K, base_limit=base)
+    assert (st.cpu().numpy() == o.stats).all()
+    assert (c.cpu().numpy() == o.coef).all()
+    assert (t.cpu().numpy() == o.t_app).all()
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_metrics(seed):
+    """fs_fairness_metrics on random outputs of random traces; every fourth case with
+    5,000 users (the global-memory aggregation)."""
+    import torch
+    import paper_2411_15997_amd as fs
+    tr, W, t_user, t_app, step, *_, rng = _case(15000 + seed)
+    if seed % 4 == 3:
+        tr = tg.Trace(**{**tr.__dict__, "n_users": 5000,
+                         "user": (tr.user * 997 + 13) % 5000})
+    n = tr.n
+    cost = rng.integers(0, 10 ** 6, n).astype(np.int64)
+    status = rng.choice(np.array([0, 0, 1, 2, 3], np.int8), n)
+    admit_step = np.where(status == 0, tr.ts_us // step + rng.integers(0, 3, n),
+                          -1).astype(np.int32)
+    max_gap = rng.integers(0, 2 ** 40, tr.n_replicas).astype(np.int64)
+    delay = int(rng.integers(0, 3))
+    say("fuzz metrics", seed, n, tr.n_users, delay)
+    mo = oracle.fairness_metrics(tr, cost, status, admit_step, max_gap, step, delay)
+    dt = fs.DeviceTrace(tr)
+    out = fs.Outputs(dt, parity=False)
+    if n:
+        out.status[:n].copy_(torch.as_tensor(status))
+        out.admit_step[:n].copy_(torch.as_tensor(admit_step))
+    out.max_gap.copy_(torch.as_tensor(max_gap))
+    eng = fs.make_engine(step, 1000, 1000)
+    m = fs.fs_fairness_metrics(dt, torch.as_tensor(cost).to(dt.device), out, eng, delay).host()
+    for k in ("throttled", "aborted_midway", "wasted_tokens"):
+        assert (m[k] == getattr(mo, k)).all(), k
+    for k in ("jain", "max_gap_tokens", "svc_req_pct", "svc_int_pct", "served_users_pct",
+              "delayed_users_pct"):
+        np.testing.assert_allclose(m[k], getattr(mo, k), rtol=1e-9, atol=0, err_msg=k)

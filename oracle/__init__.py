@@ -253,8 +253,7 @@ def fairness_metrics(tr, cost_arr, status, admit_step, max_gap, step_us, delay_s
 
 def weights_for(wl, tr):
     """Oracle-side Q16 coefficient table [R|1][A][J][3] and whether it is per replica."""
-    from paper_2411_15997_amd import tracegen as tg
-    direct = tg.coef_direct_table(wl, tr)
+    direct = wl.direct_coef_table(tr)
     if direct is not None:
         return direct, direct.shape[0] > 1
     e_in, e_sys, e_out = wl.expectations()

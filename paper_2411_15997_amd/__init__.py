@@ -412,9 +412,10 @@ def fs_coef_from_expectations(e_in, e_sys, e_out, K=1024):
 
 
 def workload_weights(wl, tr):
-    """Product-side Q16 coefficient table for a workload: [R|1][A][J][3], per-replica flag."""
-    from . import tracegen as tg
-    direct = tg.coef_direct_table(wl, tr)
+    """Product-side Q16 coefficient table for a workload description `wl` (any object
+    with direct_coef_table(trace), expectations() and weight_K): [R|1][A][J][3] and
+    whether it is per replica."""
+    direct = wl.direct_coef_table(tr)
     if direct is not None:
         return direct, direct.shape[0] > 1
     e_in, e_sys, e_out = wl.expectations()

@@ -4,7 +4,7 @@ import sys
 
 import numpy as np
 
-from paper_2411_15997_amd import tracegen as tg
+import tracegen as tg
 
 
 def say(*a):

@@ -6,7 +6,7 @@ import oracle
 import paper_2411_15997_amd as fs
 from gpu_common import say, workload_trace
 from tiny import random_trace
-from paper_2411_15997_amd import tracegen as tg
+import tracegen as tg
 
 pytestmark = pytest.mark.gpu
 

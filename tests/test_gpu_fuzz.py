@@ -8,7 +8,7 @@ import pytest
 import oracle
 from gpu_common import compare_sim, gpu_schedule, gpu_throttle, say
 from tiny import random_trace
-from paper_2411_15997_amd import tracegen as tg
+import tracegen as tg
 
 pytestmark = pytest.mark.gpu
 

@@ -6,7 +6,7 @@ import pytest
 import oracle
 from gpu_common import say, workload_trace
 from tiny import random_trace
-from paper_2411_15997_amd import tracegen as tg
+import tracegen as tg
 import paper_2411_15997_amd as fs
 
 pytestmark = pytest.mark.gpu

@@ -7,7 +7,7 @@ import oracle
 import paper_2411_15997_amd as fs
 from gpu_common import compare_sim, gpu_schedule, gpu_throttle, say, workload_trace
 from tiny import load_golden, random_trace, trace_from_case
-from paper_2411_15997_amd import tracegen as tg
+import tracegen as tg
 
 pytestmark = pytest.mark.gpu
 

@@ -5,7 +5,7 @@ import pytest
 import oracle
 from gpu_common import bits_of, gpu_throttle, say, workload_trace
 from tiny import load_golden, random_trace
-from paper_2411_15997_amd import tracegen as tg
+import tracegen as tg
 import paper_2411_15997_amd as fs
 
 pytestmark = pytest.mark.gpu

@@ -12,8 +12,8 @@ import pytest
 
 import oracle
 from tiny import random_trace
-from paper_2411_15997_amd import tracegen as tg
-from paper_2411_15997_amd.tracegen import Trace, concat
+import tracegen as tg
+from tracegen import Trace, concat
 
 
 def _trace(app, call, lin, lsys, lout, n_apps, head=None, prev=None):

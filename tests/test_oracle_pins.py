@@ -18,8 +18,8 @@ import pytest
 import oracle
 import naive_model as nm
 from tiny import load_golden, random_trace, trace_from_case
-from paper_2411_15997_amd import tracegen as tg
-from paper_2411_15997_amd.tracegen import Trace, concat
+import tracegen as tg
+from tracegen import Trace, concat
 
 # ---------------------------------------------------------------- golden cases
 

@@ -6,7 +6,7 @@ import os
 
 import numpy as np
 
-from paper_2411_15997_amd.tracegen import Trace, concat
+from tracegen import Trace, concat
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 

@@ -8,7 +8,9 @@ Fig. 4 discussion and Table 2), calls spread out in time, system prompts
 (Sec. 3, Fig. 5 discussion) and heavy-tailed per-user activity (Sec. 3,
 Fig. 2 discussion).
 
-This module is shared by the CPU oracle's tests and the HIP path.  It holds
+This module is shared by the CPU oracle's tests and the HIP path's tests and
+benchmark; it lives outside both (the oracle and the library import nothing from
+each other, and neither imports it for arithmetic).  It holds
 none of the method's arithmetic: no cost, no window counting, no weights.
 It only draws random requests and records the workload constants (limits,
 engine capacity, expected token counts) that the method takes as inputs.
@@ -111,6 +113,10 @@ class Workload:
     @property
     def step_us(self) -> int:
         return int(round(self.step_ms * 1000))
+
+    def direct_coef_table(self, trace) -> Optional[np.ndarray]:
+        """The Q16 table this workload fixes directly (None: derive it with Eq. 1)."""
+        return coef_direct_table(self, trace)
 
     def expectations(self):
         """Nominal expected token counts per (app, stage): arrays [A][J] for in, sys, out."""
@@ -434,7 +440,8 @@ def generate(wl: Workload, replicas: Optional[Sequence[int]] = None) -> Trace:
 
 
 def coef_direct_table(wl: Workload, trace: Trace) -> Optional[np.ndarray]:
-    """Q16 coefficient table [R or 1][A][J][3] for workloads that fix it directly.
+    """Q16 coefficient table [R or 1][A][J][3] for workloads that fix it directly
+    (the workload's constants, or the weight pair each replica drew).
 
     Returns None when the table must be derived from expectations via Eq. 1.
     """

@@ -49,7 +49,7 @@ typedef enum fs_status {
   FS_E_ARG = 1,       /* bad argument or shape (synchronous) */
   FS_E_ORDER = 2,     /* ts_us decreases inside a replica */
   FS_E_RANGE = 3,     /* id, token count, coefficient, priority, cost or chain link out of range */
-  FS_E_OVERFLOW = 4,  /* a cost or a service counter reaches 2^62 */
+  FS_E_OVERFLOW = 4,  /* a cost, a service counter or a replica's charged total reaches 2^62 */
   FS_E_WORKSPACE = 5, /* workspace or state buffer too small (synchronous) */
   FS_E_STATE = 6,     /* state buffer not initialised for this trace, or wrong version */
   FS_E_HIP = 7        /* a HIP runtime call failed */
@@ -187,7 +187,8 @@ typedef struct fs_metrics {
 fs_status fs_cost(const fs_trace *t, const fs_weights *w, int64_t *cost, int32_t *err,
                   hipStream_t stream);
 
-/* Bytes of device workspace fs_throttle needs for this trace. */
+/* Bytes of device workspace fs_throttle needs for this trace (0 for a trace it
+ * rejects, see the key-space limit below). */
 size_t fs_throttle_workspace(const fs_trace *t);
 
 /* OIT (Alg. 1 monitoring stream, limit checks; Sec. 4, OIT).  For each record the
@@ -198,7 +199,10 @@ size_t fs_throttle_workspace(const fs_trace *t);
  * iff its interaction's first call was throttled (code 3); bitmap bit i = throttled.
  * bitmap: [ceil(N/32)] uint32, bit i%32 of word i/32 (global record index).
  * reason [N] uint8, cnt_user [N], cnt_app [N] int32 (the window counts) may be NULL.
- * ws: device workspace of at least fs_throttle_workspace(t) bytes, 256-byte aligned. */
+ * ws: device workspace of at least fs_throttle_workspace(t) bytes, 256-byte aligned.
+ * Key-space limit: with b(x) the bits of x - 1 (at least 1), the trace must have
+ * b(n_replicas * n_users) + b(n_apps) <= 32 and that sum + b(N) + 1 <= 64 (N records);
+ * otherwise FS_E_ARG (also from fs_run_trace, before anything is enqueued). */
 #define FS_THROTTLE_RAW 1u
 fs_status fs_throttle(const fs_trace *t, const fs_limits *lim, const uint8_t *overloaded,
                       uint32_t flags, uint32_t *bitmap, uint8_t *reason, int32_t *cnt_user,
@@ -226,9 +230,13 @@ fs_status fs_schedule_step(void *state, const fs_trace *t, const int64_t *cost,
                            const uint8_t *exceed_reason, const fs_engine *eng, fs_outputs *out,
                            int64_t n_steps, hipStream_t stream);
 
-/* The whole hot path: fs_cost, fs_throttle (raw), fs_state_init and
- * fs_schedule_step until drained, using caller workspace of at least
- * fs_run_trace_workspace(t) bytes (256-byte aligned). */
+/* The whole hot path of Alg. 1 over a trace: the per-call service of Eq. 2 (fs_cost),
+ * the OIT window tests of the monitoring stream (fs_throttle, raw), then the
+ * monitoring and execution streams step by step (fs_state_init, fs_schedule_step until
+ * drained), using caller workspace of at least fs_run_trace_workspace(t) bytes
+ * (256-byte aligned; 0 is returned for a trace outside fs_throttle's key-space limit).
+ * The cost and raw reasons stay in the workspace: the cost at offset 0 (int64 [N]),
+ * the reasons (uint8 [N]) at the next 256-byte boundary. */
 size_t fs_run_trace_workspace(const fs_trace *t);
 fs_status fs_run_trace(const fs_trace *t, const fs_weights *w, const fs_limits *lim,
                        const fs_engine *eng, fs_outputs *out, void *ws, size_t ws_bytes,
@@ -236,7 +244,10 @@ fs_status fs_run_trace(const fs_trace *t, const fs_weights *w, const fs_limits *
 
 /* Per-replica metrics from a finished run (Sec. 5 definitions plus Jain's index).
  * ws: device workspace of at least fs_metrics_workspace(t) bytes (256-byte aligned).
- * out->err receives data-dependent errors. */
+ * out->err receives data-dependent errors: FS_E_RANGE for an id or interaction link out
+ * of range or an admitted request whose cost is outside [0, 2^62) (not counted), and
+ * FS_E_OVERFLOW when a replica's total charged service (the sum of its admitted costs)
+ * reaches 2^62; below that every sum of Jain's index is exact. */
 size_t fs_metrics_workspace(const fs_trace *t);
 fs_status fs_fairness_metrics(const fs_trace *t, const int64_t *cost, const fs_outputs *out,
                               const fs_engine *eng, int32_t delay_steps, fs_metrics *m, void *ws,

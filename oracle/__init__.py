@@ -15,20 +15,26 @@ from typing import Optional
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB = os.path.join(HERE, "libfs_oracle.so")
+# FSO_ORACLE_LIB names another build of the same source (the sanitizer build of the
+# oracle's own tests); by default the in-tree library.
+LIB = os.environ.get("FSO_ORACLE_LIB") or os.path.join(HERE, "libfs_oracle.so")
 SRC = os.path.join(HERE, "fs_oracle.cpp")
 
 OK, E_ARG, E_ORDER, E_RANGE, E_OVERFLOW = 0, 1, 2, 3, 4
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with the host compiler (no GPU code)."""
-    if force or not os.path.exists(LIB):
-        cmd = ["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-pthread", "-Wall",
-               SRC, "-o", LIB + ".tmp"]
-        subprocess.run(cmd, check=True)
-        os.replace(LIB + ".tmp", LIB)
-    return LIB
+def build(force: bool = True, out: Optional[str] = None, sanitize: bool = False) -> str:
+    """Compile the oracle with the host compiler (no GPU code).  sanitize: with
+    AddressSanitizer and UndefinedBehaviorSanitizer (host code only), into `out`."""
+    dst = out or LIB
+    if force or not os.path.exists(dst):
+        cmd = ["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-pthread", "-Wall"]
+        if sanitize:
+            cmd += ["-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                    "-fno-sanitize-recover=undefined"]
+        subprocess.run(cmd + [SRC, "-o", dst + ".tmp"], check=True)
+        os.replace(dst + ".tmp", dst)
+    return dst
 
 
 class _Trace(C.Structure):

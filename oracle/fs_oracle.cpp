@@ -46,7 +46,8 @@ Replica replica(const fso_trace *t, int32_t r) {
 int worse(int a, int b) { return a > b ? a : b; }
 
 // Structural checks.  Each entry point checks the fields it reads.
-enum Need : unsigned { kIds = 1, kOrder = 2, kChain = 4, kLengths = 8 };
+// kIds: app ids (and stages); kUsers: user ids.
+enum Need : unsigned { kIds = 1, kOrder = 2, kChain = 4, kLengths = 8, kUsers = 16 };
 
 int validate_trace(const fso_trace *t, unsigned need) {
   if (!t || t->n_replicas < 1 || t->n_users < 1 || t->n_apps < 1 || !t->rep_off || !t->ts_us ||
@@ -69,8 +70,9 @@ int validate_trace(const fso_trace *t, unsigned need) {
         if (t->ts_us[g] < 0) code = worse(code, FSO_E_RANGE);
         if (i > 0 && t->ts_us[g] < t->ts_us[g - 1]) code = worse(code, FSO_E_ORDER);
       }
+      if ((need & kUsers) && (t->user[g] < 0 || t->user[g] >= t->n_users))
+        code = worse(code, FSO_E_RANGE);
       if (need & kIds) {
-        if (t->user[g] < 0 || t->user[g] >= t->n_users) code = worse(code, FSO_E_RANGE);
         if (t->app[g] < 0 || t->app[g] >= t->n_apps) code = worse(code, FSO_E_RANGE);
         if (all && t->call[g] < 0) code = worse(code, FSO_E_RANGE);
       }
@@ -511,13 +513,15 @@ int fso_weights_from_history(const fso_trace *t, int32_t n_stages, int64_t K, in
 int fso_cost(const fso_trace *t, int32_t n_stages, int64_t coef_rep_stride, const int64_t *coef,
              int64_t prio_rep_stride, const int32_t *prio, int64_t *cost) {
   if (n_stages < 1 || !coef || !cost || coef_rep_stride < 0 || prio_rep_stride < 0) return FSO_E_ARG;
-  int code = validate_trace(t, kIds | kLengths);
+  // Eq. 2 reads the user only through its priority E_i: user ids are checked only
+  // when priorities are given.
+  int code = validate_trace(t, kIds | kLengths | (prio ? unsigned(kUsers) : 0u));
   if (code == FSO_E_ARG) return code;
   for (int32_t r = 0; r < t->n_replicas; ++r) {
     Replica rp = replica(t, r);
     for (int64_t i = 0; i < rp.n; ++i) {
       int64_t g = rp.base + i;
-      int32_t a = t->app[g], k = t->user[g];
+      int32_t a = t->app[g], k = prio ? t->user[g] : 0;
       if (a < 0 || a >= t->n_apps || k < 0 || k >= t->n_users) continue;  // reported above
       int32_t j = t->call ? std::min(std::max(t->call[g], 0), n_stages - 1) : 0;
       const int64_t *c = coef + r * coef_rep_stride + (int64_t(a) * n_stages + j) * 3;
@@ -559,7 +563,7 @@ int fso_throttle_scoped(const fso_trace *t, int64_t window_us, int32_t t_user,
                         int32_t *cnt_app) {
   if (window_us <= 0 || t_user < 0 || !t_app || !reason || app_scope < 0 || app_scope > 1)
     return FSO_E_ARG;
-  int code = validate_trace(t, kIds | kOrder | (raw ? 0u : unsigned(kChain)));
+  int code = validate_trace(t, kIds | kUsers | kOrder | (raw ? 0u : unsigned(kChain)));
   if (code == FSO_E_ARG) return code;
   for (int32_t a = 0; a < t->n_apps; ++a)
     if (t_app[a] < 0) return FSO_E_ARG;
@@ -610,7 +614,7 @@ int fso_simulate(const fso_trace *t, const int64_t *cost, const uint8_t *exceed_
   if (!e || !out || !out->status || !cost) return FSO_E_ARG;
   if (e->step_us <= 0 || e->cap_tokens <= 0 || e->cap_tokens > kCapLimit) return FSO_E_ARG;
   if (e->flags & ~uint32_t(FSO_FCFS | FSO_BLIND | FSO_LITERAL)) return FSO_E_ARG;
-  int code = validate_trace(t, kIds | kOrder | kChain | kLengths);
+  int code = validate_trace(t, kIds | kUsers | kOrder | kChain | kLengths);
   if (code != FSO_OK) return code;
   int64_t N = t->rep_off[t->n_replicas];
   for (int64_t g = 0; g < N; ++g) {
@@ -631,7 +635,7 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
                          const int32_t *admit_step, const int64_t *max_gap, int64_t step_us,
                          int32_t delay_steps, fso_metrics *m) {
   if (!cost || !status || !admit_step || !m || step_us <= 0 || delay_steps < 0) return FSO_E_ARG;
-  int code = validate_trace(t, kIds | kChain);
+  int code = validate_trace(t, kIds | kUsers | kChain);
   if (code != FSO_OK) return code;
   const int32_t U = t->n_users;
   for (int32_t r = 0; r < t->n_replicas; ++r) {
@@ -640,6 +644,7 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
     std::vector<int64_t> charged(U, 0);
     std::vector<uint8_t> any_served(rp.n, 0), any_blocked(rp.n, 0);  // indexed by interaction head
     int64_t admitted = 0, throttled = 0, interactions = 0;
+    unsigned __int128 total = 0;  // the replica's charged service, exact
     for (int64_t i = 0; i < rp.n; ++i) {
       int64_t g = rp.base + i;
       int32_t k = t->user[g];
@@ -648,7 +653,14 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
       if (is_first_call(t, g)) ++interactions;
       if (status[g] == 0) {
         ++admitted;
-        charged[k] += cost[g];
+        // charged service is a cost in [0, 2^62); another value is an error (not added)
+        if (cost[g] < 0 || cost[g] >= kValueLimit) {
+          code = worse(code, FSO_E_RANGE);
+        } else {
+          total += uint64_t(cost[g]);
+          // below 2^62 in total (else an overflow error below), so no sum wraps
+          if (total < (unsigned __int128)kValueLimit) charged[k] += cost[g];
+        }
         any_served[h] = 1;
         if (admit_step[g] - t->ts_us[g] / step_us > delay_steps) delayed[k] = 1;
       } else {
@@ -671,14 +683,16 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
       int64_t h = is_first_call(t, g) ? i : t->head[g];
       if (status[g] == 0 && any_served[h] && any_blocked[h]) wasted += tokens(t, g);
     }
-    // Jain's index over users with at least one request: (sum x)^2 / (n * sum x^2).
-    __int128 s1 = 0, s2 = 0;
+    if (total >= (unsigned __int128)kValueLimit) code = worse(code, FSO_E_OVERFLOW);
+    // Jain's index over users with at least one request: (sum x)^2 / (n * sum x^2),
+    // exact: sum x < 2^62 and sum x^2 <= (sum x)^2 < 2^124.
+    unsigned __int128 s1 = 0, s2 = 0;
     int64_t n_users = 0, n_full = 0, n_delayed = 0;
     for (int32_t k = 0; k < U; ++k) {
       if (!has[k]) continue;
       ++n_users;
-      s1 += charged[k];
-      s2 += (__int128)charged[k] * charged[k];
+      s1 += uint64_t(charged[k]);
+      s2 += (unsigned __int128)uint64_t(charged[k]) * uint64_t(charged[k]);
       n_full += full_user[k];
       n_delayed += delayed[k];
     }
@@ -694,7 +708,7 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
     if (m->aborted_midway) m->aborted_midway[r] = aborted;
     if (m->wasted_tokens) m->wasted_tokens[r] = wasted;
   }
-  return FSO_OK;
+  return code;
 }
 
 }  // extern "C"

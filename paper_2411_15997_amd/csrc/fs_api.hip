@@ -8,6 +8,7 @@
 
 namespace fs {
 
+
 __global__ void k_zero_i32(int32_t *p) {
   if (threadIdx.x == 0) *p = 0;
 }
@@ -171,7 +172,7 @@ fs_status fs_cost(const fs_trace *t, const fs_weights *w, int64_t *cost, int32_t
 }
 
 size_t fs_throttle_workspace(const fs_trace *t) {
-  if (check_trace(t, false) != FS_OK) return 0;
+  if (check_trace(t, false) != FS_OK || !throttle_shape_ok(t)) return 0;
   return throttle_workspace_bytes(t);
 }
 
@@ -182,7 +183,8 @@ fs_status fs_throttle(const fs_trace *t, const fs_limits *lim, const uint8_t *ov
   fs_status s = check_trace(t, false);
   if (s == FS_OK) s = check_limits(t, lim);
   if (s != FS_OK) return s;
-  if ((flags & ~FS_THROTTLE_RAW) || !per_request(t, bitmap) || !err) return FS_E_ARG;
+  if ((flags & ~FS_THROTTLE_RAW) || !per_request(t, bitmap) || !err || !throttle_shape_ok(t))
+    return FS_E_ARG;
   if (!ws || !aligned(ws) || ws_bytes < throttle_workspace_bytes(t)) return FS_E_WORKSPACE;
   if (launch_zero_i32(err, stream) != hipSuccess) return FS_E_HIP;
   return hip_status(launch_throttle(t, lim, overloaded, flags, bitmap, reason, cnt_user, cnt_app,
@@ -214,7 +216,7 @@ fs_status fs_schedule_step(void *state, const fs_trace *t, const int64_t *cost,
 }
 
 size_t fs_run_trace_workspace(const fs_trace *t) {
-  if (check_trace(t, false) != FS_OK) return 0;
+  if (check_trace(t, false) != FS_OK || !throttle_shape_ok(t)) return 0;
   int64_t N = n_records(t);
   size_t b = round_up(size_t(N) * sizeof(int64_t));   // cost
   b += round_up(size_t(N));                           // raw reasons
@@ -233,6 +235,7 @@ fs_status fs_run_trace(const fs_trace *t, const fs_weights *w, const fs_limits *
   if (s == FS_OK) s = check_engine(eng);
   if (s == FS_OK) s = check_outputs(t, out);
   if (s != FS_OK) return s;
+  if (!throttle_shape_ok(t)) return FS_E_ARG;
   if (!ws || !aligned(ws) || ws_bytes < fs_run_trace_workspace(t)) return FS_E_WORKSPACE;
   int64_t N = n_records(t);
   char *p = static_cast<char *>(ws);
@@ -277,5 +280,6 @@ fs_status fs_fairness_metrics(const fs_trace *t, const int64_t *cost, const fs_o
   if (launch_zero_i32(out->err, stream) != hipSuccess) return FS_E_HIP;
   return hip_status(launch_metrics(t, cost, out, eng, delay_steps, m, ws, stream));
 }
+
 
 }  // extern "C"

@@ -1,8 +1,9 @@
 // Weighted service cost of one LLM call (Eq. 2, one term of the sum; Alg. 1 charge):
 //   cost = floor(E_u * (c_in*L_I + c_sys*L_S + c_out*L_O) / 2^8)
 // with Q16 coefficients c (class weight over w_aj, Eq. 1) and Q8 priority E_u.
-// A pure HBM stream: each record reads app, lengths (and call, user when used)
-// and writes one int64.  Four records per thread with 16-byte loads and stores.
+// A pure HBM stream: each record reads app, lengths (and call, and the user when
+// priorities are given: Eq. 2 reads the user only through E_i) and writes one int64.
+// Four records per thread with 16-byte loads and stores.
 #include "fs_device.h"
 #include "fs_launch.h"
 
@@ -21,7 +22,7 @@ struct CostArgs {
 __device__ inline int64_t cost_one(const CostArgs &a, int64_t g, int32_t rep, int32_t app,
                                    int32_t user, int32_t call, int32_t li, int32_t ls, int32_t lo,
                                    int32_t &code) {
-  if (app < 0 || app >= a.t.A || user < 0 || user >= a.t.U || call < 0) {
+  if (app < 0 || app >= a.t.A || (a.prio && (user < 0 || user >= a.t.U)) || call < 0) {
     code = code > FS_E_RANGE ? code : FS_E_RANGE;
     return 0;
   }
@@ -56,7 +57,7 @@ __device__ inline int64_t cost_one(const CostArgs &a, int64_t g, int32_t rep, in
   return int64_t(v);
 }
 
-template <bool PER_REP>
+template <bool PER_REP, bool PRIO>
 __global__ void __launch_bounds__(256) k_cost_vec4(CostArgs a, int64_t n_vec) {
   int32_t code = 0;
   for (int64_t v = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; v < n_vec;
@@ -69,7 +70,7 @@ __global__ void __launch_bounds__(256) k_cost_vec4(CostArgs a, int64_t n_vec) {
                           : make_int4(0, 0, 0, 0);
     int4 call = a.t.call ? __ldg(reinterpret_cast<const int4 *>(a.t.call) + v)
                          : make_int4(0, 0, 0, 0);
-    int4 user = __ldg(reinterpret_cast<const int4 *>(a.t.user) + v);
+    int4 user = PRIO ? __ldg(reinterpret_cast<const int4 *>(a.t.user) + v) : make_int4(0, 0, 0, 0);
     int32_t r0 = 0, r1 = 0, r2 = 0, r3 = 0;
     if (PER_REP) {
       r0 = replica_of(a.t.rep_off, a.t.R, g0);
@@ -99,8 +100,8 @@ __global__ void __launch_bounds__(256) k_cost_scalar(CostArgs a, int64_t g_begin
     int32_t r = PER_REP ? replica_of(a.t.rep_off, a.t.R, g) : 0;
     int32_t ls = a.t.len_sys ? a.t.len_sys[g] : 0;
     int32_t call = a.t.call ? a.t.call[g] : 0;
-    a.cost[g] = cost_one(a, g, r, a.t.app[g], a.t.user[g], call, a.t.len_in[g], ls,
-                         a.t.len_out[g], code);
+    a.cost[g] = cost_one(a, g, r, a.t.app[g], a.prio ? a.t.user[g] : 0, call, a.t.len_in[g],
+                         ls, a.t.len_out[g], code);
   }
   if (code) raise_err(a.err, code);
 }
@@ -122,17 +123,22 @@ hipError_t launch_cost(const fs_trace *t, const fs_weights *w, int64_t *cost, in
   if (N == 0) return hipSuccess;
   bool per_rep = (a.coef_stride != 0 || a.prio_stride != 0) && a.t.R > 1;
   bool vec = aligned16(t->app) && aligned16(t->len_in) && aligned16(t->len_out) &&
-             aligned16(t->user) && aligned16(cost) && (!t->len_sys || aligned16(t->len_sys)) &&
-             (!t->call || aligned16(t->call));
+             (!a.prio || aligned16(t->user)) && aligned16(cost) &&
+             (!t->len_sys || aligned16(t->len_sys)) && (!t->call || aligned16(t->call));
   int64_t n_vec = vec ? N / 4 : 0;
   const int threads = 256;
   if (n_vec > 0) {
     int64_t blocks = (n_vec + threads - 1) / threads;
     if (blocks > 65536) blocks = 65536;
-    if (per_rep)
-      hipLaunchKernelGGL(k_cost_vec4<true>, dim3(blocks), dim3(threads), 0, stream, a, n_vec);
+    const bool pr = a.prio != nullptr;
+    if (per_rep && pr)
+      hipLaunchKernelGGL((k_cost_vec4<true, true>), dim3(blocks), dim3(threads), 0, stream, a, n_vec);
+    else if (per_rep)
+      hipLaunchKernelGGL((k_cost_vec4<true, false>), dim3(blocks), dim3(threads), 0, stream, a, n_vec);
+    else if (pr)
+      hipLaunchKernelGGL((k_cost_vec4<false, true>), dim3(blocks), dim3(threads), 0, stream, a, n_vec);
     else
-      hipLaunchKernelGGL(k_cost_vec4<false>, dim3(blocks), dim3(threads), 0, stream, a, n_vec);
+      hipLaunchKernelGGL((k_cost_vec4<false, false>), dim3(blocks), dim3(threads), 0, stream, a, n_vec);
   }
   int64_t tail = N - n_vec * 4;
   if (tail > 0) {

@@ -10,6 +10,7 @@ hipError_t launch_cost(const fs_trace *t, const fs_weights *w, int64_t *cost, in
                        hipStream_t stream);
 
 size_t throttle_workspace_bytes(const fs_trace *t);
+bool throttle_shape_ok(const fs_trace *t);
 hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_t *overloaded,
                            uint32_t flags, uint32_t *bitmap, uint8_t *reason, int32_t *cnt_user,
                            int32_t *cnt_app, void *ws, int32_t *err, hipStream_t stream);

@@ -3,13 +3,21 @@
 // interactions and wasted tokens) plus Jain's index of the charged service.
 // Integer accumulation only (atomics on integers are order-independent, so the
 // result is deterministic); Jain's sums are exact 128-bit before the fp64 division.
+// Each replica's total charged service is also summed exactly (the low and high 32-bit
+// halves of every admitted cost in two 64-bit counters): at 2^62 or more the call
+// reports an overflow, and below that no per-user sum can wrap.
 #include "fs_device.h"
 #include "fs_launch.h"
 
 namespace fs {
 namespace {
 
-enum : int { C_ADMITTED, C_THROTTLED, C_INTERACTIONS, C_FULL, C_ABORTED, C_WASTED, C_NUM = 8 };
+enum : int {
+  C_ADMITTED, C_THROTTLED, C_INTERACTIONS, C_FULL, C_ABORTED, C_WASTED,
+  C_COST_LO,  // sum of the low 32 bits of the admitted costs
+  C_COST_HI,  // sum of their high bits (costs are below 2^62)
+  C_NUM = 8
+};
 enum : uint32_t { U_HAS = 1, U_FULL = 2, U_DELAYED = 4 };
 enum : uint32_t { I_SERVED = 1, I_UNSERVED = 2 };
 
@@ -187,6 +195,30 @@ __device__ inline void wave_count3(bool active, int32_t r, unsigned long long *c
   }
 }
 
+// An admitted cost as charged service: in [0, 2^62), else a range error (not added).
+__device__ inline bool cost_ok(int64_t c) { return c >= 0 && c < kValueLimit; }
+
+// The exact per-replica total of the admitted costs: the low and high 32-bit halves of
+// each cost summed separately (neither sum can wrap: fewer than 2^31 records).
+__device__ inline void wave_cost2(bool active, int32_t r, unsigned long long *counters,
+                                  int64_t c) {
+  const int lane = threadIdx.x & 63;
+  uint64_t pending = __ballot(active && c != 0);
+  while (pending) {
+    const int leader = __ffsll((long long)pending) - 1;
+    const int32_t rl = __shfl(r, leader, 64);
+    const bool mine = active && r == rl;
+    const unsigned long long lo = wave_sum(mine ? (uint64_t(c) & 0xffffffffull) : 0ull);
+    const unsigned long long hi = wave_sum(mine ? (uint64_t(c) >> 32) : 0ull);
+    if (lane == leader) {
+      unsigned long long *cr = counters + int64_t(rl) * C_NUM;
+      if (lo) atomicAdd(cr + C_COST_LO, lo);
+      if (hi) atomicAdd(cr + C_COST_HI, hi);
+    }
+    pending &= ~__ballot(mine);
+  }
+}
+
 // The replica of record g, walking forward from the replica of the block's first
 // record (records of a replica are contiguous, so a block spans few of them).
 __device__ inline int32_t replica_from(const int64_t *rep_off, int32_t r0, int64_t g) {
@@ -230,14 +262,20 @@ __global__ void __launch_bounds__(256) k_m_records(MArgs a) {
     }
     const int8_t st = ok ? a.status[g] : int8_t(-1);
     const bool served = ok && st == 0;
+    int64_t cg = served ? a.cost[g] : 0;
+    if (!cost_ok(cg)) {
+      code = max(code, int32_t(FS_E_RANGE));
+      cg = 0;
+    }
     uint32_t uf = U_HAS;
     if (served && is_delayed(a.admit_step[g], t.ts[g], a.tau, a.D)) uf |= U_DELAYED;
     if (ok && h != i) atomicOr(a.iflags + base + h, own_iflag(st));
     const int64_t uk = int64_t(r) * t.U + k;
-    wave_add_by_key_hashed(ok, uk, served ? (unsigned long long)a.cost[g] : 0ull, a.charged, uf,
-                           a.uflags, ks[threadIdx.x >> 6]);
+    wave_add_by_key_hashed(ok, uk, (unsigned long long)cg, a.charged, uf, a.uflags,
+                           ks[threadIdx.x >> 6]);
     wave_count3(ok, r, a.counters, C_ADMITTED, served ? 1u : 0u, C_THROTTLED,
                 (ok && st > 0) ? 1u : 0u, C_INTERACTIONS, (ok && first_call(t, g)) ? 1u : 0u);
+    wave_cost2(ok, r, a.counters, cg);
   }
   if (code) raise_err(a.err, code);
 }
@@ -293,11 +331,30 @@ __device__ inline void block_count3(uint32_t x0, uint32_t x1, uint32_t x2,
   }
 }
 
+// Adds the work-group's sums of the admitted costs' low and high halves to the
+// replica's counters (each block sum is below 2^45).
+__device__ inline void block_cost2(unsigned long long lo, unsigned long long hi,
+                                   unsigned long long *cr, unsigned long long (*s_red)[4]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long tl = wave_sum(lo), th = wave_sum(hi);
+  if (lane == 0) {
+    s_red[0][wave] = tl;
+    s_red[1][wave] = th;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned long long l = s_red[0][0] + s_red[0][1] + s_red[0][2] + s_red[0][3];
+    const unsigned long long h = s_red[1][0] + s_red[1][1] + s_red[1][2] + s_red[1][3];
+    if (l) atomicAdd(cr + C_COST_LO, l);
+    if (h) atomicAdd(cr + C_COST_HI, h);
+  }
+}
+
 // Pass 1, LDS tables (U <= kLdsUsers): dynamic LDS of U * 12 bytes.
 constexpr int kRecBatch = 4;  // records per thread whose loads are issued together
 __global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
   extern __shared__ unsigned long long s_dyn[];
-  __shared__ unsigned long long s_red[1][4];
+  __shared__ unsigned long long s_red[2][4];
   const DevTrace &t = a.t;
   unsigned long long *const s_chg = s_dyn;
   uint32_t *const s_uf = reinterpret_cast<uint32_t *>(s_dyn + t.U);
@@ -315,6 +372,7 @@ __global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
     }
     __syncthreads();
     uint32_t n_adm = 0, n_thr = 0, n_int = 0;
+    unsigned long long c_lo = 0, c_hi = 0;
     for (int64_t g0 = s0 + threadIdx.x; g0 < s1; g0 += kRecBatch * 256) {
       int32_t uk[kRecBatch], ap[kRecBatch], cl[kRecBatch], hd[kRecBatch], as[kRecBatch];
       int8_t st[kRecBatch];
@@ -353,7 +411,13 @@ __global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
         uint32_t uf = U_HAS;
         if (served && is_delayed(as[j], ts[j], a.tau, a.D)) uf |= U_DELAYED;
         if (!fc) atomicOr(a.iflags + base + h, own_iflag(st[j]));
-        if (served) atomicAdd(&s_chg[k], (unsigned long long)cs[j]);
+        if (served && !cost_ok(cs[j])) {
+          code = int32_t(FS_E_RANGE);
+        } else if (served && cs[j]) {
+          atomicAdd(&s_chg[k], (unsigned long long)cs[j]);
+          c_lo += uint64_t(cs[j]) & 0xffffffffull;
+          c_hi += uint64_t(cs[j]) >> 32;
+        }
         atomicOr(&s_uf[k], uf);
         n_adm += served ? 1u : 0u;
         n_thr += st[j] > 0 ? 1u : 0u;
@@ -373,6 +437,8 @@ __global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
     block_count3(n_adm, n_thr, n_int, a.counters + int64_t(r) * C_NUM, C_ADMITTED, C_THROTTLED,
                  C_INTERACTIONS, s_red);
     __syncthreads();
+    block_cost2(c_lo, c_hi, a.counters + int64_t(r) * C_NUM, s_red);
+    __syncthreads();
   }
   if (code) raise_err(a.err, code);
 }
@@ -380,7 +446,7 @@ __global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
 // Pass 2, LDS tables (U <= kLdsUsers).
 __global__ void __launch_bounds__(256) k_m_interactions_lds(MArgs a) {
   extern __shared__ unsigned long long s_dyn[];
-  __shared__ unsigned long long s_red[1][4];
+  __shared__ unsigned long long s_red[2][4];
   const DevTrace &t = a.t;
   uint8_t *const s_full = reinterpret_cast<uint8_t *>(s_dyn);
   const int64_t c0 = blockIdx.x * int64_t(kChunk);
@@ -499,6 +565,11 @@ __global__ void __launch_bounds__(256) k_m_finish(MArgs a) {
     const int64_t n = a.t.rep_off[r + 1] - a.t.rep_off[r];
     U128 S1 = s1s[0], S2 = s2s[0];
     const unsigned long long nu = cnt[0][0];
+    // the exact total charged service: hi * 2^32 + lo
+    const unsigned long long lo = C[C_COST_LO], hi = C[C_COST_HI];
+    if ((hi >> 30) != 0 || ((hi << 32) + lo) < (hi << 32) ||
+        (hi << 32) + lo >= (unsigned long long)kValueLimit)
+      raise_err(a.err, FS_E_OVERFLOW);
     double jain = 1.0;
     if (S2.lo != 0 || S2.hi != 0) {
       double d1 = to_double(S1);

@@ -723,12 +723,19 @@ hipError_t exclusive_scan(uint32_t *data, int64_t n, uint32_t *part, hipStream_t
 
 size_t throttle_workspace_bytes(const fs_trace *t) { return layout(t).total; }
 
+// The packed element holds the key (replica * U + user, then the app) and the record
+// index: the key must fit 32 bits and key + index + flag 64 bits.
+bool throttle_shape_ok(const fs_trace *t) {
+  const Pack pk = make_pack(t, t->rep_off_h[t->n_replicas]);
+  return pk.Bk <= 32 && pk.Bk + pk.Bi + 1 <= 64;
+}
+
 hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_t *overloaded,
                            uint32_t flags, uint32_t *bitmap, uint8_t *reason, int32_t *cnt_user,
                            int32_t *cnt_app, void *ws, int32_t *err, hipStream_t s) {
   Layout L = layout(t);
   const Pack &pk = L.pk;
-  if (pk.Bk > 32 || pk.Bk + pk.Bi + 1 > 64) return hipErrorInvalidValue;
+  if (!throttle_shape_ok(t)) return hipErrorInvalidValue;  // rejected by the callers first
   if (L.N == 0) return hipSuccess;
   char *w = static_cast<char *>(ws);
   uint64_t *A = reinterpret_cast<uint64_t *>(w + L.off_a);

@@ -101,3 +101,40 @@ def test_history_arguments_and_workspace_need_no_gpu():
                                        None) == fs.FS_E_ARG          # no stats buffer
     assert lib.fs_weights_from_history(C.byref(t), 3, 1024, 30, 256, None, None, 256, ws - 1,
                                        16, None) == fs.FS_E_WORKSPACE
+
+
+def test_throttle_key_space_limit_needs_no_gpu():
+    """fs_throttle packs (replica * U + user, app) into 32 key bits and the record index
+    beside them: a larger key space is FS_E_ARG from fs_throttle and fs_run_trace (before
+    anything is enqueued) and a zero workspace size, not a HIP error."""
+    lib = fs._lib()
+    rep = np.array([0, 4], np.int64)
+    # 2^22 users (22 bits) x 1024 apps (10 bits) = 32 bits: accepted
+    ok = fs.fs_trace(1, 1 << 22, 1024, rep.ctypes.data, 16, 16, 16, 16, None, None, None, 16,
+                     None, 16)
+    assert lib.fs_throttle_workspace(C.byref(ok)) > 0
+    assert lib.fs_run_trace_workspace(C.byref(ok)) > 0
+    # one more user bit: 33 key bits
+    big = fs.fs_trace(1, (1 << 22) + 1, 1024, rep.ctypes.data, 16, 16, 16, 16, None, None, None,
+                      16, None, 16)
+    assert lib.fs_throttle_workspace(C.byref(big)) == 0
+    assert lib.fs_run_trace_workspace(C.byref(big)) == 0
+    t_app = np.ones(1024, np.int32)
+    lim = fs.fs_limits(1000, 5, t_app.ctypes.data)
+    assert lib.fs_throttle(C.byref(big), C.byref(lim), None, 1, 16, None, None, None, 256,
+                           1 << 40, 16, None) == fs.FS_E_ARG
+    coef = 256
+    w = fs.fs_weights(1, 0, coef, 0, None)
+    eng = fs.fs_engine(10, 10, 10, 0)
+    out = fs.fs_outputs(*([16] * 10))
+    assert lib.fs_run_trace(C.byref(big), C.byref(w), C.byref(lim), C.byref(eng), C.byref(out),
+                            256, 1 << 40, None) == fs.FS_E_ARG
+    # replicas x users multiply: 2^12 replicas x 2^11 users x 2^9 apps = 32 bits, one more
+    # replica makes 33
+    rep2 = np.zeros((1 << 12) + 2, np.int64)
+    r_ok = fs.fs_trace(1 << 12, 1 << 11, 512, rep2[:(1 << 12) + 1].ctypes.data, 16, 16, 16, 16,
+                       None, None, None, 16, None, 16)
+    assert lib.fs_throttle_workspace(C.byref(r_ok)) > 0
+    r_big = fs.fs_trace((1 << 12) + 1, 1 << 11, 512, rep2.ctypes.data, 16, 16, 16, 16, None,
+                        None, None, 16, None, 16)
+    assert lib.fs_throttle_workspace(C.byref(r_big)) == 0

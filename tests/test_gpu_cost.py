@@ -72,13 +72,17 @@ def test_cost_errors_match_oracle():
     huge = np.full((1, 2, 1, 3), (1 << 36) - 1, np.int64)
     prio = np.full((1, 4), 65535, np.int32)
     lens = tg.Trace(**{**tr.__dict__, "len_in": np.full(64, (1 << 24) - 1, np.int32)})
-    for t, c, p, code in ((bad_user, coef, None, fs.FS_E_RANGE), (tr, big, None, fs.FS_E_RANGE),
+    unit = np.full((1, 4), 256, np.int32)
+    for t, c, p, code in ((bad_user, coef, unit, fs.FS_E_RANGE), (tr, big, None, fs.FS_E_RANGE),
                           (lens, huge, prio, fs.FS_E_OVERFLOW)):
         with pytest.raises(oracle.OracleError) as oe:
             oracle.cost(t, c, p)
         with pytest.raises(fs.FairServeError) as ge:
             _gpu_cost(t, c, p)
         assert ge.value.code == oe.value.code == code
+    # Eq. 2 reads the user only through its priority: without priorities the user id is
+    # not read, on either side
+    assert (_gpu_cost(bad_user, coef, None) == oracle.cost(bad_user, coef, None)).all()
 
 
 def test_cost_empty_trace():

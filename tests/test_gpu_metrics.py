@@ -70,3 +70,42 @@ def test_metrics_single_call_interactions(U):
     say("metrics single-call", U)
     mo = _check(tr, rng, 1)
     assert (mo.aborted_midway == 0).all() and (mo.wasted_tokens == 0).all()
+
+
+def _gpu_metrics(tr, cost, status, admit_step, max_gap, step_us):
+    import torch
+    n = tr.n
+    dt = fs.DeviceTrace(tr)
+    out = fs.Outputs(dt, parity=False)
+    out.status[:n].copy_(torch.as_tensor(status))
+    out.admit_step[:n].copy_(torch.as_tensor(admit_step))
+    out.max_gap.copy_(torch.as_tensor(max_gap))
+    eng = fs.make_engine(step_us, 1000, 1000)
+    return fs.fs_fairness_metrics(dt, torch.as_tensor(cost).to(dt.device), out, eng, 0).host()
+
+
+@pytest.mark.parametrize("U", [4, 5000])
+def test_metrics_charged_service_limit(U):
+    """Admitted costs near 2^62 (both aggregation paths): below a replica total of 2^62
+    the GPU's Jain index matches the oracle, at 2^62 both report an overflow, and an
+    admitted cost out of range is a range error on both sides."""
+    q = 1 << 60
+    n = 8
+    tr = tg.Trace(2, U, 1, np.array([0, 4, 8], np.int64), np.zeros(n, np.int64),
+                  np.array([0, 1, 2, 3] * 2, np.int32) % U, np.zeros(n, np.int32), None, None,
+                  None, np.ones(n, np.int32), None, np.zeros(n, np.int32))
+    st = np.zeros(n, np.int8)
+    adm = np.zeros(n, np.int32)
+    mg = np.zeros(2, np.int64)
+    ok = np.array([3 * q - 1, q - 1, 0, 0, q - 1, q - 1, q - 1, q - 1], np.int64)
+    want = oracle.fairness_metrics(tr, ok, st, adm, mg, 10)
+    got = _gpu_metrics(tr, ok, st, adm, mg, 10)
+    np.testing.assert_allclose(got["jain"], want.jain, rtol=1e-9, atol=0)
+    for bad, code in ((np.array([q, q, q, q, 1, 1, 1, 1], np.int64), fs.FS_E_OVERFLOW),
+                      (np.array([(1 << 62) - 1] * 8, np.int64), fs.FS_E_OVERFLOW),
+                      (np.array([1, 1, 1, 1, 1, -1, 1, 1], np.int64), fs.FS_E_RANGE)):
+        with pytest.raises(oracle.OracleError) as oe:
+            oracle.fairness_metrics(tr, bad, st, adm, mg, 10)
+        with pytest.raises(fs.FairServeError) as ge:
+            _gpu_metrics(tr, bad, st, adm, mg, 10)
+        assert ge.value.code == oe.value.code == code

@@ -298,3 +298,106 @@ def test_empty_trace_every_entry_point(multi):
     for raw in (True, False):
         gt = gpu_throttle(tr, 100, 3, [2, 2], raw=raw, counts=True)
         assert gt["reason"].size == 0
+
+
+def test_state_of_another_trace_is_rejected():
+    """fs_schedule_step on a state buffer initialised for another trace (another request
+    count), with a corrupted version word, or never initialised: FS_E_STATE, and nothing
+    else is written."""
+    rng = np.random.default_rng(71)
+    tr = random_trace(rng, 40, 4, 2, 200, multi=True)
+    other = random_trace(rng, 30, 4, 2, 200, multi=True)
+    cost = np.ones(tr.n, np.int64)
+    dt, do = fs.DeviceTrace(tr), fs.DeviceTrace(other)
+    c = torch.as_tensor(cost).cuda()
+    eng = fs.make_engine(10, 50, 5)
+    cases = []
+    st = fs.fs_state_init(do)                       # initialised for `other`
+    big = torch.zeros(max(st.numel(), fs.fs_state_bytes(dt)), dtype=torch.uint8, device="cuda")
+    big[:st.numel()].copy_(st)
+    cases.append(("other trace", big))
+    bad = fs.fs_state_init(dt)
+    bad[8:12].copy_(torch.tensor([99, 0, 0, 0], dtype=torch.uint8))  # the version word
+    cases.append(("version", bad))
+    cases.append(("never initialised", torch.zeros(fs.fs_state_bytes(dt), dtype=torch.uint8,
+                                                   device="cuda")))
+    for what, state in cases:
+        say("state case", what)
+        out = fs.Outputs(dt)
+        out.steps.fill_(-7)
+        with pytest.raises(fs.FairServeError) as ge:
+            fs.fs_schedule_step(dt, state, c, None, eng, out, -1)
+        assert ge.value.code == fs.FS_E_STATE, what
+        assert (out.steps.cpu().numpy() == -7).all(), what
+    # the right state still runs
+    o = oracle.simulate(tr, cost, None, 10, 50, 5)
+    compare_sim(gpu_schedule(tr, cost, None, 10, 50, 5), o)
+
+
+def test_empty_trace_null_pointers_through_the_abi():
+    """A trace without requests whose per-request arrays are all NULL (only the replica
+    offsets set), passed to every entry point through the C-ABI: each call succeeds and
+    the per-replica outputs are the oracle's."""
+    import ctypes as C
+    L = fs._lib()
+    R, U, A = 3, 5, 2
+    rep_h = np.zeros(R + 1, np.int64)
+    rep_d = torch.zeros(R + 1, dtype=torch.int64, device="cuda")
+    t = fs.fs_trace(R, U, A, rep_h.ctypes.data, rep_d.data_ptr(), None, None, None, None, None,
+                    None, None, None, None)
+    err = fs.err_word()
+    S = fs._stream()
+    coef = torch.full((1, A, 1, 3), 1 << 16, dtype=torch.int64, device="cuda")
+    w = fs.fs_weights(1, 0, coef.data_ptr(), 0, None)
+    assert L.fs_cost(C.byref(t), C.byref(w), None, err.data_ptr(), S) == fs.FS_OK
+    t_app = np.array([2, 2], np.int32)
+    lim = fs.fs_limits(100, 3, t_app.ctypes.data, 0)
+    wsb = int(L.fs_throttle_workspace(C.byref(t)))
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device="cuda")
+    for flags in (0, fs.FS_THROTTLE_RAW):
+        assert L.fs_throttle(C.byref(t), C.byref(lim), None, flags, None, None, None, None,
+                             ws.data_ptr(), wsb, err.data_ptr(), S) == fs.FS_OK
+    assert fs.fs_sync_status(err) == fs.FS_OK
+    sb = int(L.fs_state_bytes(C.byref(t)))
+    state = torch.empty(sb, dtype=torch.uint8, device="cuda")
+    assert L.fs_state_init(state.data_ptr(), sb, C.byref(t), S) == fs.FS_OK
+    counter = torch.full((R * U,), -1, dtype=torch.int64, device="cuda")
+    steps, dec, gap = (torch.full((R,), -1, dtype=torch.int64, device="cuda") for _ in range(3))
+    out = fs.fs_outputs(None, None, None, None, None, counter.data_ptr(), steps.data_ptr(),
+                        dec.data_ptr(), gap.data_ptr(), err.data_ptr())
+    eng = fs.make_engine(10, 50, 5)
+    assert L.fs_schedule_step(state.data_ptr(), C.byref(t), None, None, C.byref(eng),
+                              C.byref(out), -1, S) == fs.FS_OK
+    assert fs.fs_sync_status(err) == fs.FS_OK
+    tr = tg.Trace(R, U, A, rep_h, np.zeros(0, np.int64), np.zeros(0, np.int32),
+                  np.zeros(0, np.int32), None, None, None, np.zeros(0, np.int32), None,
+                  np.zeros(0, np.int32))
+    o = oracle.simulate(tr, np.zeros(0, np.int64), None, 10, 50, 5)
+    assert (counter.cpu().numpy() == o.counter).all()
+    assert (steps.cpu().numpy() == o.steps).all() and (dec.cpu().numpy() == o.decisions).all()
+    assert (gap.cpu().numpy() == o.max_gap).all()
+    rb = int(L.fs_run_trace_workspace(C.byref(t)))
+    rws = torch.empty(max(rb, 256), dtype=torch.uint8, device="cuda")
+    assert L.fs_run_trace(C.byref(t), C.byref(w), C.byref(lim), C.byref(eng), C.byref(out),
+                          rws.data_ptr(), rb, S) == fs.FS_OK
+    assert fs.fs_sync_status(err) == fs.FS_OK
+    m = fs.Metrics(fs.DeviceTrace(tr))
+    mb = int(L.fs_metrics_workspace(C.byref(t)))
+    mws = torch.empty(max(mb, 256), dtype=torch.uint8, device="cuda")
+    assert L.fs_fairness_metrics(C.byref(t), None, C.byref(out), C.byref(eng), 0, C.byref(m.s),
+                                 mws.data_ptr(), mb, S) == fs.FS_OK
+    assert fs.fs_sync_status(err) == fs.FS_OK
+    mo = oracle.fairness_metrics(tr, np.zeros(0, np.int64), np.zeros(0, np.int8),
+                                 np.zeros(0, np.int32), gap.cpu().numpy(), 10)
+    mh = m.host()
+    for k in ("jain", "svc_req_pct", "svc_int_pct", "served_users_pct", "delayed_users_pct"):
+        np.testing.assert_allclose(mh[k], getattr(mo, k), rtol=1e-9, atol=0, err_msg=k)
+    for k in ("throttled", "aborted_midway", "wasted_tokens"):
+        assert (mh[k] == getattr(mo, k)).all(), k
+    hb = int(L.fs_history_workspace(C.byref(t), 1))
+    hws = torch.empty(max(hb, 256), dtype=torch.uint8, device="cuda")
+    stats = torch.full((A, 1, 5), -1, dtype=torch.int64, device="cuda")
+    assert L.fs_weights_from_history(C.byref(t), 1, 1024, 30, stats.data_ptr(), None, None,
+                                     hws.data_ptr(), hb, err.data_ptr(), S) == fs.FS_OK
+    assert fs.fs_sync_status(err) == fs.FS_OK
+    assert (stats.cpu().numpy() == 0).all()

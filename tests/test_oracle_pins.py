@@ -496,6 +496,37 @@ def test_jain_special_cases():
     assert abs(two.jain[0] - 16.0 / (4 * 10)) < 1e-15
 
 
+def test_jain_near_the_charged_service_limit():
+    """Costs near 2^62: the replica's total charged service decides.  Below 2^62 the sums
+    are exact (Jain's index of equal shares is 1, of a 3:1 split 0.8 by hand); at 2^62 or
+    more the call reports an overflow instead of a wrapped sum; an admitted cost outside
+    [0, 2^62) is a range error."""
+    n = 4
+    tr = Trace(1, n, 1, np.array([0, n], np.int64), np.zeros(n, np.int64),
+               np.array([0, 1, 2, 3], np.int32), np.zeros(n, np.int32), None, None, None,
+               np.ones(n, np.int32), None, np.zeros(n, np.int32))
+    st = np.zeros(n, np.int8); adm = np.zeros(n, np.int32)
+    q = 1 << 60
+    eq = oracle.fairness_metrics(tr, np.array([q - 1] * 4, np.int64), st, adm, None, 10)
+    assert eq.jain[0] == 1.0
+    # two users share 2^62 - 1 as 3:1 (the other two are dropped): J = 4^2 / (4 * 10) * ...
+    st2 = np.array([0, 0, 1, 1], np.int8)
+    x, y = 3 * q - 1, q - 1        # total 2^62 - 2
+    m = oracle.fairness_metrics(tr, np.array([x, y, 5, 5], np.int64), st2, adm, None, 10)
+    want = float(x + y) ** 2 / (4.0 * (float(x) ** 2 + float(y) ** 2))
+    assert abs(m.jain[0] - want) < 1e-15 and abs(want - 16.0 / 40.0) < 1e-12
+    with pytest.raises(oracle.OracleError) as e:    # total exactly 2^62
+        oracle.fairness_metrics(tr, np.array([q] * 4, np.int64), st, adm, None, 10)
+    assert e.value.code == oracle.E_OVERFLOW
+    big = (1 << 62) - 1                              # four of them would wrap 64 bits
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.fairness_metrics(tr, np.array([big] * 4, np.int64), st, adm, None, 10)
+    assert e.value.code == oracle.E_OVERFLOW
+    with pytest.raises(oracle.OracleError) as e:     # an admitted cost out of range
+        oracle.fairness_metrics(tr, np.array([1, -1, 1, 1], np.int64), st, adm, None, 10)
+    assert e.value.code == oracle.E_RANGE
+
+
 def test_served_experience_metrics_by_hand():
     # two interactions of user 0 (one throttled), one of user 1 served late
     tr = Trace(1, 2, 1, np.array([0, 4], np.int64), np.array([0, 0, 5, 20], np.int64),

@@ -253,6 +253,19 @@ fs_status fs_fairness_metrics(const fs_trace *t, const int64_t *cost, const fs_o
                               const fs_engine *eng, int32_t delay_steps, fs_metrics *m, void *ws,
                               size_t ws_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): fs_fairness_metrics with the
+ * library's own workspace, a fixed device array of fs_metrics_noalloc_limit() bytes
+ * (32 MiB) per GPU, held until the process ends.  Same arguments and results as
+ * fs_fairness_metrics without ws/ws_bytes; FS_E_WORKSPACE (synchronous) when
+ * fs_metrics_workspace(t) exceeds the limit.  The call allocates nothing.  Every call on
+ * one GPU uses that GPU's array (each call clears it first): calls that overlap on one
+ * GPU (other streams, other host threads) race and must be serialised by the caller. */
+size_t fs_metrics_noalloc_limit(void);
+fs_status fs_fairness_metrics_noalloc(const fs_trace *t, const int64_t *cost,
+                                      const fs_outputs *out, const fs_engine *eng,
+                                      int32_t delay_steps, fs_metrics *m, hipStream_t stream);
+
 /* Eq. 1 host helper: w_aj = 1*e_in + 2*e_sys + 1*e_out (expected tokens of app a at
  * stage j) and coef_h[a][j][x] = round-half-even(double(2^16 * K * class_weight_x) / w_aj)
  * computed in IEEE double.  Host arrays [A][J]; coef_h [A][J][3].  Synchronous. */

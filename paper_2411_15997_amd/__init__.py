@@ -91,6 +91,9 @@ def _lib():
             "fs_run_trace": ([T, C.POINTER(fs_weights), C.POINTER(fs_limits), C.POINTER(fs_engine),
                               C.POINTER(fs_outputs), P, SZ, S], I32),
             "fs_metrics_workspace": ([T], SZ),
+            "fs_metrics_noalloc_limit": ([], SZ),
+            "fs_fairness_metrics_noalloc": ([T, P, C.POINTER(fs_outputs), C.POINTER(fs_engine),
+                                             I32, C.POINTER(fs_metrics), S], I32),
             "fs_fairness_metrics": ([T, P, C.POINTER(fs_outputs), C.POINTER(fs_engine), I32,
                                      C.POINTER(fs_metrics), P, SZ, S], I32),
             "fs_coef_from_expectations": ([I32, I32, P, P, P, I64, P], I32),
@@ -107,8 +110,8 @@ def _lib():
 
 EXPORTED = ("fs_cost", "fs_history_workspace", "fs_weights_from_history", "fs_throttle_workspace", "fs_throttle", "fs_state_bytes", "fs_state_init",
             "fs_schedule_step", "fs_run_trace_workspace", "fs_run_trace", "fs_metrics_workspace",
-            "fs_fairness_metrics", "fs_coef_from_expectations", "fs_sync_status",
-            "fs_status_string")
+            "fs_fairness_metrics", "fs_metrics_noalloc_limit", "fs_fairness_metrics_noalloc",
+            "fs_coef_from_expectations", "fs_sync_status", "fs_status_string")
 
 
 def _check(code: int, where: str):
@@ -395,6 +398,23 @@ def fs_fairness_metrics(dt: DeviceTrace, cost, out: Outputs, engine, delay_steps
                                       _stream()), "fs_fairness_metrics")
     if check:
         sync_check(out.err, "fs_fairness_metrics")
+    return m
+
+
+def fs_metrics_noalloc_limit() -> int:
+    return int(_lib().fs_metrics_noalloc_limit())
+
+
+def fs_fairness_metrics_noalloc(dt: DeviceTrace, cost, out: Outputs, engine, delay_steps=0,
+                                m=None, check=True):
+    """fs_fairness_metrics with the library's own fixed workspace (allocates nothing but
+    the Metrics outputs when `m` is not given)."""
+    m = Metrics(dt) if m is None else m
+    _check(_lib().fs_fairness_metrics_noalloc(dt.ref, _ptr(cost), out.ref, C.byref(engine),
+                                              int(delay_steps), C.byref(m.s), _stream()),
+           "fs_fairness_metrics_noalloc")
+    if check:
+        sync_check(out.err, "fs_fairness_metrics_noalloc")
     return m
 
 

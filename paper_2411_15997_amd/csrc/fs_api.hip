@@ -2,12 +2,19 @@
 // synchronous argument checks, workspace layout, and kernel sequencing.
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "fs_device.h"
 #include "fs_launch.h"
 
 namespace fs {
 
+// Workspace of fs_fairness_metrics_noalloc: one copy per GPU, held until the process
+// ends.  Host code never passes this name to a kernel or a copy (on the host it is only
+// a stand-in for the symbol): it uses the device address that hipGetSymbolAddress gives
+// for the current GPU.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 __global__ void k_zero_i32(int32_t *p) {
   if (threadIdx.x == 0) *p = 0;
@@ -88,6 +95,24 @@ fs_status hip_status(hipError_t e) { return e == hipSuccess ? FS_OK : FS_E_HIP; 
 int64_t n_records(const fs_trace *t) { return t->rep_off_h[t->n_replicas]; }
 
 size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// The device address of `scratch` on the current GPU, looked up once per device.
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices] = {};
+
+fs_status scratch_on_current_device(void **ptr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FS_E_HIP;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FS_E_HIP;
+    scratch_ptr[dev] = p;
+  }
+  *ptr = scratch_ptr[dev];
+  return FS_OK;
+}
 
 }  // namespace
 }  // namespace fs
@@ -281,5 +306,28 @@ fs_status fs_fairness_metrics(const fs_trace *t, const int64_t *cost, const fs_o
   return hip_status(launch_metrics(t, cost, out, eng, delay_steps, m, ws, stream));
 }
 
+size_t fs_metrics_noalloc_limit(void) { return kScratchBytes; }
+
+fs_status fs_fairness_metrics_noalloc(const fs_trace *t, const int64_t *cost,
+                                      const fs_outputs *out, const fs_engine *eng,
+                                      int32_t delay_steps, fs_metrics *m, hipStream_t stream) {
+  fs_status s = check_trace(t, true);
+  if (s == FS_OK) s = check_engine(eng);
+  if (s != FS_OK) return s;
+  if (!per_request(t, cost) || !out || !per_request(t, out->status) ||
+      !per_request(t, out->admit_step) || !out->max_gap || !out->err || !m || delay_steps < 0)
+    return FS_E_ARG;
+  if (!m->jain || !m->max_gap_tokens || !m->svc_req_pct || !m->svc_int_pct ||
+      !m->served_users_pct || !m->delayed_users_pct || !m->throttled || !m->aborted_midway ||
+      !m->wasted_tokens)
+    return FS_E_ARG;
+  if (metrics_workspace_bytes(t) > kScratchBytes) return FS_E_WORKSPACE;
+  void *ws = nullptr;
+  s = scratch_on_current_device(&ws);
+  if (s != FS_OK) return s;
+  if (launch_zero_i32(out->err, stream) != hipSuccess) return FS_E_HIP;
+  // the first kernel clears every part of the workspace the others accumulate into
+  return hip_status(launch_metrics(t, cost, out, eng, delay_steps, m, ws, stream));
+}
 
 }  // extern "C"

@@ -65,6 +65,14 @@ class _Metrics(C.Structure):
                                            "aborted_midway", "wasted_tokens")]
 
 
+class _WStats(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("minutes", "user_req", "user_tok", "user_app_req",
+                                           "user_app_tok", "rate_hist", "len_hist", "len_sum",
+                                           "size_hist", "graph")]
+
+
+RATE_BINS, LEN_BINS, SIZE_BINS, GRAPH_BINS = 128, 32, 64, 7
+
 _lib = None
 
 
@@ -87,6 +95,7 @@ def lib():
                                           C.c_void_p, C.c_void_p, C.c_void_p]
         L.fso_simulate.argtypes = [C.POINTER(_Trace), C.c_void_p, C.c_void_p, C.POINTER(_Engine),
                                    C.c_int64, C.c_int32, C.c_int32, C.POINTER(_Outputs)]
+        L.fso_workload_stats.argtypes = [C.POINTER(_Trace), C.c_int64, C.POINTER(_WStats)]
         L.fso_fairness_metrics.argtypes = [C.POINTER(_Trace), C.c_void_p, C.c_void_p, C.c_void_p,
                                            C.c_void_p, C.c_int64, C.c_int32, C.POINTER(_Metrics)]
         _lib = L
@@ -275,3 +284,31 @@ def run_workload(wl, tr, n_threads=1, check=False, max_steps=-1, counts=False):
                    max_steps=max_steps, n_threads=n_threads, check=check)
     met = fairness_metrics(tr, c, sim.status, sim.admit_step, sim.max_gap, wl.step_us)
     return c, th, sim, met
+
+
+@dataclass
+class WorkloadStats:
+    minutes: np.ndarray       # [R]
+    user_req: np.ndarray      # [R][U]
+    user_tok: np.ndarray      # [R][U]
+    user_app_req: np.ndarray  # [R][U][A]
+    user_app_tok: np.ndarray  # [R][U][A]
+    rate_hist: np.ndarray     # [R][A+1][2][RATE_BINS]
+    len_hist: np.ndarray      # [R][A][3][LEN_BINS]
+    len_sum: np.ndarray       # [R][A][3]
+    size_hist: np.ndarray     # [R][A][SIZE_BINS]
+    graph: np.ndarray         # [R][GRAPH_BINS][5]
+
+
+def workload_stats(tr, minute_us=60_000_000):
+    """The workload analysis of Sec. 3 (Figs. 2-5, Table 2), per replica."""
+    t = _TraceRef(tr)
+    R, U, A = tr.n_replicas, tr.n_users, tr.n_apps
+    z = lambda *shape: np.zeros(shape, np.int64)
+    res = WorkloadStats(z(R), z(R, U), z(R, U), z(R, U, A), z(R, U, A),
+                        z(R, A + 1, 2, RATE_BINS), z(R, A, 3, LEN_BINS), z(R, A, 3),
+                        z(R, A, SIZE_BINS), z(R, GRAPH_BINS, 5))
+    w = _WStats(*(_p(getattr(res, f)) for f in WorkloadStats.__dataclass_fields__))
+    _check(lib().fso_workload_stats(C.byref(t.s), int(minute_us), C.byref(w)),
+           "fso_workload_stats")
+    return res

@@ -711,4 +711,138 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
   return code;
 }
 
+// ---------------------------------------------------------------------------
+// Workload analysis (Sec. 3: Fig. 2 rates per user overall and per application,
+// Figs. 3 and 5 token lengths per application, Fig. 4 calls per interaction, Table 2
+// graph sizes and their tokens).
+
+// floor(log2(x / M)) for x >= 1, M >= 1, by plain comparison: the largest k with
+// M * 2^k <= x (k may be negative: then M <= x * 2^-k).
+static int64_t floor_log2_ratio(int64_t x, int64_t M) {
+  const unsigned __int128 X = uint64_t(x), Mm = uint64_t(M);
+  int64_t k = 0;
+  if (X >= Mm) {
+    while ((Mm << (k + 1)) <= X) ++k;
+  } else {
+    k = -1;
+    while ((X << (-k)) < Mm) --k;
+  }
+  return k;
+}
+
+static int rate_bin(int64_t x, int64_t M) {
+  if (x == 0) return 0;
+  return int(64 + floor_log2_ratio(x, M));
+}
+
+static int len_bin(int64_t L) {
+  if (L == 0) return 0;
+  int b = 0;
+  while ((int64_t(1) << (b + 1)) <= L) ++b;  // floor(log2 L)
+  return 1 + b;
+}
+
+static int graph_bin(int64_t s) {
+  if (s <= 1) return 0;
+  if (s <= 10) return 1;
+  if (s <= 20) return 2;
+  if (s <= 30) return 3;
+  if (s <= 40) return 4;
+  if (s <= 50) return 5;
+  return 6;
+}
+
+int fso_workload_stats(const fso_trace *t, int64_t minute_us, fso_wstats *o) {
+  if (minute_us <= 0 || !o || !o->minutes || !o->user_req || !o->user_tok || !o->rate_hist ||
+      !o->len_hist || !o->len_sum || !o->size_hist || !o->graph)
+    return FSO_E_ARG;
+  int code = validate_trace(t, kIds | kUsers | kLengths);
+  if (code == FSO_E_ARG) return code;
+  const int32_t R = t->n_replicas, U = t->n_users, A = t->n_apps;
+  for (int32_t r = 0; r < R; ++r) {
+    Replica rp = replica(t, r);
+    int64_t max_ts = -1;
+    for (int64_t i = 0; i < rp.n; ++i) max_ts = std::max(max_ts, t->ts_us[rp.base + i]);
+    const int64_t M = rp.n > 0 ? max_ts / minute_us + 1 : 0;
+    o->minutes[r] = M;
+    std::vector<int64_t> req(U, 0), tok(U, 0), areq(int64_t(U) * A, 0), atok(int64_t(U) * A, 0);
+    std::vector<int64_t> lh(int64_t(A) * 3 * FSO_LEN_BINS, 0), ls(int64_t(A) * 3, 0);
+    std::vector<int64_t> size(rp.n, 0);  // records per first call (interaction)
+    for (int64_t i = 0; i < rp.n; ++i) {
+      const int64_t g = rp.base + i;
+      const int32_t u = t->user[g], a = t->app[g];
+      const int64_t L[3] = {t->len_in[g], t->len_sys ? t->len_sys[g] : 0, t->len_out[g]};
+      bool ok = u >= 0 && u < U && a >= 0 && a < A;
+      for (int x = 0; x < 3; ++x) ok = ok && L[x] >= 0 && L[x] < kLenLimit;
+      int64_t h = i;
+      if (!is_first_call(t, g)) {
+        h = t->head[g];
+        if (h < 0 || h >= i) ok = false;
+      }
+      if (!ok) {
+        code = worse(code, FSO_E_RANGE);
+        continue;
+      }
+      const int64_t tk = L[0] + L[1] + L[2];
+      req[u] += 1;
+      tok[u] += tk;
+      areq[int64_t(u) * A + a] += 1;
+      atok[int64_t(u) * A + a] += tk;
+      for (int x = 0; x < 3; ++x) {
+        lh[(int64_t(a) * 3 + x) * FSO_LEN_BINS + len_bin(L[x])] += 1;
+        ls[int64_t(a) * 3 + x] += L[x];
+      }
+      size[h] += 1;
+    }
+    int64_t *rh = o->rate_hist + int64_t(r) * (A + 1) * 2 * FSO_RATE_BINS;
+    for (int64_t k = 0; k < int64_t(A + 1) * 2 * FSO_RATE_BINS; ++k) rh[k] = 0;
+    for (int32_t u = 0; u < U; ++u) {
+      o->user_req[int64_t(r) * U + u] = req[u];
+      o->user_tok[int64_t(r) * U + u] = tok[u];
+      if (req[u] > 0) {  // a user with a request, overall (row A)
+        rh[(int64_t(A) * 2 + 0) * FSO_RATE_BINS + rate_bin(req[u], M)] += 1;
+        rh[(int64_t(A) * 2 + 1) * FSO_RATE_BINS + rate_bin(tok[u], M)] += 1;
+      }
+      for (int32_t a = 0; a < A; ++a) {
+        const int64_t n_ua = areq[int64_t(u) * A + a], t_ua = atok[int64_t(u) * A + a];
+        if (o->user_app_req) o->user_app_req[(int64_t(r) * U + u) * A + a] = n_ua;
+        if (o->user_app_tok) o->user_app_tok[(int64_t(r) * U + u) * A + a] = t_ua;
+        if (n_ua > 0) {  // a user of application a
+          rh[(int64_t(a) * 2 + 0) * FSO_RATE_BINS + rate_bin(n_ua, M)] += 1;
+          rh[(int64_t(a) * 2 + 1) * FSO_RATE_BINS + rate_bin(t_ua, M)] += 1;
+        }
+      }
+    }
+    for (int64_t k = 0; k < int64_t(A) * 3 * FSO_LEN_BINS; ++k)
+      o->len_hist[int64_t(r) * A * 3 * FSO_LEN_BINS + k] = lh[k];
+    for (int64_t k = 0; k < int64_t(A) * 3; ++k) o->len_sum[int64_t(r) * A * 3 + k] = ls[k];
+    int64_t *sh = o->size_hist + int64_t(r) * A * FSO_SIZE_BINS;
+    for (int64_t k = 0; k < int64_t(A) * FSO_SIZE_BINS; ++k) sh[k] = 0;
+    int64_t *gr = o->graph + int64_t(r) * FSO_GRAPH_BINS * 5;
+    for (int k = 0; k < FSO_GRAPH_BINS * 5; ++k) gr[k] = 0;
+    for (int64_t i = 0; i < rp.n; ++i) {  // interactions, at their first call
+      const int64_t g = rp.base + i;
+      if (!is_first_call(t, g) || size[i] == 0) continue;
+      const int32_t a = t->app[g];
+      if (a < 0 || a >= A) continue;
+      sh[int64_t(a) * FSO_SIZE_BINS + std::min<int64_t>(size[i], FSO_SIZE_BINS) - 1] += 1;
+      gr[graph_bin(size[i]) * 5 + 0] += 1;
+    }
+    for (int64_t i = 0; i < rp.n; ++i) {  // requests, by the size of their interaction
+      const int64_t g = rp.base + i;
+      const bool first = is_first_call(t, g);
+      const int64_t h = first ? i : t->head[g];
+      if (h < 0 || (first ? h != i : h >= i) || t->user[g] < 0 || t->user[g] >= U ||
+          t->app[g] < 0 || t->app[g] >= A)
+        continue;
+      int64_t *row = gr + graph_bin(size[h]) * 5;
+      row[1] += 1;
+      row[2] += t->len_in[g];
+      row[3] += t->len_out[g];
+      row[4] += t->len_sys ? t->len_sys[g] : 0;
+    }
+  }
+  return code;
+}
+
 }  // extern "C"

@@ -114,6 +114,38 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
                          const int32_t *admit_step, const int64_t *max_gap, int64_t step_us,
                          int32_t delay_steps, fso_metrics *m);
 
+/* Workload analysis of Sec. 3 (the users' request and token rates of Fig. 2 overall and
+ * per application, the token lengths per application of Figs. 3 and 5, the LLM calls per
+ * interaction of Fig. 4, and the graph-size table, Table 2), per replica.  minute_us is
+ * the length of a minute; the replica's horizon is M = floor(max ts / minute_us) + 1
+ * minutes (0 without requests), a user's RPM = requests / M and TPM = tokens / M
+ * (tokens = L_I + L_S + L_O), overall and within each application.
+ * Bins:
+ *   rate bin of x / M:   0 if x == 0, else 64 + floor(log2(x / M))  (exact, in [1, 127])
+ *   length bin of L:     0 if L == 0, else 1 + floor(log2 L)
+ *   size bin of s calls: min(s, 64) - 1
+ *   graph bins (Table 2 rows): 1, 2-10, 11-20, 21-30, 31-40, 41-50, more than 50 calls
+ * An interaction's size is the number of the replica's records whose first call
+ * (head) is its first call.
+ * Outputs (host arrays, every one written in full):
+ *   minutes     [R]
+ *   user_req, user_tok            [R][U]
+ *   user_app_req, user_app_tok    [R][U][A]  (may be NULL)
+ *   rate_hist   [R][A + 1][2][FSO_RATE_BINS]  users with a request (overall: row A; in app
+ *               a: row a) by the rate bin of their RPM ([0]) and TPM ([1])
+ *   len_hist    [R][A][3][FSO_LEN_BINS]  requests by the length bin of L_I, L_S, L_O
+ *   len_sum     [R][A][3]                sums of L_I, L_S, L_O
+ *   size_hist   [R][A][FSO_SIZE_BINS]    interactions (by their first call's app) by size bin
+ *   graph       [R][FSO_GRAPH_BINS][5]   per graph bin: interactions, requests, sum L_I,
+ *                                        sum L_O, sum L_S over those requests
+ * FSO_E_ARG for minute_us <= 0; FSO_E_RANGE for an id, a length or a link out of range. */
+enum { FSO_RATE_BINS = 128, FSO_LEN_BINS = 32, FSO_SIZE_BINS = 64, FSO_GRAPH_BINS = 7 };
+typedef struct fso_wstats {
+  int64_t *minutes, *user_req, *user_tok, *user_app_req, *user_app_tok;
+  int64_t *rate_hist, *len_hist, *len_sum, *size_hist, *graph;
+} fso_wstats;
+int fso_workload_stats(const fso_trace *t, int64_t minute_us, fso_wstats *out);
+
 #ifdef __cplusplus
 }
 #endif

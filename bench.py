@@ -35,6 +35,7 @@ STAGE_SRC = {
     "schedule": ["fs_sched_onchip.hip", "fs_sched_common.h"],
     "metrics": ["fs_metrics.hip"],
     "history": ["fs_history.hip"],
+    "workload": ["fs_workload.hip"],
 }
 
 # HBM traffic of a stage's kernels from rocprofv3 --pmc runs: FETCH_SIZE and
@@ -92,7 +93,17 @@ def algo_bytes(stage, tr, raw=True, parity=False, prio=False):
         return 1 + 4 + 8 + 4 + 8 + (8 if has_call else 0)
     if stage == "history":                            # app, (call), lengths, read once
         return 4 + (4 if has_call else 0) + lens
+    if stage == "workload":                           # ts, user, app, lengths, (call, head)
+        return 8 + 4 + 4 + lens + (8 if has_call else 0)
     return 0.0
+
+
+def workload_out_bytes(tr):
+    """Bytes the workload analysis writes: per (replica, user, app) requests and tokens,
+    per (replica, user) the same, and the per-replica histograms."""
+    R, U, A = tr.n_replicas, tr.n_users, tr.n_apps
+    return 8 * (2 * R * U * A + 2 * R * U + R * ((A + 1) * 2 * 128 + A * 3 * 32 + A * 3 + A * 64
+                                                 + 7 * 5 + 1))
 
 
 def policy_settings(wl, n_apps, policy):
@@ -156,7 +167,7 @@ def main():
     ap.add_argument("--cpu-protocol", action="store_true",
                     help="time only the CPU oracle on every workload and print a table")
     ap.add_argument("--stage-only", default="", help="time only this stage (profiling runs): "
-                    "cost, throttle, schedule, metrics or history")
+                    "cost, throttle, schedule, metrics, history or workload")
     ap.add_argument("--policy", default="fs", choices=["fs", "wsc_only", "vtc", "rpm"],
                     help="the paper's policy (default) or one it compares with")
     ap.add_argument("--engine", default="step", choices=["step", "literal"],
@@ -249,8 +260,15 @@ def main():
         if "history" in stages:
             evs[i].record(); i += 1
             fs.fs_weights_from_history(dt, J, K=wl.weight_K, base_limit=30, err=err, check=False)
+        if "workload" in stages:
+            evs[i].record(); i += 1
+            fs.fs_workload_stats(dt, 60_000_000, out=wstat, ws=wstat_ws, err=err, check=False)
         evs[i].record()
 
+    wstat = wstat_ws = None
+    if args.stage_only == "workload":
+        wstat = fs.WorkloadStats(dt)
+        wstat_ws = torch.empty(max(fs.fs_workload_workspace(dt), 1), dtype=torch.uint8, device=dev)
     if args.stage_only == "schedule":
         stages = ["init", "schedule"]
     if args.stage_only in ("schedule", "metrics"):
@@ -357,6 +375,26 @@ def main():
         result["extra_stages"] = {"history": {"ms": round(hms, 4), "achieved_gbs": round(hgbs, 2),
                                               "frac": round(hgbs / HBM_PEAK_GBS, 4),
                                               "bytes_per_record": hb}}
+        # the workload analysis of Sec. 3 on this trace (timed on its own)
+        wout = fs.WorkloadStats(dt)
+        wws = torch.empty(max(fs.fs_workload_workspace(dt), 1), dtype=torch.uint8, device=dev)
+        wl_ev = []
+        for it in range(args.warmup + args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fs.fs_workload_stats(dt, 60_000_000, out=wout, ws=wws, err=err, check=False)
+            e1.record()
+            if it >= args.warmup:
+                wl_ev.append((e0, e1))
+        torch.cuda.synchronize()
+        fs.sync_check(err, "workload stats")
+        wms = median([a.elapsed_time(b) for a, b in wl_ev])
+        wbytes = algo_bytes("workload", tr) * N + workload_out_bytes(tr)
+        wgbs = wbytes / (wms / 1000.0) / 1e9
+        result["extra_stages"]["workload"] = {"ms": round(wms, 4), "achieved_gbs": round(wgbs, 2),
+                                              "frac": round(wgbs / HBM_PEAK_GBS, 4),
+                                              "algorithmic_bytes": int(wbytes)}
+        del wout, wws
     cpu = None
     if not args.no_cpu_baseline and not args.stage_only:
         cpu = cpu_baseline(wl, tr, args.cpu_threads, throttle_only, args.policy,

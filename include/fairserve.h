@@ -194,9 +194,11 @@ size_t fs_throttle_workspace(const fs_trace *t);
 /* OIT (Alg. 1 monitoring stream, limit checks; Sec. 4, OIT).  For each record the
  * raw reason is 0 (within limits), 1 (user limit exceeded) or 2 (app limit exceeded).
  * flags & FS_THROTTLE_RAW: bitmap bit i = raw reason != 0, reason[i] = raw reason.
- * Otherwise (gated): a first call is throttled iff overloaded[i] (NULL = always) and
- * its raw reason is nonzero; a later call (call > 0) is never checked and is dropped
- * iff its interaction's first call was throttled (code 3); bitmap bit i = throttled.
+ * Otherwise (gated): a first call (head == its own index) is throttled iff
+ * overloaded[i] (NULL = always) and its raw reason is nonzero; a later call is never
+ * checked and is dropped iff its interaction's first call was throttled (code 3);
+ * bitmap bit i = throttled.  The call reads ts_us, user, app and (gated) head, with
+ * 0 <= head <= own index (else FS_E_RANGE); call and prev are not read.
  * bitmap: [ceil(N/32)] uint32, bit i%32 of word i/32 (global record index).
  * reason [N] uint8, cnt_user [N], cnt_app [N] int32 (the window counts) may be NULL.
  * ws: device workspace of at least fs_throttle_workspace(t) bytes, 256-byte aligned.
@@ -297,6 +299,40 @@ fs_status fs_weights_from_history(const fs_trace *hist, int32_t n_stages, int64_
                                   int32_t base_limit, int64_t *stats, int64_t *coef,
                                   int32_t *t_app, void *ws, size_t ws_bytes, int32_t *err,
                                   hipStream_t stream);
+
+/* Workload analysis of Sec. 3, per replica: the users' requests and tokens per minute
+ * overall and within each application (Fig. 2), the token lengths per application
+ * (Figs. 3 and 5), the LLM calls per interaction per application (Fig. 4) and the
+ * graph-size table (Table 2).  minute_us > 0 is a minute's length; a replica's horizon
+ * is M = floor(max ts / minute_us) + 1 minutes (0 without requests), a user's RPM is
+ * requests / M and TPM tokens / M (tokens = L_I + L_S + L_O).  Bins:
+ *   rate bin of x / M     0 if x == 0, else 64 + floor(log2(x / M)), exact (1..127)
+ *   length bin of L       0 if L == 0, else 1 + floor(log2 L)
+ *   size bin of s calls   min(s, 64) - 1 (an interaction's size is the number of the
+ *                         replica's requests whose first call is its first call)
+ *   graph bins            1, 2-10, 11-20, 21-30, 31-40, 41-50, more than 50 calls
+ * Device outputs (int64, each written in full):
+ *   minutes [R]; user_req, user_tok [R][U]; user_app_req, user_app_tok [R][U][A] (may be
+ *   NULL); rate_hist [R][A + 1][2][FS_RATE_BINS]: users with a request by the rate bin of
+ *   their RPM ([0]) and TPM ([1]), within app a (row a) or overall (row A);
+ *   len_hist [R][A][3][FS_LEN_BINS]: requests by the length bin of L_I, L_S, L_O;
+ *   len_sum [R][A][3]; size_hist [R][A][FS_SIZE_BINS]: interactions (by the app of their
+ *   first call) by size bin; graph [R][FS_GRAPH_BINS][5]: per graph bin its
+ *   interactions, requests, and the sums of L_I, L_O, L_S over those requests.
+ * ws: at least fs_workload_workspace(t) bytes, 256-byte aligned.  Device errors (err):
+ * FS_E_RANGE for an id, length, interaction link or negative arrival time (the request
+ * is not counted). */
+#define FS_RATE_BINS 128
+#define FS_LEN_BINS 32
+#define FS_SIZE_BINS 64
+#define FS_GRAPH_BINS 7
+typedef struct fs_wstats {
+  int64_t *minutes, *user_req, *user_tok, *user_app_req, *user_app_tok;
+  int64_t *rate_hist, *len_hist, *len_sum, *size_hist, *graph;
+} fs_wstats;
+size_t fs_workload_workspace(const fs_trace *t);
+fs_status fs_workload_stats(const fs_trace *t, int64_t minute_us, const fs_wstats *out, void *ws,
+                            size_t ws_bytes, int32_t *err, hipStream_t stream);
 
 /* Waits for `stream` and returns the device status word `err`. */
 fs_status fs_sync_status(hipStream_t stream, const int32_t *err);

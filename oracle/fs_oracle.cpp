@@ -46,8 +46,12 @@ Replica replica(const fso_trace *t, int32_t r) {
 int worse(int a, int b) { return a > b ? a : b; }
 
 // Structural checks.  Each entry point checks the fields it reads.
-// kIds: app ids (and stages); kUsers: user ids.
-enum Need : unsigned { kIds = 1, kOrder = 2, kChain = 4, kLengths = 8, kUsers = 16 };
+// kIds: app ids and stages; kApps: app ids only; kUsers: user ids; kChain: the whole
+// interaction chain (head and previous call); kHeads: only each request's link to its
+// interaction's first call (itself for a first call), 0 <= head <= own index.
+enum Need : unsigned {
+  kIds = 1, kOrder = 2, kChain = 4, kLengths = 8, kUsers = 16, kHeads = 32, kApps = 64
+};
 
 int validate_trace(const fso_trace *t, unsigned need) {
   if (!t || t->n_replicas < 1 || t->n_users < 1 || t->n_apps < 1 || !t->rep_off || !t->ts_us ||
@@ -72,10 +76,14 @@ int validate_trace(const fso_trace *t, unsigned need) {
       }
       if ((need & kUsers) && (t->user[g] < 0 || t->user[g] >= t->n_users))
         code = worse(code, FSO_E_RANGE);
+      if ((need & kApps) && (t->app[g] < 0 || t->app[g] >= t->n_apps))
+        code = worse(code, FSO_E_RANGE);
       if (need & kIds) {
         if (t->app[g] < 0 || t->app[g] >= t->n_apps) code = worse(code, FSO_E_RANGE);
         if (all && t->call[g] < 0) code = worse(code, FSO_E_RANGE);
       }
+      if ((need & kHeads) && all && (t->head[g] < 0 || t->head[g] > i))
+        code = worse(code, FSO_E_RANGE);
       if ((need & kChain) && all) {
         int32_t c = t->call[g], h = t->head[g], p = t->prev[g];
         bool ok;
@@ -563,7 +571,9 @@ int fso_throttle_scoped(const fso_trace *t, int64_t window_us, int32_t t_user,
                         int32_t *cnt_app) {
   if (window_us <= 0 || t_user < 0 || !t_app || !reason || app_scope < 0 || app_scope > 1)
     return FSO_E_ARG;
-  int code = validate_trace(t, kIds | kUsers | kOrder | (raw ? 0u : unsigned(kChain)));
+  // The limit tests read arrival times, users and apps; the gated mode also each
+  // request's link to its interaction's first call, which is itself for a first call.
+  int code = validate_trace(t, kApps | kUsers | kOrder | (raw ? 0u : unsigned(kHeads)));
   if (code == FSO_E_ARG) return code;
   for (int32_t a = 0; a < t->n_apps; ++a)
     if (t_app[a] < 0) return FSO_E_ARG;
@@ -574,6 +584,7 @@ int fso_throttle_scoped(const fso_trace *t, int64_t window_us, int32_t t_user,
     // OIT's dictionaries: user -> arrival times, (user, app) -> arrival times (or
     // app -> arrival times for the app-level limit).
     std::unordered_map<int64_t, std::deque<int64_t>> by_user, by_user_app;
+    std::vector<uint8_t> raw_why(rp.n, 0);  // each request's own limit test
     for (int64_t i = 0; i < rp.n; ++i) {
       int64_t g = rp.base + i, ts = t->ts_us[g];
       std::deque<int64_t> &du = by_user[t->user[g]];
@@ -588,14 +599,18 @@ int fso_throttle_scoped(const fso_trace *t, int64_t window_us, int32_t t_user,
       if (cnt_app) cnt_app[g] = int32_t(ca);
       // user limit first, then the application limit
       uint8_t why = cu > t_user ? 1 : (ca > t_app[t->app[g]] ? 2 : 0);
+      raw_why[i] = why;
       if (raw) {
         reason[g] = why;
-      } else if (is_first_call(t, g)) {
+      } else if (!t->head || t->head[g] == i) {  // a first call
         bool over = overloaded ? overloaded[g] != 0 : true;
         reason[g] = over ? why : 0;
       } else {
-        // a later call inherits its interaction's fate: stalled, never throttled itself
-        reason[g] = reason[rp.base + t->head[g]] != 0 ? 3 : 0;
+        // a later call inherits its interaction's fate: stalled, never throttled itself;
+        // dropped iff its first call (at head) was over a limit while overloaded
+        const int64_t h = t->head[g];
+        const bool hover = overloaded ? overloaded[rp.base + h] != 0 : true;
+        reason[g] = (hover && raw_why[h] != 0) ? 3 : 0;
       }
     }
   }
@@ -772,7 +787,7 @@ int fso_workload_stats(const fso_trace *t, int64_t minute_us, fso_wstats *o) {
       const int64_t g = rp.base + i;
       const int32_t u = t->user[g], a = t->app[g];
       const int64_t L[3] = {t->len_in[g], t->len_sys ? t->len_sys[g] : 0, t->len_out[g]};
-      bool ok = u >= 0 && u < U && a >= 0 && a < A;
+      bool ok = u >= 0 && u < U && a >= 0 && a < A && t->ts_us[g] >= 0;
       for (int x = 0; x < 3; ++x) ok = ok && L[x] >= 0 && L[x] < kLenLimit;
       int64_t h = i;
       if (!is_first_call(t, g)) {

@@ -138,7 +138,8 @@ int fso_fairness_metrics(const fso_trace *t, const int64_t *cost, const int8_t *
  *   size_hist   [R][A][FSO_SIZE_BINS]    interactions (by their first call's app) by size bin
  *   graph       [R][FSO_GRAPH_BINS][5]   per graph bin: interactions, requests, sum L_I,
  *                                        sum L_O, sum L_S over those requests
- * FSO_E_ARG for minute_us <= 0; FSO_E_RANGE for an id, a length or a link out of range. */
+ * FSO_E_ARG for minute_us <= 0; FSO_E_RANGE for an id, a length, a link or an arrival
+ * time (negative) out of range. */
 enum { FSO_RATE_BINS = 128, FSO_LEN_BINS = 32, FSO_SIZE_BINS = 64, FSO_GRAPH_BINS = 7 };
 typedef struct fso_wstats {
   int64_t *minutes, *user_req, *user_tok, *user_app_req, *user_app_tok;

@@ -67,6 +67,14 @@ class fs_metrics(C.Structure):
                                            "aborted_midway", "wasted_tokens")]
 
 
+class fs_wstats(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("minutes", "user_req", "user_tok", "user_app_req",
+                                           "user_app_tok", "rate_hist", "len_hist", "len_sum",
+                                           "size_hist", "graph")]
+
+
+RATE_BINS, LEN_BINS, SIZE_BINS, GRAPH_BINS = 128, 32, 64, 7
+
 _LIB = None
 
 
@@ -91,6 +99,8 @@ def _lib():
             "fs_run_trace": ([T, C.POINTER(fs_weights), C.POINTER(fs_limits), C.POINTER(fs_engine),
                               C.POINTER(fs_outputs), P, SZ, S], I32),
             "fs_metrics_workspace": ([T], SZ),
+            "fs_workload_workspace": ([T], SZ),
+            "fs_workload_stats": ([T, I64, C.POINTER(fs_wstats), P, SZ, P, S], I32),
             "fs_metrics_noalloc_limit": ([], SZ),
             "fs_fairness_metrics_noalloc": ([T, P, C.POINTER(fs_outputs), C.POINTER(fs_engine),
                                              I32, C.POINTER(fs_metrics), S], I32),
@@ -111,6 +121,7 @@ def _lib():
 EXPORTED = ("fs_cost", "fs_history_workspace", "fs_weights_from_history", "fs_throttle_workspace", "fs_throttle", "fs_state_bytes", "fs_state_init",
             "fs_schedule_step", "fs_run_trace_workspace", "fs_run_trace", "fs_metrics_workspace",
             "fs_fairness_metrics", "fs_metrics_noalloc_limit", "fs_fairness_metrics_noalloc",
+            "fs_workload_workspace", "fs_workload_stats",
             "fs_coef_from_expectations", "fs_sync_status", "fs_status_string")
 
 
@@ -399,6 +410,50 @@ def fs_fairness_metrics(dt: DeviceTrace, cost, out: Outputs, engine, delay_steps
     if check:
         sync_check(out.err, "fs_fairness_metrics")
     return m
+
+
+class WorkloadStats:
+    """Device outputs of fs_workload_stats and their fs_wstats descriptor."""
+
+    FIELDS = ("minutes", "user_req", "user_tok", "user_app_req", "user_app_tok", "rate_hist",
+              "len_hist", "len_sum", "size_hist", "graph")
+
+    def __init__(self, dt: DeviceTrace, per_app=True):
+        torch = _torch()
+        R, U, A, d = dt.n_replicas, dt.n_users, dt.n_apps, dt.device
+        e = lambda *shape: _empty(shape, torch.int64, d)
+        self.minutes = e(R)
+        self.user_req, self.user_tok = e(R, U), e(R, U)
+        self.user_app_req = e(R, U, A) if per_app else None
+        self.user_app_tok = e(R, U, A) if per_app else None
+        self.rate_hist = e(R, A + 1, 2, RATE_BINS)
+        self.len_hist = e(R, A, 3, LEN_BINS)
+        self.len_sum = e(R, A, 3)
+        self.size_hist = e(R, A, SIZE_BINS)
+        self.graph = e(R, GRAPH_BINS, 5)
+        self.s = fs_wstats(*(_ptr(getattr(self, k)) for k in self.FIELDS))
+
+    def host(self):
+        return {k: (None if getattr(self, k) is None else getattr(self, k).cpu().numpy())
+                for k in self.FIELDS}
+
+
+def fs_workload_workspace(dt: DeviceTrace) -> int:
+    return int(_lib().fs_workload_workspace(dt.ref))
+
+
+def fs_workload_stats(dt: DeviceTrace, minute_us=60_000_000, out=None, ws=None, err=None,
+                      per_app=True, check=True):
+    torch = _torch()
+    out = WorkloadStats(dt, per_app) if out is None else out
+    nb = fs_workload_workspace(dt)
+    ws = _empty((max(nb, 1),), torch.uint8, dt.device) if ws is None else ws
+    err = err_word(dt.device) if err is None else err
+    _check(_lib().fs_workload_stats(dt.ref, int(minute_us), C.byref(out.s), _ptr(ws), ws.numel(),
+                                    _ptr(err), _stream()), "fs_workload_stats")
+    if check:
+        sync_check(err, "fs_workload_stats")
+    return out
 
 
 def fs_metrics_noalloc_limit() -> int:

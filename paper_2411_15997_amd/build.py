@@ -9,8 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libfairserve.so")
 SOURCES = ["fs_api.hip", "fs_cost.hip", "fs_history.hip", "fs_throttle.hip", "fs_sched.hip",
-           "fs_sched_onchip.hip",
-           "fs_metrics.hip"]
+           "fs_sched_onchip.hip", "fs_metrics.hip", "fs_workload.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -306,6 +306,23 @@ fs_status fs_fairness_metrics(const fs_trace *t, const int64_t *cost, const fs_o
   return hip_status(launch_metrics(t, cost, out, eng, delay_steps, m, ws, stream));
 }
 
+size_t fs_workload_workspace(const fs_trace *t) {
+  if (check_trace(t, false) != FS_OK) return 0;
+  return workload_workspace_bytes(t);
+}
+
+fs_status fs_workload_stats(const fs_trace *t, int64_t minute_us, const fs_wstats *out, void *ws,
+                            size_t ws_bytes, int32_t *err, hipStream_t stream) {
+  fs_status s = check_trace(t, true);
+  if (s != FS_OK) return s;
+  if (minute_us <= 0 || !out || !err || !out->minutes || !out->user_req || !out->user_tok ||
+      !out->rate_hist || !out->len_hist || !out->len_sum || !out->size_hist || !out->graph)
+    return FS_E_ARG;
+  if (!ws || !aligned(ws) || ws_bytes < workload_workspace_bytes(t)) return FS_E_WORKSPACE;
+  if (launch_zero_i32(err, stream) != hipSuccess) return FS_E_HIP;
+  return hip_status(launch_workload(t, minute_us, out, ws, err, stream));
+}
+
 size_t fs_metrics_noalloc_limit(void) { return kScratchBytes; }
 
 fs_status fs_fairness_metrics_noalloc(const fs_trace *t, const int64_t *cost,

@@ -32,6 +32,10 @@ hipError_t launch_history(const fs_trace *t, int32_t n_stages, int64_t K, int32_
                           hipStream_t stream);
 int64_t history_max_records();
 
+size_t workload_workspace_bytes(const fs_trace *t);
+hipError_t launch_workload(const fs_trace *t, int64_t minute_us, const fs_wstats *out, void *ws,
+                           int32_t *err, hipStream_t stream);
+
 hipError_t launch_zero_i32(int32_t *p, hipStream_t stream);
 
 // Device-wide exclusive prefix sum of n uint32 values in place; `part` needs

@@ -26,6 +26,19 @@
 // construction), a device-wide exclusive scan, then a stable scatter (wave-match
 // ranking, the tile reordered in LDS so the global writes of each digit run are
 // contiguous).
+//
+// Fused path (user limit T_u <= kHaloMax, per-(user, app) key, no window counts
+// asked for): only the user bits are sorted, and one kernel tests both limits in user
+// order.  When the user limit holds, the user has at most T_u requests in the window,
+// all among its last T_u positions; so the app limit is exceeded iff the T_a-th
+// previous request of the same app within those positions is in the window.  A tile
+// keeps T_u positions of halo in LDS and finds that request through a stable counting
+// sort of its positions by app (the T_a-th previous entry of the app's list, checked
+// to be the same user's and recent enough).  Only the requests whose reason
+// is used are stored (every request raw; first calls gated), as bytes over a fill with
+// the likelier reason (estimated from a sample of the user test).
+#include <algorithm>
+
 #include "fs_device.h"
 #include "fs_launch.h"
 
@@ -251,7 +264,8 @@ __global__ void __launch_bounds__(kThreads) k_thr_span(const int64_t *rep_off, c
 struct InitArgs {
   DevTrace t;
   Pack pk;
-  bool check_chain;
+  bool gated;      // gated mode: checks the links to the first calls
+  int mark;        // flag bit: 0 none, 1 every request, 2 first calls only
   const int32_t *sh;
   uint64_t *el;
   int shift;      // first radix digit
@@ -296,24 +310,12 @@ __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
       if (!ok_ids) code = max(code, int32_t(FS_E_RANGE));
       if (ts < 0) code = max(code, int32_t(FS_E_RANGE));
       if (g > r_base && tr.ts[g - 1] > ts) code = max(code, int32_t(FS_E_ORDER));
-      if (tr.call) {
-        const int32_t c = tr.call[g];
-        if (c < 0) code = max(code, int32_t(FS_E_RANGE));
-        if (a.check_chain) {
-          const int64_t li = g - r_base;
-          const int32_t hd = tr.head[g], pv = tr.prev[g];
-          bool ok;
-          if (c == 0) {
-            ok = hd == li && pv == -1;
-          } else {
-            ok = c > 0 && pv >= 0 && pv < li;
-            if (ok) {
-              const int64_t gp = r_base + pv;
-              ok = tr.call[gp] == c - 1 && tr.user[gp] == u && tr.head[gp] == hd;
-            }
-          }
-          if (!ok) code = max(code, int32_t(FS_E_RANGE));
-        }
+      bool first = true;
+      if (tr.head && a.gated) {  // the only link the gated mode follows: to the first call
+        const int64_t li = g - r_base;
+        const int32_t hd = tr.head[g];
+        if (hd < 0 || hd > li) code = max(code, int32_t(FS_E_RANGE));
+        first = hd == li;
       }
       const uint64_t key = ok_ids ? ((uint64_t(ap) << a.pk.Bu) | uint64_t(int64_t(r) * tr.U + u)) : 0;
       uint64_t q = 0;
@@ -322,7 +324,8 @@ __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
         q = rel > 0 ? uint64_t(rel) >> sh : 0;
         if (q > a.pk.qmask) q = a.pk.qmask;  // only for unsorted input, which is an error
       }
-      const uint64_t e = (key << a.pk.SK) | (uint64_t(g) << a.pk.SI) | (q << 1);
+      const uint64_t fl = (a.mark == 1 || (a.mark == 2 && first)) ? 1u : 0u;
+      const uint64_t e = (key << a.pk.SK) | (uint64_t(g) << a.pk.SI) | (q << 1) | fl;
       a.el[g] = e;
       d = uint32_t(e >> (a.pk.SK + a.shift)) & a.mask;
     }
@@ -598,6 +601,227 @@ __global__ void __launch_bounds__(kThreads) k_thr_apptest(AppTestArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- fused limit tests
+
+constexpr int kHaloMax = 1024;              // largest user limit the fused path takes
+constexpr int kFTile = 4096;                // positions tested per work-group
+constexpr int kFThreads = 512;              // threads of a fused work-group
+constexpr int kFSpan = kFTile + kHaloMax;   // elements held in LDS (tile and halo)
+
+// Background of the fused path: 1 when most sampled requests whose reason is stored
+// are over the user limit, else 0 (counts in slots 0 and 1 of the flag counters).
+__device__ inline uint8_t fused_background(const int32_t *n_flag) {
+  return int64_t(n_flag[kFlagStride]) * 2 > int64_t(n_flag[0]) ? 1 : 0;
+}
+
+struct SampleArgs {
+  const uint64_t *el;  // user order
+  int64_t N;
+  int32_t t_user;
+  uint64_t user_mask;
+  Win win;
+  int32_t *n_flag;
+};
+
+// The user test on every 997th position (a sample for the background's choice).
+constexpr int kSampleStride = 997;
+__global__ void __launch_bounds__(kThreads) k_thr_sample(SampleArgs a) {
+  const Win win = load_win(a.win);
+  int32_t flagged = 0, over = 0;
+  const int64_t ns = (a.N + kSampleStride - 1) / kSampleStride;
+  for (int64_t k = blockIdx.x * int64_t(kThreads) + threadIdx.x; k < ns;
+       k += int64_t(gridDim.x) * kThreads) {
+    const int64_t p = k * kSampleStride;
+    const uint64_t e = a.el[p];
+    if (!(e & 1u)) continue;
+    ++flagged;
+    if (int64_t(a.t_user) <= p) {
+      const uint64_t eq = a.el[p - a.t_user];
+      if (((e ^ eq) & a.user_mask) == 0 && in_window(e, eq, win)) ++over;
+    }
+  }
+#pragma unroll
+  for (int d = 32; d > 0; d >>= 1) {
+    flagged += __shfl_xor(flagged, d, 64);
+    over += __shfl_xor(over, d, 64);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    if (flagged) atomicAdd(a.n_flag, flagged);
+    if (over) atomicAdd(a.n_flag + kFlagStride, over);
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) k_thr_fill_fused(uint8_t *rb, int64_t N,
+                                                              const int32_t *n_flag) {
+  const uint32_t v = uint32_t(fused_background(n_flag)) * 0x01010101u;
+  const uint4 q = make_uint4(v, v, v, v);
+  const int64_t n16 = N >> 4;
+  uint4 *r4 = reinterpret_cast<uint4 *>(rb);
+  for (int64_t i = blockIdx.x * int64_t(kThreads) + threadIdx.x; i < n16;
+       i += int64_t(gridDim.x) * kThreads)
+    r4[i] = q;
+  if (blockIdx.x == 0 && threadIdx.x < (N & 15)) rb[(n16 << 4) + threadIdx.x] = uint8_t(v);
+}
+
+struct FusedArgs {
+  const uint64_t *el;  // user order (each user's requests in stream order)
+  int64_t N;
+  int32_t t_user;      // <= kHaloMax
+  const int32_t *t_app;
+  int32_t A;
+  int app_bits;
+  uint64_t user_mask;
+  Win win;
+  uint8_t *rb;         // raw reasons in stream order, filled with the background
+  const int32_t *n_flag;
+};
+
+// Dynamic LDS of the fused test, sized per launch for span = T_u + kFTile positions and
+// A apps: the span's elements, and its positions grouped by app (a stable counting sort:
+// list[rank[j]] = j, each app's positions in order).
+struct FusedLds {
+  uint64_t *el;        // [span]
+  uint16_t *list;      // [span]
+  uint16_t *rank;      // [span]
+  uint16_t *cnt;       // [kFThreads / 64][A] per wave: positions of each app so far
+  uint16_t *start;     // [A] first list index of each app
+  uint32_t *waves;     // [kFThreads / 64] (16-byte aligned)
+};
+__host__ __device__ inline size_t fused_lds_bytes(int span, int A) {
+  return size_t(span) * 12 + size_t(kFThreads / 64) * A * 2 + size_t(A) * 2 + 16 +
+         size_t(kFThreads / 64) * 4;
+}
+__device__ inline FusedLds fused_lds(char *base, int span, int A) {
+  FusedLds sm;
+  sm.el = reinterpret_cast<uint64_t *>(base);
+  sm.list = reinterpret_cast<uint16_t *>(sm.el + span);
+  sm.rank = sm.list + span;
+  sm.cnt = sm.rank + span;
+  sm.start = sm.cnt + (kFThreads / 64) * A;
+  sm.waves = reinterpret_cast<uint32_t *>(
+      (reinterpret_cast<uintptr_t>(sm.start + A) + 15) & ~uintptr_t(15));
+  return sm;
+}
+
+__global__ void __launch_bounds__(kFThreads) k_thr_fused(FusedArgs a) {
+  extern __shared__ __align__(16) char fused_smem[];
+  const Win win = load_win(a.win);
+  const Pack &pk = win.pk;
+  const uint8_t bg = fused_background(a.n_flag);
+  const int H = a.t_user;
+  const int64_t p0 = xcd_tile(blockIdx.x, gridDim.x) * int64_t(kFTile);
+  const int64_t g0 = p0 - H;  // global position of el[0]
+  const int span = H + kFTile;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int A = a.A;
+  const FusedLds sm = fused_lds(fused_smem, span, A);
+  const uint32_t amask = (1u << pk.Ba) - 1u;
+  {  // every load of the span is issued before the first store to LDS
+    constexpr int kIters = (kFSpan + kFThreads - 1) / kFThreads;
+    uint64_t v[kIters];
+#pragma unroll
+    for (int i = 0; i < kIters; ++i) {
+      const int j = threadIdx.x + i * kFThreads;
+      const int64_t g = g0 + j;
+      v[i] = (j < span && g >= 0 && g < a.N) ? a.el[g] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < kIters; ++i) {
+      const int j = threadIdx.x + i * kFThreads;
+      if (j < span) sm.el[j] = v[i];
+    }
+  }
+  for (int k = threadIdx.x; k < (kFThreads / 64) * A; k += kFThreads) sm.cnt[k] = 0;
+  __syncthreads();
+  // 1. stable ranks by app: wave w takes rows [w * rows, (w + 1) * rows) of 64 positions
+  const int n_rows = (span + 63) / 64;
+  const int rows = (n_rows + kFThreads / 64 - 1) / (kFThreads / 64);
+  const uint64_t lt = (uint64_t(1) << lane) - 1;
+  uint16_t *const my = sm.cnt + wave * A;
+  for (int rw = wave * rows; rw < (wave + 1) * rows && rw < n_rows; ++rw) {
+    const int j = rw * 64 + lane;
+    const int64_t g = g0 + j;
+    const bool valid = j < span && g >= 0 && g < a.N;
+    const uint32_t ap = valid ? uint32_t(sm.el[j] >> (pk.SK + pk.Bu)) & amask : 0u;
+    const uint64_t peers = digit_peers(ap, valid, a.app_bits);
+    const uint32_t before = valid ? my[ap] : 0u;
+    if (valid) sm.rank[j] = uint16_t(before + __popcll(peers & lt));
+    if (valid && (peers & lt) == 0) my[ap] = uint16_t(before + __popcll(peers));
+  }
+  __syncthreads();
+  // 2. each app's list start and each wave's offset within it
+  uint32_t tot4 = 0;
+  uint32_t tots[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {  // apps 4t .. 4t + 3 (A <= 1024 <= 4 * kFThreads)
+    const int ap = threadIdx.x * 4 + q;
+    uint32_t tot = 0;
+    if (ap < A) {
+#pragma unroll
+      for (int w = 0; w < kFThreads / 64; ++w) {
+        const uint32_t c = sm.cnt[w * A + ap];
+        sm.cnt[w * A + ap] = uint16_t(tot);
+        tot += c;
+      }
+    }
+    tots[q] = tot;
+    tot4 += tot;
+  }
+  uint32_t total;
+  const uint32_t incl = block_inclusive_scan(tot4, sm.waves, total);
+  uint32_t run = incl - tot4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int ap = threadIdx.x * 4 + q;
+    if (ap < A) sm.start[ap] = uint16_t(run);
+    run += tots[q];
+  }
+  __syncthreads();
+  // 3. final list indices
+  for (int rw = wave * rows; rw < (wave + 1) * rows && rw < n_rows; ++rw) {
+    const int j = rw * 64 + lane;
+    const int64_t g = g0 + j;
+    if (j < span && g >= 0 && g < a.N) {
+      const uint32_t ap = uint32_t(sm.el[j] >> (pk.SK + pk.Bu)) & amask;
+      const uint32_t idx = uint32_t(sm.start[ap]) + sm.cnt[wave * A + ap] + sm.rank[j];
+      sm.rank[j] = uint16_t(idx);
+      sm.list[idx] = uint16_t(j);
+    }
+  }
+  __syncthreads();
+  // 4. the tests of the tile's positions whose reason is stored
+  const int64_t n_here = a.N - p0 < kFTile ? a.N - p0 : kFTile;
+  for (int t = threadIdx.x; t < n_here; t += kFThreads) {
+    const int64_t p = p0 + t;
+    const int j = t + H;
+    const uint64_t e = sm.el[j];
+    if (!(e & 1u)) continue;  // a request whose own reason is not used (a later call, gated)
+    uint8_t why = 0;
+    if (int64_t(H) <= p) {  // the user limit: the T_u-th previous request of the user
+      const uint64_t eq = sm.el[j - H];
+      if (((e ^ eq) & a.user_mask) == 0 && in_window(e, eq, win)) why = 1;
+    }
+    if (!why) {
+      const uint32_t ap = uint32_t(e >> (pk.SK + pk.Bu)) & amask;
+      const int32_t ta = ap < uint32_t(A) ? a.t_app[ap] : INT32_MAX;
+      if (ta == 0) {
+        why = 2;  // the request itself is over a zero limit
+      } else if (ta < H) {  // (ta >= T_u: at most T_u requests of the user in the window)
+        // the ta-th previous request of the app: the same user's iff the user has ta of
+        // them before j; in the window only if among the last T_u - 1 positions
+        const int r = int(sm.rank[j]) - ta;
+        if (r >= int(sm.start[ap])) {
+          const int x = sm.list[r];
+          const int64_t gx = g0 + x;
+          const uint64_t ex = sm.el[x];
+          if (gx > p - H && ((e ^ ex) & a.user_mask) == 0 && in_window(e, ex, win)) why = 2;
+        }
+      }
+    }
+    if (why != bg) a.rb[(e >> pk.SI) & pk.imask] = why;
+  }
+}
+
 // ---------------------------------------------------------------- app-level limit
 
 // With the app limit counted over all users of an app, the user test runs on the user
@@ -664,35 +888,76 @@ struct CombineArgs {
   int64_t n_words;
 };
 
-constexpr int kCombineSpan = kThreads * 16;  // records per combine block
+constexpr int kCombineRows = 16;
+constexpr int kCombineSpan = kThreads * kCombineRows;  // records per combine block
 
+// Gated mode: a first call (head == itself) is throttled iff overloaded and over a limit;
+// a later call is dropped iff its first call was.  All of a thread's loads are issued
+// before the interaction gathers, which all come before the stores.
 __global__ void __launch_bounds__(kThreads) k_thr_combine(CombineArgs a) {
   const int64_t N = a.t.N;
   const int lane = threadIdx.x & 63;
   const int64_t start = xcd_tile(blockIdx.x, gridDim.x) * kCombineSpan;
-  const int64_t stop = start + kCombineSpan < N ? start + kCombineSpan : N;
-  for (int64_t base = start; base < stop; base += blockDim.x) {
-    const int64_t g = base + threadIdx.x;
-    uint8_t code = 0;
-    if (g < N) {
-      const uint8_t rr = a.rb[g];
-      if (a.raw) {
-        code = rr;
-      } else if (!a.t.call || a.t.call[g] == 0) {
-        const bool over = a.overloaded ? a.overloaded[g] != 0 : true;
-        code = over ? rr : 0;
-      } else {
-        const int32_t r = replica_of(a.t.rep_off, a.t.R, g);
-        const int64_t lo = a.t.rep_off[r], hi = a.t.rep_off[r + 1];
-        const int64_t h = lo + a.t.head[g];
-        if (h >= lo && h < hi) {
-          const bool hover = a.overloaded ? a.overloaded[h] != 0 : true;
-          code = (hover && a.rb[h] != 0) ? 3 : 0;
-        }
+  uint8_t code[kCombineRows];
+  // global index of the interaction's first call for a later call; -1 for a first call,
+  // -2 for a later call whose link is out of range (reported by the element pass)
+  int64_t hg[kCombineRows];
+  const bool links = !a.raw && a.t.head;
+  int32_t hd[kCombineRows];
+#pragma unroll
+  for (int i = 0; i < kCombineRows; ++i) {
+    const int64_t g = start + i * kThreads + threadIdx.x;
+    code[i] = g < N ? a.rb[g] : 0;
+    hd[i] = (links && g < N) ? a.t.head[g] : 0;
+  }
+  if (links) {
+    // the replica of each row, walking forward from the block's first record (the
+    // offsets are read only where a replica ends inside the block)
+    int32_t r = start < N ? replica_of(a.t.rep_off, a.t.R, start) : 0;
+    int64_t lo = a.t.rep_off[r], hi = a.t.rep_off[r + 1];
+#pragma unroll
+    for (int i = 0; i < kCombineRows; ++i) {
+      const int64_t g = start + i * kThreads + threadIdx.x;
+      hg[i] = -1;
+      if (g >= N) continue;
+      while (g >= hi) {
+        ++r;
+        lo = hi;
+        hi = a.t.rep_off[r + 1];
       }
-      if (a.reason) a.reason[g] = code;
+      const int64_t h = lo + hd[i];
+      if (h != g) hg[i] = (h >= lo && h < g) ? h : -2;
     }
-    const uint64_t bits = __ballot(g < N && code != 0);
+  }
+  if (!links) {
+#pragma unroll
+    for (int i = 0; i < kCombineRows; ++i) hg[i] = -1;
+  }
+  if (!a.raw) {
+    uint8_t hr[kCombineRows];
+#pragma unroll
+    for (int i = 0; i < kCombineRows; ++i) hr[i] = hg[i] >= 0 ? a.rb[hg[i]] : 0;
+#pragma unroll
+    for (int i = 0; i < kCombineRows; ++i) {
+      const int64_t g = start + i * kThreads + threadIdx.x;
+      if (g >= N) continue;
+      if (hg[i] >= 0) {
+        const bool hover = a.overloaded ? a.overloaded[hg[i]] != 0 : true;
+        code[i] = (hover && hr[i] != 0) ? 3 : 0;
+      } else if (hg[i] == -2) {
+        code[i] = 0;
+      } else {
+        const bool over = a.overloaded ? a.overloaded[g] != 0 : true;
+        code[i] = over ? code[i] : 0;
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kCombineRows; ++i) {
+    const int64_t base = start + i * kThreads;
+    const int64_t g = base + threadIdx.x;
+    if (a.reason && g < N) a.reason[g] = code[i];
+    const uint64_t bits = __ballot(g < N && code[i] != 0);
     if (lane == 0) {
       const int64_t w = (base + (threadIdx.x & ~63)) >> 5;
       if (w < a.n_words) a.bitmap[w] = uint32_t(bits);
@@ -771,15 +1036,21 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
     left -= wd;
   }
 
-  InitArgs ia{dt, pk, !raw, sh, A, dig[0].shift, (1u << dig[0].width) - 1u, hist, L.tiles, err};
+  const bool app_level = lim->app_scope != 0;
+  // the fused path: user bits only, both limits tested in one pass over the user order
+  const bool fused = !app_level && !cnt_user && !cnt_app && lim->t_user >= 0 &&
+                     lim->t_user <= kHaloMax;
+  const int mark = fused ? (raw ? 1 : 2) : 0;
+  InitArgs ia{dt, pk, !raw, mark, sh, A, dig[0].shift, (1u << dig[0].width) - 1u, hist, L.tiles,
+              err};
   hipLaunchKernelGGL(k_thr_init, dim3(L.tiles), dim3(kThreads), 0, s, ia);
 
   const Win win{lim->window_us, sh, 0, pk.Bq > 0, pk, dt.ts};
 
   const uint64_t user_mask = ((uint64_t(1) << pk.Bu) - 1) << pk.SK;
-  const bool app_level = lim->app_scope != 0;
   uint64_t *in = A, *out = B;
-  for (int k = 0; k < nd; ++k) {
+  const int n_pass = fused ? n_user : nd;
+  for (int k = 0; k < n_pass; ++k) {
     const uint32_t mask = (1u << dig[k].width) - 1u;
     const int shift = pk.SK + dig[k].shift;
     if (k == n_user && app_level) {
@@ -814,9 +1085,25 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
     in = out;
     out = tmp;
   }
-  // app test in (user, app) order; raw reasons to stream order in the free sort buffer
+  // raw reasons to stream order in the free sort buffer
   uint8_t *rb = reinterpret_cast<uint8_t *>(out);
-  {
+  if (fused) {
+    const int64_t ns = (L.N + kSampleStride - 1) / kSampleStride;
+    SampleArgs sa{in, L.N, lim->t_user, user_mask, win, sh + kFlagStride};
+    hipLaunchKernelGGL(k_thr_sample, dim3(std::min<int64_t>((ns + kThreads - 1) / kThreads, 1024)),
+                       dim3(kThreads), 0, s, sa);
+    hipLaunchKernelGGL(k_thr_fill_fused, dim3(grid_for((L.N >> 4) + 1, kThreads)), dim3(kThreads),
+                       0, s, rb, L.N, sh + kFlagStride);
+    FusedArgs fa{in, L.N, lim->t_user, tapp, t->n_apps, pk.Ba, user_mask, win, rb,
+                 sh + kFlagStride};
+    const size_t lds = fused_lds_bytes(lim->t_user + kFTile, t->n_apps);
+    if (lds > 65536)
+      (void)hipFuncSetAttribute(reinterpret_cast<const void *>(k_thr_fused),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    hipLaunchKernelGGL(k_thr_fused, dim3(uint32_t((L.N + kFTile - 1) / kFTile)), dim3(kFThreads),
+                       lds, s, fa);
+  } else {  // app test in (user, app) order
+
     const KeySel app_key{((uint64_t(1) << pk.Bk) - 1) << pk.SK, app_level, pk.SK, pk.Bu,
                          uint32_t(t->n_users)};
     hipLaunchKernelGGL(k_thr_fill, dim3(grid_for((L.N >> 4) + 1, kThreads)), dim3(kThreads), 0, s,

@@ -153,3 +153,69 @@ def test_app_level_limit_workloads(name, kw):
     say("throttle app-level", name, tr.n)
     g, o = _check(tr, wl.window_us, wl.t_user, ta, app_scope=1)
     assert (o.reason == 2).sum() > tr.n // 100
+
+
+def _check_fused(tr, W, tu, ta, overloaded=None, raw=True):
+    """Without the window counts (the fused path when t_user <= 1024)."""
+    return _check(tr, W, tu, ta, overloaded=overloaded, raw=raw, counts=False)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_fused_limit_tests_random(seed):
+    """Both limits tested in one pass over the user order: user limits from 0 to past the
+    largest the fused path takes (1,024), app limits from 0 to above the user limit,
+    heavy users whose windows span several 64-position blocks and tiles of 4,096, up to
+    1,024 apps (ten bit planes), several replicas, raw and gated."""
+    rng = np.random.default_rng(7000 + seed)
+    n = int(rng.choice([1, 100, 5000, 20000]))
+    U = int(rng.choice([1, 2, 7, 300]))
+    A = int(rng.choice([1, 3, 16, 1024]))
+    tr = random_trace(rng, n, U, A, int(rng.integers(1, 4 * n + 2)), multi=bool(seed % 3),
+                      n_replicas=int(rng.integers(1, 4)))
+    W = int(rng.integers(1, 400))
+    tu = int(rng.choice([0, 1, 2, 63, 64, 65, 300, 1024, 1025]))
+    ta = rng.integers(0, max(2, tu + 3), size=A).tolist()
+    say("fused throttle", seed, tr.n, U, A, tu)
+    _check_fused(tr, W, tu, ta)
+    ov = rng.integers(0, 2, size=tr.n).astype(np.uint8)
+    _check_fused(tr, W, tu, ta, overloaded=ov, raw=False)
+    _check_fused(tr, W, tu, ta, raw=False)
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c2_replicas", dict(replicas=4, records=30001)),
+    ("c3_throttle", dict(records=1_000_003)),
+    ("c4_sweep", dict(replicas=64)),
+    ("c5_tenant", dict(records=300_007, users=30_000)),
+])
+def test_fused_workloads(name, kw):
+    wl, tr = workload_trace(name, **kw)
+    say("fused throttle", name, tr.n)
+    _check_fused(tr, wl.window_us, wl.t_user, wl.t_app)
+    _check_fused(tr, wl.window_us, wl.t_user, wl.t_app, raw=False)
+
+
+def test_gated_reads_only_the_first_call_link():
+    """The gated mode reads only each request's link to its interaction's first call (a
+    request whose link is itself is a first call): a trace whose call numbers and
+    previous-call links are broken but whose first-call links are valid is throttled as
+    the oracle does, and a link past the request itself is a range error."""
+    rng = np.random.default_rng(13)
+    tr = random_trace(rng, 3000, 6, 2, 3000, multi=True)
+    later = np.nonzero(tr.call > 0)[0]
+    broken = tg.Trace(**{**tr.__dict__, "prev": tr.prev.copy(), "call": tr.call.copy()})
+    broken.prev[later[::3]] = 0
+    broken.call[later[1::3]] = -5
+    for counts in (True, False):
+        _check(broken, 200, 4, [2, 3], raw=False, counts=counts)
+    selfish = tg.Trace(**{**tr.__dict__, "head": tr.head.copy()})
+    selfish.head[later[::4]] = later[::4]  # links to itself: a first call
+    for counts in (True, False):
+        _check(selfish, 200, 4, [2, 3], raw=False, counts=counts)
+    bad = tg.Trace(**{**tr.__dict__, "head": tr.head.copy()})
+    bad.head[later[5]] = later[5] + 1       # past the request itself
+    with pytest.raises(oracle.OracleError) as oe:
+        oracle.throttle(bad, 200, 4, [2, 3], raw=False)
+    with pytest.raises(fs.FairServeError) as ge:
+        gpu_throttle(bad, 200, 4, [2, 3], raw=False, counts=False)
+    assert ge.value.code == oe.value.code == fs.FS_E_RANGE

@@ -138,6 +138,9 @@ struct XMem {
     set_key(last, kEmptyKey);
   }
   __device__ int32_t slot(int32_t i, int32_t) const { return i; }
+  // one slot per lane (not wave-uniform)
+  __device__ uint64_t key_at(int32_t x) const { return ld_fresh(k + x); }
+  __device__ uint32_t user_at(int32_t x) const { return uint32_t(ld_fresh(user + x)); }
   __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
     uint64_t kk = kEmptyKey;
     uint32_t us = 0xffffffffu, bx = 0xffffffffu;
@@ -228,6 +231,9 @@ struct XLds {
     set_key(last, kEmptyKey);
   }
   __device__ int32_t slot(int32_t i, int32_t) const { return i; }
+  // one slot per lane (not wave-uniform)
+  __device__ uint64_t key_at(int32_t x) const { return k[x]; }
+  __device__ uint32_t user_at(int32_t x) const { return uint32_t(user[x]); }
   __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
     uint64_t kk = kEmptyKey;
     uint32_t us = 0xffffffffu, bx = 0xffffffffu;
@@ -258,6 +264,17 @@ struct XLds {
 };
 constexpr size_t kXLdsBytesPerUser = 8 + 8 + 10 * 4;  // counter, key, nine fields and xs
 
+// Per block of 64 X slots, in LDS: the least (key, user), and the least and largest
+// counter.  The argmin then reads the block minima and one block, and the gap sample
+// the block extremes, instead of every slot.  Kept while more than 64 users are
+// backlogged (and their blocks fit, cap); rebuilt from X when that starts.
+struct XBlocks {
+  uint64_t *k, *umin, *umax;
+  uint32_t *u;
+  int32_t cap;  // blocks that fit (0: single-level scans only)
+};
+constexpr size_t kXBlockBytes = 8 + 8 + 8 + 4;
+
 // ---------------------------------------------------------------------------
 // The scheduler body.  All control flow is wave-uniform; the arrival window holds
 // one record per lane.  Per-record outputs are collected in registers and written
@@ -265,7 +282,8 @@ constexpr size_t kXLdsBytesPerUser = 8 + 8 + 10 * 4;  // counter, key, nine fiel
 // admissions by admission order.
 // ---------------------------------------------------------------------------
 template <bool G, class XT>
-__device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool onchip) {
+__device__ void run_replica(const SchedArgs &a, Store &S, XT &X, const XBlocks &XB, int32_t r,
+                            bool onchip) {
   const int lane = threadIdx.x;
   const DevTrace &t = a.t;
   const int64_t base = t.rep_off[r];
@@ -314,8 +332,93 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
 
   auto get_u = [&](int32_t k) -> int64_t { return S.users_global ? ld_fresh(S.u + k) : S.u[k]; };
   auto slot_u = [&](int32_t x) -> int64_t { return int64_t(X.key(x) & kValMask); };
+
+  // ---- two-level argmin over X (block minima of 64 slots) while nX > 64
+  bool hier = false;
+  auto blk_set = [&](int32_t b) {  // block b's least (key, user) and counter range
+    const int32_t sx = b * 64 + lane;
+    uint64_t kk = kEmptyKey, lo = kEmptyKey, hi = 0;
+    uint32_t us = 0xffffffffu, bx = 0xffffffffu;
+    if (sx < nX) {
+      kk = X.key_at(sx);
+      us = X.user_at(sx);
+      bx = uint32_t(sx);
+      lo = hi = kk & kValMask;
+    }
+    wave_argmin(kk, us, bx);
+    wave_minmax(lo, hi);
+    if (lane == 63) {
+      XB.k[b] = kk;
+      XB.u[b] = us;
+      XB.umin[b] = lo;
+      XB.umax[b] = hi;
+    }
+  };
+  auto blk_touch = [&](int32_t x) {  // slot x changed (key, or moved / freed)
+    if (!hier) return;
+    wave_fence();
+    blk_set(x >> 6);
+  };
+  auto blk_sync = [&]() {  // nX changed: start or stop keeping the block minima
+    const bool want = nX > 64 && ((nX + 63) >> 6) <= XB.cap;
+    if (want && !hier) {
+      hier = true;
+      wave_fence();
+      for (int32_t b = 0; b * 64 < nX; ++b) blk_set(b);
+    } else if (!want) {
+      hier = false;
+    }
+  };
+  // least (key, user) among the backlogged users: its slot, key and user
+  auto argmin_x = [&](uint64_t &bk, int32_t &bu) -> int32_t {
+    if (!hier) return X.argmin(nX, bk, bu);
+    wave_fence();
+    const int32_t nb = (nX + 63) >> 6;
+    uint64_t kk = kEmptyKey;
+    uint32_t us = 0xffffffffu, bx = 0xffffffffu;
+    for (int32_t b = lane; b < nb; b += 64) {
+      const uint64_t v = XB.k[b];
+      const uint32_t w = XB.u[b];
+      const bool take = v < kk || (v == kk && w < us);
+      kk = take ? v : kk;
+      us = take ? w : us;
+      bx = take ? uint32_t(b) : bx;
+    }
+    wave_argmin(kk, us, bx);
+    const int32_t b = rdl(int32_t(bx), 63);
+    const int32_t sx = b * 64 + lane;
+    uint64_t k2 = kEmptyKey;
+    uint32_t u2 = 0xffffffffu, x2 = 0xffffffffu;
+    if (sx < nX) {
+      k2 = X.key_at(sx);
+      u2 = X.user_at(sx);
+      x2 = uint32_t(sx);
+    }
+    wave_argmin(k2, u2, x2);
+    bk = uint64_t(rdl64(int64_t(k2), 63));
+    bu = rdl(int32_t(u2), 63);
+    return rdl(int32_t(x2), 63);
+  };
+  // least and largest counter among the backlogged users (nX > 0)
+  auto minmax_x = [&](int64_t &mn, int64_t &mx) {
+    if (!hier) {
+      X.minmax(nX, mn, mx);
+      return;
+    }
+    wave_fence();
+    uint64_t lo = kEmptyKey, hi = 0;
+    for (int32_t b = lane; b * 64 < nX; b += 64) {
+      const uint64_t l = XB.umin[b], h = XB.umax[b];
+      lo = l < lo ? l : lo;
+      hi = h > hi ? h : hi;
+    }
+    wave_minmax(lo, hi);
+    mn = rdl64(int64_t(lo), 63);
+    mx = rdl64(int64_t(hi), 63);
+  };
   auto set_key = [&](int32_t x, int64_t uval) {
     X.set_key(x, (uint64_t(X.get_rdy(x) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval));
+    blk_touch(x);
   };
   auto tokens_at = [&](int64_t i) -> int32_t {
     const int64_t g = base + i;
@@ -415,6 +518,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     X.set_rh(x, -1);
     X.set_rdy(x, 0);
     X.set_key(x, (uint64_t(1) << kTierShift) | uint64_t(uval));
+    if (hier) blk_touch(x);
+    blk_sync();
     return x;
   };
   auto leave_x = [&](int32_t x, int32_t k, int64_t uval) {
@@ -422,6 +527,10 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     c_u = (w_user == k) ? uval : c_u;
     X.release(x, k, nX, S);
     --nX;
+    // the last slot moved into x, and the old last slot (now nX) is free
+    if (hier && (nX >> 6) != (x >> 6)) blk_touch(nX);
+    blk_touch(x);
+    blk_sync();
   };
 
   // ---- pool
@@ -802,7 +911,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
       int32_t k;
       int32_t x;
       if (!a.fcfs) {
-        x = X.argmin(nX, bk, k);
+        x = argmin_x(bk, k);
       } else {
         // the earliest queued request: the first arrived record still undecided (a
         // later call waiting for its previous call cannot be it); its user's FIFO head
@@ -966,7 +1075,7 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, int32_t r, bool
     }
     if (nX > 0) {
       int64_t mn, mx;
-      X.minmax(nX, mn, mx);
+      minmax_x(mn, mx);
       gap = mx - mn > gap ? mx - mn : gap;
       minX = mn;
     }
@@ -1051,6 +1160,17 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   S.pcap = cap;
   S.e = reinterpret_cast<Entry *>(st + L.e_all) + off;
   S.e_free = reinterpret_cast<int32_t *>(st + L.e_free) + off;
+  XBlocks XB;
+  {
+    const size_t tab = a.oc.glds ? size_t(a.t.U) * kXLdsBytesPerUser : 0;
+    char *b = gsm + (tab + 15) / 16 * 16;
+    const int32_t nb = a.oc.hblk > 0 ? a.oc.hblk : 0;
+    XB.cap = a.oc.hblk;
+    XB.k = reinterpret_cast<uint64_t *>(b);
+    XB.umin = XB.k + nb;
+    XB.umax = XB.umin + nb;
+    XB.u = reinterpret_cast<uint32_t *>(XB.umax + nb);
+  }
   if (a.oc.glds) {  // the table and the counters in LDS
     const int32_t U = a.t.U;
     XLds X;
@@ -1070,7 +1190,7 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
     X.xs = p += U;
     S.xslot = nullptr;
     S.users_global = false;
-    run_replica<true>(a, S, X, r, false);
+    run_replica<true>(a, S, X, XB, r, false);
     if (threadIdx.x == 0) rs->overflow = 0;
     return;
   }
@@ -1089,7 +1209,7 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
   S.u = reinterpret_cast<int64_t *>(st + L.u_all) + int64_t(r) * a.t.U;
   S.xslot = reinterpret_cast<int32_t *>(st + L.xslot_all) + int64_t(r) * a.t.U;
   S.users_global = true;
-  run_replica<true>(a, S, X, r, false);
+  run_replica<true>(a, S, X, XB, r, false);
   if (threadIdx.x == 0) rs->overflow = 0;
 }
 
@@ -1309,12 +1429,18 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   const int32_t R = t->n_replicas;
   const size_t per_cu = R <= 256 ? 1 : R <= 512 ? 2 : R <= 768 ? 3 : 4;
   a.oc.glds = (glds <= 65536 && glds <= size_t(160 * 1024) / per_cu - 1024) ? 1 : 0;
+  // the block minima of the two-level argmin after the table, while all fits in 64 KB
+  const size_t tab = a.oc.glds ? (glds + 15) / 16 * 16 : 0;
+  const int32_t nblk = (t->n_users + 63) / 64 + 1;
+  const size_t hb = size_t(nblk) * kXBlockBytes;
+  a.oc.hblk = tab + hb <= 65536 ? nblk : 0;
+  const size_t gl_lds = tab + (a.oc.hblk ? hb : 0);
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
   hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);
   const dim3 grid(t->n_replicas), block(64);
   if (!a.global_only) launch_onchip(a, s);
-  hipLaunchKernelGGL(k_schedule_global, grid, block, a.oc.glds ? glds : 0, s, a);
+  hipLaunchKernelGGL(k_schedule_global, grid, block, gl_lds, s, a);
   return hipGetLastError();
 }
 

@@ -105,6 +105,7 @@ struct OnchipCfg {
   int32_t batch;      // literal engine: running calls kept on chip (power of two), else 0
   int32_t user_tab;   // entries (power of two) of the per-user tables for a batch of arrivals
   int32_t glds;       // global-memory kernel: 1 = its user table and counters in LDS
+  int32_t hblk;       // global-memory kernel: block minima of X kept in LDS (0: none)
   size_t lds_bytes;
 };
 

@@ -1295,6 +1295,7 @@ OnchipCfg onchip_config(int32_t R, int32_t U, bool literal) {
   }
   c.batch = batch;
   c.glds = 0;
+  c.hblk = 0;
   const size_t bat_bytes = size_t(batch) * (sizeof(Ent) + 4);
   c.users_lds = size_t(U) * 8 <= budget / 4 ? 1 : 0;
   const size_t users = c.users_lds ? size_t(U) * 8 : 0;

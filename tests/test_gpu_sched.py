@@ -401,3 +401,19 @@ def test_empty_trace_null_pointers_through_the_abi():
                                      hws.data_ptr(), hb, err.data_ptr(), S) == fs.FS_OK
     assert fs.fs_sync_status(err) == fs.FS_OK
     assert (stats.cpu().numpy() == 0).all()
+
+
+@pytest.mark.parametrize("users,multi,fcfs", [(3000, False, False), (5000, True, False),
+                                              (20000, True, False), (3000, True, True)])
+def test_global_memory_path_large_backlog(users, multi, fcfs):
+    """Thousands of users backlogged at once on the global-memory path (capacity far
+    below the offered load): the argmin reads the minima of blocks of 64 slots and one
+    block; run in one call and in chunks of steps, bit-exact against the oracle."""
+    rng = np.random.default_rng(users + 7 * multi + 3 * fcfs)
+    n = 4 * users
+    tr = random_trace(rng, n, users, 3, 20 * users, multi=multi, max_tok=30)
+    cost = rng.integers(1, 1 << 20, n).astype(np.int64)
+    say("large backlog", users, n, multi, fcfs)
+    o = oracle.simulate(tr, cost, None, 40, 200, 10 ** 9, flags=oracle.FSO_FCFS if fcfs else 0)
+    compare_sim(gpu_schedule(tr, cost, None, 40, 200, 10 ** 9, global_only=True, fcfs=fcfs), o)
+    compare_sim(gpu_schedule(tr, cost, None, 40, 200, 10 ** 9, chunks=97, fcfs=fcfs), o)

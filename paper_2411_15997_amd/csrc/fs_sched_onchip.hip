@@ -105,8 +105,10 @@ __device__ __forceinline__ T arg_at(uint32_t off) {
 #define STATE(T, field) reinterpret_cast<T *>(KARG(state) + KARG(L.field))
 
 // FCFS: first come, first served; BLIND: interaction-blind limits; LITERAL: the literal
-// engine (the engine flags).
-template <bool FCFS, bool BLIND, bool LITERAL>
+// engine (the engine flags).  LINKS: the trace has interactions of several calls (its
+// call, head and prev arrays are set); without them every request is a first call, so
+// nothing is ever a ready later call and the interaction bookkeeping compiles away.
+template <bool FCFS, bool BLIND, bool LITERAL, bool LINKS>
 __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int32_t r = blockIdx.x;
@@ -487,19 +489,19 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const size_t o_succ = KARG(L.succ), o_seg = KARG(L.seg_start), o_fate = KARG(L.fate);
     if (i < n) {
       const int64_t g = base + i;
-      const int32_t call = T.call ? T.call[g] : 0;
+      const int32_t call = LINKS ? T.call[g] : 0;
       const int32_t usr = T.user[g];
       const int64_t ts = T.ts[g];
-      const int32_t hd = T.call ? T.head[g] : i;
-      const int32_t pv = T.call ? T.prev[g] : -1;
+      const int32_t hd = LINKS ? T.head[g] : i;
+      const int32_t pv = LINKS ? T.prev[g] : -1;
       const int32_t tok = T.len_in[g] + T.len_out[g] + (T.len_sys ? T.len_sys[g] : 0);
       const int64_t cst = costp[g];
       const int32_t why = reason ? reason[g] : 0;
-      const int32_t sc = reinterpret_cast<const int32_t *>(st + o_succ)[g];
+      const int32_t sc = LINKS ? reinterpret_cast<const int32_t *>(st + o_succ)[g] : -1;
       const uint32_t sb = reinterpret_cast<const uint32_t *>(st + o_seg)[int64_t(r) * U + usr];
       const int64_t uu = ulds ? u_lds[usr] : ld_fresh(u_all + usr);
       int32_t fl = call == 0 ? kFirst : 0;
-      if (call > 0) {
+      if (LINKS && call > 0) {
         const int8_t *const fate = reinterpret_cast<const int8_t *>(st + o_fate) + base;
         const int8_t pf = ld_fresh(fate + pv), hf = ld_fresh(fate + hd);
         fl |= (pf == 0 ? kPrevAdm : 0) | ((hf == 1 || hf == 2) ? kHeadBlk : 0) |
@@ -525,7 +527,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
                      "v"(w_succ), "v"(w_seg), "v"(w_lo), "v"(w_hi), "v"(c_u));
     const int32_t lo_ = wbase + 64 - M;
     cache_lo = lo_ > cache_from ? lo_ : cache_from;
-    w_wait = __ballot(w_user >= 0 && !(w_flags & (kFirst | kPrevAdm))) != 0;
+    w_wait = LINKS && __ballot(w_user >= 0 && !(w_flags & (kFirst | kPrevAdm))) != 0;
     match_window();
   };
   auto advance_window = [&]() {
@@ -544,7 +546,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   // on-chip capacity might not suffice (the arrivals then go one at a time).
   auto arrive_batch = [&](int32_t j0, int32_t j1) -> bool {
     const bool inb = lane >= j0 && lane < j1;
-    const bool first = (w_flags & kFirst) != 0;
+    const bool first = !LINKS || (w_flags & kFirst) != 0;
     const int32_t why = (w_flags >> kReasonShift) & 3;
     const uint32_t tok = w_lo & uint32_t(kTokMask);
     bool bf = false;  // a first call throttled (over a limit while the system is overloaded)
@@ -567,7 +569,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const bool bl = inb && !first && ((w_flags & kHeadBlk) || hb_new);
     const bool blk = bf || bl;
     const uint64_t ub = __ballot(inb && !blk);
-    const uint64_t rdym = fcfs ? 0 : __ballot(inb && !blk && !first && (w_flags & kPrevAdm));
+    const uint64_t rdym =
+        (fcfs || !LINKS) ? 0 : __ballot(inb && !blk && !first && (w_flags & kPrevAdm));
     if (__ballot(inb && !blk && (w_flags & kBig)) || __popcll(ub) > kSlots - nX ||
         __popcll(rdym) > kSlots - __popcll(pocc))
       return false;
@@ -880,7 +883,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       }
       bool blocked;
       int32_t why;
-      if ((fl & kFirst) || (blind && !(fl & kPrevDrop))) {
+      if (!LINKS || (fl & kFirst) || (blind && !(fl & kPrevDrop))) {
         why = (fl >> kReasonShift) & 3;
         blocked = backlog > theta && why != 0;
       } else if (blind) {  // interaction-blind limits: an earlier call of it was dropped
@@ -903,7 +906,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         }
       } else {
         // capacity first: on overflow the state is as before this arrival
-        const bool padm = !(fl & kFirst) && (fl & kPrevAdm) && !fcfs;
+        const bool padm = LINKS && !(fl & kFirst) && (fl & kPrevAdm) && !fcfs;
         if (FS_RARE((fl & kBig) || (!fm && nX == kSlots) || (padm && pocc == ~uint64_t(0)))) {
           overflow = true;
           break;
@@ -913,7 +916,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         const uint32_t lo = rdlu(w_lo, j), hi = rdlu(w_hi, j);
         const int32_t sc = rdl(w_succ, j);
         if (lane == x) ++xq;
-        if ((fl & kFirst) || fcfs)
+        if (!LINKS || (fl & kFirst) || fcfs)
           fifo_push(x, rec, sc, lo, hi);
         else if (padm)
           ready_add(x, rec, sc, lo, hi);
@@ -944,13 +947,13 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
           const uint32_t mv = wave_min32v(k32);
           cand = k32 == mv;
           const uint32_t m = uint32_t(uni(int32_t(mv)));
-          tier0 = m < kRelTier1;
+          tier0 = LINKS && m < kRelTier1;
           uk = B + int64_t(m & kRelMax);
         } else {
           const uint32_t mh = wave_min32(kh);
           const uint32_t ml = wave_min32(kh == mh ? kl : 0xffffffffu);
           cand = kh == mh && kl == ml;
-          tier0 = mh < kTier1;
+          tier0 = LINKS && mh < kTier1;
           uk = int64_t((uint64_t(mh & kValHi) << 32) | ml);
         }
         const uint64_t eq = __ballot(cand);
@@ -980,7 +983,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         lo = rdlu(hlo, x);
         hi = rdlu(hhi, x);
       }
-      bool sc_now = !fcfs && sc >= 0 && sc < nxt;  // its next call already arrived
+      bool sc_now = LINKS && !fcfs && sc >= 0 && sc < nxt;  // its next call already arrived
       if (blind && sc_now) {  // interaction-blind limits may have dropped it
         if (sc >= cache_lo)
           sc_now = uni(cache[sc & (M - 1)].rec) >= 0;  // a dropped arrival's entry is marked
@@ -1033,7 +1036,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         kv_used += tok;
       }
       if (FS_RARE(++nd == 64)) flush_decisions();
-      if (w_wait) w_flags |= (w_prev == rec) ? kPrevAdm : 0;
+      if (LINKS && w_wait) w_flags |= (w_prev == rec) ? kPrevAdm : 0;
       const int32_t q = rdl(xq, x) - 1;
       if (tier0) {
         pocc &= ~(uint64_t(1) << l);
@@ -1082,9 +1085,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
         const uint32_t rv = rel_of(unew);
         if (lane == x) {
           --xq;
-          kh = uint32_t(uint64_t(unew) >> 32) | (xn > 0 ? 0u : kTier1);
+          kh = uint32_t(uint64_t(unew) >> 32) | ((LINKS && xn > 0) ? 0u : kTier1);
           kl = uint32_t(uint64_t(unew));
-          k32 = (xn > 0 ? 0u : kRelTier1) | rv;
+          k32 = ((LINKS && xn > 0) ? 0u : kRelTier1) | rv;
         }
       }
     }
@@ -1317,13 +1320,19 @@ OnchipCfg onchip_config(int32_t R, int32_t U, bool literal) {
   return c;
 }
 
-template <bool FCFS, bool BLIND, bool LITERAL>
-void launch_mode(const SchedArgs &a, hipStream_t s) {
-  const void *k = reinterpret_cast<const void *>(&k_schedule_onchip<FCFS, BLIND, LITERAL>);
+template <bool FCFS, bool BLIND, bool LITERAL, bool LINKS>
+void launch_links(const SchedArgs &a, hipStream_t s) {
+  const void *k = reinterpret_cast<const void *>(&k_schedule_onchip<FCFS, BLIND, LITERAL, LINKS>);
   if (a.oc.lds_bytes > 65536)
     (void)hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(a.oc.lds_bytes));
-  hipLaunchKernelGGL((k_schedule_onchip<FCFS, BLIND, LITERAL>), dim3(a.t.R), dim3(64),
+  hipLaunchKernelGGL((k_schedule_onchip<FCFS, BLIND, LITERAL, LINKS>), dim3(a.t.R), dim3(64),
                      a.oc.lds_bytes, s, a);
+}
+
+template <bool FCFS, bool BLIND, bool LITERAL>
+void launch_mode(const SchedArgs &a, hipStream_t s) {
+  a.t.call ? launch_links<FCFS, BLIND, LITERAL, true>(a, s)
+           : launch_links<FCFS, BLIND, LITERAL, false>(a, s);
 }
 
 template <bool LITERAL>

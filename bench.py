@@ -45,12 +45,12 @@ STAGE_SRC = {
 # the stage's sources hash to `src`.
 MEASURED_TRAFFIC = {
     # k_schedule_onchip on the 1,024-replica weight sweep (20.48M requests)
-    ("c4_sweep", "schedule"): {"src": "e54b779cc0911a8b", "fetch_kib": 353983.4375,
-                               "write_kib": 137776.03125, "fetch_factor": 1.99988,
+    ("c4_sweep", "schedule"): {"src": "f432eead15f31ddb", "fetch_kib": 313230.9375,
+                               "write_kib": 137670.5625, "fetch_factor": 1.99992,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
-    ("c3_throttle", "throttle"): {"src": "e7d650dbb7b01d78", "fetch_kib": 2711800.6875,
-                                  "write_kib": 2219110.96875, "fetch_factor": 1.99993,
+    ("c3_throttle", "throttle"): {"src": "d1d4af8cbaffee13", "fetch_kib": 1458943.5625,
+                                  "write_kib": 1522346.75, "fetch_factor": 1.99992,
                                   "write_factor": 1.0},
 }
 

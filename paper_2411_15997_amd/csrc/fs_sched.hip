@@ -144,13 +144,22 @@ struct XMem {
   __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
     uint64_t kk = kEmptyKey;
     uint32_t us = 0xffffffffu, bx = 0xffffffffu;
-    for (int32_t x = threadIdx.x; x < nX; x += 64) {
-      const uint64_t a = ld_fresh(k + x);
-      const uint32_t b = uint32_t(ld_fresh(user + x));
-      const bool take = a < kk || (a == kk && b < us);
-      kk = take ? a : kk;
-      us = take ? b : us;
-      bx = take ? uint32_t(x) : bx;
+    for (int32_t x0 = threadIdx.x; x0 < nX; x0 += 256) {  // four slots a lane, loads together
+      uint64_t a[4];
+      uint32_t b[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int32_t x = x0 + 64 * j;
+        a[j] = x < nX ? ld_fresh(k + x) : kEmptyKey;
+        b[j] = x < nX ? uint32_t(ld_fresh(user + x)) : 0xffffffffu;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool take = a[j] < kk || (a[j] == kk && b[j] < us);
+        kk = take ? a[j] : kk;
+        us = take ? b[j] : us;
+        bx = take ? uint32_t(x0 + 64 * j) : bx;
+      }
     }
     wave_argmin(kk, us, bx);
     bk = uint64_t(rdl64(int64_t(kk), 63));
@@ -159,10 +168,19 @@ struct XMem {
   }
   __device__ void minmax(int32_t nX, int64_t &mn, int64_t &mx) const {
     uint64_t lo = kEmptyKey, hi = 0;
-    for (int32_t x = threadIdx.x; x < nX; x += 64) {
-      const uint64_t v = ld_fresh(k + x) & kValMask;
-      lo = v < lo ? v : lo;
-      hi = v > hi ? v : hi;
+    for (int32_t x0 = threadIdx.x; x0 < nX; x0 += 256) {
+      uint64_t v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int32_t x = x0 + 64 * j;
+        v[j] = x < nX ? ld_fresh(k + x) & kValMask : kEmptyKey;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int32_t x = x0 + 64 * j;
+        lo = v[j] < lo ? v[j] : lo;
+        hi = x < nX && v[j] > hi ? v[j] : hi;
+      }
     }
     wave_minmax(lo, hi);
     mn = rdl64(int64_t(lo), 63);
@@ -237,13 +255,22 @@ struct XLds {
   __device__ int32_t argmin(int32_t nX, uint64_t &bk, int32_t &bu) const {
     uint64_t kk = kEmptyKey;
     uint32_t us = 0xffffffffu, bx = 0xffffffffu;
-    for (int32_t x = threadIdx.x; x < nX; x += 64) {
-      const uint64_t a = k[x];
-      const uint32_t b = uint32_t(user[x]);
-      const bool take = a < kk || (a == kk && b < us);
-      kk = take ? a : kk;
-      us = take ? b : us;
-      bx = take ? uint32_t(x) : bx;
+    for (int32_t x0 = threadIdx.x; x0 < nX; x0 += 256) {  // four slots a lane, loads together
+      uint64_t a[4];
+      uint32_t b[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int32_t x = x0 + 64 * j;
+        a[j] = x < nX ? k[x] : kEmptyKey;
+        b[j] = x < nX ? uint32_t(user[x]) : 0xffffffffu;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool take = a[j] < kk || (a[j] == kk && b[j] < us);
+        kk = take ? a[j] : kk;
+        us = take ? b[j] : us;
+        bx = take ? uint32_t(x0 + 64 * j) : bx;
+      }
     }
     wave_argmin(kk, us, bx);
     bk = uint64_t(rdl64(int64_t(kk), 63));
@@ -252,10 +279,19 @@ struct XLds {
   }
   __device__ void minmax(int32_t nX, int64_t &mn, int64_t &mx) const {
     uint64_t lo = kEmptyKey, hi = 0;
-    for (int32_t x = threadIdx.x; x < nX; x += 64) {
-      const uint64_t v = k[x] & kValMask;
-      lo = v < lo ? v : lo;
-      hi = v > hi ? v : hi;
+    for (int32_t x0 = threadIdx.x; x0 < nX; x0 += 256) {
+      uint64_t v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int32_t x = x0 + 64 * j;
+        v[j] = x < nX ? k[x] & kValMask : kEmptyKey;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int32_t x = x0 + 64 * j;
+        lo = v[j] < lo ? v[j] : lo;
+        hi = x < nX && v[j] > hi ? v[j] : hi;
+      }
     }
     wave_minmax(lo, hi);
     mn = rdl64(int64_t(lo), 63);
@@ -264,16 +300,18 @@ struct XLds {
 };
 constexpr size_t kXLdsBytesPerUser = 8 + 8 + 10 * 4;  // counter, key, nine fields and xs
 
-// Per block of 64 X slots, in LDS: the least (key, user), and the least and largest
-// counter.  The argmin then reads the block minima and one block, and the gap sample
-// the block extremes, instead of every slot.  Kept while more than 64 users are
-// backlogged (and their blocks fit, cap); rebuilt from X when that starts.
+// Per block of 64 X slots, in LDS: the least (key, user).  The argmin then reads the
+// block minima and one block instead of every slot.  Kept while many users are
+// backlogged (more than kHierOn; dropped at kHierOff or fewer, and while their blocks
+// fit, cap); rebuilt from X when that starts.  Below that a flat scan of X, four slots
+// a lane with their loads issued together, costs less than keeping the minima.
 struct XBlocks {
-  uint64_t *k, *umin, *umax;
+  uint64_t *k;
   uint32_t *u;
   int32_t cap;  // blocks that fit (0: single-level scans only)
 };
-constexpr size_t kXBlockBytes = 8 + 8 + 8 + 4;
+constexpr size_t kXBlockBytes = 8 + 4;
+constexpr int32_t kHierOn = 512, kHierOff = 256;
 
 // ---------------------------------------------------------------------------
 // The scheduler body.  All control flow is wave-uniform; the arrival window holds
@@ -281,8 +319,10 @@ constexpr size_t kXBlockBytes = 8 + 8 + 8 + 4;
 // with one store per field for up to 64 records: arrival outcomes by window lane,
 // admissions by admission order.
 // ---------------------------------------------------------------------------
+// Inlined into the kernel for each table kind: as a called function its argument
+// structs would live in scratch memory and every field read would go through it.
 template <bool G, class XT>
-__device__ void run_replica(const SchedArgs &a, Store &S, XT &X, const XBlocks &XB, int32_t r,
+__device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X, const XBlocks &XB, int32_t r,
                             bool onchip) {
   const int lane = threadIdx.x;
   const DevTrace &t = a.t;
@@ -335,23 +375,19 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, const XBlocks &
 
   // ---- two-level argmin over X (block minima of 64 slots) while nX > 64
   bool hier = false;
-  auto blk_set = [&](int32_t b) {  // block b's least (key, user) and counter range
+  auto blk_set = [&](int32_t b) {  // block b's least (key, user)
     const int32_t sx = b * 64 + lane;
-    uint64_t kk = kEmptyKey, lo = kEmptyKey, hi = 0;
+    uint64_t kk = kEmptyKey;
     uint32_t us = 0xffffffffu, bx = 0xffffffffu;
     if (sx < nX) {
       kk = X.key_at(sx);
       us = X.user_at(sx);
       bx = uint32_t(sx);
-      lo = hi = kk & kValMask;
     }
     wave_argmin(kk, us, bx);
-    wave_minmax(lo, hi);
     if (lane == 63) {
       XB.k[b] = kk;
       XB.u[b] = us;
-      XB.umin[b] = lo;
-      XB.umax[b] = hi;
     }
   };
   auto blk_touch = [&](int32_t x) {  // slot x changed (key, or moved / freed)
@@ -360,12 +396,12 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, const XBlocks &
     blk_set(x >> 6);
   };
   auto blk_sync = [&]() {  // nX changed: start or stop keeping the block minima
-    const bool want = nX > 64 && ((nX + 63) >> 6) <= XB.cap;
-    if (want && !hier) {
+    const bool fits = ((nX + 63) >> 6) <= XB.cap;
+    if (!hier && nX > kHierOn && fits) {
       hier = true;
       wave_fence();
       for (int32_t b = 0; b * 64 < nX; ++b) blk_set(b);
-    } else if (!want) {
+    } else if (hier && (nX <= kHierOff || !fits)) {
       hier = false;
     }
   };
@@ -399,23 +435,8 @@ __device__ void run_replica(const SchedArgs &a, Store &S, XT &X, const XBlocks &
     bu = rdl(int32_t(u2), 63);
     return rdl(int32_t(x2), 63);
   };
-  // least and largest counter among the backlogged users (nX > 0)
-  auto minmax_x = [&](int64_t &mn, int64_t &mx) {
-    if (!hier) {
-      X.minmax(nX, mn, mx);
-      return;
-    }
-    wave_fence();
-    uint64_t lo = kEmptyKey, hi = 0;
-    for (int32_t b = lane; b * 64 < nX; b += 64) {
-      const uint64_t l = XB.umin[b], h = XB.umax[b];
-      lo = l < lo ? l : lo;
-      hi = h > hi ? h : hi;
-    }
-    wave_minmax(lo, hi);
-    mn = rdl64(int64_t(lo), 63);
-    mx = rdl64(int64_t(hi), 63);
-  };
+  // least and largest counter among the backlogged users (nX > 0; once a step)
+  auto minmax_x = [&](int64_t &mn, int64_t &mx) { X.minmax(nX, mn, mx); };
   auto set_key = [&](int32_t x, int64_t uval) {
     X.set_key(x, (uint64_t(X.get_rdy(x) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval));
     blk_touch(x);
@@ -1167,9 +1188,7 @@ __global__ void __launch_bounds__(64) k_schedule_global(SchedArgs a) {
     const int32_t nb = a.oc.hblk > 0 ? a.oc.hblk : 0;
     XB.cap = a.oc.hblk;
     XB.k = reinterpret_cast<uint64_t *>(b);
-    XB.umin = XB.k + nb;
-    XB.umax = XB.umin + nb;
-    XB.u = reinterpret_cast<uint32_t *>(XB.umax + nb);
+    XB.u = reinterpret_cast<uint32_t *>(XB.k + nb);
   }
   if (a.oc.glds) {  // the table and the counters in LDS
     const int32_t U = a.t.U;

@@ -328,6 +328,219 @@ __global__ void __launch_bounds__(kThreads) k_ws_users(WsArgs a, int64_t RU) {
   }
 }
 
+// One work-group per replica when the replica's (user, app) table fits in LDS (and
+// there are replicas enough to fill the chip): records, interaction sizes, graph rows
+// and rate bins of the replica in one kernel, every accumulation an LDS atomic (the
+// graph rows aggregated per wave first: almost every request adds to the same row),
+// and every output of the replica written once with plain stores.  Three passes over
+// the replica's records: the tables and the later calls' counts at their first calls;
+// the interaction sizes into the size histogram and graph rows; the users' totals
+// and rate bins from the table.
+constexpr int kRepThreads = 1024;
+constexpr int32_t kRepMin = 256;                 // replicas for the per-replica kernel (a CU each)
+constexpr size_t kRepLdsMax = 150 * 1024;        // its LDS, at most
+
+struct RepLds {  // byte offsets into the dynamic LDS of k_ws_replica
+  size_t tok, ls, gr, red, req, lh, sh, rate, total;
+};
+
+__host__ __device__ inline RepLds rep_lds(int32_t U, int32_t A) {
+  RepLds L;
+  const size_t ua = size_t(U) * size_t(A);
+  size_t o = 0;
+  L.tok = o;  o += ua * 8;                                 // tokens per (user, app)
+  L.ls = o;   o += size_t(A) * 3 * 8;                      // length sums [A][3]
+  L.gr = o;   o += size_t(kGraphBins) * 5 * 8;             // Table 2 rows
+  L.red = o;  o += size_t(kRepThreads / 64) * 8;           // per-wave maxima
+  L.req = o;  o += ua * 4;                                 // requests per (user, app)
+  L.lh = o;   o += size_t(A) * 3 * kLenBins * 4;           // length histograms
+  L.sh = o;   o += size_t(A) * kSizeBins * 4;              // size histogram
+  L.rate = o; o += size_t(A + 1) * 2 * kRateBins * 4;      // rate histograms
+  L.total = (o + 15) / 16 * 16;
+  return L;
+}
+
+__device__ inline unsigned long long wmax64(unsigned long long v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const unsigned long long o = (unsigned long long)__shfl_xor((long long)v, m, 64);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+__global__ void __launch_bounds__(kRepThreads) k_ws_replica(WsArgs a) {
+  extern __shared__ __align__(16) unsigned char dsm[];
+  const DevTrace &t = a.t;
+  const int32_t r = blockIdx.x, U = t.U, A = t.A;
+  const RepLds L = rep_lds(U, A);
+  unsigned long long *const tok = reinterpret_cast<unsigned long long *>(dsm + L.tok);
+  unsigned long long *const ls = reinterpret_cast<unsigned long long *>(dsm + L.ls);
+  unsigned long long *const gr = reinterpret_cast<unsigned long long *>(dsm + L.gr);
+  unsigned long long *const red = reinterpret_cast<unsigned long long *>(dsm + L.red);
+  uint32_t *const req = reinterpret_cast<uint32_t *>(dsm + L.req);
+  uint32_t *const lh = reinterpret_cast<uint32_t *>(dsm + L.lh);
+  uint32_t *const sh = reinterpret_cast<uint32_t *>(dsm + L.sh);
+  uint32_t *const rate = reinterpret_cast<uint32_t *>(dsm + L.rate);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t UA = int64_t(U) * A;
+  for (int64_t k = tid; k < UA; k += kRepThreads) {
+    tok[k] = 0;
+    req[k] = 0;
+  }
+  for (int k = tid; k < A * 3; k += kRepThreads) ls[k] = 0;
+  for (int k = tid; k < kGraphBins * 5; k += kRepThreads) gr[k] = 0;
+  for (int k = tid; k < A * 3 * kLenBins; k += kRepThreads) lh[k] = 0;
+  for (int k = tid; k < A * kSizeBins; k += kRepThreads) sh[k] = 0;
+  for (int k = tid; k < (A + 1) * 2 * kRateBins; k += kRepThreads) rate[k] = 0;
+  const int64_t base = t.rep_off[r], n = t.rep_off[r + 1] - base;
+  if (t.call)  // an interaction's size starts at one for its first call
+    for (int64_t i = tid; i < n; i += kRepThreads) a.size[base + i] = t.call[base + i] != 0 ? 0u : 1u;
+  __syncthreads();
+
+  // pass 1: the (user, app) table, length histograms and sums, latest arrival, and one
+  // count at the first call of each later call (the checks of k_ws_records)
+  int32_t code = 0;
+  unsigned long long mts = 0;
+  bool any = false;
+  for (int64_t i0 = tid; i0 < n; i0 += 2 * kRepThreads) {  // two records a thread, loads together
+    int32_t u[2], ap[2];
+    int64_t ts[2], Lx[2][3], h[2];
+    bool ok[2], first[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int64_t i = i0 + j * kRepThreads, g = base + i;
+      ok[j] = i < n;
+      u[j] = ok[j] ? t.user[g] : 0;
+      ap[j] = ok[j] ? t.app[g] : 0;
+      ts[j] = ok[j] ? t.ts[g] : 0;
+      Lx[j][0] = ok[j] ? t.len_in[g] : 0;
+      Lx[j][1] = (ok[j] && t.len_sys) ? t.len_sys[g] : 0;
+      Lx[j][2] = ok[j] ? t.len_out[g] : 0;
+      first[j] = !(ok[j] && t.call && t.call[g] != 0);
+      h[j] = first[j] ? i : int64_t(t.head[g]);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int64_t i = i0 + j * kRepThreads;
+      if (i >= n) continue;
+      bool v = u[j] >= 0 && u[j] < U && ap[j] >= 0 && ap[j] < A && ts[j] >= 0 &&
+               len_ok(int32_t(Lx[j][0])) && len_ok(int32_t(Lx[j][1])) && len_ok(int32_t(Lx[j][2]));
+      if (v && !first[j]) v = h[j] >= 0 && h[j] < i;
+      if (!v) {
+        code = FS_E_RANGE;
+        continue;
+      }
+      mts = (unsigned long long)ts[j] > mts ? (unsigned long long)ts[j] : mts;
+      any = true;
+      const int64_t k = int64_t(u[j]) * A + ap[j];
+      atomicAdd(&req[k], 1u);
+      atomicAdd(&tok[k], (unsigned long long)(Lx[j][0] + Lx[j][1] + Lx[j][2]));
+#pragma unroll
+      for (int x = 0; x < 3; ++x) {
+        atomicAdd(&lh[(ap[j] * 3 + x) * kLenBins + len_bin(Lx[j][x])], 1u);
+        if (Lx[j][x]) atomicAdd(&ls[ap[j] * 3 + x], (unsigned long long)Lx[j][x]);
+      }
+      if (!first[j]) atomicAdd(a.size + base + h[j], 1u);
+    }
+  }
+  mts = wmax64(mts);
+  if (lane == 0) red[wave] = (__ballot(any) != 0) ? mts + 1 : 0;  // 0: no valid request
+  __syncthreads();
+  unsigned long long mx = 0;
+  for (int w = 0; w < kRepThreads / 64; ++w) mx = red[w] > mx ? red[w] : mx;
+  const uint64_t M = n > 0 ? (mx ? mx - 1 : 0) / uint64_t(a.minute_us) + 1 : 0;
+
+  // pass 2: sizes into the size histogram (first calls) and the graph rows (every
+  // request, by its interaction's size; the checks of k_ws_graph)
+  for (int64_t i0 = 0; i0 < n; i0 += kRepThreads) {
+    const int64_t i = i0 + tid, g = base + i;
+    bool ok = i < n;
+    bool first = true;
+    int32_t ap = 0;
+    uint32_t sz = 0;
+    unsigned long long l0 = 0, l1 = 0, l2 = 0;
+    if (ok) {
+      const int32_t uu = t.user[g];
+      ap = t.app[g];
+      first = first_of(t, g);
+      const int64_t hh = first ? i : int64_t(t.head[g]);
+      ok = uu >= 0 && uu < U && ap >= 0 && ap < A && hh >= 0 && (first ? hh == i : hh < i);
+      if (ok) {
+        // (written by this work-group's atomics: read past the L1 cache)
+        sz = t.call ? __hip_atomic_load(a.size + base + hh, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                    : 1u;
+        l0 = (unsigned long long)t.len_in[g];
+        l1 = (unsigned long long)t.len_out[g];
+        l2 = t.len_sys ? (unsigned long long)t.len_sys[g] : 0ull;
+        if (first && sz > 0) atomicAdd(&sh[ap * kSizeBins + (sz < kSizeBins ? int(sz) : kSizeBins) - 1], 1u);
+      }
+    }
+    // graph rows: per distinct bin among the wave's lanes, one add per field
+    const int b = graph_bin(sz);
+    uint64_t pending = __ballot(ok);
+    while (pending) {
+      const int bl = __shfl(b, __ffsll((long long)pending) - 1, 64);
+      const bool mine = ok && b == bl;
+      const uint64_t mm = __ballot(mine);
+      const unsigned long long nf = __popcll(__ballot(mine && first));
+      const unsigned long long nr = __popcll(mm);
+      const unsigned long long s0 = wsum64(mine ? l0 : 0ull), s1 = wsum64(mine ? l1 : 0ull),
+                               s2 = wsum64(mine ? l2 : 0ull);
+      if (lane == 0) {
+        unsigned long long *row = gr + bl * 5;
+        if (nf) atomicAdd(row, nf);
+        atomicAdd(row + 1, nr);
+        if (s0) atomicAdd(row + 2, s0);
+        if (s1) atomicAdd(row + 3, s1);
+        if (s2) atomicAdd(row + 4, s2);
+      }
+      pending &= ~mm;
+    }
+  }
+  __syncthreads();
+
+  // pass 3: the table's entries (per-app rate bins) and each user's totals
+  const int64_t ro = int64_t(r) * UA;
+  for (int64_t k = tid; k < UA; k += kRepThreads) {
+    const uint32_t nq = req[k];
+    const unsigned long long tk = tok[k];
+    if (a.o.user_app_req) a.o.user_app_req[ro + k] = int64_t(nq);
+    if (a.o.user_app_tok) a.o.user_app_tok[ro + k] = int64_t(tk);
+    if (nq > 0) {
+      const int ap = int(k % A);
+      atomicAdd(&rate[(ap * 2) * kRateBins + rate_bin(nq, M)], 1u);
+      atomicAdd(&rate[(ap * 2 + 1) * kRateBins + rate_bin(tk, M)], 1u);
+    }
+  }
+  for (int32_t u = tid; u < U; u += kRepThreads) {
+    unsigned long long nq = 0, nt = 0;
+    for (int32_t ap = 0; ap < A; ++ap) {
+      nq += req[int64_t(u) * A + ap];
+      nt += tok[int64_t(u) * A + ap];
+    }
+    a.o.user_req[int64_t(r) * U + u] = int64_t(nq);
+    a.o.user_tok[int64_t(r) * U + u] = int64_t(nt);
+    if (nq > 0) {
+      atomicAdd(&rate[(A * 2) * kRateBins + rate_bin(nq, M)], 1u);
+      atomicAdd(&rate[(A * 2 + 1) * kRateBins + rate_bin(nt, M)], 1u);
+    }
+  }
+  __syncthreads();
+  // the replica's histograms and sums, written once
+  if (tid == 0) a.o.minutes[r] = int64_t(M);
+  for (int k = tid; k < (A + 1) * 2 * kRateBins; k += kRepThreads)
+    a.o.rate_hist[int64_t(r) * (A + 1) * 2 * kRateBins + k] = int64_t(rate[k]);
+  for (int k = tid; k < A * 3 * kLenBins; k += kRepThreads)
+    a.o.len_hist[int64_t(r) * A * 3 * kLenBins + k] = int64_t(lh[k]);
+  for (int k = tid; k < A * 3; k += kRepThreads) a.o.len_sum[int64_t(r) * A * 3 + k] = int64_t(ls[k]);
+  for (int k = tid; k < A * kSizeBins; k += kRepThreads)
+    a.o.size_hist[int64_t(r) * A * kSizeBins + k] = int64_t(sh[k]);
+  for (int k = tid; k < kGraphBins * 5; k += kRepThreads)
+    a.o.graph[int64_t(r) * kGraphBins * 5 + k] = int64_t(gr[k]);
+  if (code) raise_err(a.err, code);
+}
+
 int grid_for(int64_t n) {
   int64_t b = (n + kThreads - 1) / kThreads;
   if (b < 1) b = 1;
@@ -375,6 +588,21 @@ hipError_t launch_workload(const fs_trace *t, int64_t minute_us, const fs_wstats
   a.err = err;
   const int64_t RU = int64_t(t->n_replicas) * t->n_users, RUA = RU * t->n_apps;
   const int64_t N = a.t.N;
+  // one work-group per replica when its table fits in LDS and replicas fill the chip
+  const RepLds RL = rep_lds(t->n_users, t->n_apps);
+  int64_t most_n = 0;
+  for (int32_t r = 0; r < t->n_replicas; ++r)
+    most_n = std::max<int64_t>(most_n, t->rep_off_h[r + 1] - t->rep_off_h[r]);
+  if (t->n_replicas >= kRepMin && RL.total <= kRepLdsMax && most_n < (int64_t(1) << 31)) {
+    if (RL.total > 65536) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k_ws_replica),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               int(RL.total));
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_ws_replica, dim3(t->n_replicas), dim3(kRepThreads), RL.total, s, a);
+    return hipGetLastError();
+  }
   const int64_t most = std::max<int64_t>(std::max<int64_t>(RUA, N),
                                          int64_t(t->n_replicas) * (t->n_apps + 1) * 2 * kRateBins);
   hipLaunchKernelGGL(k_ws_zero, dim3(grid_for(most)), dim3(kThreads), 0, s, a, RUA, RU);

@@ -52,8 +52,43 @@ def test_random_traces(seed):
     _compare(tr, minute=int(rng.choice([1, 1000, 60_000])), per_app=bool(seed % 2))
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_random_many_replicas(seed):
+    """256 or more replicas whose (user, app) tables fit in LDS: one work-group per
+    replica does every accumulation (empty and one-request replicas, interactions or
+    none, system tokens or none, tables from a few entries to about 9,000)."""
+    rng = np.random.default_rng(950 + seed)
+    R = int(rng.integers(256, 300))
+    U = int(rng.choice([1, 7, 300, 1100]))
+    A = int(rng.integers(1, 9))
+    multi = bool(seed % 2)
+    parts = [random_trace(rng, int(rng.choice([0, 1, 20, 300])), U, A,
+                          int(rng.integers(1, 10 ** 6)), multi=multi,
+                          max_tok=int(rng.choice([0, 3, 5000]))) for _ in range(R)]
+    tr = tg.concat(parts)
+    if seed % 3 == 0:
+        tr = tg.Trace(**{**tr.__dict__, "len_sys": None})
+    say("workload stats many replicas", seed, tr.n_replicas, tr.n_users, tr.n_apps, tr.n)
+    _compare(tr, minute=int(rng.choice([1, 1000, 60_000])), per_app=bool(seed % 2))
+
+
+def test_errors_many_replicas():
+    rng = np.random.default_rng(5)
+    tr = random_trace(rng, 40, 6, 3, 1000, multi=True, n_replicas=260)
+    bad = tg.Trace(**{**tr.__dict__, "user": tr.user.copy(), "head": tr.head.copy()})
+    bad.user[int(tr.rep_off[17]) + 3] = 6
+    later = np.nonzero(tr.call[int(tr.rep_off[30]):int(tr.rep_off[31])] > 0)[0]
+    if later.size:
+        bad.head[int(tr.rep_off[30]) + int(later[0])] = int(later[0]) + 1  # ahead of itself
+    with pytest.raises(oracle.OracleError) as oe:
+        oracle.workload_stats(bad)
+    with pytest.raises(fs.FairServeError) as ge:
+        fs.fs_workload_stats(fs.DeviceTrace(bad))
+    assert ge.value.code == oe.value.code == fs.FS_E_RANGE
+
+
 @pytest.mark.parametrize("name,kw", [("c1_small", {}), ("c2_replicas", dict(replicas=5, records=20000)),
-                                     ("c4_sweep", dict(replicas=40)),
+                                     ("c4_sweep", dict(replicas=40)), ("c4_sweep", dict(replicas=300)),
                                      ("c5_tenant", dict(records=200_003, users=30_000))])
 def test_workload_recipes(name, kw):
     wl, tr = workload_trace(name, **kw)

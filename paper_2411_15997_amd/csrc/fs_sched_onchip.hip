@@ -820,6 +820,126 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   }
   if (nxt < n) load_window();
 
+  // Admissions of a step taken together (traces without interactions, counters the
+  // decisions move, least-counter choice, relative keys in use).  Every backlogged user's
+  // FIFO head is a candidate; in the order of (key, user id) they are the step's
+  // admissions until the budget runs out, as long as no user admitted earlier in that
+  // order comes back (with its next request, at its charged counter) ahead of the next
+  // candidate.  Each user's rank and the tokens ranked before it come from one pass over
+  // the occupied lanes; the users that stay give the first rank their return would
+  // pre-empt; the ranks before the least of those are admitted lane-parallel.  Returns
+  // the number admitted; the sequential loop takes the rest of the step.
+  auto batch_admit = [&](int64_t &budget) -> int32_t {
+    const bool oc = xu >= 0;
+    const uint64_t lt_l = (uint64_t(1) << lane) - 1;
+    const uint64_t key = oc ? ((uint64_t(k32) << 32) | uint32_t(xu)) : ~uint64_t(0);
+    const uint32_t tok = hlo & uint32_t(kTokMask);
+    uint32_t rank = 0, pre = 0;
+    for (uint64_t om = occ; om; om &= om - 1) {
+      const int32_t j = ff1(om);
+      const uint64_t kj = (uint64_t(rdlu(uint32_t(key >> 32), j)) << 32) | rdlu(uint32_t(key), j);
+      const bool lt = kj < key;
+      rank += lt ? 1u : 0u;
+      pre += lt ? rdlu(tok, j) : 0u;
+    }
+    const bool adm = oc && int64_t(pre) < budget;  // the budget is positive before it
+    const int64_t uk = B + int64_t(k32 & kRelMax);
+    const int64_t unew = uk + int64_t(((uint64_t(hhi) << 32) | hlo) >> 24);
+    const bool stay = adm && xq > 1;
+    const int64_t d = unew - B;
+    const bool nsat = d < 0 || d >= int64_t(kRelMax);
+    const uint32_t nk = kRelTier1 | (nsat ? kRelMax : uint32_t(d));
+    uint32_t cut = uint32_t(64 - nd);  // room left in the output staging
+    for (uint64_t sm = __ballot(stay); sm; sm &= sm - 1) {
+      const int32_t j = ff1(sm);
+      uint32_t cj = rdlu(rank, j) + 1;  // (a saturated return: stop after it, full keys follow)
+      if (!rdlu(uint32_t(nsat), j)) {
+        const uint64_t nkj = (uint64_t(rdlu(nk, j)) << 32) | rdlu(uint32_t(xu), j);
+        const uint32_t cnt = uint32_t(__popcll(__ballot(oc && key < nkj)));
+        cj = cnt > cj ? cnt : cj;
+      }
+      cut = cj < cut ? cj : cut;
+    }
+    const bool fin = adm && rank < cut;
+    const uint64_t fm = __ballot(fin);
+    if (!fm || __ballot(fin && unew >= kValueLimit)) return 0;
+    const int32_t m = __popcll(fm);
+    // lane of each rank (occupied lanes by rank, free lanes after them)
+    const uint32_t dst = oc ? rank : uint32_t(nX + __popcll(~occ & lt_l));
+    const int32_t inv = __builtin_amdgcn_ds_permute(int(dst << 2), lane);
+    // outputs, in admission order, into staging lanes nd .. nd + m - 1
+    const bool st = lane >= nd && lane < nd + m;
+    const int32_t src = __builtin_amdgcn_ds_bpermute((st ? lane - nd : lane) << 2, inv);
+    const int32_t o_rec = __builtin_amdgcn_ds_bpermute(src << 2, hrec);
+    const uint32_t o_lo = uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(uint32_t(unew))));
+    const uint32_t o_hi = uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(uint32_t(uint64_t(unew) >> 32))));
+    if (st) {
+      d_rec = o_rec;
+      d_step = s;
+      d_cnt = int64_t((uint64_t(o_hi) << 32) | o_lo);
+    }
+    const int32_t lastl = rdl(inv, m - 1);  // the last admitted
+    const uint32_t used = rdlu(pre + tok, lastl);
+    budget -= int64_t(used);
+    backlog -= int64_t(used);
+    seq += m;
+    nd += m;
+    // users that leave Q: the last one in admission order is e; counters back to u;
+    // window lanes of those users (w_slot is the slot of a lane's user) take the counter
+    const bool lv = fin && xq == 1;
+    const uint64_t lm = __ballot(lv);
+    if (lm) {
+      int32_t r = m - 1, ll = lastl;
+      while (!((lm >> ll) & 1)) ll = rdl(inv, --r);
+      last_exit = rdl(xu, ll);
+      last_exit_u = rdl64(unew, ll);
+      if (lv) {
+        if (ulds)
+          u_lds[xu] = unew;
+        else
+          u_all[xu] = unew;
+      }
+      const bool wh = w_slot >= 0 && ((lm >> (w_slot & 63)) & 1);
+      const int wsrc = (w_slot >= 0 ? w_slot : lane) << 2;
+      const uint32_t wl = uint32_t(__builtin_amdgcn_ds_bpermute(wsrc, int(uint32_t(unew))));
+      const uint32_t wh32 = uint32_t(__builtin_amdgcn_ds_bpermute(wsrc, int(uint32_t(uint64_t(unew) >> 32))));
+      if (wh) {
+        c_u = int64_t((uint64_t(wh32) << 32) | wl);
+        w_slot = -1;
+      }
+      occ &= ~lm;
+      nX -= __popcll(lm);
+    }
+    // users that stay: the next head of the FIFO (refilled from the segment first when
+    // its on-chip part is used up) and the key at the charged counter
+    if (fin) {
+      ++xf;
+      --xq;
+    }
+    for (uint64_t rm = __ballot(stay && fin && xf == xr && xr < xt); rm; rm &= rm - 1)
+      fifo_refill(ff1(rm));
+    if (stay && fin) {
+      if (xf < xt) {
+        const Ent v = ring[lane * D + (xf & (D - 1))];
+        hrec = v.rec;
+        hsucc = v.succ;
+        hlo = v.lo;
+        hhi = v.hi;
+      }
+      kh = uint32_t(uint64_t(unew) >> 32) | kTier1;
+      kl = uint32_t(uint64_t(unew));
+      k32 = nk;
+    }
+    if (__ballot(stay && fin && nsat)) wide = true;
+    if (lv) {
+      kh = kl = k32 = 0xffffffffu;
+      xu = -1;
+      xq = 0;
+    }
+    if (FS_RARE(nd == 64)) flush_decisions();
+    return m;
+  };
+
   // ---- steps
   while (true) {
     if (s >= s_end) break;
@@ -930,6 +1050,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     // execution stream: admit while the step has budget (literal engine: while the
     // chosen call fits in the free KV cache, or nothing runs)
     int64_t budget = C + debt;
+    if (!FCFS && !BLIND && !LITERAL && !LINKS && !wide && nX > 1 && budget > 0)
+      batch_admit(budget);
     while ((LITERAL || budget > 0) && nX > 0) {
       // least (key, user id): the ready tier first, then the least counter
       bool cand, tier0;

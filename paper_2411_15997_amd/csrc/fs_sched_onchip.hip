@@ -1050,8 +1050,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     // execution stream: admit while the step has budget (literal engine: while the
     // chosen call fits in the free KV cache, or nothing runs)
     int64_t budget = C + debt;
-    if (!FCFS && !BLIND && !LITERAL && !LINKS && !wide && nX > 1 && budget > 0)
-      batch_admit(budget);
+    if (!FCFS && !BLIND && !LITERAL && !LINKS)
+      while (!wide && nX > 1 && budget > 0 && batch_admit(budget) > 1) {
+      }
     while ((LITERAL || budget > 0) && nX > 0) {
       // least (key, user id): the ready tier first, then the least counter
       bool cand, tier0;

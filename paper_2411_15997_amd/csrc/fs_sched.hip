@@ -373,6 +373,13 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   auto get_u = [&](int32_t k) -> int64_t { return S.users_global ? ld_fresh(S.u + k) : S.u[k]; };
   auto slot_u = [&](int32_t x) -> int64_t { return int64_t(X.key(x) & kValMask); };
 
+  // Literal engine: the choice whose call did not fit in the free KV cache, kept while
+  // it stays the least (key, user): keys only grow under charges, so it is dropped
+  // only when its own key changes or users join, leave or gain a ready call.  A step
+  // that retries after a finish then tests the fit without a scan of X.
+  int32_t st_x = -1, st_user = 0, st_tok = 0;
+  uint64_t st_key = 0;
+
   // ---- two-level argmin over X (block minima of 64 slots) while nX > 64
   bool hier = false;
   auto blk_set = [&](int32_t b) {  // block b's least (key, user)
@@ -438,6 +445,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   // least and largest counter among the backlogged users (nX > 0; once a step)
   auto minmax_x = [&](int64_t &mn, int64_t &mx) { X.minmax(nX, mn, mx); };
   auto set_key = [&](int32_t x, int64_t uval) {
+    if (x == st_x) st_x = -1;
     X.set_key(x, (uint64_t(X.get_rdy(x) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval));
     blk_touch(x);
   };
@@ -527,6 +535,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
 
   // ---- backlogged users
   auto join_x = [&](int32_t k, int64_t uval, int32_t segb) -> int32_t {
+    st_x = -1;
     const int32_t x = X.alloc(k, nX, S);
     ++nX;
     X.set_user(x, k);
@@ -544,6 +553,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
     return x;
   };
   auto leave_x = [&](int32_t x, int32_t k, int64_t uval) {
+    st_x = -1;
     if (lane == 0) S.u[k] = uval;
     c_u = (w_user == k) ? uval : c_u;
     X.release(x, k, nX, S);
@@ -598,6 +608,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
     X.set_ft(x, e);
   };
   auto ready_push = [&](int32_t x, int32_t e) {
+    st_x = -1;  // (its user's key drops to the ready tier)
     if (lane == 0) S.e[e].next = X.get_rh(x);
     X.set_rh(x, e);
     X.set_rdy(x, X.get_rdy(x) + 1);
@@ -932,7 +943,17 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
       int32_t k;
       int32_t x;
       if (!a.fcfs) {
-        x = argmin_x(bk, k);
+        if (literal && st_x >= 0) {  // the call that did not fit is still the least
+          x = st_x;
+          bk = st_key;
+          k = st_user;
+          if (n_run > 0 && kv_used + st_tok > C) {
+            stalled = true;
+            break;
+          }
+        } else {
+          x = argmin_x(bk, k);
+        }
       } else {
         // the earliest queued request: the first arrived record still undecided (a
         // later call waiting for its previous call cannot be it); its user's FIFO head
@@ -986,9 +1007,18 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           code = FS_E_STATE;
           break;
         }
-        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[be].tok)) > C) {
-          stalled = true;
-          break;
+        if (literal && n_run > 0) {
+          const int32_t tk = uni(RD<G>(&S.e[be].tok));
+          if (kv_used + tk > C) {
+            stalled = true;
+            if (!a.fcfs) {
+              st_x = x;
+              st_key = bk;
+              st_user = k;
+              st_tok = tk;
+            }
+            break;
+          }
         }
         e = be;
         const int32_t nx = uni(RD<G>(&S.e[e].next));
@@ -1013,15 +1043,25 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           code = FS_E_STATE;
           break;
         }
-        if (literal && n_run > 0 && kv_used + uni(RD<G>(&S.e[e].tok)) > C) {
-          stalled = true;
-          break;
+        if (literal && n_run > 0) {
+          const int32_t tk = uni(RD<G>(&S.e[e].tok));
+          if (kv_used + tk > C) {
+            stalled = true;
+            if (!a.fcfs) {
+              st_x = x;
+              st_key = bk;
+              st_user = k;
+              st_tok = tk;
+            }
+            break;
+          }
         }
         const int32_t nx = uni(RD<G>(&S.e[e].next));
         X.set_fh(x, nx);
         if (nx < 0) X.set_ft(x, -1);
       }
       const Entry v = ld_entry<G>(&S.e[e]);
+      st_x = -1;  // admitted
       const int32_t left = X.get_q(x) - 1;
       free_e(e);
       X.set_q(x, left);

@@ -379,6 +379,10 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   // that retries after a finish then tests the fit without a scan of X.
   int32_t st_x = -1, st_user = 0, st_tok = 0;
   uint64_t st_key = 0;
+  // The least and largest counter in X as of the last gap sample, reused while no key
+  // of X has changed since (steps of finishes that charge only idle users).
+  bool x_dirty = true;
+  int64_t x_mn = 0, x_mx = 0;
 
   // ---- two-level argmin over X (block minima of 64 slots) while nX > 64
   bool hier = false;
@@ -446,6 +450,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   auto minmax_x = [&](int64_t &mn, int64_t &mx) { X.minmax(nX, mn, mx); };
   auto set_key = [&](int32_t x, int64_t uval) {
     if (x == st_x) st_x = -1;
+    x_dirty = true;
     X.set_key(x, (uint64_t(X.get_rdy(x) > 0 ? 0 : 1) << kTierShift) | uint64_t(uval));
     blk_touch(x);
   };
@@ -536,6 +541,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   // ---- backlogged users
   auto join_x = [&](int32_t k, int64_t uval, int32_t segb) -> int32_t {
     st_x = -1;
+    x_dirty = true;
     const int32_t x = X.alloc(k, nX, S);
     ++nX;
     X.set_user(x, k);
@@ -554,6 +560,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   };
   auto leave_x = [&](int32_t x, int32_t k, int64_t uval) {
     st_x = -1;
+    x_dirty = true;
     if (lane == 0) S.u[k] = uval;
     c_u = (w_user == k) ? uval : c_u;
     X.release(x, k, nX, S);
@@ -1135,10 +1142,12 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
       debt = budget < 0 ? budget : 0;
     }
     if (nX > 0) {
-      int64_t mn, mx;
-      minmax_x(mn, mx);
-      gap = mx - mn > gap ? mx - mn : gap;
-      minX = mn;
+      if (x_dirty) {
+        minmax_x(x_mn, x_mx);
+        x_dirty = false;
+      }
+      gap = x_mx - x_mn > gap ? x_mx - x_mn : gap;
+      minX = x_mn;
     }
     ++s;
   }

@@ -795,6 +795,51 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
     return n_run > 0 ? int64_t(wave_min32(mf)) : INT64_MAX;
   };
   int64_t min_fin = batch_min_fin();
+  // Chunk mode (while the batch has at most kChunkCap entries): finished entries become
+  // dead marks and lane c holds the least live finish step of entries [64c, 64c + 64),
+  // so a step visits only the chunks with a finish due; the array is compacted when it
+  // fills or is saved.  Otherwise every finish pass scans and compacts the whole batch.
+  constexpr uint32_t kDeadFin = 0x7fffffffu;
+  constexpr int64_t kChunkCap = 64 * 64;
+  uint32_t cmin = 0xffffffffu;
+  int64_t n_live = n_run;
+  bool cm = false;
+  // least live finish step of chunk c, into lane c
+  auto chunk_min = [&](int64_t c) {
+    const int64_t i = c * 64 + lane;
+    const uint32_t f = i < n_run ? uint32_t(ld_fresh(run_fin + i)) : 0xffffffffu;
+    const uint32_t m = wave_min32(f == kDeadFin ? 0xffffffffu : f);
+    if (lane == c) cmin = m;
+  };
+  // removes the dead entries, keeping the admission order, and rebuilds the minima
+  auto compact = [&]() {
+    wave_fence();
+    int64_t kept = 0;
+    for (int64_t b0 = 0; b0 < n_run; b0 += 64) {
+      const int64_t i = b0 + lane;
+      const bool valid = i < n_run;
+      const int32_t rr = valid ? ld_fresh(run_rec + i) : -1;
+      const int32_t ff = valid ? ld_fresh(run_fin + i) : int32_t(kDeadFin);
+      const bool live = valid && uint32_t(ff) != kDeadFin;
+      const uint64_t km = __ballot(live);
+      if (live) {
+        const int64_t to = kept + __popcll(km & ((uint64_t(1) << lane) - 1));
+        run_rec[to] = rr;
+        run_fin[to] = ff;
+      }
+      kept += __popcll(km);
+    }
+    n_run = kept;
+    wave_fence();
+    cmin = 0xffffffffu;
+    if (cm)
+      for (int64_t c = 0; c * 64 < n_run; ++c) chunk_min(c);
+  };
+  if (literal && n_run <= kChunkCap / 2) {
+    cm = true;
+    wave_fence();
+    for (int64_t c = 0; c * 64 < n_run; ++c) chunk_min(c);
+  }
   // literal engine: the last admission attempt found the chosen call too large for the
   // free KV cache and nothing has changed since (no arrival, no finish): every step
   // until the next arrival or finish would repeat it, so those steps are skipped
@@ -802,6 +847,63 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   // Calls whose last output token is decoded in step s finish, in admission order: each
   // user is charged its call's cost (Eq. 2) and the call's KV tokens are freed; the
   // batch is compacted in place.
+  // Charges one finishing call (record rec): its user pays its cost (Eq. 2) and its KV
+  // tokens are freed.
+  auto charge_finish = [&](int32_t rec) -> bool {
+    const int64_t g = base + rec;
+    const int32_t k = uni(t.user[g]);
+    const int64_t cst = uni64(a.cost[g]);
+    const int32_t xs = X.find(k, S);
+    int64_t unew;
+    if (xs >= 0) {
+      unew = slot_u(xs) + cst;
+      if (unew < kValueLimit) set_key(xs, unew);
+    } else {
+      unew = uni64(get_u(k)) + cst;
+      if (unew < kValueLimit) {
+        if (lane == 0) S.u[k] = unew;
+        c_u = (w_user == k) ? unew : c_u;
+      }
+    }
+    if (unew >= kValueLimit) {
+      code = FS_E_OVERFLOW;
+      return false;
+    }
+    if (k == last_exit) last_exit_u = unew;
+    if (lane == 0 && a.counter_after) a.counter_after[g] = unew;
+    kv_used -= uni(tokens_at(rec));
+    return true;
+  };
+  // Chunk mode: the calls whose last output token falls in step s, chunk by chunk in
+  // admission order, charged and marked dead.
+  auto finish_chunks = [&]() {
+    wave_fence();
+    for (uint64_t due = __ballot(cmin <= uint32_t(s)); due && code == 0; due &= due - 1) {
+      const int64_t c = __ffsll((long long)due) - 1;
+      const int64_t i = c * 64 + lane;
+      const bool valid = i < n_run;
+      const int32_t rr = valid ? ld_fresh(run_rec + i) : -1;
+      const int32_t ff = valid ? ld_fresh(run_fin + i) : int32_t(kDeadFin);
+      const bool done = valid && int64_t(ff) == s;
+      if (done) run_fin[i] = int32_t(kDeadFin);
+      uint64_t dm = __ballot(done);
+      n_live -= __popcll(dm);
+      while (dm) {
+        const int l = __ffsll((long long)dm) - 1;
+        dm &= dm - 1;
+        if (!charge_finish(rdl(rr, l))) break;
+      }
+      const uint32_t m = wave_min32((valid && !done && uint32_t(ff) != kDeadFin) ? uint32_t(ff)
+                                                                                : 0xffffffffu);
+      if (lane == c) cmin = m;
+    }
+    if (n_live == 0) {  // nothing runs: start the array afresh
+      n_run = 0;
+      cmin = 0xffffffffu;
+    }
+    const uint32_t mf = wave_min32(cmin);
+    min_fin = mf == 0xffffffffu ? INT64_MAX : int64_t(mf);
+  };
   auto finish_calls = [&]() {
     wave_fence();
     int64_t kept = 0;
@@ -850,13 +952,14 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
       }
     }
     n_run = kept;
+    n_live = kept;
     min_fin = n_run > 0 ? int64_t(wave_min32(mf)) : INT64_MAX;
   };
 
   // ---- steps
   while (!overflow && code == 0) {
     if (s >= s_end) break;
-    if (nxt == n && nX == 0 && n_run == 0) break;
+    if (nxt == n && nX == 0 && n_live == 0) break;
     if (nxt < n && nxt - wbase >= 64) advance_window();
     if (literal && (nX == 0 || stalled)) {
       // nothing queued, or the queue waits for KV: nothing happens before the next
@@ -954,7 +1057,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           x = st_x;
           bk = st_key;
           k = st_user;
-          if (n_run > 0 && kv_used + st_tok > C) {
+          if (n_live > 0 && kv_used + st_tok > C) {
             stalled = true;
             break;
           }
@@ -1014,7 +1117,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           code = FS_E_STATE;
           break;
         }
-        if (literal && n_run > 0) {
+        if (literal && n_live > 0) {
           const int32_t tk = uni(RD<G>(&S.e[be].tok));
           if (kv_used + tk > C) {
             stalled = true;
@@ -1050,7 +1153,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           code = FS_E_STATE;
           break;
         }
-        if (literal && n_run > 0) {
+        if (literal && n_live > 0) {
           const int32_t tk = uni(RD<G>(&S.e[e].tok));
           if (kv_used + tk > C) {
             stalled = true;
@@ -1087,12 +1190,21 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           code = FS_E_OVERFLOW;
           break;
         }
+        if (cm && n_run == kChunkCap) {  // full: drop the dead marks
+          compact();
+          if (n_run > kChunkCap / 2) {  // too many running for chunk mode
+            cm = false;
+            cmin = 0xffffffffu;
+          }
+        }
         if (lane == 0) {
           run_rec[n_run] = v.rec;
           run_fin[n_run] = int32_t(fin);
           if (a.counter_after) a.counter_after[base + v.rec] = -1;  // until it finishes
         }
+        if (cm && lane == (n_run >> 6)) cmin = uint32_t(fin) < cmin ? uint32_t(fin) : cmin;
         ++n_run;
+        ++n_live;
         kv_used += v.tok;
         min_fin = fin < min_fin ? fin : min_fin;
       }
@@ -1134,7 +1246,10 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
     if (code || overflow) break;
     if (literal) {
       if (min_fin <= s) {
-        finish_calls();
+        if (cm)
+          finish_chunks();
+        else
+          finish_calls();
         stalled = false;
       }
       if (code) break;
@@ -1155,6 +1270,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   if (code) raise_err(a.err, code);
   flush_window();
   flush_decisions();
+  if (cm && n_run > n_live) compact();  // the saved batch holds live calls only
 
   // ---- save: counters of queued users back to u; the queue itself is recovered next
   // time from the records that have arrived and are still undecided
@@ -1183,7 +1299,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
     low += 64;
   }
   if (low > nxt) low = nxt;
-  const bool drained = nxt == n && nX == 0 && n_run == 0;
+  const bool drained = nxt == n && nX == 0 && n_live == 0;
   if (lane == 0) {
     rs->s = s;
     rs->nxt = nxt;

@@ -537,8 +537,9 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     load_window();
   };
 
-  // All arrivals of the current step in window lanes [j0, j1) at once (X not empty,
-  // so a user outside X is lifted to the least counter in X).  The overload test of
+  // All arrivals of the current step in window lanes [j0, j1) at once (a user outside
+  // X is lifted to minX, the least counter in X; with X empty the caller sets it to the
+  // counter the first arrival joins with).  The overload test of
   // each arrival needs the tokens queued before it: as the queue only grows during
   // the arrivals, the first arrival that finds it above the threshold is found from
   // a prefix sum taken as if none were throttled, and every later arrival of the
@@ -980,12 +981,35 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       const int j = nxt - wbase;
       if (rdl(w_step, j) > s) break;
       if (LITERAL) stalled = false;
-      if (nX > 0 && !blind) {  // the step's arrivals in this window, together
+      // the step's arrivals in this window, together; with Q empty (traces without
+      // interactions, a threshold of zero or more) the first arrival cannot be throttled
+      // (nothing is queued), joins lifted to the last exit's counter, and is then the
+      // least counter in Q, so the others are lifted to it
+      if (!blind && (nX > 0 || (!LINKS && theta >= 0))) {
         const uint64_t after = __ballot(w_step > s) & (~uint64_t(0) << j);
         const int32_t j1 = after ? ff1(after) : 64;
-        if (j1 - j > 1 && arrive_batch(j, j1)) {
-          nxt = wbase + j1;
-          continue;
+        if (j1 - j > 1) {
+          bool done;
+          if (nX > 0) {
+            done = arrive_batch(j, j1);
+          } else {
+            const int64_t m0 = minX, b0 = B;
+            const bool w0 = wide;
+            const int64_t u0 = rdl64(c_u, j), l0 = last_exit >= 0 ? last_exit_u : 0;
+            minX = u0 > l0 ? u0 : l0;
+            B = minX;
+            wide = false;
+            done = arrive_batch(j, j1);
+            if (!done) {  // (nothing changed)
+              minX = m0;
+              B = b0;
+              wide = w0;
+            }
+          }
+          if (done) {
+            nxt = wbase + j1;
+            continue;
+          }
         }
       }
       const int32_t rec = nxt;

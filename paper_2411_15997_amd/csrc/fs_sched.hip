@@ -1442,10 +1442,13 @@ __global__ void k_state_records(char *state, StateLayout L, int64_t N) {
 // next-call links (succ[prev] = i) and the number of requests per (replica, user), the
 // size of the user's segment (a FIFO holds at most all of its user's requests); links
 // and ids are checked again before the scheduler runs.  Each block counts a tile of
-// records by (replica, user) in an LDS hash table (open addressing, at most half full)
-// and adds each distinct key's count to global memory once, so a heavy user costs one
-// global atomic per tile instead of one per request.
+// records by (replica, user) in LDS and adds each distinct key's count to global memory
+// once, so a heavy user costs one global atomic per tile instead of one per request.
+// When the replicas the tile spans times the users fit in the table, the count of
+// (r, u) sits at (r - r0) * U + u (one LDS atomic per record); otherwise in a hash
+// table (open addressing, at most half full).
 constexpr int kLinkTile = 4096;
+constexpr int kLinkPer = kLinkTile / 256;
 constexpr int kLinkSlots = 2 * kLinkTile;
 constexpr uint32_t kLinkEmpty = 0xffffffffu;
 
@@ -1453,39 +1456,76 @@ __global__ void __launch_bounds__(256) k_state_links(char *state, StateLayout L,
   __shared__ uint32_t hk[kLinkSlots], hc[kLinkSlots];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(state + L.seg_start);
   const int64_t g0 = int64_t(blockIdx.x) * kLinkTile;
+  const int64_t g_end = g0 + kLinkTile < t.N ? g0 + kLinkTile : t.N;
+  // the tile's users (and calls and previous calls) are loaded before any is counted,
+  // so that a thread's loads are in flight together
+  int32_t us[kLinkPer], cs[kLinkPer], ps[kLinkPer];
+#pragma unroll
+  for (int k = 0; k < kLinkPer; ++k) {
+    const int64_t g = g0 + k * 256 + threadIdx.x;
+    us[k] = g < g_end ? t.user[g] : -1;
+    cs[k] = g < g_end && t.call ? t.call[g] : 0;
+    ps[k] = g < g_end && t.call ? t.prev[g] : -1;
+  }
+  const int32_t r0 = replica_of(t.rep_off, t.R, g0);
+  const int32_t r1 = replica_of(t.rep_off, t.R, g_end - 1);
+  const int64_t span = int64_t(r1 - r0 + 1) * t.U;
+  const bool dense = span <= kLinkSlots;
   for (int j = threadIdx.x; j < kLinkSlots; j += 256) {
-    hk[j] = kLinkEmpty;
+    if (!dense) hk[j] = kLinkEmpty;
     hc[j] = 0;
   }
-  const int32_t r0 = replica_of(t.rep_off, t.R, g0 < t.N ? g0 : t.N - 1);
-  const int64_t r0_end = t.rep_off[r0 + 1];
+  int32_t r = r0;
+  int64_t r_beg = t.rep_off[r0], r_end = t.rep_off[r0 + 1];
   __syncthreads();
-  for (int64_t g = g0 + threadIdx.x; g < g0 + kLinkTile && g < t.N; g += 256) {
-    const int32_t c = t.call ? t.call[g] : 0;
-    const int32_t r = g < r0_end ? r0 : replica_of(t.rep_off, t.R, g);
-    const int64_t b = t.rep_off[r], i = g - b;
-    const int32_t u = t.user[g];
+#pragma unroll
+  for (int k = 0; k < kLinkPer; ++k) {
+    const int64_t g = g0 + k * 256 + threadIdx.x;
+    if (g >= g_end) break;
+    if (g >= r_end) {  // a later replica of the tile: search (r, r1]
+      int32_t lo = r + 1, hi = r1;
+      while (lo < hi) {
+        const int32_t mid = (lo + hi + 1) >> 1;
+        if (t.rep_off[mid] <= g)
+          lo = mid;
+        else
+          hi = mid - 1;
+      }
+      r = lo;
+      r_beg = t.rep_off[r];
+      r_end = t.rep_off[r + 1];
+    }
+    const int32_t u = us[k];
     if (u >= 0 && u < t.U) {
-      // (replica, user) < R * U <= 2^31: fits below the empty marker
-      const uint32_t key = uint32_t(int64_t(r) * t.U + u);
-      uint32_t h = (key * 2654435761u) >> 19;  // top 13 bits: a slot in [0, 8192)
-      while (true) {
-        const uint32_t prev = atomicCAS(hk + h, kLinkEmpty, key);
-        if (prev == kLinkEmpty || prev == key) {
-          atomicAdd(hc + h, 1u);
-          break;
+      if (dense) {
+        atomicAdd(hc + (int64_t(r - r0) * t.U + u), 1u);
+      } else {
+        // (replica, user) < R * U <= 2^31: fits below the empty marker
+        const uint32_t key = uint32_t(int64_t(r) * t.U + u);
+        uint32_t h = (key * 2654435761u) >> 19;  // top 13 bits: a slot in [0, 8192)
+        while (true) {
+          const uint32_t prev = atomicCAS(hk + h, kLinkEmpty, key);
+          if (prev == kLinkEmpty || prev == key) {
+            atomicAdd(hc + h, 1u);
+            break;
+          }
+          h = (h + 1) & (kLinkSlots - 1);
         }
-        h = (h + 1) & (kLinkSlots - 1);
       }
     }
-    if (c > 0) {
-      const int32_t p = t.prev[g];
-      if (p >= 0 && p < i) reinterpret_cast<int32_t *>(state + L.succ)[b + p] = int32_t(i);
-    }
+    const int32_t p = ps[k];
+    if (cs[k] > 0 && p >= 0 && p < g - r_beg)
+      reinterpret_cast<int32_t *>(state + L.succ)[r_beg + p] = int32_t(g - r_beg);
   }
   __syncthreads();
-  for (int j = threadIdx.x; j < kLinkSlots; j += 256)
-    if (hk[j] != kLinkEmpty) atomicAdd(cnt + hk[j], hc[j]);
+  if (dense) {
+    uint32_t *base = cnt + int64_t(r0) * t.U;
+    for (int j = threadIdx.x; j < span; j += 256)
+      if (hc[j]) atomicAdd(base + j, hc[j]);
+  } else {
+    for (int j = threadIdx.x; j < kLinkSlots; j += 256)
+      if (hk[j] != kLinkEmpty) atomicAdd(cnt + hk[j], hc[j]);
+  }
 }
 
 struct CheckArgs {
@@ -1497,6 +1537,8 @@ struct CheckArgs {
   int32_t *err;
 };
 
+constexpr int kCheckRows = 4;
+
 __global__ void __launch_bounds__(256) k_sched_check(CheckArgs a) {
   const DevTrace &t = a.t;
   int32_t code = 0;
@@ -1506,21 +1548,43 @@ __global__ void __launch_bounds__(256) k_sched_check(CheckArgs a) {
           h->N == t.N))
       code = FS_E_STATE;
   }
-  for (int64_t g0 = blockIdx.x * int64_t(blockDim.x); g0 < t.N;
-       g0 += int64_t(gridDim.x) * blockDim.x) {
-    const int64_t g = g0 + threadIdx.x;
-    // one search per work-group row, then a short walk (a row spans few replicas)
-    int32_t r = replica_of(t.rep_off, t.R, g0);
-    if (g >= t.N) continue;
-    while (t.rep_off[r + 1] <= g) ++r;
-    const int64_t base = t.rep_off[r], i = g - base;
-    const int32_t u = t.user[g], ap = t.app[g];
-    const int64_t ts = t.ts[g];
-    if (u < 0 || u >= t.U || ap < 0 || ap >= t.A) code = max(code, int32_t(FS_E_RANGE));
-    if (ts < 0) code = max(code, int32_t(FS_E_RANGE));
-    if (g > base && t.ts[g - 1] > ts) code = max(code, int32_t(FS_E_ORDER));
-    if (!len_ok(t.len_in[g]) || !len_ok(t.len_out[g]) || (t.len_sys && !len_ok(t.len_sys[g])))
-      code = max(code, int32_t(FS_E_RANGE));
+  // a block checks kCheckRows rows of 256 records; every field of the rows is loaded
+  // before the first test, then one search finds the first row's replica and short
+  // walks the others (a row spans few replicas)
+  const int64_t t0 = int64_t(blockIdx.x) * (kCheckRows * 256);
+  int64_t ts[kCheckRows], tsp[kCheckRows], cst[kCheckRows];
+  int32_t u[kCheckRows], ap[kCheckRows], li[kCheckRows], lo[kCheckRows], ls[kCheckRows];
+  uint8_t rs[kCheckRows];
+#pragma unroll
+  for (int k = 0; k < kCheckRows; ++k) {
+    const int64_t g = t0 + k * 256 + threadIdx.x;
+    const bool in = g < t.N;
+    ts[k] = in ? t.ts[g] : 0;
+    tsp[k] = in && g > 0 ? t.ts[g - 1] : 0;
+    u[k] = in ? t.user[g] : 0;
+    ap[k] = in ? t.app[g] : 0;
+    li[k] = in ? t.len_in[g] : 0;
+    lo[k] = in ? t.len_out[g] : 0;
+    ls[k] = in && t.len_sys ? t.len_sys[g] : 0;
+    cst[k] = in ? a.cost[g] : 0;
+    rs[k] = in && a.reason ? a.reason[g] : 0;
+  }
+  int32_t r = t0 < t.N ? replica_of(t.rep_off, t.R, t0) : 0;
+  int64_t base = t.rep_off[r], r_end = t.rep_off[r + 1];
+#pragma unroll
+  for (int k = 0; k < kCheckRows; ++k) {
+    const int64_t g = t0 + k * 256 + threadIdx.x;
+    if (g >= t.N) break;
+    while (r_end <= g) {
+      ++r;
+      base = r_end;
+      r_end = t.rep_off[r + 1];
+    }
+    const int64_t i = g - base;
+    if (u[k] < 0 || u[k] >= t.U || ap[k] < 0 || ap[k] >= t.A) code = max(code, int32_t(FS_E_RANGE));
+    if (ts[k] < 0) code = max(code, int32_t(FS_E_RANGE));
+    if (g > base && tsp[k] > ts[k]) code = max(code, int32_t(FS_E_ORDER));
+    if (!len_ok(li[k]) || !len_ok(lo[k]) || !len_ok(ls[k])) code = max(code, int32_t(FS_E_RANGE));
     if (t.call) {
       const int32_t c = t.call[g], h = t.head[g], p = t.prev[g];
       bool ok;
@@ -1530,14 +1594,13 @@ __global__ void __launch_bounds__(256) k_sched_check(CheckArgs a) {
         ok = c > 0 && p >= 0 && p < i;
         if (ok) {
           const int64_t gp = base + p;
-          ok = t.call[gp] == c - 1 && t.user[gp] == u && t.head[gp] == h;
+          ok = t.call[gp] == c - 1 && t.user[gp] == u[k] && t.head[gp] == h;
         }
       }
       if (!ok) code = max(code, int32_t(FS_E_RANGE));
     }
-    const int64_t cst = a.cost[g];
-    if (cst < 0 || cst >= kValueLimit) code = max(code, int32_t(FS_E_RANGE));
-    if (a.reason && a.reason[g] > 2) code = max(code, int32_t(FS_E_RANGE));
+    if (cst[k] < 0 || cst[k] >= kValueLimit) code = max(code, int32_t(FS_E_RANGE));
+    if (rs[k] > 2) code = max(code, int32_t(FS_E_RANGE));
   }
   if (code) raise_err(a.err, code);
 }
@@ -1621,7 +1684,8 @@ hipError_t launch_schedule(void *state, const fs_trace *t, const int64_t *cost,
   const size_t gl_lds = tab + (a.oc.hblk ? hb : 0);
 
   CheckArgs ca{a.t, cost, reason, a.state, a.L, a.err};
-  hipLaunchKernelGGL(k_sched_check, dim3(grid_for(N > 0 ? N : 1, 256)), dim3(256), 0, s, ca);
+  hipLaunchKernelGGL(k_sched_check, dim3(N > 0 ? (N + kCheckRows * 256 - 1) / (kCheckRows * 256) : 1),
+                     dim3(256), 0, s, ca);
   const dim3 grid(t->n_replicas), block(64);
   if (!a.global_only) launch_onchip(a, s);
   hipLaunchKernelGGL(k_schedule_global, grid, block, gl_lds, s, a);

@@ -151,7 +151,7 @@ template <class T>
 __device__ inline T ld_fresh(const T *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
-__device__ inline void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup"); }
+__device__ inline void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
 
 // DPP moves for a full-wave reduction (result in lane 63): swap within pairs, swap
 // pairs, mirror within 8, mirror within 16, then broadcast row ends to later rows.

@@ -38,6 +38,8 @@
 // that needs it, saves the replica's state and the global-memory kernel resumes it.
 #include <stddef.h>
 
+#include <type_traits>
+
 #include "fs_sched_common.h"
 
 namespace fs {
@@ -229,13 +231,16 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     for (int32_t c = 0; c * 64 < n_run; ++c) chunk_min(c);
   };
 
+  // a user's counter store, as an LDS store or a global one (typed pointers keep the
+  // compiler from merging the two into one flat store, which would wait on both paths)
+  auto set_u = [&](int32_t k, int64_t v) {
+    if (ulds)
+      ((__attribute__((address_space(3))) int64_t *)u_lds)[k] = v;
+    else
+      ((__attribute__((address_space(1))) int64_t *)u_all)[k] = v;
+  };
   auto put_u = [&](int32_t k, int64_t v) {
-    if (lane == 0) {
-      if (ulds)
-        u_lds[k] = v;
-      else
-        u_all[k] = v;
-    }
+    if (lane == 0) set_u(k, v);
   };
 
   // ---- slots: one backlogged user per lane
@@ -343,6 +348,14 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   // the same user; slots: the window lanes of the slot's user
   int32_t w_slot = -1;
   uint64_t w_gm = 0, xwm = 0;
+  // the next window's record fields, loaded one window ahead (while the current window's
+  // arrivals and admissions run) and used raw when that window is taken
+  struct RawRec {
+    int64_t ts, cst;
+    int32_t usr, call, hd, pv, li, lo, ls, why, sc;
+  };
+  RawRec pf{0, 0, -1, 0, -1, -1, 0, 0, 0, 0, -1};
+  int32_t pf_at = -1;  // the window base pf was loaded for
   // Slot for user k with counter uk (tier 1, nothing queued yet).
   auto join = [&](int32_t k, int64_t uk, uint32_t sb) -> int32_t {
     const int32_t x = ff1(~occ);
@@ -487,26 +500,54 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const int64_t tau = KARG(tau);
     char *const st = KARG(state);
     const size_t o_succ = KARG(L.succ), o_seg = KARG(L.seg_start), o_fate = KARG(L.fate);
+    // record ii's fields, raw: no arithmetic on a loaded value here, so that nothing waits
+    // for the loads.  Every load is issued (lanes past the last record read the last
+    // record, the optional arrays are read at a stand-in address when absent), so the
+    // loads form one straight sequence.
+    auto fetch = [&](int32_t ii, RawRec &f) {
+      const int64_t g = base + (ii < n ? ii : n - 1);
+      f.call = LINKS ? T.call[g] : 0;
+      f.usr = T.user[g];
+      f.ts = T.ts[g];
+      f.hd = LINKS ? T.head[g] : ii;
+      f.pv = LINKS ? T.prev[g] : -1;
+      f.li = T.len_in[g];
+      f.lo = T.len_out[g];
+      f.ls = (T.len_sys ? T.len_sys : T.len_in)[g];
+      f.cst = costp[g];
+      f.why = (reason ? reason : reinterpret_cast<const uint8_t *>(T.len_in))[g];
+      f.sc = LINKS ? reinterpret_cast<const int32_t *>(st + o_succ)[g] : -1;
+    };
+    if (pf_at != wbase) fetch(i, pf);  // (the first window of the call)
+    const RawRec c = pf;
+    // the loads that depend on a record's user (and, with interactions, on the state of
+    // its previous and first calls) are issued before the next window's; the users of
+    // every lane are valid ids (checked before the scheduler runs)
+    const uint32_t sb = reinterpret_cast<const uint32_t *>(st + o_seg)[int64_t(r) * U + c.usr];
+    const int64_t uu = ulds ? u_lds[c.usr] : ld_fresh(u_all + c.usr);
+    int8_t pf_fate = -1, hf_fate = -1;
+    if (LINKS && i < n && c.call > 0) {
+      const int8_t *const fate = reinterpret_cast<const int8_t *>(st + o_fate) + base;
+      pf_fate = ld_fresh(fate + c.pv);
+      hf_fate = ld_fresh(fate + c.hd);
+    }
+    __asm__ volatile("" ::: "memory");
+    pf_at = wbase + 64;
+    fetch(pf_at + lane, pf);
     if (i < n) {
-      const int64_t g = base + i;
-      const int32_t call = LINKS ? T.call[g] : 0;
-      const int32_t usr = T.user[g];
-      const int64_t ts = T.ts[g];
-      const int32_t hd = LINKS ? T.head[g] : i;
-      const int32_t pv = LINKS ? T.prev[g] : -1;
-      const int32_t tok = T.len_in[g] + T.len_out[g] + (T.len_sys ? T.len_sys[g] : 0);
-      const int64_t cst = costp[g];
-      const int32_t why = reason ? reason[g] : 0;
-      const int32_t sc = LINKS ? reinterpret_cast<const int32_t *>(st + o_succ)[g] : -1;
-      const uint32_t sb = reinterpret_cast<const uint32_t *>(st + o_seg)[int64_t(r) * U + usr];
-      const int64_t uu = ulds ? u_lds[usr] : ld_fresh(u_all + usr);
+      const int32_t call = c.call;
+      const int32_t usr = c.usr;
+      const int64_t ts = c.ts;
+      const int32_t hd = c.hd;
+      const int32_t pv = c.pv;
+      const int32_t tok = c.li + c.lo + (T.len_sys ? c.ls : 0);
+      const int64_t cst = c.cst;
+      const int32_t why = reason ? c.why : 0;
+      const int32_t sc = c.sc;
       int32_t fl = call == 0 ? kFirst : 0;
-      if (LINKS && call > 0) {
-        const int8_t *const fate = reinterpret_cast<const int8_t *>(st + o_fate) + base;
-        const int8_t pf = ld_fresh(fate + pv), hf = ld_fresh(fate + hd);
-        fl |= (pf == 0 ? kPrevAdm : 0) | ((hf == 1 || hf == 2) ? kHeadBlk : 0) |
-              (pf > 0 ? kPrevDrop : 0);
-      }
+      if (LINKS && call > 0)
+        fl |= (pf_fate == 0 ? kPrevAdm : 0) | ((hf_fate == 1 || hf_fate == 2) ? kHeadBlk : 0) |
+              (pf_fate > 0 ? kPrevDrop : 0);
       fl |= (why << kReasonShift) | (cst >= kPackLimit ? kBig : 0);
       const int64_t stp = ts / tau;
       w_step = stp < INT32_MAX ? int32_t(stp) : INT32_MAX;
@@ -591,10 +632,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const int64_t lifted = c_u > minX ? c_u : minX;
     const bool is_lead = inb && lane == lead;
     if (is_lead && x0 < 0 && lifted != c_u) {
-      if (ulds)
-        u_lds[w_user] = lifted;
-      else
-        u_all[w_user] = lifted;
+      set_u(w_user, lifted);
     }
     if (want_coa) {  // (an optional output)
       const int src = (x0 >= 0 ? x0 : lane) << 2;
@@ -822,41 +860,56 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   if (nxt < n) load_window();
 
   // Admissions of a step taken together (traces without interactions, counters the
-  // decisions move, least-counter choice, relative keys in use).  Every backlogged user's
-  // FIFO head is a candidate; in the order of (key, user id) they are the step's
-  // admissions until the budget runs out, as long as no user admitted earlier in that
-  // order comes back (with its next request, at its charged counter) ahead of the next
-  // candidate.  Each user's rank and the tokens ranked before it come from one pass over
-  // the occupied lanes; the users that stay give the first rank their return would
-  // pre-empt; the ranks before the least of those are admitted lane-parallel.  Returns
-  // the number admitted; the sequential loop takes the rest of the step.
-  auto batch_admit = [&](int64_t &budget) -> int32_t {
+  // decisions move, least-counter choice).  Every backlogged user's FIFO head is a
+  // candidate; in the order of (key, user id) they are the step's admissions until the
+  // budget runs out, as long as no user admitted earlier in that order comes back (with
+  // its next request, at its charged counter) ahead of the next candidate.  Each user's
+  // rank and the tokens ranked before it come from one pass over the occupied lanes; the
+  // users that stay give the first rank their return would pre-empt; the ranks before
+  // the least of those are admitted lane-parallel.  W: the keys compared are the full
+  // ones (some relative key is saturated), else the relative ones.  Returns the number
+  // admitted; the sequential loop takes the rest of the step.
+  auto batch_admit = [&](int64_t &budget, auto w_tag) -> int32_t {
+    constexpr bool W = decltype(w_tag)::value;
     const bool oc = xu >= 0;
     const uint64_t lt_l = (uint64_t(1) << lane) - 1;
-    const uint64_t key = oc ? ((uint64_t(k32) << 32) | uint32_t(xu)) : ~uint64_t(0);
+    // relative keys: (key, user) in one word; full keys: the key word, then the user
+    const uint64_t key = !oc ? ~uint64_t(0)
+                         : W ? ((uint64_t(kh) << 32) | kl)
+                             : ((uint64_t(k32) << 32) | uint32_t(xu));
+    const uint32_t kuser = oc ? uint32_t(xu) : 0xffffffffu;
+    auto before = [&](uint64_t ka, uint32_t ua, uint64_t kb, uint32_t ub) {
+      return W ? (ka < kb || (ka == kb && ua < ub)) : ka < kb;
+    };
     const uint32_t tok = hlo & uint32_t(kTokMask);
     uint32_t rank = 0, pre = 0;
     for (uint64_t om = occ; om; om &= om - 1) {
       const int32_t j = ff1(om);
       const uint64_t kj = (uint64_t(rdlu(uint32_t(key >> 32), j)) << 32) | rdlu(uint32_t(key), j);
-      const bool lt = kj < key;
+      const uint32_t uj = W ? rdlu(kuser, j) : 0u;
+      const uint32_t tj = rdlu(tok, j);  // (read by every lane: no branch around it)
+      const bool lt = before(kj, uj, key, kuser);
       rank += lt ? 1u : 0u;
-      pre += lt ? rdlu(tok, j) : 0u;
+      pre += lt ? tj : 0u;
     }
     const bool adm = oc && int64_t(pre) < budget;  // the budget is positive before it
-    const int64_t uk = B + int64_t(k32 & kRelMax);
+    const int64_t uk = W ? int64_t((uint64_t(kh & kValHi) << 32) | kl) : B + int64_t(k32 & kRelMax);
     const int64_t unew = uk + int64_t(((uint64_t(hhi) << 32) | hlo) >> 24);
     const bool stay = adm && xq > 1;
     const int64_t d = unew - B;
     const bool nsat = d < 0 || d >= int64_t(kRelMax);
     const uint32_t nk = kRelTier1 | (nsat ? kRelMax : uint32_t(d));
+    // a stayer's return key, in the form compared
+    const uint64_t nkey = W ? (uint64_t(unew) | (uint64_t(kTier1) << 32))
+                            : ((uint64_t(nk) << 32) | uint32_t(xu));
     uint32_t cut = uint32_t(64 - nd);  // room left in the output staging
     for (uint64_t sm = __ballot(stay); sm; sm &= sm - 1) {
       const int32_t j = ff1(sm);
       uint32_t cj = rdlu(rank, j) + 1;  // (a saturated return: stop after it, full keys follow)
-      if (!rdlu(uint32_t(nsat), j)) {
-        const uint64_t nkj = (uint64_t(rdlu(nk, j)) << 32) | rdlu(uint32_t(xu), j);
-        const uint32_t cnt = uint32_t(__popcll(__ballot(oc && key < nkj)));
+      if (W || !rdlu(uint32_t(nsat), j)) {
+        const uint64_t nkj = (uint64_t(rdlu(uint32_t(nkey >> 32), j)) << 32) | rdlu(uint32_t(nkey), j);
+        const uint32_t uj = W ? rdlu(kuser, j) : 0u;
+        const uint32_t cnt = uint32_t(__popcll(__ballot(oc && before(key, kuser, nkj, uj))));
         cj = cnt > cj ? cnt : cj;
       }
       cut = cj < cut ? cj : cut;
@@ -864,22 +917,22 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const bool fin = adm && rank < cut;
     const uint64_t fm = __ballot(fin);
     if (!fm || __ballot(fin && unew >= kValueLimit)) return 0;
-    const int32_t m = __popcll(fm);
-    // lane of each rank (occupied lanes by rank, free lanes after them)
-    const uint32_t dst = oc ? rank : uint32_t(nX + __popcll(~occ & lt_l));
-    const int32_t inv = __builtin_amdgcn_ds_permute(int(dst << 2), lane);
-    // outputs, in admission order, into staging lanes nd .. nd + m - 1
-    const bool st = lane >= nd && lane < nd + m;
-    const int32_t src = __builtin_amdgcn_ds_bpermute((st ? lane - nd : lane) << 2, inv);
-    const int32_t o_rec = __builtin_amdgcn_ds_bpermute(src << 2, hrec);
-    const uint32_t o_lo = uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(uint32_t(unew))));
-    const uint32_t o_hi = uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(uint32_t(uint64_t(unew) >> 32))));
-    if (st) {
+    const int32_t m = __popcll(fm);  // the admitted hold ranks 0 .. m - 1
+    // outputs, in admission order, into staging lanes nd .. nd + m - 1: the admitted lane
+    // of rank q sends to lane nd + q, the i-th other lane to the i-th lane outside the
+    // staging range (a permutation: every lane receives from exactly one)
+    const uint32_t oi = uint32_t(__popcll(~fm & lt_l));
+    const uint32_t to = fin ? uint32_t(nd) + rank : (oi < uint32_t(nd) ? oi : oi + uint32_t(m));
+    const int32_t o_rec = __builtin_amdgcn_ds_permute(int(to << 2), hrec);
+    const uint32_t o_lo = uint32_t(__builtin_amdgcn_ds_permute(int(to << 2), int(uint32_t(unew))));
+    const uint32_t o_hi =
+        uint32_t(__builtin_amdgcn_ds_permute(int(to << 2), int(uint32_t(uint64_t(unew) >> 32))));
+    if (lane >= nd && lane < nd + m) {
       d_rec = o_rec;
       d_step = s;
       d_cnt = int64_t((uint64_t(o_hi) << 32) | o_lo);
     }
-    const int32_t lastl = rdl(inv, m - 1);  // the last admitted
+    const int32_t lastl = ff1(__ballot(fin && rank == uint32_t(m - 1)));  // the last admitted
     const uint32_t used = rdlu(pre + tok, lastl);
     budget -= int64_t(used);
     backlog -= int64_t(used);
@@ -890,16 +943,12 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const bool lv = fin && xq == 1;
     const uint64_t lm = __ballot(lv);
     if (lm) {
-      int32_t r = m - 1, ll = lastl;
-      while (!((lm >> ll) & 1)) ll = rdl(inv, --r);
+      uint32_t q = uint32_t(m - 1);
+      int32_t ll = lastl;
+      while (!((lm >> ll) & 1)) ll = ff1(__ballot(fin && rank == --q));
       last_exit = rdl(xu, ll);
       last_exit_u = rdl64(unew, ll);
-      if (lv) {
-        if (ulds)
-          u_lds[xu] = unew;
-        else
-          u_all[xu] = unew;
-      }
+      if (lv) set_u(xu, unew);
       const bool wh = w_slot >= 0 && ((lm >> (w_slot & 63)) & 1);
       const int wsrc = (w_slot >= 0 ? w_slot : lane) << 2;
       const uint32_t wl = uint32_t(__builtin_amdgcn_ds_bpermute(wsrc, int(uint32_t(unew))));
@@ -939,6 +988,76 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     }
     if (FS_RARE(nd == 64)) flush_decisions();
     return m;
+  };
+
+  // Admissions of a step with one backlogged user (traces without interactions, counters
+  // the decisions move, least-counter choice): the user's FIFO in order while the budget
+  // lasts, its on-chip part at a time, the entries read once into lanes and taken in a
+  // scalar loop (no choice to make).  Returns the number admitted (0: the sequential
+  // loop takes over, e.g. to report a counter overflow).
+  auto solo_admit = [&](int64_t &budget) -> int32_t {
+    const int32_t x = ff1(occ);
+    if (rdl(xf, x) == rdl(xr, x) && rdl(xr, x) < rdl(xt, x)) fifo_refill(x);
+    const int32_t f0 = rdl(xf, x), q0 = rdl(xq, x);
+    int32_t avail = rdl(xr, x) - f0;  // the FIFO's on-chip part
+    if (avail > q0) avail = q0;
+    if (avail > 64 - nd) avail = 64 - nd;  // room left in the output staging
+    if (avail <= 0) return 0;
+    const Ent e = lane < avail ? ring[x * D + ((f0 + lane) & (D - 1))] : mk_ent(-1, -1, 0, 0);
+    int64_t u = int64_t((uint64_t(rdlu(kh, x) & kValHi) << 32) | rdlu(kl, x));
+    int32_t k = 0;
+    for (; k < avail && budget > 0; ++k) {
+      const uint32_t lo = rdlu(e.lo, k), hi = rdlu(e.hi, k);
+      const int64_t unew = u + int64_t(((uint64_t(hi) << 32) | lo) >> 24);
+      if (FS_RARE(unew >= kValueLimit)) break;
+      const int32_t tok = int32_t(lo & uint32_t(kTokMask));
+      const int32_t st = nd + k;
+      d_rec = lane == st ? rdl(e.rec, k) : d_rec;
+      d_step = lane == st ? s : d_step;
+      d_cnt = lane == st ? unew : d_cnt;
+      budget -= tok;
+      backlog -= tok;
+      u = unew;
+    }
+    if (k == 0) return 0;
+    seq += k;
+    nd += k;
+    if (lane == x) {
+      xf += k;
+      xq -= k;
+    }
+    if (q0 == k) {  // the user leaves Q
+      const int32_t ku = rdl(xu, x);
+      occ = 0;
+      nX = 0;
+      if (lane == x) {
+        kh = kl = k32 = 0xffffffffu;
+        xu = -1;
+        xq = 0;
+      }
+      last_exit = ku;
+      last_exit_u = u;
+      put_u(ku, u);
+      c_u = (w_user == ku) ? u : c_u;
+      w_slot = (w_user == ku) ? -1 : w_slot;
+    } else {
+      // the next head (refilled from the segment first when the on-chip part is used
+      // up) and the key at the charged counter
+      if (FS_RARE((__ballot(xf == xr && xr < xt) >> x) & 1)) fifo_refill(x);
+      const uint32_t rv = rel_of(u);
+      if (lane == x) {
+        const Ent v = ring[x * D + (xf & (D - 1))];
+        hrec = v.rec;
+        hsucc = v.succ;
+        hlo = v.lo;
+        hhi = v.hi;
+        kh = uint32_t(uint64_t(u) >> 32) | kTier1;
+        kl = uint32_t(uint64_t(u));
+        k32 = kRelTier1 | rv;
+      }
+    }
+    if (FS_RARE(nd == 64)) flush_decisions();
+    return k;
   };
 
   // ---- steps
@@ -1074,9 +1193,13 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     // execution stream: admit while the step has budget (literal engine: while the
     // chosen call fits in the free KV cache, or nothing runs)
     int64_t budget = C + debt;
-    if (!FCFS && !BLIND && !LITERAL && !LINKS)
-      while (!wide && nX > 1 && budget > 0 && batch_admit(budget) > 1) {
+    if (!FCFS && !BLIND && !LITERAL && !LINKS) {
+      while (nX > 1 && budget > 0 &&
+             (wide ? batch_admit(budget, std::true_type()) : batch_admit(budget, std::false_type())) > 1) {
       }
+      while (nX == 1 && budget > 0 && solo_admit(budget) > 0) {
+      }
+    }
     while ((LITERAL || budget > 0) && nX > 0) {
       // least (key, user id): the ready tier first, then the least counter
       bool cand, tier0;

@@ -54,6 +54,27 @@ def test_random_throttle_and_schedule(seed):
     compare_sim(g, o)
 
 
+@pytest.mark.parametrize("seed", range(80))
+def test_random_wide_keys(seed):
+    """Costs from a few tokens' worth up to 2^40, so that the counters of the backlogged
+    users spread over more than 2^31 (the on-chip scheduler then compares full keys, also
+    when it takes a step's admissions together)."""
+    tr, W, t_user, t_app, step, literal, cap, theta, fcfs, blind, mode, _, rng = _case(7000 + seed)
+    fcfs = fcfs and seed % 4 == 0
+    blind = blind and seed % 4 == 1
+    bits = rng.integers(0, 41, tr.n)
+    cost = (rng.integers(0, 1 << 20, tr.n).astype(np.int64) << 20) >> (40 - bits)
+    say("fuzz wide", seed, tr.n_replicas, tr.n_users, tr.n, literal, fcfs, blind, mode)
+    o_th = oracle.throttle(tr, W, t_user, t_app, raw=True, counts=False)
+    flags = ((oracle.FSO_FCFS if fcfs else 0) | (oracle.FSO_BLIND if blind else 0) |
+             (oracle.FSO_LITERAL if literal else 0))
+    o = oracle.simulate(tr, cost, o_th.reason, step, cap, theta, flags=flags)
+    chunks = int(rng.integers(1, 40)) if mode == 2 else None
+    g = gpu_schedule(tr, cost, o_th.reason, step, cap, theta, chunks=chunks,
+                     global_only=(mode == 1), fcfs=fcfs, blind=blind, literal=literal)
+    compare_sim(g, o)
+
+
 @pytest.mark.parametrize("seed", range(150))
 def test_random_throttle_modes(seed):
     """Gated (random overload flags or always overloaded) and raw, per-(user, app) and

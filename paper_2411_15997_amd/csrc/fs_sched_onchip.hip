@@ -413,8 +413,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     nd = 0;
   };
 
-  auto flush_window = [&]() {
-    const int32_t done = nxt - wbase;
+  auto flush_window = [&](int32_t wb) {
+    const int32_t done = nxt - wb;
     int8_t *const fate = STATE(int8_t, fate);
     int8_t *const status = KARG(status);
     int32_t *const astep = KARG(admit_step);
@@ -422,7 +422,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     int64_t *const ca = KARG(counter_after);
     int64_t *const coa = KARG(counter_on_arrival);
     if (lane < done) {
-      const int64_t g = base + wbase + lane;
+      const int64_t g = base + wb + lane;
       if (o_st > 0) {
         fate[g] = int8_t(o_st);
         status[g] = int8_t(o_st);
@@ -477,7 +477,10 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     }
     w_gm = wv ? g : 0;
   };
-  auto load_window = [&]() {
+  // old >= 0: the window that starts at old is done; its outputs are written here (after
+  // the new window's dependent loads, or before them with interactions, whose loads read
+  // the fates written), so that no wait for those loads also waits for these stores.
+  auto load_window = [&](int32_t old) {
     wave_fence();
     const int32_t i = wbase + lane;
     w_step = INT32_MAX;
@@ -518,6 +521,10 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       f.why = (reason ? reason : reinterpret_cast<const uint8_t *>(T.len_in))[g];
       f.sc = LINKS ? reinterpret_cast<const int32_t *>(st + o_succ)[g] : -1;
     };
+    if (LINKS && old >= 0) {
+      flush_window(old);
+      flush_decisions();
+    }
     if (pf_at != wbase) fetch(i, pf);  // (the first window of the call)
     const RawRec c = pf;
     // the loads that depend on a record's user (and, with interactions, on the state of
@@ -531,9 +538,6 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       pf_fate = ld_fresh(fate + c.pv);
       hf_fate = ld_fresh(fate + c.hd);
     }
-    __asm__ volatile("" ::: "memory");
-    pf_at = wbase + 64;
-    fetch(pf_at + lane, pf);
     if (i < n) {
       const int32_t call = c.call;
       const int32_t usr = c.usr;
@@ -566,16 +570,22 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     // every loaded value is in its register from here on: no later wait on HBM
     __asm__ volatile("" ::"v"(w_step), "v"(w_user), "v"(w_flags), "v"(w_head), "v"(w_prev),
                      "v"(w_succ), "v"(w_seg), "v"(w_lo), "v"(w_hi), "v"(c_u));
+    if (!LINKS && old >= 0) {
+      flush_window(old);
+      flush_decisions();
+    }
+    // the next window's records, into the registers this window's just left
+    pf_at = wbase + 64;
+    fetch(pf_at + lane, pf);
     const int32_t lo_ = wbase + 64 - M;
     cache_lo = lo_ > cache_from ? lo_ : cache_from;
     w_wait = LINKS && __ballot(w_user >= 0 && !(w_flags & (kFirst | kPrevAdm))) != 0;
     match_window();
   };
   auto advance_window = [&]() {
-    flush_window();
-    flush_decisions();
+    const int32_t old = wbase;
     wbase = nxt;
-    load_window();
+    load_window(old);
   };
 
   // All arrivals of the current step in window lanes [j0, j1) at once (a user outside
@@ -857,7 +867,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     minX = int64_t((uint64_t(mh) << 32) | ml);
     rebase_full(minX);
   }
-  if (nxt < n) load_window();
+  if (nxt < n) load_window(-1);
 
   // Admissions of a step taken together (traces without interactions, counters the
   // decisions move, least-counter choice).  Every backlogged user's FIFO head is a
@@ -1060,16 +1070,26 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     return k;
   };
 
+  // Step of the next arrival (nxt < n): its window lane, or, when the window is used up,
+  // the first record of the next window, already loaded.  (The window itself advances in
+  // one place, the arrivals below, so the next window's registers have one definition in
+  // the loop: no copies of them that would wait for their loads.)
+  auto next_arrival_step = [&]() -> int32_t {
+    const int32_t j = nxt - wbase;
+    if (j < 64) return rdl(w_step, j);
+    const int64_t stp = rdl64(pf.ts, 0) / KARG(tau);
+    return stp < INT32_MAX ? int32_t(stp) : INT32_MAX;
+  };
+
   // ---- steps
   while (true) {
     if (s >= s_end) break;
     if (nxt == n && nX == 0 && n_live == 0) break;
-    if (nxt < n && nxt - wbase >= 64) advance_window();
     if (LITERAL) {
       if (nX == 0 || stalled) {
         // nothing queued, or the queue waits for KV: nothing happens before the next
         // arrival or the next finish
-        int64_t target = nxt < n ? int64_t(rdl(w_step, nxt - wbase)) : INT64_MAX;
+        int64_t target = nxt < n ? int64_t(next_arrival_step()) : INT64_MAX;
         const uint32_t mf = wave_min32(cmin);
         if (n_live > 0 && int64_t(mf) < target) target = int64_t(mf);
         if (target > s_end) target = s_end;
@@ -1080,7 +1100,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       }
     } else if (nX == 0 && nxt < n) {
       // nothing queued: the steps before the next arrival only pay back debt
-      int64_t target = rdl(w_step, nxt - wbase);
+      int64_t target = next_arrival_step();
       if (target > s_end) target = s_end;
       if (target > s) {
         const int64_t k = target - s;
@@ -1468,7 +1488,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   }
 
   if (code) raise_err(a.err, code);
-  flush_window();
+  flush_window(wbase);
   flush_decisions();
 
   // ---- save: counters of queued users back to u; the queue itself is rebuilt from

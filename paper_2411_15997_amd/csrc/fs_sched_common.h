@@ -229,6 +229,26 @@ __device__ inline uint32_t wave_max32v(uint32_t v) {
   const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
   return vmax(r[0], r[1]);
 }
+// Both at once, the two chains interleaved step by step (each fills the other's wait
+// states between dependent DPP moves).
+__device__ inline void wave_minmax32v(uint32_t &mn, uint32_t &mx) {
+  mn = vmin(mn, dpp_id<0xB1>(~0u, mn));
+  mx = vmax(mx, dpp_id<0xB1>(0u, mx));
+  mn = vmin(mn, dpp_id<0x4E>(~0u, mn));
+  mx = vmax(mx, dpp_id<0x4E>(0u, mx));
+  mn = vmin(mn, dpp_id<0x141>(~0u, mn));
+  mx = vmax(mx, dpp_id<0x141>(0u, mx));
+  mn = vmin(mn, dpp_id<0x140>(~0u, mn));
+  mx = vmax(mx, dpp_id<0x140>(0u, mx));
+  const auto h = __builtin_amdgcn_permlane32_swap(mn, mn, false, false);
+  const auto g = __builtin_amdgcn_permlane32_swap(mx, mx, false, false);
+  mn = vmin(h[0], h[1]);
+  mx = vmax(g[0], g[1]);
+  const auto r = __builtin_amdgcn_permlane16_swap(mn, mn, false, false);
+  const auto q = __builtin_amdgcn_permlane16_swap(mx, mx, false, false);
+  mn = vmin(r[0], r[1]);
+  mx = vmax(q[0], q[1]);
+}
 // The same, returned in a scalar register.
 __device__ inline uint32_t wave_min32(uint32_t v) { return uint32_t(uni(int32_t(wave_min32v(v)))); }
 __device__ inline uint32_t wave_max32(uint32_t v) { return uint32_t(uni(int32_t(wave_max32v(v)))); }

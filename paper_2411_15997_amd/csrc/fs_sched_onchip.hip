@@ -1147,6 +1147,7 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
           }
           if (done) {
             nxt = wbase + j1;
+            if (j1 < 64) break;  // lane j1 arrives in a later step
             continue;
           }
         }
@@ -1465,18 +1466,21 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
       const bool oc = xu >= 0;
       if (!wide) {
         const uint32_t rv = k32 & kRelMax;
-        const uint32_t mnr = wave_min32(oc ? rv : kRelMax);
-        const uint32_t mxr = wave_max32(oc ? rv : 0u);
+        uint32_t mnv = oc ? rv : kRelMax, mxv = oc ? rv : 0u;
+        wave_minmax32v(mnv, mxv);
+        const uint32_t mnr = uint32_t(uni(int32_t(mnv))), mxr = uint32_t(uni(int32_t(mxv)));
         gap = int64_t(mxr - mnr) > gap ? int64_t(mxr - mnr) : gap;
         minX = B + mnr;
         B = minX;  // rebase: the relative keys only shrink
         if (oc) k32 -= mnr;
       } else {
         const uint32_t uh = kh & kValHi;
-        const uint32_t mnh = wave_min32(oc ? uh : 0xffffffffu);
-        const uint32_t mxh = wave_max32(oc ? uh : 0u);
-        const uint32_t mnl = wave_min32(oc && uh == mnh ? kl : 0xffffffffu);
-        const uint32_t mxl = wave_max32(oc && uh == mxh ? kl : 0u);
+        uint32_t hv = oc ? uh : 0xffffffffu, hx = oc ? uh : 0u;
+        wave_minmax32v(hv, hx);
+        const uint32_t mnh = uint32_t(uni(int32_t(hv))), mxh = uint32_t(uni(int32_t(hx)));
+        uint32_t lv = oc && uh == mnh ? kl : 0xffffffffu, lx = oc && uh == mxh ? kl : 0u;
+        wave_minmax32v(lv, lx);
+        const uint32_t mnl = uint32_t(uni(int32_t(lv))), mxl = uint32_t(uni(int32_t(lx)));
         const int64_t mn = int64_t((uint64_t(mnh) << 32) | mnl);
         const int64_t mx = int64_t((uint64_t(mxh) << 32) | mxl);
         gap = mx - mn > gap ? mx - mn : gap;

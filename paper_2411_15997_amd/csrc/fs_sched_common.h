@@ -106,6 +106,8 @@ struct OnchipCfg {
   int32_t user_tab;   // entries (power of two) of the per-user tables for a batch of arrivals
   int32_t glds;       // global-memory kernel: 1 = its user table and counters in LDS
   int32_t hblk;       // global-memory kernel: block minima of X kept in LDS (0: none)
+  int32_t inl_glds;   // the same two, for the global-memory pass that an on-chip
+  int32_t inl_hblk;   // instance continues with, within its own LDS allocation
   size_t lds_bytes;
 };
 

@@ -40,7 +40,7 @@
 
 #include <type_traits>
 
-#include "fs_sched_common.h"
+#include "fs_sched_global.h"
 
 namespace fs {
 namespace sched {
@@ -111,8 +111,7 @@ __device__ __forceinline__ T arg_at(uint32_t off) {
 // call, head and prev arrays are set); without them every request is a first call, so
 // nothing is ever a ready later call and the interaction bookkeeping compiles away.
 template <bool FCFS, bool BLIND, bool LITERAL, bool LINKS>
-__global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
-  extern __shared__ __align__(16) char smem[];
+__device__ __forceinline__ void onchip_replica(const SchedArgs &a, char *smem) {
   const int32_t r = blockIdx.x;
   if (*a.err) return;
   if (!state_header_ok(a)) return;
@@ -1558,6 +1557,27 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   if (!overflow) {
     int64_t *const counter = KARG(counter) + int64_t(r) * U;
     for (int32_t k = lane; k < U; k += 64) counter[k] = ulds ? u_lds[k] : ld_fresh(u_all + k);
+  }
+}
+
+// One replica per work-group (one wave).  With the engine's policy flags or the literal
+// engine, whose queues outgrow the chip on the comparison workloads, a replica handed
+// over continues in the global-memory pass in the same launch (its on-chip state is in
+// the state buffer by then), so that a replica's two passes follow each other rather
+// than every replica's on-chip pass finishing before any global pass starts.
+template <bool FCFS, bool BLIND, bool LITERAL, bool LINKS>
+__global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  onchip_replica<FCFS, BLIND, LITERAL, LINKS>(a, smem);
+  if constexpr (FCFS || BLIND || LITERAL) {
+    const int32_t r = blockIdx.x;
+    wave_fence();
+    if (uni(ld_fresh(a.err))) return;
+    if (!state_header_ok(a)) return;
+    const RepState *rs = reinterpret_cast<const RepState *>(a.state + a.L.reps) + r;
+    if (!uni(ld_fresh(&rs->overflow))) return;
+    __syncthreads();
+    global_replica(a, r, smem, a.oc.inl_glds != 0, a.oc.inl_hblk);
   }
 }
 

@@ -323,7 +323,9 @@ constexpr int32_t kHierOn = 512, kHierOff = 256;
 // ---------------------------------------------------------------------------
 // Inlined into the kernel for each table kind: as a called function its argument
 // structs would live in scratch memory and every field read would go through it.
-template <bool G, class XT>
+// EF >= 0: the engine flags fixed at compile time (1 first come first served, 2
+// interaction-blind, 4 literal), else read from the arguments.
+template <bool G, class XT, int EF = -1>
 __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X, const XBlocks &XB, int32_t r,
                             bool onchip) {
   const int lane = threadIdx.x;
@@ -360,7 +362,9 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
   int64_t fcfs_lo = low;  // every record below is decided (first-come choice)
   const int64_t mid_budget = uni64(rs->mid_budget);
   // literal engine: the running batch (admission order) and the KV tokens it holds
-  const bool literal = a.literal;
+  const bool literal = EF >= 0 ? (EF & 4) != 0 : a.literal;
+  const bool e_fcfs = EF >= 0 ? (EF & 1) != 0 : a.fcfs;
+  const bool e_blind = EF >= 0 ? (EF & 2) != 0 : a.blind;
   int64_t kv_used = uni64(rs->kv_used), n_run = uni64(rs->n_run);
 
   if (!S.users_global)
@@ -1011,7 +1015,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
       }
       bool blocked;
       int32_t why;
-      if (call > 0 && !a.blind) {
+      if (call > 0 && !e_blind) {
         blocked = rdl(c_head_blk, j) != 0;
         why = 3;
       } else if (call > 0 && rdl(c_prev_drop, j) != 0) {
@@ -1054,7 +1058,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
       uint64_t bk;
       int32_t k;
       int32_t x;
-      if (!a.fcfs) {
+      if (!e_fcfs) {
         if (literal && st_x >= 0) {  // the call that did not fit is still the least
           x = st_x;
           bk = st_key;
@@ -1123,7 +1127,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           const int32_t tk = uni(RD<G>(&S.e[be].tok));
           if (kv_used + tk > C) {
             stalled = true;
-            if (!a.fcfs) {
+            if (!e_fcfs) {
               st_x = x;
               st_key = bk;
               st_user = k;
@@ -1159,7 +1163,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
           const int32_t tk = uni(RD<G>(&S.e[e].tok));
           if (kv_used + tk > C) {
             stalled = true;
-            if (!a.fcfs) {
+            if (!e_fcfs) {
               st_x = x;
               st_key = bk;
               st_user = k;
@@ -1218,7 +1222,7 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
       if (++nd == 64) flush_decisions();
       c_prev_adm = (w_prev == v.rec) ? 1 : c_prev_adm;
       int32_t sc = v.succ;
-      if (a.blind && sc >= 0 && sc < nxt) {  // interaction-blind limits may have dropped it
+      if (e_blind && sc >= 0 && sc < nxt) {  // interaction-blind limits may have dropped it
         wave_fence();
         if (ld_fresh(fate + sc) > 0) sc = -1;
       }
@@ -1330,11 +1334,41 @@ __device__ __forceinline__ void run_replica(const SchedArgs &a, Store &S, XT &X,
       a.counter[int64_t(r) * U + k] = S.users_global ? ld_fresh(u_all + k) : u_all[k];
 }
 
+// The global-memory form of the same pass (X and the counters in the state buffer).
+__device__ __forceinline__ void global_replica_mem(const SchedArgs &a, int32_t r, Store &S,
+                                                  const XBlocks &XB, RepState *rs) {
+  const int64_t off = a.t.rep_off[r] + r;
+  const int32_t cap = int32_t(a.t.rep_off[r + 1] - a.t.rep_off[r]) + 1;
+  char *st = a.state;
+  const StateLayout &L = a.L;
+  XMem X;
+  X.cap = cap;
+  X.k = reinterpret_cast<uint64_t *>(st + L.xkey) + off;
+  X.user = reinterpret_cast<int32_t *>(st + L.xuser) + off;
+  X.q = reinterpret_cast<int32_t *>(st + L.xq) + off;
+  X.fh = reinterpret_cast<int32_t *>(st + L.xfh) + off;
+  X.ft = reinterpret_cast<int32_t *>(st + L.xft) + off;
+  X.hh = reinterpret_cast<int32_t *>(st + L.xhh) + off;
+  X.ht = reinterpret_cast<int32_t *>(st + L.xht) + off;
+  X.sb = reinterpret_cast<int32_t *>(st + L.xsb) + off;
+  X.rh = reinterpret_cast<int32_t *>(st + L.xrh) + off;
+  X.rdy = reinterpret_cast<int32_t *>(st + L.xrdy) + off;
+  S.u = reinterpret_cast<int64_t *>(st + L.u_all) + int64_t(r) * a.t.U;
+  S.xslot = reinterpret_cast<int32_t *>(st + L.xslot_all) + int64_t(r) * a.t.U;
+  S.users_global = true;
+  run_replica<true>(a, S, X, XB, r, false);
+  if (threadIdx.x == 0) rs->overflow = 0;
+}
+
+
 // A replica that overflowed on chip (or every replica, with global memory only), resumed
 // from the state buffer.  gsm: the work-group's dynamic LDS; tab_lds: the user table and
 // counters go there (U * kXLdsBytesPerUser bytes), hblk: block minima of X kept there
 // after the table (0: none).  Called by the global-memory kernel, and by on-chip
 // instances right after their own pass (the replica continues in the same launch).
+// LDS_ONLY: only the LDS-table form is compiled (the caller has checked that it fits);
+// EF: as for run_replica.
+template <bool LDS_ONLY = false, int EF = -1>
 __device__ __forceinline__ void global_replica(const SchedArgs &a, int32_t r, char *gsm, bool tab_lds,
                                                int32_t hblk) {
   RepState *rs = reinterpret_cast<RepState *>(a.state + a.L.reps) + r;
@@ -1374,27 +1408,11 @@ __device__ __forceinline__ void global_replica(const SchedArgs &a, int32_t r, ch
     X.xs = p += U;
     S.xslot = nullptr;
     S.users_global = false;
-    run_replica<true>(a, S, X, XB, r, false);
+    run_replica<true, XLds, EF>(a, S, X, XB, r, false);
     if (threadIdx.x == 0) rs->overflow = 0;
     return;
   }
-  XMem X;
-  X.cap = cap;
-  X.k = reinterpret_cast<uint64_t *>(st + L.xkey) + off;
-  X.user = reinterpret_cast<int32_t *>(st + L.xuser) + off;
-  X.q = reinterpret_cast<int32_t *>(st + L.xq) + off;
-  X.fh = reinterpret_cast<int32_t *>(st + L.xfh) + off;
-  X.ft = reinterpret_cast<int32_t *>(st + L.xft) + off;
-  X.hh = reinterpret_cast<int32_t *>(st + L.xhh) + off;
-  X.ht = reinterpret_cast<int32_t *>(st + L.xht) + off;
-  X.sb = reinterpret_cast<int32_t *>(st + L.xsb) + off;
-  X.rh = reinterpret_cast<int32_t *>(st + L.xrh) + off;
-  X.rdy = reinterpret_cast<int32_t *>(st + L.xrdy) + off;
-  S.u = reinterpret_cast<int64_t *>(st + L.u_all) + int64_t(r) * a.t.U;
-  S.xslot = reinterpret_cast<int32_t *>(st + L.xslot_all) + int64_t(r) * a.t.U;
-  S.users_global = true;
-  run_replica<true>(a, S, X, XB, r, false);
-  if (threadIdx.x == 0) rs->overflow = 0;
+  if constexpr (!LDS_ONLY) global_replica_mem(a, r, S, XB, rs);
 }
 
 }  // namespace

@@ -1561,15 +1561,18 @@ __device__ __forceinline__ void onchip_replica(const SchedArgs &a, char *smem) {
 }
 
 // One replica per work-group (one wave).  With the engine's policy flags or the literal
-// engine, whose queues outgrow the chip on the comparison workloads, a replica handed
-// over continues in the global-memory pass in the same launch (its on-chip state is in
-// the state buffer by then), so that a replica's two passes follow each other rather
-// than every replica's on-chip pass finishing before any global pass starts.
+// engine, whose queues outgrow the chip on the comparison workloads, a replica of a
+// trace with interactions that is handed over continues in the global-memory pass in
+// the same launch when that pass's user table fits in this work-group's LDS (its
+// on-chip state is in the state buffer by then), so that a replica's two passes follow
+// each other rather than every replica's on-chip pass finishing before any global pass
+// starts.
 template <bool FCFS, bool BLIND, bool LITERAL, bool LINKS>
 __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   extern __shared__ __align__(16) char smem[];
   onchip_replica<FCFS, BLIND, LITERAL, LINKS>(a, smem);
-  if constexpr (FCFS || BLIND || LITERAL) {
+  if constexpr ((FCFS || BLIND || LITERAL) && LINKS) {
+    if (!a.oc.inl_glds) return;  // (the global-memory kernel resumes it)
     const int32_t r = blockIdx.x;
     wave_fence();
     if (uni(ld_fresh(a.err))) return;
@@ -1577,7 +1580,8 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const RepState *rs = reinterpret_cast<const RepState *>(a.state + a.L.reps) + r;
     if (!uni(ld_fresh(&rs->overflow))) return;
     __syncthreads();
-    global_replica(a, r, smem, a.oc.inl_glds != 0, a.oc.inl_hblk);
+    global_replica<true, (FCFS ? 1 : 0) | (BLIND ? 2 : 0) | (LITERAL ? 4 : 0)>(a, r, smem, true,
+                                                                          a.oc.inl_hblk);
   }
 }
 

@@ -1580,8 +1580,15 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const RepState *rs = reinterpret_cast<const RepState *>(a.state + a.L.reps) + r;
     if (!uni(ld_fresh(&rs->overflow))) return;
     __syncthreads();
-    global_replica<true, (FCFS ? 1 : 0) | (BLIND ? 2 : 0) | (LITERAL ? 4 : 0)>(a, r, smem, true,
-                                                                          a.oc.inl_hblk);
+    // the arguments read afresh through an opaque offset, so that no value of the on-chip
+    // pass stays live into this one (scalar registers are the on-chip pass's bottleneck)
+    uint32_t off0 = 0;
+    __asm__ volatile("" : "+s"(off0));
+    const __attribute__((address_space(4))) char *kp =
+        (const __attribute__((address_space(4))) char *)__builtin_amdgcn_kernarg_segment_ptr();
+    const SchedArgs &ka = *(const SchedArgs *)(const __attribute__((address_space(4))) SchedArgs *)(kp + off0);
+    global_replica<true, (FCFS ? 1 : 0) | (BLIND ? 2 : 0) | (LITERAL ? 4 : 0)>(ka, r, smem, true,
+                                                                          ka.oc.inl_hblk);
   }
 }
 

@@ -1572,14 +1572,6 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
   extern __shared__ __align__(16) char smem[];
   onchip_replica<FCFS, BLIND, LITERAL, LINKS>(a, smem);
   if constexpr ((FCFS || BLIND || LITERAL) && LINKS) {
-    if (!a.oc.inl_glds) return;  // (the global-memory kernel resumes it)
-    const int32_t r = blockIdx.x;
-    wave_fence();
-    if (uni(ld_fresh(a.err))) return;
-    if (!state_header_ok(a)) return;
-    const RepState *rs = reinterpret_cast<const RepState *>(a.state + a.L.reps) + r;
-    if (!uni(ld_fresh(&rs->overflow))) return;
-    __syncthreads();
     // the arguments read afresh through an opaque offset, so that no value of the on-chip
     // pass stays live into this one (scalar registers are the on-chip pass's bottleneck)
     uint32_t off0 = 0;
@@ -1587,6 +1579,14 @@ __global__ void __launch_bounds__(64) k_schedule_onchip(SchedArgs a) {
     const __attribute__((address_space(4))) char *kp =
         (const __attribute__((address_space(4))) char *)__builtin_amdgcn_kernarg_segment_ptr();
     const SchedArgs &ka = *(const SchedArgs *)(const __attribute__((address_space(4))) SchedArgs *)(kp + off0);
+    if (!ka.oc.inl_glds) return;  // (the global-memory kernel resumes it)
+    const int32_t r = blockIdx.x;
+    wave_fence();
+    if (uni(ld_fresh(ka.err))) return;
+    if (!state_header_ok(ka)) return;
+    const RepState *rs = reinterpret_cast<const RepState *>(ka.state + ka.L.reps) + r;
+    if (!uni(ld_fresh(&rs->overflow))) return;
+    __syncthreads();
     global_replica<true, (FCFS ? 1 : 0) | (BLIND ? 2 : 0) | (LITERAL ? 4 : 0)>(ka, r, smem, true,
                                                                           ka.oc.inl_hblk);
   }

@@ -45,8 +45,8 @@ STAGE_SRC = {
 # the stage's sources hash to `src`.
 MEASURED_TRAFFIC = {
     # k_schedule_onchip on the 1,024-replica weight sweep (20.48M requests)
-    ("c4_sweep", "schedule"): {"src": "a0ba7e67f9c587aa", "fetch_kib": 313475.375,
-                               "write_kib": 137752.25, "fetch_factor": 1.99992,
+    ("c4_sweep", "schedule"): {"src": "df9073c9ab2d1903", "fetch_kib": 313379.0,
+                               "write_kib": 137709.46875, "fetch_factor": 1.99991,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
     ("c3_throttle", "throttle"): {"src": "d1d4af8cbaffee13", "fetch_kib": 1458943.5625,

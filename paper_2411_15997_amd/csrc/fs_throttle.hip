@@ -888,7 +888,7 @@ struct CombineArgs {
   int64_t n_words;
 };
 
-constexpr int kCombineRows = 16;
+constexpr int kCombineRows = 8;
 constexpr int kCombineSpan = kThreads * kCombineRows;  // records per combine block
 
 // Gated mode: a first call (head == itself) is throttled iff overloaded and over a limit;

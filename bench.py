@@ -49,8 +49,8 @@ MEASURED_TRAFFIC = {
                                "write_kib": 137709.46875, "fetch_factor": 1.99991,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
-    ("c3_throttle", "throttle"): {"src": "d1d4af8cbaffee13", "fetch_kib": 1458943.5625,
-                                  "write_kib": 1522346.75, "fetch_factor": 1.99992,
+    ("c3_throttle", "throttle"): {"src": "cf9919faebb18767", "fetch_kib": 1458827.0,
+                                  "write_kib": 1522194.9375, "fetch_factor": 1.99988,
                                   "write_factor": 1.0},
 }
 

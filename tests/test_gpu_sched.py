@@ -195,6 +195,25 @@ def test_counter_overflow_reported():
     assert ge.value.code == oe.value.code == fs.FS_E_OVERFLOW
 
 
+@pytest.mark.parametrize("users", [1, 2])
+def test_counter_overflow_reported_on_chip(users):
+    """Counters that reach 2^62 through many admissions of packable costs (below 2^40): the
+    on-chip kernel's single-user pass (one user) and batched admissions (two users) stop
+    before the overflowing admission, and the error is the oracle's."""
+    n = users * ((1 << 22) + 1)
+    z32 = np.zeros(n, np.int32)
+    user = (np.arange(n) % users).astype(np.int32)
+    tr = tg.Trace(1, users, 1, np.array([0, n], np.int64), np.zeros(n, np.int64), user, z32,
+                  None, None, None, np.ones(n, np.int32), None, z32)
+    cost = np.full(n, (1 << 40) - 1, np.int64)
+    say("sched overflow on chip", users, n)
+    with pytest.raises(oracle.OracleError) as oe:
+        oracle.simulate(tr, cost, None, 10, 1 << 30, 1 << 40)
+    with pytest.raises(fs.FairServeError) as ge:
+        gpu_schedule(tr, cost, None, 10, 1 << 30, 1 << 40)
+    assert ge.value.code == oe.value.code == fs.FS_E_OVERFLOW
+
+
 def test_run_trace_and_metrics_full_path():
     """fs_run_trace (cost + raw throttle + steps) and fs_fairness_metrics end to end."""
     wl, tr = workload_trace("c2_replicas", replicas=3, records=30000)

@@ -313,9 +313,10 @@ constexpr int kLdsUsers = 4096;
 
 // Sums three per-thread counts over the work-group (256 threads) and adds them to the
 // replica's counters c0, c1, c2 (c < 0: unused).
+// (c0b >= 0: x0's total also goes to counter c0b)
 __device__ inline void block_count3(uint32_t x0, uint32_t x1, uint32_t x2,
                                     unsigned long long *cr, int c0, int c1, int c2,
-                                    unsigned long long (*s_red)[4]) {
+                                    unsigned long long (*s_red)[4], int c0b = -1) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const unsigned long long packed =
       uint64_t(x0) | (uint64_t(x1) << 21) | (uint64_t(x2) << 42);  // each at most kChunk
@@ -326,6 +327,7 @@ __device__ inline void block_count3(uint32_t x0, uint32_t x1, uint32_t x2,
     const unsigned long long t = s_red[0][0] + s_red[0][1] + s_red[0][2] + s_red[0][3];
     const unsigned long long m = (uint64_t(1) << 21) - 1;
     if (c0 >= 0 && (t & m)) atomicAdd(cr + c0, t & m);
+    if (c0b >= 0 && (t & m)) atomicAdd(cr + c0b, t & m);
     if (c1 >= 0 && ((t >> 21) & m)) atomicAdd(cr + c1, (t >> 21) & m);
     if (c2 >= 0 && ((t >> 42) & m)) atomicAdd(cr + c2, (t >> 42) & m);
   }
@@ -410,6 +412,9 @@ __global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
         const bool served = st[j] == 0;
         uint32_t uf = U_HAS;
         if (served && is_delayed(as[j], ts[j], a.tau, a.D)) uf |= U_DELAYED;
+        // without interaction links a served request is a fully served interaction (the
+        // interaction pass is not run)
+        if (served && !t.call) uf |= U_FULL;
         if (!fc) atomicOr(a.iflags + base + h, own_iflag(st[j]));
         if (served && !cost_ok(cs[j])) {
           code = int32_t(FS_E_RANGE);
@@ -435,7 +440,7 @@ __global__ void __launch_bounds__(256) k_m_records_lds(MArgs a) {
       if ((ufg[k] & f) != f) atomicOr(ufg + k, f);
     }
     block_count3(n_adm, n_thr, n_int, a.counters + int64_t(r) * C_NUM, C_ADMITTED, C_THROTTLED,
-                 C_INTERACTIONS, s_red);
+                 C_INTERACTIONS, s_red, t.call ? -1 : int(C_FULL));
     __syncthreads();
     block_cost2(c_lo, c_hi, a.counters + int64_t(r) * C_NUM, s_red);
     __syncthreads();
@@ -627,7 +632,8 @@ hipError_t launch_metrics(const fs_trace *t, const int64_t *cost, const fs_outpu
     const int64_t chunks = (N + kChunk - 1) / kChunk;
     if (t->n_users <= kLdsUsers) {
       hipLaunchKernelGGL(k_m_records_lds, dim3(chunks), dim3(256), size_t(t->n_users) * 12, s, a);
-      hipLaunchKernelGGL(k_m_interactions_lds, dim3(chunks), dim3(256), size_t(t->n_users), s, a);
+      if (t->call)  // (without links the records pass counts the fully served interactions)
+        hipLaunchKernelGGL(k_m_interactions_lds, dim3(chunks), dim3(256), size_t(t->n_users), s, a);
     } else {
       hipLaunchKernelGGL(k_m_records, dim3(grid_for(N, 256)), dim3(256), 0, s, a);
       hipLaunchKernelGGL(k_m_interactions, dim3(grid_for(N, 256)), dim3(256), 0, s, a);

@@ -1016,11 +1016,20 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   const DevTrace dt = dev_trace(t);
   hipLaunchKernelGGL(k_thr_span, dim3(1), dim3(kThreads), 0, s, dt.rep_off, dt.ts, dt.R, pk.Bq, sh);
 
-  // digits: the user bits in passes of at most kRadixBits, then the app bits
+  // digits: the user bits in passes of at most kRadixBits, then the app bits.  With a
+  // power-of-two user count the key is replica << log2(U) | user, and since the stream
+  // is replica-major and the sort stable, sorting the user bits alone already leaves
+  // every (replica, user) run contiguous and in time order: the replica bits need no
+  // pass.  The runs are then not in key order, which only the window counts rely on
+  // (they binary-search a key's first position), so counts keep the full sort.
   struct Digit { int shift, width; };
   Digit dig[8];
   int nd = 0, n_user = 0;
-  for (int b0 = 0, left = pk.Bu; left > 0;) {
+  int user_bits = pk.Bu;
+  if (!cnt_user && !cnt_app && t->n_replicas > 1 && t->n_users >= 2 &&
+      (t->n_users & (t->n_users - 1)) == 0)
+    user_bits = __builtin_ctz(uint32_t(t->n_users));
+  for (int b0 = 0, left = user_bits; left > 0;) {
     const int passes = (left + kRadixBits - 1) / kRadixBits;
     const int wd = (left + passes - 1) / passes;
     dig[nd++] = {b0, wd};

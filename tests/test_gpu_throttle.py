@@ -182,6 +182,26 @@ def test_fused_limit_tests_random(seed):
     _check_fused(tr, W, tu, ta, raw=False)
 
 
+@pytest.mark.parametrize("U,R", [(2, 2), (4, 7), (64, 3), (256, 9), (1024, 5), (2048, 3)])
+def test_power_of_two_users_multi_replica(U, R):
+    """A power-of-two user count over several replicas (the key's replica bits then sit
+    above its user bits, and without window counts only the user bits are sorted):
+    fused and unfused limit tests, app-level limits, raw and gated, counts on and off."""
+    rng = np.random.default_rng(500 + U + R)
+    n = int(rng.integers(2000, 5000))
+    tr = random_trace(rng, n, U, 5, int(rng.integers(1, 4 * n)), multi=True, n_replicas=R)
+    W = int(rng.integers(1, 300))
+    ta = rng.integers(0, 8, size=tr.n_apps).tolist()
+    ov = rng.integers(0, 2, size=tr.n).astype(np.uint8)
+    say("throttle pow2 users", U, R, tr.n)
+    for tu in (3, 1500):
+        _check(tr, W, tu, ta, counts=False)
+        _check(tr, W, tu, ta, overloaded=ov, raw=False, counts=False)
+        _check(tr, W, tu, ta)
+        _check(tr, W, tu, ta, raw=False, counts=False, app_scope=1)
+        _check(tr, W, tu, ta, app_scope=1)
+
+
 @pytest.mark.parametrize("name,kw", [
     ("c2_replicas", dict(replicas=4, records=30001)),
     ("c3_throttle", dict(records=1_000_003)),

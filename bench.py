@@ -49,8 +49,8 @@ MEASURED_TRAFFIC = {
                                "write_kib": 137709.46875, "fetch_factor": 1.99991,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
-    ("c3_throttle", "throttle"): {"src": "cf9919faebb18767", "fetch_kib": 1458827.0,
-                                  "write_kib": 1522194.9375, "fetch_factor": 1.99988,
+    ("c3_throttle", "throttle"): {"src": "40db6dc0ec560fa4", "fetch_kib": 1458803.5,
+                                  "write_kib": 1522312.75, "fetch_factor": 1.9999,
                                   "write_factor": 1.0},
 }
 

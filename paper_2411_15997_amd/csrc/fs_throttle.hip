@@ -147,12 +147,17 @@ __device__ uint32_t block_inclusive_scan(uint32_t v, uint32_t *s_waves, uint32_t
 // Lanes of the wave holding the same digit as this lane (one ballot per digit bit;
 // `width` is the digit's bit count, at most kRadixBits).
 __device__ inline uint64_t digit_peers(uint32_t d, bool valid, int width) {
-  uint64_t peers = __ballot(valid);
+  const uint64_t v = __ballot(valid);
+  uint32_t lo = uint32_t(v), hi = uint32_t(v >> 32);
   for (int b = 0; b < width; ++b) {
-    const uint64_t m = __ballot((d >> b) & 1u);
-    peers &= ((d >> b) & 1u) ? m : ~m;
+    // s: all ones where the lane's bit b is set; m: the lanes whose bit b is set.  A
+    // lane keeps the lanes where m agrees with its own bit: those of ~(m ^ s).
+    const uint32_t s = uint32_t(__builtin_amdgcn_sbfe(int32_t(d), uint32_t(b), 1u));
+    const uint64_t m = __builtin_amdgcn_uicmp(s, 0u, 33);  // the ballot of s != 0
+    lo &= ~(uint32_t(m) ^ s);
+    hi &= ~(uint32_t(m >> 32) ^ s);
   }
-  return peers;
+  return (uint64_t(hi) << 32) | lo;
 }
 
 __host__ __device__ inline int mask_width(uint32_t mask) {
@@ -681,6 +686,7 @@ struct FusedArgs {
 // list[rank[j]] = j, each app's positions in order).
 struct FusedLds {
   uint64_t *el;        // [span]
+  int32_t *tapp;       // [A] the app limits
   uint16_t *list;      // [span]
   uint16_t *rank;      // [span]
   uint16_t *cnt;       // [kFThreads / 64][A] per wave: positions of each app so far
@@ -688,13 +694,14 @@ struct FusedLds {
   uint32_t *waves;     // [kFThreads / 64] (16-byte aligned)
 };
 __host__ __device__ inline size_t fused_lds_bytes(int span, int A) {
-  return size_t(span) * 12 + size_t(kFThreads / 64) * A * 2 + size_t(A) * 2 + 16 +
-         size_t(kFThreads / 64) * 4;
+  return size_t(span) * 12 + size_t(A) * 4 + size_t(kFThreads / 64) * A * 2 + size_t(A) * 2 +
+         16 + size_t(kFThreads / 64) * 4;
 }
 __device__ inline FusedLds fused_lds(char *base, int span, int A) {
   FusedLds sm;
   sm.el = reinterpret_cast<uint64_t *>(base);
-  sm.list = reinterpret_cast<uint16_t *>(sm.el + span);
+  sm.tapp = reinterpret_cast<int32_t *>(sm.el + span);
+  sm.list = reinterpret_cast<uint16_t *>(sm.tapp + A);
   sm.rank = sm.list + span;
   sm.cnt = sm.rank + span;
   sm.start = sm.cnt + (kFThreads / 64) * A;
@@ -725,10 +732,22 @@ __global__ void __launch_bounds__(kFThreads) k_thr_fused(FusedArgs a) {
       const int64_t g = g0 + j;
       v[i] = (j < span && g >= 0 && g < a.N) ? a.el[g] : 0u;
     }
+    constexpr int kAppIters = (1024 + kFThreads - 1) / kFThreads;  // A <= 1024
+    int32_t tv[kAppIters];
+#pragma unroll
+    for (int i = 0; i < kAppIters; ++i) {
+      const int k = threadIdx.x + i * kFThreads;
+      tv[i] = k < A ? a.t_app[k] : 0;
+    }
 #pragma unroll
     for (int i = 0; i < kIters; ++i) {
       const int j = threadIdx.x + i * kFThreads;
       if (j < span) sm.el[j] = v[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kAppIters; ++i) {
+      const int k = threadIdx.x + i * kFThreads;
+      if (k < A) sm.tapp[k] = tv[i];
     }
   }
   for (int k = threadIdx.x; k < (kFThreads / 64) * A; k += kFThreads) sm.cnt[k] = 0;
@@ -803,7 +822,7 @@ __global__ void __launch_bounds__(kFThreads) k_thr_fused(FusedArgs a) {
     }
     if (!why) {
       const uint32_t ap = uint32_t(e >> (pk.SK + pk.Bu)) & amask;
-      const int32_t ta = ap < uint32_t(A) ? a.t_app[ap] : INT32_MAX;
+      const int32_t ta = ap < uint32_t(A) ? sm.tapp[ap] : INT32_MAX;
       if (ta == 0) {
         why = 2;  // the request itself is over a zero limit
       } else if (ta < H) {  // (ta >= T_u: at most T_u requests of the user in the window)

@@ -93,7 +93,7 @@ struct Layout {
   int64_t N;
   int64_t tiles;
   Pack pk;
-  size_t off_a, off_b, off_hist, off_part, off_tapp, off_sh;
+  size_t off_a, off_b, off_dig, off_hist, off_part, off_tapp, off_sh;
   size_t total;
 };
 
@@ -107,6 +107,7 @@ Layout layout(const fs_trace *t) {
   size_t o = 0;
   L.off_a = o; o += up(n * 8);
   L.off_b = o; o += up(n * 8);
+  L.off_dig = o; o += up(n);  // the next pass's digit of each element, one byte
   L.off_hist = o; o += up(hist_len * 4);
   L.off_part = o; o += up(((hist_len + kScanChunk - 1) / kScanChunk + 1) * 4);
   L.off_tapp = o; o += up(kMaxApps * 4);
@@ -363,6 +364,37 @@ __global__ void __launch_bounds__(kThreads) k_radix_hist(const uint64_t *el, int
   if (t <= int(mask)) hist[int64_t(t) * tiles + blockIdx.x] = hist_total(h, t);
 }
 
+// The same tile histogram from the digits the previous pass's scatter wrote out, one byte
+// per element at its new position: 1 byte read per element instead of 8.  Thread t
+// counts the tile's 16 consecutive elements from 16 t.
+__global__ void __launch_bounds__(kThreads) k_radix_hist8(const uint8_t *dig, int64_t N,
+                                                           uint32_t mask, uint32_t *hist,
+                                                           int64_t tiles) {
+  static_assert(kTile == kThreads * 16, "one 16-byte load per thread");
+  __shared__ uint32_t h[kHistWords];
+  const int t = threadIdx.x;
+  for (int j = t; j < kHistWords; j += kThreads) h[j] = 0;
+  const int64_t e0 = blockIdx.x * int64_t(kTile) + int64_t(t) * 16;
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  if (e0 + 16 <= N) {
+    const uint4 q = *reinterpret_cast<const uint4 *>(dig + e0);
+    w[0] = q.x;
+    w[1] = q.y;
+    w[2] = q.z;
+    w[3] = q.w;
+  } else {
+    for (int i = 0; i < 16; ++i)
+      if (e0 + i < N) w[i >> 2] |= uint32_t(dig[e0 + i]) << (8 * (i & 3));
+  }
+  __syncthreads();
+  const int width = mask_width(mask);
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    hist_add(h, (w[i >> 2] >> (8 * (i & 3))) & mask, e0 + i < N, width);
+  __syncthreads();
+  if (t <= int(mask)) hist[int64_t(t) * tiles + blockIdx.x] = hist_total(h, t);
+}
+
 struct ScatterArgs {
   const uint64_t *in;
   uint64_t *out;
@@ -376,6 +408,9 @@ struct ScatterArgs {
   uint64_t user_mask;  // element bits of the user part of the key
   Win win;
   int32_t *n_flag;     // counters of records over the user limit (TEST_USER)
+  uint8_t *next_dig;   // when set: each element's next digit, at its new position
+  int next_shift;
+  uint32_t next_mask;
 };
 
 // Stable scatter of one tile.  Wave w owns the contiguous sub-tile
@@ -460,7 +495,10 @@ __global__ void __launch_bounds__(kThreads) k_radix_scatter(ScatterArgs a) {
     const uint64_t el = s_el[j];
     const uint32_t d = uint32_t(el >> a.shift) & a.mask;
     const uint32_t dst = goff[d] + (uint32_t(j) - loc[d]);
-    if (dst < a.N) a.out[dst] = el;
+    if (dst < a.N) {
+      a.out[dst] = el;
+      if (a.next_dig) a.next_dig[dst] = uint8_t(uint32_t(el >> a.next_shift) & a.next_mask);
+    }
   }
 }
 
@@ -1028,6 +1066,7 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   uint32_t *part = reinterpret_cast<uint32_t *>(w + L.off_part);
   int32_t *tapp = reinterpret_cast<int32_t *>(w + L.off_tapp);
   int32_t *sh = reinterpret_cast<int32_t *>(w + L.off_sh);
+  uint8_t *dig_b = reinterpret_cast<uint8_t *>(w + L.off_dig);
   const bool raw = (flags & FS_THROTTLE_RAW) != 0;
   hipError_t e = hipMemcpyAsync(tapp, lim->t_app_h, sizeof(int32_t) * t->n_apps,
                                 hipMemcpyHostToDevice, s);
@@ -1078,6 +1117,7 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   const uint64_t user_mask = ((uint64_t(1) << pk.Bu) - 1) << pk.SK;
   uint64_t *in = A, *out = B;
   const int n_pass = fused ? n_user : nd;
+  bool have_dig = false;  // the digits of this pass were written out by the last scatter
   for (int k = 0; k < n_pass; ++k) {
     const uint32_t mask = (1u << dig[k].width) - 1u;
     const int shift = pk.SK + dig[k].shift;
@@ -1095,7 +1135,10 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
       in = out;
       out = tmp;
     }
-    if (k > 0)
+    if (k > 0 && have_dig)
+      hipLaunchKernelGGL(k_radix_hist8, dim3(L.tiles), dim3(kThreads), 0, s, dig_b, L.N, mask,
+                         hist, L.tiles);
+    else if (k > 0)
       hipLaunchKernelGGL(k_radix_hist, dim3(L.tiles), dim3(kThreads), 0, s, in, L.N, shift, mask,
                          hist, L.tiles);
     (void)exclusive_scan(hist, int64_t(mask + 1) * L.tiles, part, s);
@@ -1103,8 +1146,13 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
       CountArgs ca{in, L.N, KeySel{user_mask, false, pk.SK, pk.Bu, 1u}, win, cnt_user};
       hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
     }
+    // the next pass's digits go out with the elements, unless the app-level user test
+    // puts the elements back in stream order before that pass
+    have_dig = k + 1 < n_pass && !(app_level && k + 1 == n_user);
     ScatterArgs sa{in, out, L.N, shift, mask, hist, L.tiles, lim->t_user,
-                   user_mask, win, sh + kFlagStride};
+                   user_mask, win, sh + kFlagStride, have_dig ? dig_b : nullptr,
+                   have_dig ? pk.SK + dig[k + 1].shift : 0,
+                   have_dig ? (1u << dig[k + 1].width) - 1u : 0u};
     if (k == n_user && !app_level)
       hipLaunchKernelGGL(k_radix_scatter<true>, dim3(L.tiles), dim3(kThreads), 0, s, sa);
     else

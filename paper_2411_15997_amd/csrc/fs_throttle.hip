@@ -945,80 +945,134 @@ struct CombineArgs {
   int64_t n_words;
 };
 
-constexpr int kCombineRows = 8;
-constexpr int kCombineSpan = kThreads * kCombineRows;  // records per combine block
+constexpr int kCombineItems = 8;                        // consecutive records a thread
+constexpr int kCombineWords = kCombineItems / 4;        // of reason bytes
+constexpr int kCombineSpan = kThreads * kCombineItems;  // records per combine block
 
 // Gated mode: a first call (head == itself) is throttled iff overloaded and over a limit;
-// a later call is dropped iff its first call was.  All of a thread's loads are issued
-// before the interaction gathers, which all come before the stores.
+// a later call is dropped iff its first call was.  Each thread takes 8 consecutive
+// records: their reason bytes and overload flags in one 8-byte load each, their links
+// in two 16-byte loads (when the link array is 16-byte aligned), the first calls' bytes
+// gathered after all of those, the reasons out in one 8-byte store and the bitmap bits
+// in one byte.
 __global__ void __launch_bounds__(kThreads) k_thr_combine(CombineArgs a) {
+  __shared__ int32_t s_rep[2];
   const int64_t N = a.t.N;
-  const int lane = threadIdx.x & 63;
   const int64_t start = xcd_tile(blockIdx.x, gridDim.x) * kCombineSpan;
-  uint8_t code[kCombineRows];
-  // global index of the interaction's first call for a later call; -1 for a first call,
-  // -2 for a later call whose link is out of range (reported by the element pass)
-  int64_t hg[kCombineRows];
-  const bool links = !a.raw && a.t.head;
-  int32_t hd[kCombineRows];
-#pragma unroll
-  for (int i = 0; i < kCombineRows; ++i) {
-    const int64_t g = start + i * kThreads + threadIdx.x;
-    code[i] = g < N ? a.rb[g] : 0;
-    hd[i] = (links && g < N) ? a.t.head[g] : 0;
+  const int64_t g0 = start + int64_t(threadIdx.x) * kCombineItems;
+  const bool links = !a.raw && a.t.head != nullptr;
+  if (links && threadIdx.x == 0 && start < N) {  // the replicas of the block's first and last
+    const int64_t last = start + kCombineSpan < N ? start + kCombineSpan - 1 : N - 1;
+    s_rep[0] = replica_of(a.t.rep_off, a.t.R, start);
+    s_rep[1] = replica_of(a.t.rep_off, a.t.R, last);
   }
-  if (links) {
-    // the replica of each row, walking forward from the block's first record (the
-    // offsets are read only where a replica ends inside the block)
-    int32_t r = start < N ? replica_of(a.t.rep_off, a.t.R, start) : 0;
-    int64_t lo = a.t.rep_off[r], hi = a.t.rep_off[r + 1];
-#pragma unroll
-    for (int i = 0; i < kCombineRows; ++i) {
-      const int64_t g = start + i * kThreads + threadIdx.x;
-      hg[i] = -1;
-      if (g >= N) continue;
-      while (g >= hi) {
-        ++r;
-        lo = hi;
-        hi = a.t.rep_off[r + 1];
-      }
-      const int64_t h = lo + hd[i];
-      if (h != g) hg[i] = (h >= lo && h < g) ? h : -2;
-    }
+  __syncthreads();
+  uint8_t *const bm = reinterpret_cast<uint8_t *>(a.bitmap);
+  if (g0 >= N) {
+    if (g0 < a.n_words * 32) bm[g0 >> 3] = 0;
+    return;
   }
-  if (!links) {
+  const bool full = g0 + kCombineItems <= N;
+  uint32_t cw[kCombineWords];  // reason bytes, four a word
+  if (full) {
+    const uint2 q = *reinterpret_cast<const uint2 *>(a.rb + g0);
+    cw[0] = q.x;
+    cw[1] = q.y;
+  } else {
 #pragma unroll
-    for (int i = 0; i < kCombineRows; ++i) hg[i] = -1;
+    for (int k = 0; k < kCombineWords; ++k) cw[k] = 0;
+    for (int i = 0; i < kCombineItems; ++i)
+      if (g0 + i < N) cw[i >> 2] |= uint32_t(a.rb[g0 + i]) << (8 * (i & 3));
   }
   if (!a.raw) {
-    uint8_t hr[kCombineRows];
+    int32_t hd[kCombineItems];
+    if (links) {
+      if (full && (reinterpret_cast<uintptr_t>(a.t.head) & 15) == 0) {
 #pragma unroll
-    for (int i = 0; i < kCombineRows; ++i) hr[i] = hg[i] >= 0 ? a.rb[hg[i]] : 0;
-#pragma unroll
-    for (int i = 0; i < kCombineRows; ++i) {
-      const int64_t g = start + i * kThreads + threadIdx.x;
-      if (g >= N) continue;
-      if (hg[i] >= 0) {
-        const bool hover = a.overloaded ? a.overloaded[hg[i]] != 0 : true;
-        code[i] = (hover && hr[i] != 0) ? 3 : 0;
-      } else if (hg[i] == -2) {
-        code[i] = 0;
+        for (int k = 0; k < kCombineItems / 4; ++k) {
+          const int4 q = reinterpret_cast<const int4 *>(a.t.head + g0)[k];
+          hd[4 * k] = q.x;
+          hd[4 * k + 1] = q.y;
+          hd[4 * k + 2] = q.z;
+          hd[4 * k + 3] = q.w;
+        }
       } else {
-        const bool over = a.overloaded ? a.overloaded[g] != 0 : true;
-        code[i] = over ? code[i] : 0;
+#pragma unroll
+        for (int i = 0; i < kCombineItems; ++i) hd[i] = g0 + i < N ? a.t.head[g0 + i] : 0;
       }
     }
-  }
+    uint32_t ow[kCombineWords];  // own overload flags
 #pragma unroll
-  for (int i = 0; i < kCombineRows; ++i) {
-    const int64_t base = start + i * kThreads;
-    const int64_t g = base + threadIdx.x;
-    if (a.reason && g < N) a.reason[g] = code[i];
-    const uint64_t bits = __ballot(g < N && code[i] != 0);
-    if (lane == 0) {
-      const int64_t w = (base + (threadIdx.x & ~63)) >> 5;
-      if (w < a.n_words) a.bitmap[w] = uint32_t(bits);
-      if (w + 1 < a.n_words) a.bitmap[w + 1] = uint32_t(bits >> 32);
+    for (int k = 0; k < kCombineWords; ++k) ow[k] = 0xffffffffu;
+    if (a.overloaded) {
+      if (full) {
+        const uint2 q = *reinterpret_cast<const uint2 *>(a.overloaded + g0);
+        ow[0] = q.x;
+        ow[1] = q.y;
+      } else {
+        for (int i = 0; i < kCombineItems; ++i)
+          if (g0 + i < N && a.overloaded[g0 + i] == 0) ow[i >> 2] &= ~(0xffu << (8 * (i & 3)));
+      }
+    }
+    // each record's first call: -1 itself, -2 a link out of range (reported by the
+    // element pass), else its global index
+    int64_t hg[kCombineItems];
+#pragma unroll
+    for (int i = 0; i < kCombineItems; ++i) hg[i] = -1;
+    if (links) {
+      // the thread's first replica: the last of the block's whose offset is <= g0
+      int32_t r = s_rep[0];
+      for (int32_t b = s_rep[1]; r < b;) {
+        const int32_t m = (r + b + 1) >> 1;
+        if (a.t.rep_off[m] <= g0)
+          r = m;
+        else
+          b = m - 1;
+      }
+      int64_t lo = a.t.rep_off[r], hi = a.t.rep_off[r + 1];
+#pragma unroll
+      for (int i = 0; i < kCombineItems; ++i) {
+        const int64_t g = g0 + i;
+        if (g >= N) continue;
+        while (g >= hi) {
+          ++r;
+          lo = hi;
+          hi = a.t.rep_off[r + 1];
+        }
+        const int64_t h = lo + hd[i];
+        if (h != g) hg[i] = (h >= lo && h < g) ? h : -2;
+      }
+    }
+    uint8_t hr[kCombineItems], ho[kCombineItems];
+#pragma unroll
+    for (int i = 0; i < kCombineItems; ++i) {
+      hr[i] = hg[i] >= 0 ? a.rb[hg[i]] : 0;
+      ho[i] = (hg[i] >= 0 && a.overloaded) ? a.overloaded[hg[i]] : 1;
+    }
+#pragma unroll
+    for (int i = 0; i < kCombineItems; ++i) {
+      const int sh = 8 * (i & 3);
+      uint32_t c = (cw[i >> 2] >> sh) & 0xffu;
+      if (hg[i] >= 0)
+        c = (ho[i] != 0 && hr[i] != 0) ? 3u : 0u;
+      else if (hg[i] == -2)
+        c = 0;
+      else
+        c = ((ow[i >> 2] >> sh) & 0xffu) != 0 ? c : 0u;
+      cw[i >> 2] = (cw[i >> 2] & ~(0xffu << sh)) | (c << sh);
+    }
+  }
+  uint32_t bits = 0;
+#pragma unroll
+  for (int i = 0; i < kCombineItems; ++i)
+    bits |= (((cw[i >> 2] >> (8 * (i & 3))) & 0xffu) != 0 ? 1u : 0u) << i;
+  bm[g0 >> 3] = uint8_t(bits);  // (bytes past N are zero, so are their bits)
+  if (a.reason) {
+    if (full && (reinterpret_cast<uintptr_t>(a.reason) & 7) == 0) {
+      *reinterpret_cast<uint2 *>(a.reason + g0) = make_uint2(cw[0], cw[1]);
+    } else {
+      for (int i = 0; i < kCombineItems; ++i)
+        if (g0 + i < N) a.reason[g0 + i] = uint8_t(cw[i >> 2] >> (8 * (i & 3)));
     }
   }
 }

@@ -49,8 +49,8 @@ MEASURED_TRAFFIC = {
                                "write_kib": 137709.46875, "fetch_factor": 1.99991,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
-    ("c3_throttle", "throttle"): {"src": "40db6dc0ec560fa4", "fetch_kib": 1458803.5,
-                                  "write_kib": 1522312.75, "fetch_factor": 1.9999,
+    ("c3_throttle", "throttle"): {"src": "3e692007d079695e", "fetch_kib": 1287884.875,
+                                  "write_kib": 1618594.5625, "fetch_factor": 1.99989,
                                   "write_factor": 1.0},
 }
 

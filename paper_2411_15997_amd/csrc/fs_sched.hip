@@ -152,6 +152,40 @@ __global__ void __launch_bounds__(256) k_state_links(char *state, StateLayout L,
   }
 }
 
+// The same counts and links with one work-group per replica, for traces of many replicas
+// of moderate size: the replica's counts are its own, kept in an LDS table of U entries
+// and stored once at the end, without a global atomic.
+constexpr int kLinkRepMinR = 512;              // replicas (work-groups) at least
+constexpr int64_t kLinkRepMaxN = int64_t(1) << 16;  // records per replica at most
+__global__ void __launch_bounds__(256) k_state_links_rep(char *state, StateLayout L, DevTrace t) {
+  extern __shared__ uint32_t hc_rep[];  // [U]
+  const int32_t r = blockIdx.x;
+  const int64_t b = t.rep_off[r], e = t.rep_off[r + 1];
+  for (int j = threadIdx.x; j < t.U; j += 256) hc_rep[j] = 0;
+  __syncthreads();
+  int32_t *succ = reinterpret_cast<int32_t *>(state + L.succ);
+  for (int64_t g0 = b; g0 < e; g0 += int64_t(kLinkPer) * 256) {
+    int32_t us[kLinkPer], cs[kLinkPer], ps[kLinkPer];
+#pragma unroll
+    for (int k = 0; k < kLinkPer; ++k) {
+      const int64_t g = g0 + k * 256 + threadIdx.x;
+      us[k] = g < e ? t.user[g] : -1;
+      cs[k] = g < e && t.call ? t.call[g] : 0;
+      ps[k] = g < e && t.call ? t.prev[g] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < kLinkPer; ++k) {
+      const int64_t g = g0 + k * 256 + threadIdx.x;
+      if (g >= e) break;
+      if (us[k] >= 0 && us[k] < t.U) atomicAdd(hc_rep + us[k], 1u);
+      if (cs[k] > 0 && ps[k] >= 0 && ps[k] < g - b) succ[b + ps[k]] = int32_t(g - b);
+    }
+  }
+  __syncthreads();
+  uint32_t *cnt = reinterpret_cast<uint32_t *>(state + L.seg_start) + int64_t(r) * t.U;
+  for (int j = threadIdx.x; j < t.U; j += 256) cnt[j] = hc_rep[j];
+}
+
 struct CheckArgs {
   DevTrace t;
   const int64_t *cost;
@@ -253,8 +287,15 @@ hipError_t launch_state_init(void *state, const fs_trace *t, hipStream_t s) {
   hipLaunchKernelGGL(k_state_users, dim3(grid_for(RU + 1, 256)), dim3(256), 0, s, st, L, RU);
   if (N > 0) {
     hipLaunchKernelGGL(k_state_records, dim3(grid_for(N, 256)), dim3(256), 0, s, st, L, N);
-    hipLaunchKernelGGL(k_state_links, dim3((N + kLinkTile - 1) / kLinkTile), dim3(256), 0, s, st,
-                       L, dev_trace(t));
+    int64_t max_rep = 0;
+    for (int32_t r = 0; r < t->n_replicas; ++r)
+      max_rep = std::max<int64_t>(max_rep, t->rep_off_h[r + 1] - t->rep_off_h[r]);
+    if (t->n_replicas >= kLinkRepMinR && t->n_users <= kLinkSlots && max_rep <= kLinkRepMaxN)
+      hipLaunchKernelGGL(k_state_links_rep, dim3(t->n_replicas), dim3(256),
+                         size_t(t->n_users) * sizeof(uint32_t), s, st, L, dev_trace(t));
+    else
+      hipLaunchKernelGGL(k_state_links, dim3((N + kLinkTile - 1) / kLinkTile), dim3(256), 0, s,
+                         st, L, dev_trace(t));
   }
   // per-user first-call segments: exclusive prefix of the counts
   hipError_t e = exclusive_scan(reinterpret_cast<uint32_t *>(st + L.seg_start), RU + 1,

@@ -45,6 +45,21 @@ def test_many_tiny_replicas_one_launch(seed):
     compare_sim(g, o)
 
 
+@pytest.mark.parametrize("seed,multi", [(0, True), (1, True), (2, False)])
+def test_many_replicas_counted_per_replica(seed, multi):
+    """Enough replicas (at least 512, each of at most 2^16 requests) that the state's
+    per-(replica, user) counts and next-call links are taken one work-group a replica."""
+    rng = np.random.default_rng(70 + seed)
+    tr = _batch_of_random(rng, 700, 60, 9, multi=multi)
+    cost = rng.integers(0, 50, tr.n).astype(np.int64)
+    reason = rng.integers(0, 3, tr.n).astype(np.uint8)
+    step, cap, theta = int(rng.integers(1, 40)), int(rng.integers(1, 12)), int(rng.integers(-1, 8))
+    say("sched per-replica counts", seed, tr.n_replicas, tr.n)
+    o = oracle.simulate(tr, cost, reason, step, cap, theta)
+    g = gpu_schedule(tr, cost, reason, step, cap, theta)
+    compare_sim(g, o)
+
+
 def _run_workload(wl, tr, global_only=False):
     coef, per_rep = fs.workload_weights(wl, tr)
     c = oracle.cost(tr, coef, coef_per_replica=per_rep)

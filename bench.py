@@ -52,6 +52,10 @@ MEASURED_TRAFFIC = {
     ("c3_throttle", "throttle"): {"src": "3e692007d079695e", "fetch_kib": 1287884.875,
                                   "write_kib": 1618594.5625, "fetch_factor": 1.99989,
                                   "write_factor": 1.0},
+    # the same stream with the app limit counted per (app, replica) over all users
+    ("c3_throttle+app_scope", "throttle"): {"src": "3e692007d079695e", "fetch_kib": 2268758.0625,
+                                            "write_kib": 4063234.28125, "fetch_factor": 1.99991,
+                                            "write_factor": 1.0},
 }
 
 NO_LIMIT = 2 ** 31 - 1
@@ -178,6 +182,9 @@ def main():
                     help="literal engine: duration of one decode step")
     ap.add_argument("--kv-tokens", type=int, default=1 << 22,
                     help="literal engine: KV-cache capacity per replica, in tokens")
+    ap.add_argument("--app-scope", action="store_true",
+                    help="count the app limit per (app, replica) over all users (the other "
+                         "reading of the paper's app key) instead of per (user, app)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="copy 1 GiB on the device first (calibrates rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -205,7 +212,7 @@ def main():
     dt = fs.DeviceTrace(tr, device=dev)
     throttle_only = wl.throttle_only
     t_user, t_app, theta, fcfs, blind, equal = policy_settings(wl, tr.n_apps, args.policy)
-    lim = fs.make_limits(wl.window_us, t_user, t_app)
+    lim = fs.make_limits(wl.window_us, t_user, t_app, app_scope=1 if args.app_scope else 0)
     N = tr.n
     err = fs.err_word(dev)
     tws = torch.empty(max(fs.fs_throttle_workspace(dt), 1), dtype=torch.uint8, device=dev)
@@ -317,6 +324,8 @@ def main():
         "ms_per_step_median_events": round(step_ms_med, 4),
         "stages_ms": {k: round(v, 4) for k, v in stage_ms.items()},
     }
+    if args.app_scope:
+        result["config"]["app_scope"] = "per (app, replica)"
     if "schedule" in stages:
         result["value"] = decisions / (ms_per_step / 1000.0)
         result["unit"] = "decisions/s"
@@ -342,7 +351,12 @@ def main():
     if dom == "schedule":
         limiter = ("latency of each replica's dependent decision chain: one wave per replica, "
                    f"{R} waves on 1,024 SIMDs")
-    result["roofline"] = roofline(dom, bpr[dom] * N, stage_ms[dom], wl.name, limiter)
+    # the stored traffic was measured on the default policy and engine; the app-level
+    # limit has its own entry, any other variant reports none
+    tkey = None
+    if args.policy == "fs" and args.engine == "step":
+        tkey = wl.name + ("+app_scope" if args.app_scope else "")
+    result["roofline"] = roofline(dom, bpr[dom] * N, stage_ms[dom], tkey, limiter)
     result["stage_gbs"] = {s: round(bpr[s] * N / (stage_ms[s] / 1000.0) / 1e9, 2)
                            for s in stage_ms if bpr[s] > 0}
     # stages whose algorithmic bytes fit the 256 MB Infinity Cache may be served from it
@@ -398,7 +412,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline and not args.stage_only:
         cpu = cpu_baseline(wl, tr, args.cpu_threads, throttle_only, args.policy,
-                           (args.decode_step_us, args.kv_tokens) if literal else None)
+                           (args.decode_step_us, args.kv_tokens) if literal else None,
+                           app_scope=1 if args.app_scope else 0)
         result["cpu_baseline"] = cpu
 
     # the throttle leg: fs_throttle on the largest throttle workload, own timed region
@@ -481,9 +496,11 @@ def _key_hashed_parts(tr, parts):
     return out
 
 
-def cpu_throttle_baseline(wl, tr, threads=0):
+def cpu_throttle_baseline(wl, tr, threads=0, app_scope=0):
     """The oracle's throttle (gated, always overloaded) on the whole stream: one thread,
-    then users hashed over the host's threads (part construction not timed)."""
+    then users hashed over the host's threads (part construction not timed).  With the
+    app limit counted over all users of an app, a request's two keys (its user, its app)
+    cannot both stay within one part, so the stream runs on one thread only."""
     from concurrent.futures import ThreadPoolExecutor
 
     import oracle
@@ -491,8 +508,13 @@ def cpu_throttle_baseline(wl, tr, threads=0):
     hc = host_cpu()
     th = threads or min(16, hc["available"])
     t0 = time.perf_counter()
-    oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, raw=False, counts=False)
+    oracle.throttle(tr, wl.window_us, wl.t_user, wl.t_app, raw=False, counts=False,
+                    app_scope=app_scope)
     one = time.perf_counter() - t0
+    if app_scope:
+        return {"value": tr.n / one, "unit": "throttle evals/s", "cores": 1, "kind": "oracle",
+                "sample": f"whole {wl.name} stream ({tr.n} requests), app limit per (app, "
+                          f"replica), one thread", "seconds": round(one, 3), "host": hc}
     parts = _key_hashed_parts(tr, th)
     t0 = time.perf_counter()
     with ThreadPoolExecutor(th) as ex:
@@ -530,7 +552,7 @@ def _oracle_path(wl, tr, th, policy, literal):
     return sim
 
 
-def cpu_baseline(wl, tr, threads, throttle_only, policy="fs", literal=None):
+def cpu_baseline(wl, tr, threads, throttle_only, policy="fs", literal=None, app_scope=0):
     """The CPU oracle (as it stands) on this host, same workload, policy and engine
     (literal: (decode step, KV tokens) of the literal engine), whole path
     (cost + throttle + schedule + metrics): replicas split over the host's threads on
@@ -538,7 +560,7 @@ def cpu_baseline(wl, tr, threads, throttle_only, policy="fs", literal=None):
     import tracegen as tg
 
     if throttle_only:
-        return cpu_throttle_baseline(wl, tr, threads)
+        return cpu_throttle_baseline(wl, tr, threads, app_scope)
     hc = host_cpu()
     th = threads or min(16, hc["available"], tr.n_replicas)
     t0 = time.perf_counter()

@@ -279,6 +279,7 @@ struct InitArgs {
   uint32_t *hist;
   int64_t tiles;
   int32_t *err;
+  const uint8_t *uflag;  // when set: the flag bit is this byte per request (stream order)
 };
 
 // Builds the elements of one tile in stream order, checks the fields the throttle
@@ -330,7 +331,8 @@ __global__ void __launch_bounds__(kThreads) k_thr_init(InitArgs a) {
         q = rel > 0 ? uint64_t(rel) >> sh : 0;
         if (q > a.pk.qmask) q = a.pk.qmask;  // only for unsorted input, which is an error
       }
-      const uint64_t fl = (a.mark == 1 || (a.mark == 2 && first)) ? 1u : 0u;
+      const uint64_t fl = a.uflag ? (a.uflag[g] != 0 ? 1u : 0u)
+                                  : ((a.mark == 1 || (a.mark == 2 && first)) ? 1u : 0u);
       const uint64_t e = (key << a.pk.SK) | (uint64_t(g) << a.pk.SI) | (q << 1) | fl;
       a.el[g] = e;
       d = uint32_t(e >> (a.pk.SK + a.shift)) & a.mask;
@@ -882,19 +884,26 @@ __global__ void __launch_bounds__(kFThreads) k_thr_fused(FusedArgs a) {
 // ---------------------------------------------------------------- app-level limit
 
 // With the app limit counted over all users of an app, the user test runs on the user
-// order and the elements go back to stream order (through their index field) before
-// the app passes, so that each app's records come out in time order.
-__global__ void __launch_bounds__(kThreads) k_thr_user_unsort(ScatterArgs a) {
+// order and marks the requests over the user limit, one byte each at its stream
+// position (the bytes zeroed first); the elements are then built again in stream order
+// carrying that flag, so that the app passes leave each app's records in time order.
+__global__ void __launch_bounds__(kThreads) k_bytes_zero(uint8_t *b, int64_t n) {
+  const int64_t n16 = n >> 4;
+  uint4 *b4 = reinterpret_cast<uint4 *>(b);
+  for (int64_t i = blockIdx.x * int64_t(kThreads) + threadIdx.x; i < n16;
+       i += int64_t(gridDim.x) * kThreads)
+    b4[i] = make_uint4(0u, 0u, 0u, 0u);
+  if (blockIdx.x == 0 && threadIdx.x < (n & 15)) b[(n16 << 4) + threadIdx.x] = 0;
+}
+
+__global__ void __launch_bounds__(kThreads) k_thr_user_flags(ScatterArgs a, uint8_t *flag) {
   const Win win = load_win(a.win);
   const Pack &pk = win.pk;
   for (int64_t p = blockIdx.x * int64_t(kThreads) + threadIdx.x; p < a.N;
        p += int64_t(gridDim.x) * kThreads) {
-    uint64_t e = a.in[p];
-    if (int64_t(a.t_user) <= p) {
-      const uint64_t eq = a.in[p - a.t_user];
-      if (((e ^ eq) & a.user_mask) == 0 && in_window(e, eq, win)) e |= 1u;
-    }
-    a.out[(e >> pk.SI) & pk.imask] = e;
+    if (int64_t(a.t_user) > p) continue;
+    const uint64_t e = a.in[p], eq = a.in[p - a.t_user];
+    if (((e ^ eq) & a.user_mask) == 0 && in_window(e, eq, win)) flag[(e >> pk.SI) & pk.imask] = 1;
   }
 }
 
@@ -1175,24 +1184,32 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   for (int k = 0; k < n_pass; ++k) {
     const uint32_t mask = (1u << dig[k].width) - 1u;
     const int shift = pk.SK + dig[k].shift;
+    bool hist_ready = false;
     if (k == n_user && app_level) {
-      // user test on the user order, then back to stream order for the app passes
+      // user test on the user order, its flags to stream positions (one byte each, in
+      // the digit buffer, which the app passes do not use), then the elements again in
+      // stream order carrying them, with the first app digit's histogram
       if (cnt_user) {
         CountArgs ca{in, L.N, KeySel{user_mask, false, pk.SK, pk.Bu, 1u}, win, cnt_user};
         hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
       }
+      hipLaunchKernelGGL(k_bytes_zero, dim3(grid_for((L.N >> 4) + 1, kThreads)), dim3(kThreads),
+                         0, s, dig_b, L.N);
       ScatterArgs ua{in, out, L.N, 0, 0, nullptr, 0, lim->t_user,
                      user_mask, win, sh + kFlagStride};
-      hipLaunchKernelGGL(k_thr_user_unsort, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s,
-                         ua);
+      hipLaunchKernelGGL(k_thr_user_flags, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s,
+                         ua, dig_b);
+      InitArgs ia2{dt, pk, !raw, 0, sh, out, dig[k].shift, mask, hist, L.tiles, err, dig_b};
+      hipLaunchKernelGGL(k_thr_init, dim3(L.tiles), dim3(kThreads), 0, s, ia2);
       uint64_t *tmp = in;
       in = out;
       out = tmp;
+      hist_ready = true;
     }
-    if (k > 0 && have_dig)
+    if (!hist_ready && k > 0 && have_dig)
       hipLaunchKernelGGL(k_radix_hist8, dim3(L.tiles), dim3(kThreads), 0, s, dig_b, L.N, mask,
                          hist, L.tiles);
-    else if (k > 0)
+    else if (!hist_ready && k > 0)
       hipLaunchKernelGGL(k_radix_hist, dim3(L.tiles), dim3(kThreads), 0, s, in, L.N, shift, mask,
                          hist, L.tiles);
     (void)exclusive_scan(hist, int64_t(mask + 1) * L.tiles, part, s);
@@ -1201,7 +1218,7 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
       hipLaunchKernelGGL(k_thr_count, dim3(grid_for(L.N, kThreads)), dim3(kThreads), 0, s, ca);
     }
     // the next pass's digits go out with the elements, unless the app-level user test
-    // puts the elements back in stream order before that pass
+    // builds the elements again in stream order before that pass
     have_dig = k + 1 < n_pass && !(app_level && k + 1 == n_user);
     ScatterArgs sa{in, out, L.N, shift, mask, hist, L.tiles, lim->t_user,
                    user_mask, win, sh + kFlagStride, have_dig ? dig_b : nullptr,

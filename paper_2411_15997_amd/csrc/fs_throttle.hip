@@ -884,8 +884,9 @@ __global__ void __launch_bounds__(kFThreads) k_thr_fused(FusedArgs a) {
 // ---------------------------------------------------------------- app-level limit
 
 // With the app limit counted over all users of an app, the user test runs on the user
-// order and marks the requests over the user limit, one byte each at its stream
-// position (the bytes zeroed first); the elements are then built again in stream order
+// order and marks the requests over the user limit (of those whose own reason is used:
+// gated, the first calls), one byte each at its stream position (the bytes zeroed
+// first); the elements are then built again in stream order
 // carrying that flag, so that the app passes leave each app's records in time order.
 __global__ void __launch_bounds__(kThreads) k_bytes_zero(uint8_t *b, int64_t n) {
   const int64_t n16 = n >> 4;
@@ -902,7 +903,9 @@ __global__ void __launch_bounds__(kThreads) k_thr_user_flags(ScatterArgs a, uint
   for (int64_t p = blockIdx.x * int64_t(kThreads) + threadIdx.x; p < a.N;
        p += int64_t(gridDim.x) * kThreads) {
     if (int64_t(a.t_user) > p) continue;
-    const uint64_t e = a.in[p], eq = a.in[p - a.t_user];
+    const uint64_t e = a.in[p];
+    if (!(e & 1u)) continue;  // a request whose own reason is not used (a later call, gated)
+    const uint64_t eq = a.in[p - a.t_user];
     if (((e ^ eq) & a.user_mask) == 0 && in_window(e, eq, win)) flag[(e >> pk.SI) & pk.imask] = 1;
   }
 }
@@ -1170,7 +1173,9 @@ hipError_t launch_throttle(const fs_trace *t, const fs_limits *lim, const uint8_
   // the fused path: user bits only, both limits tested in one pass over the user order
   const bool fused = !app_level && !cnt_user && !cnt_app && lim->t_user >= 0 &&
                      lim->t_user <= kHaloMax;
-  const int mark = fused ? (raw ? 1 : 2) : 0;
+  // flag bit of the first elements: the requests whose own reason is used (every one
+  // raw, the first calls gated), for the fused test and the app-level user test
+  const int mark = (fused || app_level) ? (raw ? 1 : 2) : 0;
   InitArgs ia{dt, pk, !raw, mark, sh, A, dig[0].shift, (1u << dig[0].width) - 1u, hist, L.tiles,
               err};
   hipLaunchKernelGGL(k_thr_init, dim3(L.tiles), dim3(kThreads), 0, s, ia);

@@ -49,12 +49,12 @@ MEASURED_TRAFFIC = {
                                "write_kib": 137709.46875, "fetch_factor": 1.99991,
                                "write_factor": 1.0},
     # every kernel of one fs_throttle call on the 50M-request throttle stream
-    ("c3_throttle", "throttle"): {"src": "c18b75dcf3e166c1", "fetch_kib": 1287944.375,
-                                  "write_kib": 1618608.84375, "fetch_factor": 1.99991,
+    ("c3_throttle", "throttle"): {"src": "f12662f2bb0b6f6c", "fetch_kib": 1287878.3125,
+                                  "write_kib": 1618727.9375, "fetch_factor": 1.99991,
                                   "write_factor": 1.0},
     # the same stream with the app limit counted per (app, replica) over all users
-    ("c3_throttle+app_scope", "throttle"): {"src": "c18b75dcf3e166c1", "fetch_kib": 2586509.25,
-                                            "write_kib": 3829551.40625, "fetch_factor": 1.99992,
+    ("c3_throttle+app_scope", "throttle"): {"src": "f12662f2bb0b6f6c", "fetch_kib": 2582543.5625,
+                                            "write_kib": 3290211.28125, "fetch_factor": 1.99992,
                                             "write_factor": 1.0},
 }
 

@@ -342,22 +342,36 @@ constexpr size_t kRepLdsMax = 150 * 1024;        // its LDS, at most
 
 struct RepLds {  // byte offsets into the dynamic LDS of k_ws_replica
   size_t tok, ls, gr, red, req, lh, sh, rate, total;
+  int copies;                 // of the length sums and histograms, chosen by lane
+  int ls_stride, lh_stride;   // entries per copy (one of padding, for the banks)
 };
 
-__host__ __device__ inline RepLds rep_lds(int32_t U, int32_t A) {
+// The per-app length sums and histograms take an LDS atomic per request and field, and
+// a wave's lanes hit few of their entries (a handful of apps, lengths in a few bins):
+// when LDS allows, kWsCopies copies of them, lane l adding to copy l % kWsCopies, cut
+// the lanes of one instruction that meet on one entry by that factor.
+constexpr int kWsCopies = 8;
+__host__ __device__ inline RepLds rep_lds_n(int32_t U, int32_t A, int copies) {
   RepLds L;
   const size_t ua = size_t(U) * size_t(A);
+  L.copies = copies;
+  L.ls_stride = A * 3 + (copies > 1 ? 1 : 0);
+  L.lh_stride = A * 3 * kLenBins + (copies > 1 ? 1 : 0);
   size_t o = 0;
   L.tok = o;  o += ua * 8;                                 // tokens per (user, app)
-  L.ls = o;   o += size_t(A) * 3 * 8;                      // length sums [A][3]
+  L.ls = o;   o += size_t(copies) * L.ls_stride * 8;       // length sums [A][3]
   L.gr = o;   o += size_t(kGraphBins) * 5 * 8;             // Table 2 rows
   L.red = o;  o += size_t(kRepThreads / 64) * 8;           // per-wave maxima
   L.req = o;  o += ua * 4;                                 // requests per (user, app)
-  L.lh = o;   o += size_t(A) * 3 * kLenBins * 4;           // length histograms
+  L.lh = o;   o += size_t(copies) * L.lh_stride * 4;       // length histograms
   L.sh = o;   o += size_t(A) * kSizeBins * 4;              // size histogram
   L.rate = o; o += size_t(A + 1) * 2 * kRateBins * 4;      // rate histograms
   L.total = (o + 15) / 16 * 16;
   return L;
+}
+__host__ __device__ inline RepLds rep_lds(int32_t U, int32_t A) {
+  const RepLds c = rep_lds_n(U, A, kWsCopies);
+  return c.total <= kRepLdsMax ? c : rep_lds_n(U, A, 1);
 }
 
 __device__ inline unsigned long long wmax64(unsigned long long v) {
@@ -388,9 +402,12 @@ __global__ void __launch_bounds__(kRepThreads) k_ws_replica(WsArgs a) {
     tok[k] = 0;
     req[k] = 0;
   }
-  for (int k = tid; k < A * 3; k += kRepThreads) ls[k] = 0;
+  for (int k = tid; k < L.copies * L.ls_stride; k += kRepThreads) ls[k] = 0;
   for (int k = tid; k < kGraphBins * 5; k += kRepThreads) gr[k] = 0;
-  for (int k = tid; k < A * 3 * kLenBins; k += kRepThreads) lh[k] = 0;
+  for (int k = tid; k < L.copies * L.lh_stride; k += kRepThreads) lh[k] = 0;
+  const int cp = lane & (L.copies - 1);  // this lane's copy of the length tables
+  uint32_t *const lh_c = lh + cp * L.lh_stride;
+  unsigned long long *const ls_c = ls + cp * L.ls_stride;
   for (int k = tid; k < A * kSizeBins; k += kRepThreads) sh[k] = 0;
   for (int k = tid; k < (A + 1) * 2 * kRateBins; k += kRepThreads) rate[k] = 0;
   const int64_t base = t.rep_off[r], n = t.rep_off[r + 1] - base;
@@ -438,8 +455,8 @@ __global__ void __launch_bounds__(kRepThreads) k_ws_replica(WsArgs a) {
       atomicAdd(&tok[k], (unsigned long long)(Lx[j][0] + Lx[j][1] + Lx[j][2]));
 #pragma unroll
       for (int x = 0; x < 3; ++x) {
-        atomicAdd(&lh[(ap[j] * 3 + x) * kLenBins + len_bin(Lx[j][x])], 1u);
-        if (Lx[j][x]) atomicAdd(&ls[ap[j] * 3 + x], (unsigned long long)Lx[j][x]);
+        atomicAdd(&lh_c[(ap[j] * 3 + x) * kLenBins + len_bin(Lx[j][x])], 1u);
+        if (Lx[j][x]) atomicAdd(&ls_c[ap[j] * 3 + x], (unsigned long long)Lx[j][x]);
       }
       if (!first[j]) atomicAdd(a.size + base + h[j], 1u);
     }
@@ -531,9 +548,16 @@ __global__ void __launch_bounds__(kRepThreads) k_ws_replica(WsArgs a) {
   if (tid == 0) a.o.minutes[r] = int64_t(M);
   for (int k = tid; k < (A + 1) * 2 * kRateBins; k += kRepThreads)
     a.o.rate_hist[int64_t(r) * (A + 1) * 2 * kRateBins + k] = int64_t(rate[k]);
-  for (int k = tid; k < A * 3 * kLenBins; k += kRepThreads)
-    a.o.len_hist[int64_t(r) * A * 3 * kLenBins + k] = int64_t(lh[k]);
-  for (int k = tid; k < A * 3; k += kRepThreads) a.o.len_sum[int64_t(r) * A * 3 + k] = int64_t(ls[k]);
+  for (int k = tid; k < A * 3 * kLenBins; k += kRepThreads) {
+    uint64_t v = 0;
+    for (int c = 0; c < L.copies; ++c) v += lh[c * L.lh_stride + k];
+    a.o.len_hist[int64_t(r) * A * 3 * kLenBins + k] = int64_t(v);
+  }
+  for (int k = tid; k < A * 3; k += kRepThreads) {
+    unsigned long long v = 0;
+    for (int c = 0; c < L.copies; ++c) v += ls[c * L.ls_stride + k];
+    a.o.len_sum[int64_t(r) * A * 3 + k] = int64_t(v);
+  }
   for (int k = tid; k < A * kSizeBins; k += kRepThreads)
     a.o.size_hist[int64_t(r) * A * kSizeBins + k] = int64_t(sh[k]);
   for (int k = tid; k < kGraphBins * 5; k += kRepThreads)

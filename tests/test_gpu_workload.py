@@ -72,6 +72,20 @@ def test_random_many_replicas(seed):
     _compare(tr, minute=int(rng.choice([1, 1000, 60_000])), per_app=bool(seed % 2))
 
 
+@pytest.mark.parametrize("U,A", [(1100, 8), (1400, 8)])
+def test_many_replicas_length_table_copies(U, A):
+    """The per-replica work-group keeps copies of the per-app length sums and histograms
+    when LDS allows (1,100 users x 8 apps) and a single one when the (user, app) table
+    leaves no room for them (1,400 x 8)."""
+    rng = np.random.default_rng(990 + U)
+    parts = [random_trace(rng, int(rng.choice([0, 1, 40, 200])), U, A,
+                          int(rng.integers(1, 10 ** 6)), multi=True, max_tok=5000)
+             for _ in range(260)]
+    tr = tg.concat(parts)
+    say("workload stats length copies", U, A, tr.n)
+    _compare(tr, minute=60_000, per_app=True)
+
+
 def test_errors_many_replicas():
     rng = np.random.default_rng(5)
     tr = random_trace(rng, 40, 6, 3, 1000, multi=True, n_replicas=260)
